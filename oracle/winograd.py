@@ -1,0 +1,131 @@
+"""Reference N-D Winograd correlation (oracle; test infrastructure only).
+
+Written from §3.2-§4.1, step by step:
+
+1. tile the input: overlapping alpha^N windows stepping by m along each axis
+   (§3.3), alpha = m + r - 1; T_i = ceil(Y_i / m) tiles per axis, reads outside
+   the zero-padded input are zero;
+2. kernel transform  U = g x_1 G x_2 G ... x_N G          (eq. 3 and 4)
+3. data transform    V = d x_1 B^T ... x_N B^T            (eq. 4)
+4. for every transformed element xi, one matrix product over channels
+   M_xi = V_xi [T x C] . U_xi [C x K]                     (eq. 5)
+5. inverse transform Y = M x_1 A^T ... x_N A^T            (eq. 4)
+6. stitch the m^N output tiles and crop to Y.
+
+The n-mode product is eq. (3): (X x_n U)_{..j..} = sum_{i_n} x_{..i_n..} u_{j,i_n}.
+
+Arithmetic is fp64 by default; with ``exact=True`` every array is an object
+array of ``fractions.Fraction`` and the result is exact.
+
+Pins (tests/test_oracle_winograd.py): exact agreement with the direct
+correlation on small integer inputs for N = 1, 2, 3, every supported (m, r),
+ragged tiles and padding; the §2.2 hand example; separability (the N-D
+transform equals a Kronecker-product matrix and any axis order gives the same
+result); the 2-D case equals A[(C g C^T) . (B d B^T)]A^T of §3.2.
+"""
+from __future__ import annotations
+
+import itertools
+import math
+from fractions import Fraction
+
+import numpy as np
+
+from .toomcook import default_points, winograd_matrices
+
+
+def mode_n_product(X, U, n):
+    """Eq. (3): contract axis n of X with the columns of U (J x I_n)."""
+    U = np.asarray(U)
+    out = np.tensordot(X, U, axes=([n], [1]))          # moves the new axis last
+    return np.moveaxis(out, -1, n)
+
+
+def mode_products(X, mats, axes):
+    """X x_{axes[0]} mats[0] x_{axes[1]} mats[1] ... (applied in that order)."""
+    for U, n in zip(mats, axes):
+        X = mode_n_product(X, U, n)
+    return X
+
+
+def matrices(m, r, points=None, exact=False):
+    pts = default_points(m, r) if points is None else points
+    AT, BT, G = winograd_matrices(m, r, pts)
+    if exact:
+        cv = lambda M: np.array(M, dtype=object)
+    else:
+        cv = lambda M: np.array([[float(c) for c in row] for row in M], dtype=np.float64)
+    return cv(AT), cv(BT), cv(G)
+
+
+def _as(x, exact):
+    if exact:
+        a = np.asarray(x)
+        out = np.empty(a.shape, dtype=object)
+        flat = out.reshape(-1)
+        for i, v in enumerate(a.reshape(-1)):
+            flat[i] = Fraction(v) if not isinstance(v, Fraction) else v
+        return out
+    return np.asarray(x, dtype=np.float64)
+
+
+def tile_counts(X, pad, m, r):
+    Y = tuple(xi + 2 * pad - r + 1 for xi in X)
+    return Y, tuple(math.ceil(yi / m) for yi in Y)
+
+
+def winograd_forward(x, w, m, r, pad=0, points=None, relu=False, exact=False):
+    """Steps 1-6 above.  x: [n][C][X..], w: [K][C][r..] -> y [n][K][Y..]."""
+    N = np.ndim(x) - 2
+    alpha = m + r - 1
+    AT, BT, G = matrices(m, r, points, exact)
+    x = _as(x, exact)
+    w = _as(w, exact)
+    n, C = x.shape[:2]
+    K = w.shape[0]
+    Y, T = tile_counts(x.shape[2:], pad, m, r)
+    if any(yi < 1 for yi in Y):
+        raise ValueError("output extent must be positive")
+
+    # Step 1: zero-extended input large enough for every tile window.
+    ext = tuple(ti * m + r - 1 for ti in T)
+    zero = Fraction(0) if exact else 0.0
+    xe = np.full((n, C) + ext, zero, dtype=object if exact else np.float64)
+    sl_dst, sl_src = [], []
+    for xi, ei in zip(x.shape[2:], ext):
+        hi = min(xi, ei - pad)
+        sl_dst.append(slice(pad, pad + hi))
+        sl_src.append(slice(0, hi))
+    xe[(slice(None), slice(None)) + tuple(sl_dst)] = x[(slice(None), slice(None)) + tuple(sl_src)]
+
+    # Step 2: U[k][c] = g x_n G over the N spatial axes -> [K][C][alpha^N]
+    U = mode_products(w, [G] * N, [2 + a for a in range(N)])
+
+    # Step 3: V for every tile t = (b, t_1..t_N) and channel.
+    tiles = list(itertools.product(range(n), *[range(ti) for ti in T]))
+    Tn = len(tiles)
+    V = np.empty((Tn, C) + (alpha,) * N, dtype=U.dtype)
+    for ti, t in enumerate(tiles):
+        sl = (t[0], slice(None)) + tuple(slice(tj * m, tj * m + alpha) for tj in t[1:])
+        d = xe[sl]                                           # [C][alpha..]
+        V[ti] = mode_products(d, [BT] * N, [1 + a for a in range(N)])
+
+    # Step 4: eq. (5), one [T x C] . [C x K] product per element xi.
+    Mt = np.empty((Tn, K) + (alpha,) * N, dtype=U.dtype)
+    for xi in itertools.product(range(alpha), repeat=N):
+        sel = (slice(None), slice(None)) + xi
+        Mt[sel] = np.dot(V[sel], U[sel].T)                   # [T][C] . [C][K]
+
+    # Step 5: inverse transform of every (tile, kernel).
+    S = mode_products(Mt, [AT] * N, [2 + a for a in range(N)])   # [T][K][m..]
+
+    # Step 6: stitch and crop.
+    full = tuple(ti * m for ti in T)
+    y = np.empty((n, K) + full, dtype=U.dtype)
+    for ti, t in enumerate(tiles):
+        sl = (t[0], slice(None)) + tuple(slice(tj * m, tj * m + m) for tj in t[1:])
+        y[sl] = S[ti]
+    y = y[(slice(None), slice(None)) + tuple(slice(0, yi) for yi in Y)]
+    if relu:
+        y = np.where(y > 0, y, zero)
+    return y

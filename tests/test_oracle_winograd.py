@@ -1,0 +1,127 @@
+"""Pins for the reference Winograd (oracle/winograd.py).
+
+* Exact agreement with the direct correlation on small integer inputs, by
+  brute force in rationals: N = 1, 2, 3, every supported (m, r) and point
+  set, ragged tiles, pad 0 and 1, several channels and kernels.
+* fp64 agreement with the direct correlation on random inputs.
+* Separability (eq. 3 and 4): the N-D data transform equals the Kronecker
+  product of the 1-D transform applied to the vectorised tile, and every axis
+  order gives the same tensor.
+* The 2-D special case of §3.2: A[(C g C^T) . (B d B^T)]A^T in matrix form.
+* The §2.2 worked example.
+"""
+import itertools
+import random
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from golden_io import read_kv
+from oracle.direct import direct_blas, direct_naive
+from oracle.metric import normalised_error
+from oracle.toomcook import PAPER_F43_POINTS
+from oracle.winograd import matrices, mode_products, winograd_forward
+
+EXACT_CASES = [
+    # N, m, r, points, n, C, K, X, pad
+    (1, 2, 3, None, 2, 2, 3, (9,), 0),
+    (1, 4, 3, None, 1, 3, 2, (11,), 1),
+    (1, 3, 2, None, 1, 2, 2, (8,), 0),
+    (2, 2, 3, None, 1, 2, 3, (5, 6), 1),
+    (2, 4, 3, None, 2, 2, 2, (7, 5), 1),
+    (2, 4, 3, PAPER_F43_POINTS, 1, 2, 2, (6, 7), 0),
+    (2, 2, 2, None, 1, 3, 2, (5, 4), 0),
+    (3, 2, 3, None, 1, 2, 2, (5, 4, 6), 1),
+    (3, 2, 3, None, 2, 3, 2, (4, 4, 4), 0),
+    (3, 4, 3, None, 1, 2, 2, (5, 6, 4), 1),
+    (3, 4, 3, PAPER_F43_POINTS, 1, 2, 2, (6, 6, 6), 0),
+]
+
+
+@pytest.mark.parametrize("N,m,r,points,n,C,K,X,pad", EXACT_CASES)
+def test_exact_equals_direct(N, m, r, points, n, C, K, X, pad):
+    rng = np.random.default_rng(abs(hash((N, m, r, X))) % 2**32)
+    x = rng.integers(-3, 4, size=(n, C) + X)
+    w = rng.integers(-3, 4, size=(K, C) + (r,) * N)
+    y_ref, _ = direct_naive(x, w, pad)
+    y = winograd_forward(x, w, m, r, pad=pad, points=points, exact=True)
+    assert y.shape == y_ref.shape
+    assert all(isinstance(v, Fraction) for v in y.reshape(-1)[:5])
+    assert all(Fraction(float(a)) == b for a, b in zip(y_ref.reshape(-1), y.reshape(-1)))
+    yr = winograd_forward(x, w, m, r, pad=pad, points=points, exact=True, relu=True)
+    assert all(Fraction(float(max(a, 0))) == b for a, b in zip(y_ref.reshape(-1), yr.reshape(-1)))
+
+
+@pytest.mark.parametrize("N,m,r,X,pad", [(3, 2, 3, (7, 9, 8), 1), (2, 4, 3, (13, 10), 1),
+                                          (3, 4, 3, (9, 7, 10), 1), (1, 4, 3, (30,), 0)])
+def test_fp64_close_to_direct(N, m, r, X, pad):
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((2, 5) + X).astype(np.float32)
+    w = rng.standard_normal((3, 5) + (r,) * N).astype(np.float32)
+    y_ref, den = direct_blas(x, w, pad)
+    y = winograd_forward(x, w, m, r, pad=pad)
+    assert normalised_error(y, y_ref, den)["max"] < 1e-12
+
+
+def _kron_all(M, N):
+    K = np.array([[1]], dtype=object)
+    for _ in range(N):
+        K = np.kron(K, M)
+    return K
+
+
+@pytest.mark.parametrize("N,m,r", [(2, 2, 3), (3, 2, 3), (2, 4, 3), (3, 4, 3)])
+def test_separability(N, m, r):
+    AT, BT, G = matrices(m, r, exact=True)
+    alpha = m + r - 1
+    rng = random.Random(N * 31 + m)
+    d = np.array([Fraction(rng.randint(-4, 4)) for _ in range(alpha ** N)],
+                 dtype=object).reshape((alpha,) * N)
+    ref = _kron_all(BT, N).dot(d.reshape(-1)).reshape((alpha,) * N)
+    for order in itertools.permutations(range(N)):
+        got = mode_products(d, [BT] * N, list(order))
+        assert (got == ref).all()
+    g = np.array([Fraction(rng.randint(-4, 4)) for _ in range(r ** N)],
+                 dtype=object).reshape((r,) * N)
+    refg = _kron_all(G, N).dot(g.reshape(-1)).reshape((alpha,) * N)
+    for order in itertools.permutations(range(N)):
+        assert (mode_products(g, [G] * N, list(order)) == refg).all()
+
+
+def test_2d_lavin_form():
+    AT, BT, G = matrices(4, 3, exact=True)
+    rng = random.Random(5)
+    d = np.array([[Fraction(rng.randint(-4, 4)) for _ in range(6)] for _ in range(6)], dtype=object)
+    g = np.array([[Fraction(rng.randint(-4, 4)) for _ in range(3)] for _ in range(3)], dtype=object)
+    # The paper's A, B, C are A^T, B^T, G here: S = A[(C g C^T) . (B d B^T)]A^T.
+    S = AT.dot((G.dot(g).dot(G.T)) * (BT.dot(d).dot(BT.T))).dot(AT.T)
+    y = winograd_forward(d.reshape(1, 1, 6, 6), g.reshape(1, 1, 3, 3), 4, 3, exact=True)
+    assert (y.reshape(4, 4) == S).all()
+    y2, _ = direct_naive(d.astype(float).reshape(1, 1, 6, 6), g.astype(float).reshape(1, 1, 3, 3))
+    assert (S.astype(float) == y2.reshape(4, 4)).all()
+
+
+def test_hand_example():
+    ex = read_kv("f23_hand_example.txt")
+    d = np.array(ex["d"], dtype=object).reshape(1, 1, 4)
+    g = np.array(ex["g"], dtype=object).reshape(1, 1, 3)
+    y = winograd_forward(d, g, 2, 3, exact=True)
+    assert list(y.reshape(-1)) == ex["s"]
+
+
+def test_output_extent_must_be_positive():
+    with pytest.raises(ValueError):
+        winograd_forward(np.zeros((1, 1, 2, 2)), np.zeros((1, 1, 3, 3)), 2, 3)
+
+
+def test_nonfinite_input_poisons_tile():
+    """A NaN in x poisons every output of each tile whose window holds it; the
+    direct correlation only poisons outputs whose receptive field holds it.
+    Finite inputs are required."""
+    x = np.ones((1, 1, 8, 8), np.float32)
+    x[0, 0, 4, 4] = np.nan
+    w = np.ones((1, 1, 3, 3), np.float32)
+    y = winograd_forward(x, w, 2, 3)
+    yd, _ = direct_blas(x, w, 0)
+    assert np.isnan(y).sum() >= np.isnan(yd).sum()
