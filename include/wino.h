@@ -1,0 +1,163 @@
+/*
+ * wino.h -- C ABI of libwino, an N-dimensional Winograd correlation forward
+ * F(m^N, r^N) for 2-D and 3-D ConvNet layers on AMD MI355X (gfx950).
+ *
+ * Method: Budden et al., "Deep Tensor Convolution on Multicores" (arXiv
+ * 1611.06565).  The layer is eq. (2) of §3.1 without bias: for every sample n,
+ * kernel k and output position o,
+ *
+ *     y[n][k][o] = f( sum_c sum_{p in [0,r)^N} w[k][c][p] * x~[n][c][o + p - pad] )
+ *
+ * a cross-correlation (no kernel flip) with f = identity or ReLU and x~ equal
+ * to x zero-extended outside [0, X).  It is computed by eq. (4),
+ *
+ *     S = [ (g x_n G) (.) (d x_n B^T) ] x_n A^T      over each axis n,
+ *
+ * on overlapping alpha^N input tiles stepping by m (§3.3, alpha = m + r - 1),
+ * with the element-wise product and the channel sum fused into one matrix
+ * product per transformed element xi (eq. 5 of §4.1):
+ *
+ *     M_xi [T x K] = V_xi [T x C] . U_xi [C x K],   xi in [0, alpha^N).
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ * - Tensors are dense, C-order, float32, with the shapes given below.  Device
+ *   pointers are allocated and owned by the caller and must be 16-byte
+ *   aligned.  The library never allocates device memory.
+ * - "stream" is a hipStream_t passed as void*; NULL means the null stream.
+ *   Device work is enqueued asynchronously on it; the call returns once the
+ *   launches are enqueued and the caller synchronises.
+ * - Argument and shape errors are reported synchronously with a negative
+ *   wino_status and leave every buffer untouched.  Launch failures return
+ *   WINO_EDEVICE.  Nothing aborts or throws across the ABI.
+ * - A plan is immutable after wino_plan returns; it may be used from several
+ *   host threads and streams at once provided each call gets its own
+ *   workspace and output buffers.
+ */
+#ifndef WINO_H_
+#define WINO_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  WINO_OK = 0,
+  WINO_EINVAL = -1,        /* bad argument, shape, pointer or alignment           */
+  WINO_EUNSUPPORTED = -2,  /* (N, m, r) has no kernel instantiation                */
+  WINO_EWORKSPACE = -3,    /* workspace smaller than wino_workspace_bytes          */
+  WINO_EDEVICE = -4        /* a HIP launch or query failed                         */
+} wino_status;
+
+typedef struct wino_plan_s wino_plan_t; /* opaque, immutable after creation */
+
+/* Apply max(0, .) to every output in the output-transform epilogue
+ * (the activation f of eq. 2). */
+#define WINO_RELU 1u
+
+typedef struct {
+  /* Symmetric zero padding per spatial axis, outer to inner.  0 is the
+   * paper's unpadded correlation with S = D - G + 1 outputs per axis (§2.2). */
+  int32_t pad[3];
+  /* alpha-1 distinct finite interpolation points (the point at infinity is
+   * implied), or NULL for the default set of (m, r).  Each point must be a
+   * rational with denominator below 2^20 whose nearest double is the value
+   * passed (1/3 may be passed as 1.0/3.0).  §2.2: the polynomial m(x) built
+   * from these points is the only input of transform synthesis. */
+  const double* points;
+  int32_t n_points;
+  uint32_t flags; /* WINO_RELU or 0 */
+} wino_opts;
+
+/* Plan summary (host-side numbers only). */
+typedef struct {
+  int32_t N, m, r, alpha;
+  int32_t n_xi;          /* alpha^N transformed elements                         */
+  int32_t C, K;
+  int32_t C_pad, K_pad;  /* C and K rounded up to the GEMM step / block           */
+  int64_t batch;
+  int64_t X[3], Y[3];    /* input and output extents per axis (unused axes 1)     */
+  int64_t tiles[3];      /* ceil(Y_i / m) tiles per axis                          */
+  int64_t T, T_pad;      /* tiles over the whole batch, and rounded to the block  */
+  int32_t block_tiles;   /* GEMM rows per work-group                             */
+  int32_t block_kernels; /* GEMM columns per work-group                          */
+  int32_t default_points;/* 1 when the transform constants are compiled in        */
+} wino_plan_desc;
+
+/* Build a plan for one layer.  §3.1-§3.3 and §4.1.
+ *   N      number of spatial axes: 2 or 3
+ *   m, r   output-tile and kernel extent per axis; supported (m, r) pairs are
+ *          (2, 3) and (4, 3) for N = 2 and 3 (alpha = 4 or 6)
+ *   C, K   input channels and kernels, each >= 1
+ *   dims   [batch, X_1 .. X_N], each >= 1; the output extent per axis
+ *          Y_i = X_i + 2 pad_i - r + 1 must be >= 1
+ *   opts   may be NULL (no padding, default points, no ReLU)
+ *   out    receives the plan; unchanged on error
+ * Generates A^T (m x alpha), B^T (alpha x alpha) and G (alpha x r) in exact
+ * rational arithmetic and rounds each entry once to float32.  No device work. */
+wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims,
+                      const wino_opts* opts, wino_plan_t** out);
+
+void wino_destroy(wino_plan_t* plan);
+
+/* Fill *desc from the plan.  Returns WINO_EINVAL for NULL arguments. */
+wino_status wino_plan_describe(const wino_plan_t* plan, wino_plan_desc* desc);
+
+/* Bytes of the transformed-filter buffer U, laid out as
+ * U[alpha^N][C_pad][K_pad] (float32; padding rows and columns are zero). */
+size_t wino_filter_bytes(const wino_plan_t* plan);
+
+/* Bytes of workspace wino_forward needs: the transformed input
+ * V[alpha^N][C_pad][T_pad] (float32). */
+size_t wino_workspace_bytes(const wino_plan_t* plan);
+
+/* out[0..N+1] = [batch, K, Y_1 .. Y_N]. */
+wino_status wino_output_dims(const wino_plan_t* plan, int64_t* out);
+
+/* Test hook: copy the transform matrices, each entry the exact rational
+ * rounded once to the nearest double, row-major: AT [m][alpha],
+ * BT [alpha][alpha], G [alpha][r].  Any pointer may be NULL. */
+wino_status wino_get_matrices(const wino_plan_t* plan, double* AT, double* BT, double* G);
+
+/* Kernel transform U = g x_1 G ... x_N G for every (k, c) (eq. 4; §3.3 caches
+ * it across forwards).
+ *   w  device, [K][C][r^N] float32
+ *   U  device, wino_filter_bytes(plan) bytes, fully overwritten */
+wino_status wino_transform_filter(const wino_plan_t* plan, const float* w, float* U, void* stream);
+
+/* Data transform V = d x_1 B^T ... x_N B^T of every tile and channel (eq. 4),
+ * written in the GEMM layout V[alpha^N][C_pad][T_pad] (§4.1's reshuffle).
+ *   x          device, [batch][C][X_1..X_N] float32
+ *   workspace  device, at least wino_workspace_bytes(plan) bytes */
+wino_status wino_transform_input(const wino_plan_t* plan, const float* x, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+/* Batched product M_xi = V_xi . U_xi over all xi (eq. 5) with the inverse
+ * transform S = M x_n A^T, tile stitching, cropping and the optional ReLU
+ * fused into its epilogue (eq. 4).  Reads the workspace written by
+ * wino_transform_input.
+ *   y  device, [batch][K][Y_1..Y_N] float32, fully overwritten */
+wino_status wino_gemm_inverse(const wino_plan_t* plan, const void* workspace, size_t workspace_bytes,
+                              const float* U, float* y, void* stream);
+
+/* wino_transform_input followed by wino_gemm_inverse on the same stream. */
+wino_status wino_forward(const wino_plan_t* plan, const float* x, const float* U, float* y,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* Max-pool with window = stride and floor rounding over the trailing 3 axes
+ * of x [lead][X_1][X_2][X_3] -> y [lead][X_1/p_1][X_2/p_2][X_3/p_3]
+ * (the C3D stack's pooling layers; not part of the Winograd method).
+ *   dims    [lead, X_1, X_2, X_3], window [p_1, p_2, p_3], each >= 1 */
+wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const float* x, float* y,
+                           void* stream);
+
+const char* wino_status_string(wino_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WINO_H_ */

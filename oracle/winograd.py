@@ -74,44 +74,66 @@ def tile_counts(X, pad, m, r):
     return Y, tuple(math.ceil(yi / m) for yi in Y)
 
 
-def winograd_forward(x, w, m, r, pad=0, points=None, relu=False, exact=False):
-    """Steps 1-6 above.  x: [n][C][X..], w: [K][C][r..] -> y [n][K][Y..]."""
-    N = np.ndim(x) - 2
-    alpha = m + r - 1
-    AT, BT, G = matrices(m, r, points, exact)
-    x = _as(x, exact)
-    w = _as(w, exact)
-    n, C = x.shape[:2]
-    K = w.shape[0]
+def _extend(x, pad, m, r, exact):
+    """Step 1: zero-extended input large enough for every tile window."""
     Y, T = tile_counts(x.shape[2:], pad, m, r)
     if any(yi < 1 for yi in Y):
         raise ValueError("output extent must be positive")
-
-    # Step 1: zero-extended input large enough for every tile window.
     ext = tuple(ti * m + r - 1 for ti in T)
     zero = Fraction(0) if exact else 0.0
-    xe = np.full((n, C) + ext, zero, dtype=object if exact else np.float64)
+    xe = np.full(x.shape[:2] + ext, zero, dtype=object if exact else np.float64)
     sl_dst, sl_src = [], []
     for xi, ei in zip(x.shape[2:], ext):
         hi = min(xi, ei - pad)
         sl_dst.append(slice(pad, pad + hi))
         sl_src.append(slice(0, hi))
     xe[(slice(None), slice(None)) + tuple(sl_dst)] = x[(slice(None), slice(None)) + tuple(sl_src)]
+    return xe, Y, T
 
-    # Step 2: U[k][c] = g x_n G over the N spatial axes -> [K][C][alpha^N]
-    U = mode_products(w, [G] * N, [2 + a for a in range(N)])
 
-    # Step 3: V for every tile t = (b, t_1..t_N) and channel.
+def transform_filter(w, m, r, points=None, exact=False):
+    """Step 2: U[k][c] = g x_1 G ... x_N G  ->  [K][C][alpha..alpha]."""
+    N = np.ndim(w) - 2
+    _, _, G = matrices(m, r, points, exact)
+    w = _as(w, exact)
+    return mode_products(w, [G] * N, [2 + a for a in range(N)])
+
+
+def transform_input(x, m, r, pad=0, points=None, exact=False):
+    """Steps 1 and 3: V[t][c] = d_t x_1 B^T ... x_N B^T for every tile t
+    (t linear over sample and tile grid, last axis fastest) -> [T][C][alpha..]."""
+    N = np.ndim(x) - 2
+    alpha = m + r - 1
+    _, BT, _ = matrices(m, r, points, exact)
+    x = _as(x, exact)
+    xe, Y, T = _extend(x, pad, m, r, exact)
+    n, C = x.shape[:2]
     tiles = list(itertools.product(range(n), *[range(ti) for ti in T]))
-    Tn = len(tiles)
-    V = np.empty((Tn, C) + (alpha,) * N, dtype=U.dtype)
+    V = np.empty((len(tiles), C) + (alpha,) * N, dtype=xe.dtype)
     for ti, t in enumerate(tiles):
         sl = (t[0], slice(None)) + tuple(slice(tj * m, tj * m + alpha) for tj in t[1:])
-        d = xe[sl]                                           # [C][alpha..]
-        V[ti] = mode_products(d, [BT] * N, [1 + a for a in range(N)])
+        V[ti] = mode_products(xe[sl], [BT] * N, [1 + a for a in range(N)])
+    return V
+
+
+def winograd_forward(x, w, m, r, pad=0, points=None, relu=False, exact=False):
+    """Steps 1-6 above.  x: [n][C][X..], w: [K][C][r..] -> y [n][K][Y..]."""
+    N = np.ndim(x) - 2
+    alpha = m + r - 1
+    AT, _, _ = matrices(m, r, points, exact)
+    x = _as(x, exact)
+    n = x.shape[0]
+    Y, T = tile_counts(x.shape[2:], pad, m, r)
+    if any(yi < 1 for yi in Y):
+        raise ValueError("output extent must be positive")
+    U = transform_filter(w, m, r, points, exact)               # step 2: [K][C][alpha^N]
+    V = transform_input(x, m, r, pad, points, exact)           # steps 1, 3: [T][C][alpha^N]
+    K = U.shape[0]
+    Tn = V.shape[0]
+    tiles = list(itertools.product(range(n), *[range(ti) for ti in T]))
 
     # Step 4: eq. (5), one [T x C] . [C x K] product per element xi.
-    Mt = np.empty((Tn, K) + (alpha,) * N, dtype=U.dtype)
+    Mt = np.empty((Tn, K) + (alpha,) * N, dtype=V.dtype)
     for xi in itertools.product(range(alpha), repeat=N):
         sel = (slice(None), slice(None)) + xi
         Mt[sel] = np.dot(V[sel], U[sel].T)                   # [T][C] . [C][K]
@@ -121,11 +143,12 @@ def winograd_forward(x, w, m, r, pad=0, points=None, relu=False, exact=False):
 
     # Step 6: stitch and crop.
     full = tuple(ti * m for ti in T)
-    y = np.empty((n, K) + full, dtype=U.dtype)
+    y = np.empty((n, K) + full, dtype=S.dtype)
     for ti, t in enumerate(tiles):
         sl = (t[0], slice(None)) + tuple(slice(tj * m, tj * m + m) for tj in t[1:])
         y[sl] = S[ti]
     y = y[(slice(None), slice(None)) + tuple(slice(0, yi) for yi in Y)]
     if relu:
+        zero = Fraction(0) if exact else 0.0
         y = np.where(y > 0, y, zero)
     return y

@@ -1,0 +1,337 @@
+// libwino: plan construction, argument checking and kernel dispatch behind the
+// C ABI declared in include/wino.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+
+#include "kernels.hpp"
+#include "synth.hpp"
+#include "wino.h"
+
+using namespace wino;
+
+struct wino_plan_s {
+  int N, m, r, alpha, nxi, C, K;
+  int C_pad, K_pad;
+  int64_t batch;
+  int64_t X[3], Y[3], tiles[3];
+  int32_t pad[3];
+  int64_t T, T_pad;
+  int blk, nw;
+  uint32_t flags;
+  bool const_mats;
+  double AT[kMaxAlpha][kMaxAlpha], BT[kMaxAlpha][kMaxAlpha], G[kMaxAlpha][kMaxAlpha];
+  FMats fm;
+};
+
+namespace {
+
+constexpr int64_t kMaxI32 = 0x7fffffff;
+
+int64_t round_up(int64_t v, int64_t b) { return (v + b - 1) / b * b; }
+
+// Nearest small rational to a double point, accepted only if it rounds back
+// to exactly the same double.
+bool rationalize(double v, Rat* out) {
+  if (!std::isfinite(v) || std::fabs(v) > 1048576.0) return false;
+  // continued-fraction convergents h/k
+  int64_t h0 = 0, h1 = 1, k0 = 1, k1 = 0;
+  double x = v;
+  for (int it = 0; it < 40; ++it) {
+    const double a = std::floor(x);
+    if (std::fabs(a) > 4.0e6) return false;
+    const int64_t ai = int64_t(a);
+    const int64_t h2 = ai * h1 + h0, k2 = ai * k1 + k0;
+    if (k2 > (int64_t(1) << 20) || k2 <= 0) break;
+    h0 = h1; h1 = h2; k0 = k1; k1 = k2;
+    if (double(h1) / double(k1) == v) {
+      *out = rat(h1, k1);
+      return true;
+    }
+    const double f = x - a;
+    if (f == 0.0) break;
+    x = 1.0 / f;
+  }
+  return false;
+}
+
+bool supported(int N, int m, int r) {
+  return (N == 2 || N == 3) && r == 3 && (m == 2 || m == 4);
+}
+
+wino_status launch_status() {
+  return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EDEVICE;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// ---------------------------------------------------------------- dispatch
+template <int N, int MM, int R, bool CONST>
+struct Launch {
+  static constexpr int A = MM + R - 1;
+  static constexpr int NXI = ipow(A, N);
+  static constexpr int BLK = NXI > 64 ? 16 : 32;
+  static constexpr int NW = 4;
+
+  static wino_status filter(const wino_plan_s& p, const float* w, float* U, hipStream_t s) {
+    FilterArgs a{};
+    a.uplane = int64_t(p.C_pad) * p.K_pad;
+    a.C = p.C; a.K = p.K; a.C_pad = p.C_pad; a.K_pad = p.K_pad;
+    const int64_t n = int64_t(p.C_pad) * p.K_pad;
+    const unsigned grid = unsigned((n + 255) / 256);
+    hipLaunchKernelGGL((k_filter<N, MM, R, CONST>), dim3(grid), dim3(256), 0, s, w, U, a, p.fm);
+    return launch_status();
+  }
+
+  static wino_status input(const wino_plan_s& p, const float* x, float* V, hipStream_t s) {
+    InputArgs a{};
+    a.vplane = int64_t(p.C_pad) * p.T_pad;
+    a.xstride_c = 1;
+    for (int i = 0; i < N; ++i) a.xstride_c *= p.X[i];
+    a.C = p.C; a.C_pad = p.C_pad;
+    a.T = int32_t(p.T); a.T_pad = int32_t(p.T_pad);
+    for (int i = 0; i < 3; ++i) {
+      a.X[i] = int32_t(p.X[i]); a.tiles[i] = int32_t(p.tiles[i]); a.pad[i] = p.pad[i];
+    }
+    dim3 grid(unsigned((p.T_pad + 255) / 256), unsigned(p.C_pad));
+    hipLaunchKernelGGL((k_input<N, MM, R, CONST>), grid, dim3(256), 0, s, x, V, a, p.fm);
+    return launch_status();
+  }
+
+  static wino_status gemm(const wino_plan_s& p, const float* V, const float* U, float* y,
+                          hipStream_t s) {
+    GemmArgs g{};
+    g.vplane = int64_t(p.C_pad) * p.T_pad;
+    g.uplane = int64_t(p.C_pad) * p.K_pad;
+    g.ystride_k = 1;
+    for (int i = 0; i < N; ++i) g.ystride_k *= p.Y[i];
+    g.T = int32_t(p.T); g.T_pad = int32_t(p.T_pad);
+    g.C_pad = p.C_pad; g.K = p.K; g.K_pad = p.K_pad;
+    g.nkb = p.K_pad / BLK;
+    const int64_t nb = (p.T_pad / BLK) * int64_t(g.nkb);
+    g.nblocks = int32_t(nb);
+    for (int i = 0; i < 3; ++i) { g.tiles[i] = int32_t(p.tiles[i]); g.Y[i] = int32_t(p.Y[i]); }
+    g.relu = (p.flags & WINO_RELU) ? 1 : 0;
+    hipLaunchKernelGGL((k_gemm_inv<N, MM, R, CONST, BLK, NW>), dim3(unsigned(nb)), dim3(NW * 64), 0,
+                       s, V, U, y, g, p.fm);
+    return launch_status();
+  }
+};
+
+template <template <int, int, int, bool> class L, typename F>
+wino_status dispatch(const wino_plan_s& p, F&& f) {
+#define WINO_CASE(N_, M_, R_)                                            \
+  if (p.N == N_ && p.m == M_ && p.r == R_)                               \
+    return p.const_mats ? f(L<N_, M_, R_, true>{}) : f(L<N_, M_, R_, false>{});
+  WINO_CASE(2, 2, 3)
+  WINO_CASE(3, 2, 3)
+  WINO_CASE(2, 4, 3)
+  WINO_CASE(3, 4, 3)
+#undef WINO_CASE
+  return WINO_EUNSUPPORTED;
+}
+
+int block_for(int N, int m, int r) {
+  const int a = m + r - 1;
+  int nxi = 1;
+  for (int i = 0; i < N; ++i) nxi *= a;
+  return nxi > 64 ? 16 : 32;
+}
+
+}  // namespace
+
+extern "C" {
+
+wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, const wino_opts* opts,
+                      wino_plan_t** out) {
+  if (out == nullptr || dims == nullptr) return WINO_EINVAL;
+  if (N < 1 || N > 3 || m < 1 || r < 1 || C < 1 || K < 1) return WINO_EINVAL;
+  if (m + r - 1 > kMaxAlpha) return WINO_EUNSUPPORTED;
+  if (!supported(N, m, r)) return WINO_EUNSUPPORTED;
+  wino_opts o{};
+  if (opts) o = *opts;
+  if (o.flags & ~WINO_RELU) return WINO_EINVAL;
+  const int alpha = m + r - 1;
+
+  wino_plan_s p{};
+  p.N = N; p.m = m; p.r = r; p.alpha = alpha; p.C = C; p.K = K;
+  p.flags = o.flags;
+  p.batch = dims[0];
+  if (p.batch < 1 || p.batch > kMaxI32) return WINO_EINVAL;
+  int64_t T = p.batch;
+  for (int i = 0; i < 3; ++i) { p.X[i] = 1; p.Y[i] = 1; p.tiles[i] = 1; p.pad[i] = 0; }
+  for (int i = 0; i < N; ++i) {
+    const int64_t X = dims[1 + i];
+    const int32_t pad = o.pad[i];
+    if (X < 1 || X > kMaxI32 || pad < 0 || pad > 1 << 20) return WINO_EINVAL;
+    const int64_t Y = X + 2 * int64_t(pad) - r + 1;
+    if (Y < 1) return WINO_EINVAL;
+    p.X[i] = X; p.pad[i] = pad; p.Y[i] = Y;
+    p.tiles[i] = (Y + m - 1) / m;
+    T *= p.tiles[i];
+    if (T > kMaxI32) return WINO_EINVAL;
+  }
+  p.T = T;
+  p.blk = block_for(N, m, r);
+  p.nw = 4;
+  p.T_pad = round_up(T, p.blk);
+  p.C_pad = int(round_up(C, p.blk == 32 ? 2 : 4));
+  p.K_pad = int(round_up(K, p.blk));
+  if (p.T_pad > kMaxI32) return WINO_EINVAL;
+  if (p.C_pad > 65535) return WINO_EINVAL;  // the input transform puts channels on grid.y
+  p.nxi = 1;
+  for (int i = 0; i < N; ++i) p.nxi *= alpha;
+  if ((p.T_pad / p.blk) * (p.K_pad / p.blk) > kMaxI32) return WINO_EINVAL;
+
+  // Transform synthesis (a1): exact rationals, one rounding per entry.
+  Rat pts[kMaxAlpha];
+  int np = alpha - 1;
+  bool defaults = false;
+  if (o.points == nullptr) {
+    if (o.n_points != 0) return WINO_EINVAL;
+    int cnt = 0;
+    const Rat* d = default_points(m, r, &cnt);
+    if (d == nullptr || cnt != np) return WINO_EUNSUPPORTED;
+    for (int i = 0; i < np; ++i) pts[i] = d[i];
+    defaults = true;
+  } else {
+    if (o.n_points != np) return WINO_EINVAL;
+    for (int i = 0; i < np; ++i)
+      if (!rationalize(o.points[i], &pts[i])) return WINO_EINVAL;
+    int cnt = 0;
+    const Rat* d = default_points(m, r, &cnt);
+    defaults = d != nullptr && cnt == np;
+    for (int i = 0; defaults && i < np; ++i) defaults = eq(d[i], pts[i]);
+  }
+  const RatMats R = synthesize(m, r, pts);
+  if (!R.ok) return WINO_EINVAL;
+  for (int i = 0; i < kMaxAlpha; ++i)
+    for (int j = 0; j < kMaxAlpha; ++j) {
+      p.AT[i][j] = to_f64(R.AT[i][j]);
+      p.BT[i][j] = to_f64(R.BT[i][j]);
+      p.G[i][j] = to_f64(R.G[i][j]);
+    }
+  p.fm = to_fmats(R);
+  p.const_mats = defaults;
+
+  wino_plan_s* h = new (std::nothrow) wino_plan_s(p);
+  if (h == nullptr) return WINO_EINVAL;
+  *out = h;
+  return WINO_OK;
+}
+
+void wino_destroy(wino_plan_t* plan) { delete plan; }
+
+wino_status wino_plan_describe(const wino_plan_t* p, wino_plan_desc* d) {
+  if (p == nullptr || d == nullptr) return WINO_EINVAL;
+  std::memset(d, 0, sizeof(*d));
+  d->N = p->N; d->m = p->m; d->r = p->r; d->alpha = p->alpha; d->n_xi = p->nxi;
+  d->C = p->C; d->K = p->K; d->C_pad = p->C_pad; d->K_pad = p->K_pad;
+  d->batch = p->batch;
+  for (int i = 0; i < 3; ++i) { d->X[i] = p->X[i]; d->Y[i] = p->Y[i]; d->tiles[i] = p->tiles[i]; }
+  d->T = p->T; d->T_pad = p->T_pad;
+  d->block_tiles = p->blk; d->block_kernels = p->blk;
+  d->default_points = p->const_mats ? 1 : 0;
+  return WINO_OK;
+}
+
+size_t wino_filter_bytes(const wino_plan_t* p) {
+  return p ? size_t(p->nxi) * size_t(p->C_pad) * size_t(p->K_pad) * sizeof(float) : 0;
+}
+
+size_t wino_workspace_bytes(const wino_plan_t* p) {
+  return p ? size_t(p->nxi) * size_t(p->C_pad) * size_t(p->T_pad) * sizeof(float) : 0;
+}
+
+wino_status wino_output_dims(const wino_plan_t* p, int64_t* out) {
+  if (p == nullptr || out == nullptr) return WINO_EINVAL;
+  out[0] = p->batch;
+  out[1] = p->K;
+  for (int i = 0; i < p->N; ++i) out[2 + i] = p->Y[i];
+  return WINO_OK;
+}
+
+wino_status wino_get_matrices(const wino_plan_t* p, double* AT, double* BT, double* G) {
+  if (p == nullptr) return WINO_EINVAL;
+  const int a = p->alpha;
+  if (AT) for (int i = 0; i < p->m; ++i) for (int j = 0; j < a; ++j) AT[i * a + j] = p->AT[i][j];
+  if (BT) for (int i = 0; i < a; ++i) for (int j = 0; j < a; ++j) BT[i * a + j] = p->BT[i][j];
+  if (G) for (int i = 0; i < a; ++i) for (int j = 0; j < p->r; ++j) G[i * p->r + j] = p->G[i][j];
+  return WINO_OK;
+}
+
+wino_status wino_transform_filter(const wino_plan_t* p, const float* w, float* U, void* stream) {
+  if (p == nullptr || w == nullptr || U == nullptr) return WINO_EINVAL;
+  if (!aligned16(w) || !aligned16(U)) return WINO_EINVAL;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::filter(*p, w, U, s); });
+}
+
+wino_status wino_transform_input(const wino_plan_t* p, const float* x, void* ws, size_t ws_bytes,
+                                 void* stream) {
+  if (p == nullptr || x == nullptr || ws == nullptr) return WINO_EINVAL;
+  if (!aligned16(x) || !aligned16(ws)) return WINO_EINVAL;
+  if (ws_bytes < wino_workspace_bytes(p)) return WINO_EWORKSPACE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  float* V = static_cast<float*>(ws);
+  return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::input(*p, x, V, s); });
+}
+
+wino_status wino_gemm_inverse(const wino_plan_t* p, const void* ws, size_t ws_bytes, const float* U,
+                              float* y, void* stream) {
+  if (p == nullptr || ws == nullptr || U == nullptr || y == nullptr) return WINO_EINVAL;
+  if (!aligned16(ws) || !aligned16(U) || !aligned16(y)) return WINO_EINVAL;
+  if (ws_bytes < wino_workspace_bytes(p)) return WINO_EWORKSPACE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const float* V = static_cast<const float*>(ws);
+  return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::gemm(*p, V, U, y, s); });
+}
+
+wino_status wino_forward(const wino_plan_t* p, const float* x, const float* U, float* y, void* ws,
+                         size_t ws_bytes, void* stream) {
+  if (p == nullptr || x == nullptr || U == nullptr || y == nullptr || ws == nullptr)
+    return WINO_EINVAL;
+  if (!aligned16(x) || !aligned16(U) || !aligned16(y) || !aligned16(ws)) return WINO_EINVAL;
+  if (ws_bytes < wino_workspace_bytes(p)) return WINO_EWORKSPACE;
+  wino_status st = wino_transform_input(p, x, ws, ws_bytes, stream);
+  if (st != WINO_OK) return st;
+  return wino_gemm_inverse(p, ws, ws_bytes, U, y, stream);
+}
+
+wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const float* x, float* y,
+                           void* stream) {
+  if (dims == nullptr || window == nullptr || x == nullptr || y == nullptr) return WINO_EINVAL;
+  if (!aligned16(x) || !aligned16(y)) return WINO_EINVAL;
+  PoolArgs a{};
+  a.lead = dims[0];
+  if (a.lead < 1) return WINO_EINVAL;
+  int64_t total = a.lead;
+  for (int i = 0; i < 3; ++i) {
+    if (dims[1 + i] < 1 || dims[1 + i] > kMaxI32 || window[i] < 1) return WINO_EINVAL;
+    a.X[i] = int32_t(dims[1 + i]);
+    a.p[i] = window[i];
+    a.Y[i] = a.X[i] / a.p[i];
+    if (a.Y[i] < 1) return WINO_EINVAL;
+    total *= a.Y[i];
+  }
+  a.total = total;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(k_maxpool3d, dim3(unsigned((total + 255) / 256)), dim3(256), 0, s, x, y, a);
+  return launch_status();
+}
+
+const char* wino_status_string(wino_status s) {
+  switch (s) {
+    case WINO_OK: return "ok";
+    case WINO_EINVAL: return "invalid argument";
+    case WINO_EUNSUPPORTED: return "unsupported (N, m, r)";
+    case WINO_EWORKSPACE: return "workspace too small";
+    case WINO_EDEVICE: return "device launch failed";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

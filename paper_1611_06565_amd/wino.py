@@ -1,0 +1,269 @@
+"""ctypes binding of libwino (include/wino.h).
+
+Argument marshalling only: every step of the forward runs in the library's
+HIP kernels.  Device buffers are torch CUDA (HIP) tensors; calls are enqueued
+on torch's current stream.  If the library is not built, every entry point
+raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from fractions import Fraction
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+HEADER = os.path.join(os.path.dirname(HERE), "include", "wino.h")
+
+WINO_RELU = 1
+_STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported (N, m, r)",
+           -3: "workspace too small", -4: "device launch failed"}
+
+
+class WinoError(RuntimeError):
+    def __init__(self, status, what=""):
+        self.status = int(status)
+        super().__init__(f"{what}: {_STATUS.get(self.status, 'unknown')} ({self.status})")
+
+
+class _Opts(ctypes.Structure):
+    _fields_ = [("pad", ctypes.c_int32 * 3), ("points", ctypes.POINTER(ctypes.c_double)),
+                ("n_points", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int32), ("m", ctypes.c_int32), ("r", ctypes.c_int32),
+                ("alpha", ctypes.c_int32), ("n_xi", ctypes.c_int32),
+                ("C", ctypes.c_int32), ("K", ctypes.c_int32),
+                ("C_pad", ctypes.c_int32), ("K_pad", ctypes.c_int32),
+                ("batch", ctypes.c_int64),
+                ("X", ctypes.c_int64 * 3), ("Y", ctypes.c_int64 * 3), ("tiles", ctypes.c_int64 * 3),
+                ("T", ctypes.c_int64), ("T_pad", ctypes.c_int64),
+                ("block_tiles", ctypes.c_int32), ("block_kernels", ctypes.c_int32),
+                ("default_points", ctypes.c_int32)]
+
+
+_LIB = None
+
+
+def library_path():
+    return os.path.join(HERE, "libwino.so")
+
+
+def lib():
+    """Load libwino.so (raises if it has not been built)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = library_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run __graft_entry__.build() first")
+    L = ctypes.CDLL(path)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    P_i64 = ctypes.POINTER(i64)
+    P_dbl = ctypes.POINTER(ctypes.c_double)
+    sig = {
+        "wino_plan": (i32, [i32, i32, i32, i32, i32, P_i64, ctypes.POINTER(_Opts), ctypes.POINTER(vp)]),
+        "wino_destroy": (None, [vp]),
+        "wino_plan_describe": (i32, [vp, ctypes.POINTER(_Desc)]),
+        "wino_filter_bytes": (sz, [vp]),
+        "wino_workspace_bytes": (sz, [vp]),
+        "wino_output_dims": (i32, [vp, P_i64]),
+        "wino_get_matrices": (i32, [vp, P_dbl, P_dbl, P_dbl]),
+        "wino_transform_filter": (i32, [vp, vp, vp, vp]),
+        "wino_transform_input": (i32, [vp, vp, vp, sz, vp]),
+        "wino_gemm_inverse": (i32, [vp, vp, sz, vp, vp, vp]),
+        "wino_forward": (i32, [vp, vp, vp, vp, vp, sz, vp]),
+        "wino_maxpool3d": (i32, [P_i64, ctypes.POINTER(i32), vp, vp, vp]),
+        "wino_status_string": (ctypes.c_char_p, [i32]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _LIB = L
+    return L
+
+
+def describe_header_symbols(path=HEADER):
+    """Names of the functions include/wino.h declares."""
+    with open(path) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w]+\s*\*?\s*(wino_\w+)\s*\(", text, flags=re.M)))
+
+
+def _check(st, what):
+    if st != 0:
+        raise WinoError(st, what)
+
+
+def _stream():
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev_ptr(t, what, dtype=None):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{what} must be a CUDA (HIP) tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{what} must be {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _point(p):
+    if isinstance(p, (Fraction, str)):
+        return float(Fraction(p))
+    return float(p)
+
+
+class Plan:
+    """One planned layer: Plan(N, m, r, C, K, dims=[batch, X_1..X_N], pad, points, relu)."""
+
+    def __init__(self, N, m, r, C, K, dims, pad=0, points=None, relu=False):
+        L = lib()
+        dims = [int(d) for d in dims]
+        if len(dims) != N + 1:
+            raise ValueError("dims must be [batch, X_1..X_N]")
+        opts = _Opts()
+        pads = [pad] * N if isinstance(pad, int) else list(pad)
+        for i, p in enumerate(pads):
+            opts.pad[i] = int(p)
+        self._pts = None
+        if points is not None:
+            self._pts = (ctypes.c_double * len(points))(*[_point(p) for p in points])
+            opts.points = ctypes.cast(self._pts, ctypes.POINTER(ctypes.c_double))
+            opts.n_points = len(points)
+        opts.flags = WINO_RELU if relu else 0
+        arr = (ctypes.c_int64 * len(dims))(*dims)
+        h = ctypes.c_void_p()
+        _check(L.wino_plan(N, m, r, C, K, arr, ctypes.byref(opts), ctypes.byref(h)), "wino_plan")
+        self._h = h
+        self._L = L
+        d = _Desc()
+        _check(L.wino_plan_describe(h, ctypes.byref(d)), "wino_plan_describe")
+        self.desc = {f: (list(getattr(d, f)) if f in ("X", "Y", "tiles") else getattr(d, f))
+                     for f, _ in _Desc._fields_}
+        self.N, self.m, self.r, self.C, self.K = N, m, r, C, K
+        self.relu = relu
+        out = (ctypes.c_int64 * (N + 2))()
+        _check(L.wino_output_dims(h, out), "wino_output_dims")
+        self.output_shape = tuple(int(v) for v in out)
+        self.input_shape = (dims[0], C) + tuple(dims[1:])
+        self.weight_shape = (K, C) + (r,) * N
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            self._L.wino_destroy(h)
+            self._h = None
+
+    @property
+    def handle(self):
+        return self._h
+
+    @property
+    def filter_bytes(self):
+        return int(self._L.wino_filter_bytes(self._h))
+
+    @property
+    def workspace_bytes(self):
+        return int(self._L.wino_workspace_bytes(self._h))
+
+    def matrices(self):
+        a, m, r = self.desc["alpha"], self.m, self.r
+        AT = np.zeros((m, a))
+        BT = np.zeros((a, a))
+        G = np.zeros((a, r))
+        P = ctypes.POINTER(ctypes.c_double)
+        _check(self._L.wino_get_matrices(self._h, AT.ctypes.data_as(P), BT.ctypes.data_as(P),
+                                         G.ctypes.data_as(P)), "wino_get_matrices")
+        return AT, BT, G
+
+    # ---- device calls -------------------------------------------------
+    def _check_shape(self, t, shape, what):
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{what} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+    def new_filter(self):
+        import torch
+        d = self.desc
+        return torch.empty((d["n_xi"], d["C_pad"], d["K_pad"]), dtype=torch.float32, device="cuda")
+
+    def new_workspace(self):
+        import torch
+        return torch.empty(self.workspace_bytes // 4, dtype=torch.float32, device="cuda")
+
+    def new_output(self):
+        import torch
+        return torch.empty(self.output_shape, dtype=torch.float32, device="cuda")
+
+    def transform_filter(self, w, U=None):
+        import torch
+        self._check_shape(w, self.weight_shape, "w")
+        if U is None:
+            U = self.new_filter()
+        if U.numel() * 4 < self.filter_bytes:
+            raise ValueError("U is too small")
+        _check(self._L.wino_transform_filter(self._h, _dev_ptr(w, "w", torch.float32),
+                                             _dev_ptr(U, "U", torch.float32), _stream()),
+               "wino_transform_filter")
+        return U
+
+    def transform_input(self, x, ws=None):
+        import torch
+        self._check_shape(x, self.input_shape, "x")
+        if ws is None:
+            ws = self.new_workspace()
+        _check(self._L.wino_transform_input(self._h, _dev_ptr(x, "x", torch.float32),
+                                            _dev_ptr(ws, "workspace"), ws.numel() * ws.element_size(),
+                                            _stream()), "wino_transform_input")
+        return ws
+
+    def gemm_inverse(self, ws, U, y=None):
+        import torch
+        if y is None:
+            y = self.new_output()
+        self._check_shape(y, self.output_shape, "y")
+        _check(self._L.wino_gemm_inverse(self._h, _dev_ptr(ws, "workspace"),
+                                         ws.numel() * ws.element_size(),
+                                         _dev_ptr(U, "U", torch.float32),
+                                         _dev_ptr(y, "y", torch.float32), _stream()),
+               "wino_gemm_inverse")
+        return y
+
+    def forward(self, x, U, y=None, workspace=None):
+        import torch
+        self._check_shape(x, self.input_shape, "x")
+        if y is None:
+            y = self.new_output()
+        self._check_shape(y, self.output_shape, "y")
+        if workspace is None:
+            workspace = self.new_workspace()
+        _check(self._L.wino_forward(self._h, _dev_ptr(x, "x", torch.float32),
+                                    _dev_ptr(U, "U", torch.float32), _dev_ptr(y, "y", torch.float32),
+                                    _dev_ptr(workspace, "workspace"),
+                                    workspace.numel() * workspace.element_size(), _stream()),
+               "wino_forward")
+        return y
+
+
+def maxpool3d(x, window, y=None):
+    """Max-pool over the trailing three axes with window = stride, floor rounding."""
+    import torch
+    L = lib()
+    lead = int(np.prod(x.shape[:-3])) if x.dim() > 3 else 1
+    X = list(x.shape[-3:])
+    Y = [xi // pi for xi, pi in zip(X, window)]
+    if y is None:
+        y = torch.empty(tuple(x.shape[:-3]) + tuple(Y), dtype=torch.float32, device=x.device)
+    dims = (ctypes.c_int64 * 4)(lead, *X)
+    win = (ctypes.c_int32 * 3)(*[int(p) for p in window])
+    _check(L.wino_maxpool3d(dims, win, _dev_ptr(x, "x", torch.float32), _dev_ptr(y, "y", torch.float32),
+                            _stream()), "wino_maxpool3d")
+    return y

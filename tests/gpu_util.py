@@ -1,0 +1,90 @@
+"""Helpers for the GPU parity tests: run a layer through the C ABI and compare
+with the fp64 oracle on the same seeded inputs."""
+import sys
+
+import numpy as np
+
+from oracle.direct import direct_blas, direct_sampled
+from oracle.metric import normalised_error
+
+TOL = {2: 1e-5, 4: 1e-4}   # normalised max error per output-tile extent m
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def require_gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    import paper_1611_06565_amd.wino as wino
+    wino.lib()  # raises if the library is not built
+    return torch
+
+
+def run_layer(spec, x, w, points=None, guard=0):
+    """Plan, transform the filter and run the forward.  Returns (y numpy, plan).
+
+    With guard > 0 the output is a view inside a larger buffer whose guard
+    bands hold a sentinel; the bands are checked afterwards."""
+    torch = require_gpu()
+    from paper_1611_06565_amd.wino import Plan
+    log(f"[gpu] {spec.name} N={spec.N} m={spec.m} C={spec.C} K={spec.K} X={spec.X} "
+        f"batch={spec.batch} pad={spec.pad} points={points}")
+    plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X),
+                pad=spec.pad, points=points, relu=spec.relu)
+    xd = torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    wd = torch.from_numpy(np.ascontiguousarray(w)).cuda()
+    U = plan.transform_filter(wd)
+    ws = plan.new_workspace()
+    n_out = int(np.prod(plan.output_shape))
+    if guard:
+        buf = torch.full((n_out + 2 * guard,), 12345.5, dtype=torch.float32, device="cuda")
+        y = buf[guard:guard + n_out].view(plan.output_shape)
+    else:
+        y = plan.new_output()
+    plan.forward(xd, U, y=y, workspace=ws)
+    torch.cuda.synchronize()
+    if guard:
+        b = buf.cpu().numpy()
+        assert np.all(b[:guard] == 12345.5) and np.all(b[-guard:] == 12345.5), "guard band written"
+    return y.cpu().numpy(), plan
+
+
+def check_full(spec, y, x, w):
+    y_ref, den = direct_blas(x, w, spec.pad, relu=spec.relu)
+    err = normalised_error(y, y_ref, den)
+    log(f"  max err {err['max']:.3e} p99.99 {err['p9999']:.3e} at {err['argmax']} "
+        f"clamped {err['clamped']}")
+    assert err["nonfinite"] == 0
+    assert err["max"] <= TOL[spec.m], err
+    return err
+
+
+def sample_coords(shape, n, rng, edges=True):
+    """n uniform output coordinates plus the corners of every axis."""
+    coords = [rng.integers(0, s, size=n) for s in shape]
+    out = np.stack(coords, axis=1)
+    if edges:
+        corners = []
+        for b in (0, shape[0] - 1):
+            for k in (0, shape[1] - 1):
+                for lo in range(2 ** (len(shape) - 2)):
+                    c = [b, k] + [(shape[2 + a] - 1) if (lo >> a) & 1 else 0
+                                  for a in range(len(shape) - 2)]
+                    corners.append(c)
+        out = np.concatenate([out, np.array(corners)], axis=0)
+    return out
+
+
+def check_sampled(spec, y, x, w, n=4000, seed=0):
+    rng = np.random.default_rng(seed)
+    coords = sample_coords(y.shape, n, rng)
+    ys, dens = direct_sampled(x, w, spec.pad, coords, relu=spec.relu)
+    got = y[tuple(coords.T)]
+    err = normalised_error(got, ys, dens)
+    log(f"  sampled {len(coords)}: max err {err['max']:.3e} p99.99 {err['p9999']:.3e}")
+    assert np.all(np.isfinite(y[tuple(coords.T)]))
+    assert err["max"] <= TOL[spec.m], err
+    return err

@@ -1,0 +1,134 @@
+"""Host-side checks of the C ABI (no GPU needed: no device work is launched).
+
+* libwino.so loads and exports every function include/wino.h declares.
+* wino_plan validates its arguments and reports sizes and output extents.
+* The C++ transform synthesis equals the oracle's exact synthesis rounded
+  once to double, bit for bit (default points, the paper's F(4,3) points and
+  other caller-chosen sets).
+* Device entry points reject bad pointers and short workspaces synchronously,
+  before any launch.
+"""
+import ctypes
+import math
+
+import numpy as np
+import pytest
+
+from oracle.toomcook import PAPER_F43_POINTS, default_points, winograd_matrices
+
+wino = pytest.importorskip("paper_1611_06565_amd.wino")
+
+
+@pytest.fixture(scope="module")
+def L():
+    return wino.lib()
+
+
+def test_exports_every_header_symbol(L):
+    names = wino.describe_header_symbols()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings(L):
+    assert L.wino_status_string(0) == b"ok"
+    assert L.wino_status_string(-3) == b"workspace too small"
+
+
+def _plan_status(L, N, m, r, C, K, dims, pad=None, points=None, flags=0):
+    opts = wino._Opts()
+    if pad is not None:
+        for i, p in enumerate(pad):
+            opts.pad[i] = p
+    keep = None
+    if points is not None:
+        keep = (ctypes.c_double * len(points))(*points)
+        opts.points = ctypes.cast(keep, ctypes.POINTER(ctypes.c_double))
+        opts.n_points = len(points)
+    opts.flags = flags
+    arr = (ctypes.c_int64 * len(dims))(*dims)
+    h = ctypes.c_void_p()
+    st = L.wino_plan(N, m, r, C, K, arr, ctypes.byref(opts), ctypes.byref(h))
+    if st == 0:
+        L.wino_destroy(h)
+    return st
+
+
+def test_plan_validation(L):
+    ok = _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8])
+    assert ok == 0
+    assert _plan_status(L, 4, 2, 3, 4, 4, [1, 8, 8, 8, 8]) == -1      # N out of range
+    assert _plan_status(L, 3, 3, 3, 4, 4, [1, 8, 8, 8]) == -2         # no kernel for m = 3
+    assert _plan_status(L, 3, 2, 5, 4, 4, [1, 8, 8, 8]) == -2         # r = 5
+    assert _plan_status(L, 3, 2, 3, 0, 4, [1, 8, 8, 8]) == -1         # C = 0
+    assert _plan_status(L, 3, 2, 3, 4, 0, [1, 8, 8, 8]) == -1         # K = 0
+    assert _plan_status(L, 3, 2, 3, 4, 4, [0, 8, 8, 8]) == -1         # batch 0
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 2, 8, 8]) == -1         # Y < 1 unpadded
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 2, 8, 8], pad=[1, 0, 0]) == 0
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], pad=[-1, 0, 0]) == -1
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1, 1]) == -1   # duplicate
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1]) == -1      # count
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1, math.nan]) == -1
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1, math.pi]) == -1
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=2) == -1
+    h = ctypes.c_void_p()
+    assert L.wino_plan(3, 2, 3, 4, 4, None, None, ctypes.byref(h)) == -1
+
+
+def test_sizes_and_dims():
+    p = wino.Plan(3, 2, 3, 64, 128, [8, 16, 56, 56], pad=1)
+    d = p.desc
+    assert d["tiles"] == [8, 28, 28] and d["T"] == 8 * 8 * 28 * 28
+    assert d["n_xi"] == 64 and d["alpha"] == 4
+    assert p.filter_bytes == 4 * 64 * d["C_pad"] * d["K_pad"]
+    assert p.workspace_bytes == 4 * 64 * d["C_pad"] * d["T_pad"]
+    assert p.output_shape == (8, 128, 16, 56, 56)
+    q = wino.Plan(2, 4, 3, 3, 5, [2, 9, 10], pad=0)
+    assert q.output_shape == (2, 5, 7, 8)
+    assert q.desc["tiles"][:2] == [2, 2]
+    assert q.desc["T_pad"] % q.desc["block_tiles"] == 0
+    assert q.desc["K_pad"] % q.desc["block_kernels"] == 0
+    assert q.desc["C_pad"] >= 3
+
+
+def _oracle_f64(m, r, pts):
+    AT, BT, G = winograd_matrices(m, r, pts)
+    f = lambda M: np.array([[float(c) for c in row] for row in M])
+    return f(AT), f(BT), f(G)
+
+
+@pytest.mark.parametrize("N,m,pts", [
+    (3, 2, None), (2, 2, None), (3, 4, None), (2, 4, None),
+    (3, 4, PAPER_F43_POINTS), (2, 4, PAPER_F43_POINTS),
+    (3, 2, (1, 2, 3)), (2, 4, (0, -1, 1, 0.5, -2)), (3, 2, (0, 0.5, -0.5)),
+])
+def test_matrices_bitwise_equal_oracle(N, m, pts):
+    plan = wino.Plan(N, m, 3, 2, 2, [1] + [9] * N, pad=1, points=pts)
+    AT, BT, G = plan.matrices()
+    oAT, oBT, oG = _oracle_f64(m, 3, pts if pts is not None else default_points(m, 3))
+    for a, b in ((AT, oAT), (BT, oBT), (G, oG)):
+        assert a.shape == b.shape
+        assert np.array_equal(a.view(np.uint64), b.view(np.uint64))
+    assert plan.desc["default_points"] == (1 if pts is None else 0)
+
+
+def test_explicit_default_points_use_compiled_constants():
+    plan = wino.Plan(3, 2, 3, 2, 2, [1, 8, 8, 8], points=(0, 1, -1))
+    assert plan.desc["default_points"] == 1
+
+
+def test_device_calls_reject_bad_arguments(L):
+    p = wino.Plan(3, 2, 3, 4, 4, [1, 8, 8, 8])
+    need = p.workspace_bytes
+    vp = ctypes.c_void_p
+    # NULL pointers and misalignment are rejected before any launch.
+    assert L.wino_transform_filter(p.handle, None, vp(4096), None) == -1
+    assert L.wino_transform_filter(p.handle, vp(4096 + 4), vp(4096), None) == -1
+    assert L.wino_transform_input(p.handle, vp(4096), vp(8192), need - 4, None) == -3
+    assert L.wino_gemm_inverse(p.handle, vp(4096), need - 4, vp(8192), vp(16384), None) == -3
+    assert L.wino_forward(p.handle, vp(4096), vp(8192), vp(16384), vp(32768), 0, None) == -3
+    assert L.wino_forward(p.handle, vp(4096), vp(8192), vp(16384), None, need, None) == -1
+    dims = (ctypes.c_int64 * 4)(1, 4, 4, 4)
+    win = (ctypes.c_int32 * 3)(2, 2, 8)
+    assert L.wino_maxpool3d(dims, win, vp(4096), vp(8192), None) == -1   # 4 // 8 == 0

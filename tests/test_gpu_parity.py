@@ -1,0 +1,177 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Bar: normalised max error |y - y_ref| / sum|w||x| <= 1e-5 for m = 2 and
+<= 1e-4 for m = 4, against the direct correlation of eq. (2).  Small layers are
+compared on every output; full-size layers (in the launch configuration the
+bench times) on sampled outputs computed one receptive field at a time.
+Integer inputs with F(2^N, 3^N) must match the integer correlation bit for bit
+(every intermediate is a small dyadic rational, exact in fp32).
+"""
+import numpy as np
+import pytest
+
+from gpu_util import check_full, check_sampled, log, require_gpu, run_layer
+from oracle.direct import direct_blas
+from oracle.pool import maxpool
+from oracle.toomcook import PAPER_F43_POINTS
+from oracle.winograd import transform_filter as o_filter
+from oracle.winograd import transform_input as o_input
+from workloads import C3D_STACK, CONFIGS, LayerSpec, draw_layer, draw_stack
+
+pytestmark = pytest.mark.gpu
+
+SMALL = [
+    CONFIGS[1],
+    LayerSpec("f2x3_3d_ragged", N=3, m=2, r=3, batch=2, C=24, K=40, X=(6, 13, 15), pad=1,
+              x_dist="relu_normal", w_dist="he"),
+    LayerSpec("f4x3_2d_ragged", N=2, m=4, r=3, batch=3, C=36, K=70, X=(17, 23), pad=1,
+              x_dist="relu_normal", w_dist="he"),
+    LayerSpec("f4x3_3d_ragged", N=3, m=4, r=3, batch=1, C=20, K=24, X=(13, 11, 17), pad=1,
+              x_dist="uniform", w_dist="he"),
+    LayerSpec("f2x3_2d_ragged", N=2, m=2, r=3, batch=2, C=10, K=33, X=(19, 14), pad=1,
+              x_dist="normal", w_dist="normal"),
+    LayerSpec("f2x3_3d_relu", N=3, m=2, r=3, batch=1, C=16, K=48, X=(9, 10, 11), pad=1,
+              x_dist="normal", w_dist="he", relu=True),
+    LayerSpec("f4x3_3d_relu", N=3, m=4, r=3, batch=2, C=8, K=16, X=(7, 9, 6), pad=1,
+              x_dist="normal", w_dist="he", relu=True),
+]
+
+EDGE = [
+    LayerSpec("one_output", N=3, m=2, r=3, batch=1, C=3, K=2, X=(3, 3, 3), pad=0),
+    LayerSpec("one_output_m4", N=3, m=4, r=3, batch=1, C=3, K=2, X=(3, 3, 3), pad=0),
+    LayerSpec("c1k1", N=3, m=2, r=3, batch=1, C=1, K=1, X=(5, 7, 4), pad=1),
+    LayerSpec("c1k1_2d_m4", N=2, m=4, r=3, batch=1, C=1, K=1, X=(5, 7), pad=1),
+    LayerSpec("wide_k", N=3, m=2, r=3, batch=1, C=2, K=130, X=(4, 5, 6), pad=1),
+    LayerSpec("pad2", N=3, m=2, r=3, batch=1, C=5, K=7, X=(5, 6, 7), pad=2),
+    LayerSpec("pad2_m4_2d", N=2, m=4, r=3, batch=2, C=5, K=7, X=(5, 6), pad=2),
+    LayerSpec("batch5", N=3, m=2, r=3, batch=5, C=6, K=9, X=(3, 5, 4), pad=1),
+    LayerSpec("tiny_2d", N=2, m=2, r=3, batch=1, C=3, K=3, X=(3, 4), pad=0),
+    LayerSpec("odd_c_2d", N=2, m=4, r=3, batch=2, C=7, K=33, X=(12, 9), pad=1),
+    LayerSpec("odd_c_3d_m4", N=3, m=4, r=3, batch=1, C=5, K=17, X=(8, 6, 10), pad=1),
+]
+
+
+@pytest.mark.parametrize("spec", SMALL + EDGE, ids=lambda s: s.name)
+def test_small_layers_full_output(spec):
+    x, w = draw_layer(spec, seed=11)
+    y, _ = run_layer(spec, x, w, guard=1024)
+    assert y.shape == (spec.batch, spec.K) + spec.out_spatial
+    check_full(spec, y, x, w)
+
+
+@pytest.mark.parametrize("spec,points", [
+    (SMALL[3], PAPER_F43_POINTS), (SMALL[2], PAPER_F43_POINTS),
+    (SMALL[1], (0, 0.5, -0.5)), (SMALL[2], (0, -1, 1, 0.5, -2)),
+], ids=["f43_3d_paper_pts", "f43_2d_paper_pts", "f23_half_pts", "f43_2d_other_pts"])
+def test_caller_points(spec, points):
+    x, w = draw_layer(spec, seed=5)
+    y, plan = run_layer(spec, x, w, points=points)
+    assert plan.desc["default_points"] == 0
+    check_full(spec, y, x, w)
+
+
+@pytest.mark.parametrize("N,C", [(3, 16), (3, 5), (2, 16)])
+def test_integer_inputs_bitwise_exact(N, C):
+    spec = LayerSpec(f"int_f2x3_{N}d", N=N, m=2, r=3, batch=2, C=C, K=37,
+                     X=(7, 9, 8)[:N] if N == 3 else (13, 11), pad=1,
+                     x_dist="int2", w_dist="int2")
+    x, w = draw_layer(spec, seed=3)
+    y, _ = run_layer(spec, x, w)
+    y_ref, _ = direct_blas(x, w, spec.pad)
+    assert np.array_equal(y, y_ref.astype(np.float32))
+
+
+def test_determinism_bitwise():
+    spec = SMALL[1]
+    x, w = draw_layer(spec, seed=2)
+    y1, _ = run_layer(spec, x, w)
+    y2, _ = run_layer(spec, x, w)
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+
+
+@pytest.mark.parametrize("spec", [SMALL[1], SMALL[2], SMALL[3]], ids=lambda s: s.name)
+def test_transform_stages_match_oracle(spec):
+    """a2 and a3 on their own: U and V against the oracle's steps 2 and 3."""
+    torch = require_gpu()
+    from paper_1611_06565_amd.wino import Plan
+    x, w = draw_layer(spec, seed=8)
+    plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X), pad=spec.pad)
+    d = plan.desc
+    U = plan.transform_filter(torch.from_numpy(w).cuda())
+    ws = plan.transform_input(torch.from_numpy(x).cuda())
+    torch.cuda.synchronize()
+    nxi = d["n_xi"]
+    Ug = U.cpu().numpy().reshape(nxi, d["C_pad"], d["K_pad"])
+    Vg = ws.cpu().numpy()[: nxi * d["C_pad"] * d["T_pad"]].reshape(nxi, d["C_pad"], d["T_pad"])
+    Uo = o_filter(w, spec.m, spec.r).reshape(spec.K, spec.C, nxi).transpose(2, 1, 0)
+    Uo_abs = o_filter(np.abs(w), spec.m, spec.r, exact=False)
+    Vo = o_input(x, spec.m, spec.r, spec.pad).reshape(d["T"], spec.C, nxi).transpose(2, 1, 0)
+    assert np.all(Ug[:, spec.C:, :] == 0) and np.all(Ug[:, :, spec.K:] == 0)
+    assert np.all(Vg[:, spec.C:, :] == 0) and np.all(Vg[:, :, d["T"]:] == 0)
+    scale_u = np.abs(Uo).max() + 1e-30
+    assert np.abs(Ug[:, :spec.C, :spec.K] - Uo).max() <= 1e-6 * scale_u
+    scale_v = np.abs(Vo).max() + 1e-30
+    assert np.abs(Vg[:, :spec.C, :d["T"]] - Vo).max() <= 1e-6 * scale_v
+    del Uo_abs
+
+
+def test_maxpool_matches_oracle():
+    torch = require_gpu()
+    from paper_1611_06565_amd.wino import maxpool3d
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal((2, 3, 5, 9, 7)).astype(np.float32)
+    for win in [(1, 2, 2), (2, 2, 2), (2, 3, 1)]:
+        y = maxpool3d(torch.from_numpy(x).cuda(), win)
+        torch.cuda.synchronize()
+        assert np.array_equal(y.cpu().numpy(), maxpool(x, win))
+
+
+def test_small_c3d_stack_per_layer():
+    """A narrow, small-volume copy of the C3D stack: every layer checked on
+    every output against the oracle fed with the GPU's previous activations."""
+    from workloads import StackSpec
+    stack = StackSpec(name="c3d_small", batch=1, C_in=3, X=(16, 32, 32),
+                      widths=(8, 16, 16, 16, 32, 32, 32, 32), pools=C3D_STACK.pools,
+                      m=2, x_dist="uniform")
+    _run_stack(stack, seed=4, full=True)
+
+
+def _run_stack(stack, seed, full):
+    torch = require_gpu()
+    from paper_1611_06565_amd.wino import Plan, maxpool3d
+    x, ws = draw_stack(stack, seed)
+    cur = torch.from_numpy(x).cuda()
+    for (spec, pool), w in zip(stack.layers(), ws):
+        log(f"[gpu] {spec.name} C={spec.C} K={spec.K} X={spec.X}")
+        plan = Plan(3, spec.m, 3, spec.C, spec.K, [spec.batch] + list(spec.X), pad=1, relu=True)
+        U = plan.transform_filter(torch.from_numpy(w).cuda())
+        y = plan.forward(cur, U)
+        torch.cuda.synchronize()
+        xin = cur.cpu().numpy()
+        yh = y.cpu().numpy()
+        if full:
+            check_full(spec, yh, xin, w)
+        else:
+            check_sampled(spec, yh, xin, w, n=3000, seed=seed)
+        if pool is not None:
+            y = maxpool3d(y, pool.window)
+            torch.cuda.synchronize()
+            assert np.array_equal(y.cpu().numpy(), maxpool(yh, pool.window))
+        cur = y
+        del plan, U
+    return cur
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_full_size_configs_sampled(cfg):
+    spec = CONFIGS[cfg]
+    x, w = draw_layer(spec, seed=cfg)
+    y, _ = run_layer(spec, x, w)
+    assert y.shape == (spec.batch, spec.K) + spec.out_spatial
+    assert np.all(np.isfinite(y))
+    check_sampled(spec, y, x, w, n=6000, seed=cfg)
+
+
+def test_full_size_c3d_stack_sampled():
+    out = _run_stack(C3D_STACK, seed=5, full=False)
+    assert tuple(out.shape) == (4, 512, 1, 3, 3)
