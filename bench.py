@@ -1,0 +1,235 @@
+#!/usr/bin/env python3
+"""Throughput of the N-D Winograd forward on one MI355X.
+
+Workload: the F(2^3, 3^3) video layer, batch 8, C = 64 -> K = 128, 16x56x56,
+3x3x3 kernels, pad 1, fp32, inputs ReLU(N(0,1)) and He-normal weights from a
+seed (synthetic stand-ins for C3D activations and weights).
+
+One step is the whole hot path over the batch: kernel transform (a2), input
+transform (a3) and the batched fp32-MFMA GEMM with the fused inverse
+transform (a4 + a5).  Transform synthesis (a1) happens once, at plan time.
+Inputs are resident in HBM before timing starts.  The metric is effective
+TFLOP/s: direct-convolution FLOPs 2*n*K*C*27*prod(Y) per step time.
+
+Prints one JSON line.  Per-stage durations come from HIP events recorded on
+the stream the kernels run on; the roofline object reports the dominant
+kernel against the MI355X fp32 MFMA peak.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP32_MFMA = 157.3      # TFLOP/s, MI355X dense fp32 matrix
+PEAK_HBM = 8000.0           # GB/s, MI355X HBM3E
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+TRAFFIC_FILE = os.path.join(PROFILE_DIR, "k_gemm_inv_f2x3_c64k128_traffic.txt")
+KERNEL_SOURCES = ["paper_1611_06565_amd/csrc/kernels.hpp", "paper_1611_06565_amd/csrc/transforms.hpp",
+                  "paper_1611_06565_amd/csrc/synth.hpp", "paper_1611_06565_amd/csrc/wino.hip"]
+
+
+def kernel_hash():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(expected_hash):
+    """HBM bytes per launch of the GEMM kernel from the committed counter
+    summary, or None if absent or taken on different kernel sources."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            m = re.match(r"\s*(\w+)\s*[:=]\s*(\S+)", line)
+            if m:
+                vals[m.group(1)] = m.group(2)
+    if vals.get("kernel_sources_sha256_16") != expected_hash:
+        return None
+    try:
+        return float(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(spec, x, w, budget_s=10.0):
+    """Time the fp64 direct-correlation oracle on whole samples of the batch
+    until about budget_s seconds have elapsed."""
+    from oracle.direct import direct_blas
+    from workloads import direct_flops
+    try:
+        import threadpoolctl
+        threads = max(int(i.get("num_threads", 1)) for i in threadpoolctl.threadpool_info()) or 1
+    except Exception:  # noqa: BLE001
+        threads = os.cpu_count() or 1
+    per_sample = direct_flops(spec) / spec.batch
+    done, t_total = 0, 0.0
+    while done < spec.batch and (done == 0 or t_total < budget_s):
+        t0 = time.perf_counter()
+        direct_blas(x[done:done + 1], w, spec.pad)
+        t_total += time.perf_counter() - t0
+        done += 1
+    return {
+        "value": per_sample * done / t_total / 1e12,
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"fp64 direct correlation (per-offset BLAS form, with the |w||x| "
+                   f"denominator) on {done} of {spec.batch} samples of the same layer, "
+                   f"{t_total:.1f} s"),
+    }
+
+
+def calib_copy(nbytes=1 << 30, reps=5):
+    """A plain device copy of known size, for scaling HBM counters."""
+    import torch
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calib_copy_bytes_each_way": nbytes, "reps": reps}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--seed", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-check", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="only run a 1 GiB device copy (for HBM counter scaling)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build runs the layer on a single MI355X "
+              "(batch or slab sharding across GPUs is described in DESIGN.md but not built); "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    if args.calib_copy:
+        calib_copy()
+        return
+
+    from paper_1611_06565_amd.wino import Plan
+    from workloads import CONFIGS, direct_flops, draw_layer
+
+    spec = CONFIGS[2]
+    x, w = draw_layer(spec, seed=args.seed)
+    plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X),
+                pad=spec.pad, relu=spec.relu)
+    d = plan.desc
+    xd = torch.from_numpy(x).cuda()
+    wd = torch.from_numpy(w).cuda()
+    U = plan.new_filter()
+    ws = plan.new_workspace()
+    y = plan.new_output()
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        plan.transform_filter(wd, U)
+        if ev is not None:
+            ev[1].record()
+        plan.transform_input(xd, ws)
+        if ev is not None:
+            ev[2].record()
+        plan.gemm_inverse(ws, U, y)
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    st = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
+                   for e in evs])
+    filt_ms, inp_ms, gemm_ms = (float(v) for v in st.mean(axis=0))
+
+    flops = direct_flops(spec)
+    nxi = d["n_xi"]
+    gemm_flops = 2.0 * nxi * d["T"] * spec.C * spec.K
+    in_bytes = 4.0 * (spec.batch * spec.C * np.prod(spec.X) + nxi * d["T"] * spec.C)
+    achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
+    traffic = read_traffic(kernel_hash())
+
+    check = None
+    if not args.no_check:
+        from oracle.direct import direct_sampled
+        from oracle.metric import normalised_error
+        rng = np.random.default_rng(0)
+        yh = y.cpu().numpy()
+        coords = np.stack([rng.integers(0, s, size=2000) for s in yh.shape], axis=1)
+        ys, dens = direct_sampled(x, w, spec.pad, coords)
+        check = normalised_error(yh[tuple(coords.T)], ys, dens)["max"]
+
+    out = {
+        "metric": "effective TFLOP/s per 3D conv layer (direct FLOPs); % fp32 MFMA / HBM peak",
+        "value": flops / (ms_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "F(2^3,3^3) 3-D conv layer: batch 8, C=64, K=128, 16x56x56, 3x3x3, pad 1",
+            "N": 3, "m": 2, "r": 3, "batch": spec.batch, "C": spec.C, "K": spec.K,
+            "X": list(spec.X), "pad": spec.pad, "points": "0,1,-1,inf", "seed": args.seed,
+            "tiles": d["T"], "direct_gflop_per_step": flops / 1e9,
+        },
+        "roofline": {
+            "kernel": "k_gemm_inv (batched fp32-MFMA GEMM + fused inverse transform)",
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_FP32_MFMA,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_FP32_MFMA,
+            "traffic": traffic,
+            "algorithmic": "2*alpha^N*T*C*K = %.4g FLOP per launch" % gemm_flops,
+        },
+        "stages_ms": {"filter_transform": filt_ms, "input_transform": inp_ms,
+                      "gemm_inverse": gemm_ms},
+        "input_transform_hbm": {"achieved_GBps": in_bytes / (inp_ms * 1e-3) / 1e9,
+                                "peak_GBps": PEAK_HBM,
+                                "frac": in_bytes / (inp_ms * 1e-3) / 1e9 / PEAK_HBM},
+        "forward_U_cached_tflops": flops / ((inp_ms + gemm_ms) * 1e-3) / 1e12,
+        "max_normalised_error_sampled": check,
+        "kernel_sources_sha256_16": kernel_hash(),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(spec, x, w)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
