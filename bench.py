@@ -106,7 +106,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--seed", type=int, default=2)
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4],
+                    help="layer family (default 2, the F(2^3,3^3) C=64 K=128 video layer)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
@@ -130,8 +132,9 @@ def main():
     from paper_1611_06565_amd.wino import Plan
     from workloads import CONFIGS, direct_flops, draw_layer
 
-    spec = CONFIGS[2]
-    x, w = draw_layer(spec, seed=args.seed)
+    spec = CONFIGS[args.config]
+    seed = args.config if args.seed is None else args.seed
+    x, w = draw_layer(spec, seed=seed)
     plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X),
                 pad=spec.pad, relu=spec.relu)
     d = plan.desc
@@ -174,7 +177,7 @@ def main():
     flops = direct_flops(spec)
     nxi = d["n_xi"]
     gemm_flops = 2.0 * nxi * d["T"] * spec.C * spec.K
-    in_bytes = 4.0 * (spec.batch * spec.C * np.prod(spec.X) + nxi * d["T"] * spec.C)
+    in_bytes = 4.0 * (spec.batch * spec.C * float(np.prod(spec.X)) + nxi * d["T"] * spec.C)
     achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
     traffic = read_traffic(kernel_hash())
 
@@ -202,9 +205,12 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": "F(2^3,3^3) 3-D conv layer: batch 8, C=64, K=128, 16x56x56, 3x3x3, pad 1",
-            "N": 3, "m": 2, "r": 3, "batch": spec.batch, "C": spec.C, "K": spec.K,
-            "X": list(spec.X), "pad": spec.pad, "points": "0,1,-1,inf", "seed": args.seed,
+            "workload": "F(%d^%d,3^%d) %d-D conv layer: batch %d, C=%d, K=%d, %s, %s, pad %d" % (
+                spec.m, spec.N, spec.N, spec.N, spec.batch, spec.C, spec.K,
+                "x".join(str(v) for v in spec.X), "x".join(["3"] * spec.N), spec.pad),
+            "N": spec.N, "m": spec.m, "r": spec.r, "batch": spec.batch, "C": spec.C, "K": spec.K,
+            "X": list(spec.X), "pad": spec.pad,
+            "points": "0,1,-1,inf" if spec.m == 2 else "0,1,-1,2,-2,inf", "seed": seed,
             "tiles": d["T"], "direct_gflop_per_step": flops / 1e9,
         },
         "roofline": {

@@ -85,6 +85,7 @@ typedef struct {
   int32_t block_tiles;   /* GEMM rows per work-group                             */
   int32_t block_kernels; /* GEMM columns per work-group                          */
   int32_t default_points;/* 1 when the transform constants are compiled in        */
+  int32_t channel_group; /* CG: channels interleaved innermost in U and V          */
 } wino_plan_desc;
 
 /* Build a plan for one layer.  §3.1-§3.3 and §4.1.
@@ -106,12 +107,16 @@ void wino_destroy(wino_plan_t* plan);
 /* Fill *desc from the plan.  Returns WINO_EINVAL for NULL arguments. */
 wino_status wino_plan_describe(const wino_plan_t* plan, wino_plan_desc* desc);
 
-/* Bytes of the transformed-filter buffer U, laid out as
- * U[alpha^N][C_pad][K_pad] (float32; padding rows and columns are zero). */
+/* Bytes of the transformed-filter buffer U (float32), laid out as
+ * U[alpha^N][C_pad/CG][K_pad][CG] with CG = channel_group: element
+ * (xi, c, k) sits at ((xi*C_pad/CG + c/CG)*K_pad + k)*CG + c%CG.  Padding
+ * channels and kernels are zero. */
 size_t wino_filter_bytes(const wino_plan_t* plan);
 
-/* Bytes of workspace wino_forward needs: the transformed input
- * V[alpha^N][C_pad][T_pad] (float32). */
+/* Bytes of workspace wino_forward needs: the transformed input V (float32),
+ * laid out tile-block major as V[T_pad/B][alpha^N][C_pad/CG][B][CG] with
+ * B = block_tiles: element (xi, c, t) sits at
+ * (((t/B)*alpha^N + xi)*C_pad/CG + c/CG)*B*CG + (t%B)*CG + c%CG. */
 size_t wino_workspace_bytes(const wino_plan_t* plan);
 
 /* out[0..N+1] = [batch, K, Y_1 .. Y_N]. */
@@ -129,7 +134,7 @@ wino_status wino_get_matrices(const wino_plan_t* plan, double* AT, double* BT, d
 wino_status wino_transform_filter(const wino_plan_t* plan, const float* w, float* U, void* stream);
 
 /* Data transform V = d x_1 B^T ... x_N B^T of every tile and channel (eq. 4),
- * written in the GEMM layout V[alpha^N][C_pad][T_pad] (§4.1's reshuffle).
+ * written straight into the GEMM operand layout above (§4.1's reshuffle).
  *   x          device, [batch][C][X_1..X_N] float32
  *   workspace  device, at least wino_workspace_bytes(plan) bytes */
 wino_status wino_transform_input(const wino_plan_t* plan, const float* x, void* workspace,

@@ -8,14 +8,20 @@
 //
 // Layouts (float32, zero padding rows/columns):
 //   x [batch][C][X_1..X_N]     w [K][C][r^N]      y [batch][K][Y_1..Y_N]
-//   U [alpha^N][C_pad][K_pad]  V [alpha^N][C_pad][T_pad]
+//   U [alpha^N][C_pad/CG][K_pad][CG]
+//   V [T_pad/BLK][alpha^N][C_pad/CG][BLK][CG]
 // T counts tiles over the whole batch (tiles of every sample form the rows of
-// one GEMM, §4.1 and §4.4: the method is batch-size agnostic).
+// one GEMM, §4.1 and §4.4: the method is batch-size agnostic).  BLK is the
+// GEMM block (32 or 16 tiles / kernels) and CG the channel group (see
+// Blocking): interleaving channel groups innermost lets every lane fetch
+// VEC k-steps of an MFMA operand with one load, and storing V tile-block
+// major keeps all of one work-group's operand rows in one contiguous region.
 #pragma once
 
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "synth.hpp"
 #include "transforms.hpp"
@@ -24,6 +30,20 @@ namespace wino {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// GEMM block (tiles and kernels per work-group), operand load width and
+// channel group per (N, m, r).  A lane loads VEC consecutive channels of a
+// group per operand; MFMA k-step j of the group uses the j-th of them, so a
+// group holds KSTEP * VEC channels.
+template <int N, int MM, int R>
+struct Blocking {
+  static constexpr int A = MM + R - 1;
+  static constexpr int NXI = ipow(A, N);
+  static constexpr int BLK = NXI > 64 ? 16 : 32;
+  static constexpr int KSTEP = BLK == 32 ? 2 : 4;   // channels per MFMA
+  static constexpr int VEC = NXI > 64 ? 1 : 2;      // floats per operand load
+  static constexpr int CG = KSTEP * VEC;            // channels per group
+};
 
 // ---------------------------------------------------------------- arguments
 struct FilterArgs {
@@ -62,15 +82,19 @@ __device__ __forceinline__ int split_tile(int t, const int32_t* tiles, int* ti) 
 }
 
 // ------------------------------------------------------------ filter (a2)
+// One thread per (channel, kernel); lanes run over the channel group fastest
+// so each plane store is contiguous.
 template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(256) k_filter(const float* __restrict__ w, float* __restrict__ U,
                                                 FilterArgs a, FMats fm) {
-  constexpr int A = MM + R - 1;
-  constexpr int NXI = ipow(A, N);
+  using B = Blocking<N, MM, R>;
+  constexpr int A = B::A, NXI = B::NXI, CG = B::CG;
   constexpr int RN = ipow(R, N);
   const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  const int k = int(idx % a.K_pad);
-  const int c = int(idx / a.K_pad);
+  const int cl = int(idx % CG);
+  const int k = int((idx / CG) % a.K_pad);
+  const int cg = int(idx / (int64_t(CG) * a.K_pad));
+  const int c = cg * CG + cl;
   if (c >= a.C_pad) return;
   float u[NXI];
   if (c < a.C && k < a.K) {
@@ -83,7 +107,7 @@ __global__ void __launch_bounds__(256) k_filter(const float* __restrict__ w, flo
 #pragma unroll
     for (int i = 0; i < NXI; ++i) u[i] = 0.0f;
   }
-  float* dst = U + int64_t(c) * a.K_pad + k;
+  float* dst = U + (int64_t(cg) * a.K_pad + k) * CG + cl;
 #pragma unroll
   for (int xi = 0; xi < NXI; ++xi) dst[int64_t(xi) * a.uplane] = u[xi];
 }
@@ -91,16 +115,25 @@ __global__ void __launch_bounds__(256) k_filter(const float* __restrict__ w, flo
 // ------------------------------------------------------------- input (a3)
 // One thread per (tile, channel): gather the alpha^N window (zero outside the
 // input), transform along every axis, scatter to the alpha^N planes of V.
-// Consecutive threads take consecutive tiles, so every plane store is a
-// contiguous run.
+// A work-group covers one GEMM tile block and 256 / (BLK * CG) channel
+// groups; lanes run over channels of a group fastest, then tiles, so each
+// plane store is one contiguous run.
 template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, float* __restrict__ V,
                                                InputArgs a, FMats fm) {
-  constexpr int A = MM + R - 1;
-  constexpr int NXI = ipow(A, N);
-  const int t = int(blockIdx.x) * 256 + int(threadIdx.x);
-  const int c = int(blockIdx.y);
-  if (t >= a.T_pad) return;
+  using B = Blocking<N, MM, R>;
+  constexpr int A = B::A, NXI = B::NXI, BLK = B::BLK, CG = B::CG;
+  constexpr int GPW = 256 / (BLK * CG);   // channel groups per work-group
+  static_assert(GPW * BLK * CG == 256, "work-group shape");
+  const int tid = int(threadIdx.x);
+  const int cl = tid % CG;
+  const int tl = (tid / CG) % BLK;
+  const int gl = tid / (CG * BLK);
+  const int tb = int(blockIdx.x);
+  const int cg = int(blockIdx.y) * GPW + gl;
+  const int c = cg * CG + cl;
+  if (c >= a.C_pad) return;
+  const int t = tb * BLK + tl;
   float d[NXI];
   if (t < a.T && c < a.C) {
     int ti[3] = {0, 0, 0};
@@ -139,45 +172,46 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
   }
   float v[NXI];
   transform_nd<N, A, A>(d, v, MatRef<Which::BT, CONST, MM, R>{&fm});
-  float* dst = V + int64_t(c) * a.T_pad + t;
+  // V[tb][xi][cg][tl][cl]; consecutive xi planes are C_pad * BLK floats apart
+  const int64_t xi_stride = int64_t(a.C_pad) * BLK;
+  float* dst = V + int64_t(tb) * NXI * xi_stride + (int64_t(cg) * BLK + tl) * CG + cl;
 #pragma unroll
-  for (int xi = 0; xi < NXI; ++xi) dst[int64_t(xi) * a.vplane] = v[xi];
+  for (int xi = 0; xi < NXI; ++xi) dst[xi * xi_stride] = v[xi];
 }
 
 // ------------------------------------------------- batched GEMM (a4 + a5)
-// Work-group = BLK tiles x BLK kernels x all alpha^N elements; wave w owns
-// XPW = alpha^N / NW consecutive elements and keeps one BLK x BLK fp32 MFMA
-// accumulator per element for the whole channel reduction.  MFMA operands
-// stream straight from global memory (V from HBM/L2, U from L2) one channel
-// step ahead; the inverse transform needs every element of a (tile, kernel)
-// pair, so the epilogue exchanges accumulators through LDS in row slices.
+// Work-group = BLK tiles x BLK kernels x all alpha^N elements.  Wave w owns
+// the elements with xi_0 = w (an alpha^(N-1) slice) and keeps one BLK x BLK
+// fp32 MFMA accumulator per element for the whole channel reduction.  MFMA
+// operands stream straight from global memory (V from HBM/L2, U from L2)
+// through a DEPTH-stage register ring, DEPTH-1 channel steps ahead.
+//
+// Epilogue (eq. 4's inverse transform, separable): each lane holds, for every
+// (tile, kernel) of its accumulator registers, all elements of its wave's
+// slice, so A^T is applied along axes 1..N-1 in registers; the m^(N-1)
+// partial results per wave go through LDS once, and the last step (A^T along
+// axis 0) is done by threads laid out so that neighbouring lanes write
+// neighbouring outputs of a row.
 template <int BLK> struct MfmaShape;
 template <> struct MfmaShape<32> {
-  static constexpr int KSTEP = 2, NACC = 16, ROWS = 8;
+  static constexpr int KSTEP = 2, NACC = 16;
   using acc_t = f32x16;
   __device__ static __forceinline__ acc_t mma(float a, float b, acc_t c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
   }
-  // Output element of accumulator register `reg` in round q (regs 4q..4q+3):
-  // row 8*(reg/4) + 4*(lane/32) + reg%4, column lane%32.
-  static constexpr int ROUNDS = 4, REGS_PER_ROUND = 4;
-  __device__ static __forceinline__ int row_local(int lane, int j) { return 4 * (lane >> 5) + j; }
-  __device__ static __forceinline__ int row_global(int rl, int q) { return 8 * q + rl; }
-  __device__ static __forceinline__ int reg(int q, int j) { return 4 * q + j; }
-  __device__ static __forceinline__ int swz(int rl, int col) { return col ^ (rl << 2); }
+  // accumulator register r of a lane holds row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
+  __device__ static __forceinline__ int acc_row(int lane, int r) {
+    return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+  }
 };
 template <> struct MfmaShape<16> {
-  static constexpr int KSTEP = 4, NACC = 4, ROWS = 4;
+  static constexpr int KSTEP = 4, NACC = 4;
   using acc_t = f32x4;
   __device__ static __forceinline__ acc_t mma(float a, float b, acc_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
   }
-  // Register `reg` holds row 4*(lane/16) + reg, column lane%16.
-  static constexpr int ROUNDS = 4, REGS_PER_ROUND = 1;
-  __device__ static __forceinline__ int row_local(int lane, int) { return lane >> 4; }
-  __device__ static __forceinline__ int row_global(int rl, int q) { return 4 * rl + q; }
-  __device__ static __forceinline__ int reg(int q, int) { return q; }
-  __device__ static __forceinline__ int swz(int rl, int col) { return col ^ ((rl >> 1) << 3); }
+  // accumulator register r of a lane holds row 4*(lane/16) + r, column lane%16
+  __device__ static __forceinline__ int acc_row(int lane, int r) { return 4 * (lane >> 4) + r; }
 };
 
 // Work-groups are dispatched round-robin over the 8 XCDs.  Renumber them so
@@ -190,138 +224,192 @@ __device__ __forceinline__ int xcd_remap(int b, int nb) {
   return xcd < rem ? xcd * (per + 1) + j : rem * (per + 1) + (xcd - rem) * per + j;
 }
 
-template <int N, int MM, int R, bool CONST, int BLK, int NW>
+// Shape of one GEMM work-group.  NW waves split the alpha^N elements evenly;
+// each wave's share is made of whole "units" of the LOC trailing axes
+// (alpha^LOC consecutive elements), which is what lets the epilogue reduce
+// those axes in registers.
+template <int N, int MM, int R, int BLK, int NW, int LOC>
+struct GemmGeom {
+  static constexpr int A = MM + R - 1;
+  static constexpr int NXI = ipow(A, N);
+  static constexpr int NT = NW * 64;
+  static constexpr int XPW = NXI / NW;               // elements per wave
+  static constexpr int UNIT = ipow(A, LOC);          // elements per register-reduced unit
+  static constexpr int UPW = XPW / UNIT;             // units per wave
+  static constexpr int NUNIT = NXI / UNIT;           // units in the work-group = alpha^(N-LOC)
+  static constexpr int OLOC = ipow(MM, LOC);         // outputs per unit after the reduction
+  static constexpr int PLANES = NUNIT * OLOC;        // LDS planes of BLK x BLK partial results
+  static constexpr int PL = BLK * BLK + 32 / MM;     // plane stride, padded against bank conflicts
+  static constexpr int LDS_FLOATS = PLANES * PL;
+  static_assert(NXI % NW == 0 && XPW % UNIT == 0, "waves must own whole units");
+  static_assert(LOC >= 1 && LOC < N, "at least one axis is reduced in registers, one across waves");
+};
+
+// VEC = floats per operand load (one load feeds VEC MFMA k-steps).  DEPTH =
+// stages in the register ring (DEPTH-1 stages in flight while one is
+// consumed).
+template <int N, int MM, int R, bool CONST, int BLK, int NW, int LOC, int VEC, int DEPTH>
 __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ V,
                                                       const float* __restrict__ U,
                                                       float* __restrict__ y, GemmArgs g, FMats fm) {
   using S = MfmaShape<BLK>;
-  constexpr int A = MM + R - 1;
-  constexpr int NXI = ipow(A, N);
-  constexpr int XPW = NXI / NW;
-  static_assert(NXI % NW == 0, "elements must split evenly over waves");
-  constexpr int NT = NW * 64;
-  constexpr int P = S::ROWS * BLK;          // (tile, kernel) pairs per round
-  constexpr int TPP = NT / P;               // threads per pair
-  static_assert(TPP >= 1 && NT % P == 0, "pairs must cover the work-group");
-  constexpr int AR = ipow(A, N - 1);
+  using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
+  constexpr int A = Geo::A, NXI = Geo::NXI, NT = Geo::NT, XPW = Geo::XPW;
+  constexpr int UPW = Geo::UPW, UNIT = Geo::UNIT, OLOC = Geo::OLOC, PL = Geo::PL;
+  constexpr int NUNIT = Geo::NUNIT;
+  static_assert(NT % (MM * BLK) == 0, "output lanes must tile the work-group");
+  static_assert(VEC == 1 || VEC == 2 || VEC == 4, "operand load width");
 
-  __shared__ float sm[NXI * S::ROWS * BLK];
+  __shared__ float sm[Geo::LDS_FLOATS];
 
   const int lane = int(threadIdx.x) & 63;
   const int wave = int(threadIdx.x) >> 6;
   const int L = xcd_remap(int(blockIdx.x), g.nblocks);
   const int tb = L / g.nkb, kb = L % g.nkb;
-  const int xi0 = wave * XPW;
   const int col = lane % BLK, kr = lane / BLK;
 
-  const float* vp = V + int64_t(xi0) * g.vplane + int64_t(kr) * g.T_pad + int64_t(tb) * BLK + col;
-  const float* up = U + int64_t(xi0) * g.uplane + int64_t(kr) * g.K_pad + int64_t(kb) * BLK + col;
-  const int64_t vstep = int64_t(S::KSTEP) * g.T_pad, ustep = int64_t(S::KSTEP) * g.K_pad;
+  // Operand rows: V[tb][xi][cg][t][CG] and U[xi][cg][k][CG].  Lane (kr, col)
+  // owns channels VEC*kr .. VEC*kr+VEC-1 of every group; MFMA k-step j of a
+  // group uses channel VEC*kr + j, so the VEC steps of a group cover all CG
+  // channels.  One "stage" = one group = VEC k-steps.
+  constexpr int CG = S::KSTEP * VEC;
+  const int64_t vxi = int64_t(g.C_pad) * BLK;                      // V plane stride (floats)
+  const int64_t uxi = g.uplane;                                    // U plane stride (floats)
+  const float* vnext = V + (int64_t(tb) * NXI + int64_t(wave) * XPW) * vxi + col * CG + VEC * kr;
+  const float* unext = U + int64_t(wave) * XPW * uxi + int64_t(kb) * BLK * CG + col * CG + VEC * kr;
+  const int64_t vgstep = int64_t(BLK) * CG, ugstep = int64_t(g.K_pad) * CG;
+  const int nstages = g.C_pad / CG;
 
   typename S::acc_t acc[XPW];
 #pragma unroll
   for (int x = 0; x < XPW; ++x) acc[x] = typename S::acc_t{};
 
-  float an[XPW], bn[XPW];
+  using vec_t = typename std::conditional<VEC == 4, float4,
+                typename std::conditional<VEC == 2, float2, float>::type>::type;
+  vec_t ra[DEPTH][XPW], rb[DEPTH][XPW];
+  auto fetch = [&](vec_t* a2, vec_t* b2) {
 #pragma unroll
-  for (int x = 0; x < XPW; ++x) {
-    an[x] = vp[int64_t(x) * g.vplane];
-    bn[x] = up[int64_t(x) * g.uplane];
-  }
-  for (int c0 = 0; c0 < g.C_pad; c0 += S::KSTEP) {
-    float ac[XPW], bc[XPW];
-#pragma unroll
-    for (int x = 0; x < XPW; ++x) { ac[x] = an[x]; bc[x] = bn[x]; }
-    if (c0 + S::KSTEP < g.C_pad) {
-      vp += vstep;
-      up += ustep;
-#pragma unroll
-      for (int x = 0; x < XPW; ++x) {
-        an[x] = vp[int64_t(x) * g.vplane];
-        bn[x] = up[int64_t(x) * g.uplane];
-      }
+    for (int x = 0; x < XPW; ++x) {
+      a2[x] = *reinterpret_cast<const vec_t*>(vnext + x * vxi);
+      b2[x] = *reinterpret_cast<const vec_t*>(unext + x * uxi);
     }
+    vnext += vgstep;
+    unext += ugstep;
+  };
+  auto consume = [&](const vec_t* a2, const vec_t* b2) {
+    const float* af = reinterpret_cast<const float*>(a2);
+    const float* bf = reinterpret_cast<const float*>(b2);
 #pragma unroll
-    for (int x = 0; x < XPW; ++x) acc[x] = S::mma(ac[x], bc[x], acc[x]);
+    for (int j = 0; j < VEC; ++j)
+#pragma unroll
+      for (int x = 0; x < XPW; ++x) acc[x] = S::mma(af[x * VEC + j], bf[x * VEC + j], acc[x]);
+  };
+  // Prologue: DEPTH-1 stages in flight.
+#pragma unroll
+  for (int d = 0; d < DEPTH - 1; ++d)
+    if (d < nstages) fetch(ra[d], rb[d]);
+  // Steady state: every iteration issues DEPTH fetches and consumes DEPTH
+  // stages with no branches in between, so the wait counts the compiler
+  // inserts only ever wait for the stage being consumed.
+  int s = 0;
+  for (; s + 2 * DEPTH - 1 <= nstages; s += DEPTH) {
+#pragma unroll
+    for (int j = 0; j < DEPTH; ++j) {
+      fetch(ra[(j + DEPTH - 1) % DEPTH], rb[(j + DEPTH - 1) % DEPTH]);
+      consume(ra[j], rb[j]);
+    }
+  }
+  // Tail: the last (at most 2*DEPTH-2) stages.
+#pragma unroll
+  for (int j = 0; j < 2 * DEPTH - 2; ++j) {
+    if (s + j < nstages) {
+      if (s + j + DEPTH - 1 < nstages)
+        fetch(ra[(j + DEPTH - 1) % DEPTH], rb[(j + DEPTH - 1) % DEPTH]);
+      consume(ra[j % DEPTH], rb[j % DEPTH]);
+    }
   }
 
-  // ---- epilogue: inverse transform along every axis, stitch, crop.
+  // ---- epilogue, part 1: A^T along the LOC trailing axes in registers; the
+  // m^LOC results of every unit go to LDS plane (unit, o_loc) at [k][t ^ k].
   const MatRef<Which::AT, CONST, MM, R> AT{&fm};
-  const int tid = int(threadIdx.x);
-  const int p = tid % P, part = tid / P;
-  const int rl_c = p % S::ROWS, kl_c = p / S::ROWS;
-  const int kglob = kb * BLK + kl_c;
 #pragma unroll
-  for (int q = 0; q < S::ROUNDS; ++q) {
-    if (q) __syncthreads();
+  for (int r = 0; r < S::NACC; ++r) {
+    const int t = S::acc_row(lane, r);
 #pragma unroll
-    for (int j = 0; j < S::REGS_PER_ROUND; ++j) {
-      const int rl = S::row_local(lane, j);
-      float* dst = sm + rl * BLK + S::swz(rl, col);
+    for (int u = 0; u < UPW; ++u) {
+      float sv[UNIT];
 #pragma unroll
-      for (int x = 0; x < XPW; ++x) dst[(xi0 + x) * (S::ROWS * BLK)] = acc[x][S::reg(q, j)];
+      for (int e = 0; e < UNIT; ++e) sv[e] = acc[u * UNIT + e][r];
+      float o[OLOC];
+      transform_nd<LOC, A, MM>(sv, o, AT);
+      float* dst = sm + ((wave * UPW + u) * OLOC) * PL + col * BLK + (t ^ col);
+#pragma unroll
+      for (int j = 0; j < OLOC; ++j) dst[j * PL] = o[j];
     }
-    __syncthreads();
-    const int t = tb * BLK + S::row_global(rl_c, q);
-    if (t < g.T && kglob < g.K) {
-      int ti[3] = {0, 0, 0};
-      const int n = split_tile<N>(t, g.tiles, ti);
-      const float* src = sm + rl_c * BLK + S::swz(rl_c, kl_c);
-      float* yk = y + (int64_t(n) * g.K + kglob) * g.ystride_k;
-      for (int o0 = part; o0 < MM; o0 += TPP) {
-        const int y0 = ti[0] * MM + o0;
-        if (y0 >= g.Y[0]) break;
-        // contract axis 0 while streaming the alpha^N values from LDS
-        float s[AR];
-        bool first = true;
+  }
+  __syncthreads();
+
+  // ---- epilogue, part 2: A^T along the N-LOC leading axes, ReLU, crop, store.
+  // Item (o_loc, k, t) with the last-axis output fastest, then the tile, so
+  // neighbouring lanes write neighbouring outputs of a row.
+  const int tid = int(threadIdx.x);
+  const int o_last = tid % MM;
+  const int tl = (tid / MM) % BLK;
+  const int t = tb * BLK + tl;
+  if (t >= g.T) return;
+  int ti[3] = {0, 0, 0};
+  const int n = split_tile<N>(t, g.tiles, ti);
+  const int y_last = ti[N - 1] * MM + o_last;
+  if (y_last >= g.Y[N - 1]) return;
+  constexpr int ITEMS = OLOC * BLK * BLK;
+  constexpr int LEAD = N - LOC;                  // axes contracted here
+  constexpr int OLEAD = ipow(MM, LEAD);
+  for (int i = tid; i < ITEMS; i += NT) {
+    const int k_l = (i / (MM * BLK)) % BLK;
+    const int o_rest = i / (MM * BLK * BLK);     // o_loc without its last axis
+    const int kg = kb * BLK + k_l;
+    if (kg >= g.K) continue;
+    const int jj = o_rest * MM + o_last;         // o_loc index
+    // output coordinates of the LOC trailing axes (last one fixed per thread)
+    int yc[3] = {0, 0, 0};
+    bool ok = true;
+    {
+      int rem = o_rest;
 #pragma unroll
-        for (int x0 = 0; x0 < A; ++x0) {
-          const float cf = AT(o0, x0);
-          if (cf == 0.0f) continue;
-#pragma unroll
-          for (int rr = 0; rr < AR; ++rr) {
-            const float v = src[(x0 * AR + rr) * (S::ROWS * BLK)];
-            if (first) s[rr] = (cf == 1.0f) ? v : (cf == -1.0f ? -v : cf * v);
-            else if (cf == 1.0f) s[rr] += v;
-            else if (cf == -1.0f) s[rr] -= v;
-            else s[rr] = __builtin_fmaf(cf, v, s[rr]);
-          }
-          first = false;
-        }
-        if constexpr (N == 2) {
-          float o[MM];
-          apply_axis<1, A, MM, 1>(s, o, AT);
-#pragma unroll
-          for (int o1 = 0; o1 < MM; ++o1) {
-            const int y1 = ti[1] * MM + o1;
-            if (y1 < g.Y[1]) {
-              float v = o[o1];
-              if (g.relu) v = v > 0.0f ? v : 0.0f;
-              yk[int64_t(y0) * g.Y[1] + y1] = v;
-            }
-          }
-        } else {
-          float t1[MM * A];
-          float o[MM * MM];
-          apply_axis<1, A, MM, A>(s, t1, AT);
-          apply_axis<MM, A, MM, 1>(t1, o, AT);
-#pragma unroll
-          for (int o1 = 0; o1 < MM; ++o1) {
-            const int y1 = ti[1] * MM + o1;
-            if (y1 >= g.Y[1]) continue;
-            float* row = yk + (int64_t(y0) * g.Y[1] + y1) * g.Y[2];
-#pragma unroll
-            for (int o2 = 0; o2 < MM; ++o2) {
-              const int y2 = ti[2] * MM + o2;
-              if (y2 < g.Y[2]) {
-                float v = o[o1 * MM + o2];
-                if (g.relu) v = v > 0.0f ? v : 0.0f;
-                row[y2] = v;
-              }
-            }
-          }
-        }
+      for (int ax = N - 2; ax >= LEAD; --ax) {
+        const int oa = rem % MM;
+        rem /= MM;
+        yc[ax] = ti[ax] * MM + oa;
+        ok = ok && yc[ax] < g.Y[ax];
       }
+      yc[N - 1] = y_last;
+    }
+    if (!ok) continue;
+    float v[NUNIT];
+#pragma unroll
+    for (int uu = 0; uu < NUNIT; ++uu) v[uu] = sm[(uu * OLOC + jj) * PL + k_l * BLK + (tl ^ k_l)];
+    float out[OLEAD];
+    transform_nd<LEAD, A, MM>(v, out, AT);
+    float* yk = y + (int64_t(n) * g.K + kg) * g.ystride_k;
+#pragma unroll
+    for (int q = 0; q < OLEAD; ++q) {
+      // leading-axis output offsets of item q (axis LEAD-1 fastest)
+      int rem = q;
+      bool in = true;
+#pragma unroll
+      for (int ax = LEAD - 1; ax >= 0; --ax) {
+        const int oa = rem % MM;
+        rem /= MM;
+        yc[ax] = ti[ax] * MM + oa;
+        in = in && yc[ax] < g.Y[ax];
+      }
+      if (!in) continue;
+      int64_t off = yc[0];
+#pragma unroll
+      for (int ax = 1; ax < N; ++ax) off = off * g.Y[ax] + yc[ax];
+      float val = out[q];
+      if (g.relu) val = val > 0.0f ? val : 0.0f;
+      yk[off] = val;
     }
   }
 }

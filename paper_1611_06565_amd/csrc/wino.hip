@@ -20,7 +20,7 @@ struct wino_plan_s {
   int64_t X[3], Y[3], tiles[3];
   int32_t pad[3];
   int64_t T, T_pad;
-  int blk, nw;
+  int blk, cg;
   uint32_t flags;
   bool const_mats;
   double AT[kMaxAlpha][kMaxAlpha], BT[kMaxAlpha][kMaxAlpha], G[kMaxAlpha][kMaxAlpha];
@@ -73,14 +73,25 @@ template <int N, int MM, int R, bool CONST>
 struct Launch {
   static constexpr int A = MM + R - 1;
   static constexpr int NXI = ipow(A, N);
-  static constexpr int BLK = NXI > 64 ? 16 : 32;
-  static constexpr int NW = 4;
+  static constexpr int BLK = Blocking<N, MM, R>::BLK;
+  static constexpr int CG = Blocking<N, MM, R>::CG;
+  // GEMM work-group shape: waves, register-reduced trailing axes, operand
+  // load width and register-ring depth.
+  //   F(2^3): 8 waves (2 per SIMD) x two alpha-rows, 8-byte loads, 2 groups in flight
+  //   F(4^3): 12 waves x three alpha-rows, 4-byte loads (register budget)
+  //   (VEC and the channel group CG come from Blocking and fix the U/V layout)
+  //   2-D   : one alpha-row per wave
+  static constexpr int NW = (N == 3 && A == 6) ? 12 : (N == 3 ? 8 : A);
+  static constexpr int LOC = 1;
+  static constexpr int VEC = Blocking<N, MM, R>::VEC;
+  static constexpr int DEPTH = (N == 3 && A == 6) ? 2 : 3;
+  using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
 
   static wino_status filter(const wino_plan_s& p, const float* w, float* U, hipStream_t s) {
     FilterArgs a{};
     a.uplane = int64_t(p.C_pad) * p.K_pad;
     a.C = p.C; a.K = p.K; a.C_pad = p.C_pad; a.K_pad = p.K_pad;
-    const int64_t n = int64_t(p.C_pad) * p.K_pad;
+    const int64_t n = int64_t(p.C_pad) * p.K_pad;   // C_pad is a multiple of CG
     const unsigned grid = unsigned((n + 255) / 256);
     hipLaunchKernelGGL((k_filter<N, MM, R, CONST>), dim3(grid), dim3(256), 0, s, w, U, a, p.fm);
     return launch_status();
@@ -96,7 +107,9 @@ struct Launch {
     for (int i = 0; i < 3; ++i) {
       a.X[i] = int32_t(p.X[i]); a.tiles[i] = int32_t(p.tiles[i]); a.pad[i] = p.pad[i];
     }
-    dim3 grid(unsigned((p.T_pad + 255) / 256), unsigned(p.C_pad));
+    constexpr int GPW = 256 / (BLK * CG);
+    const int64_t groups = p.C_pad / CG;
+    dim3 grid(unsigned(p.T_pad / BLK), unsigned((groups + GPW - 1) / GPW));
     hipLaunchKernelGGL((k_input<N, MM, R, CONST>), grid, dim3(256), 0, s, x, V, a, p.fm);
     return launch_status();
   }
@@ -115,8 +128,8 @@ struct Launch {
     g.nblocks = int32_t(nb);
     for (int i = 0; i < 3; ++i) { g.tiles[i] = int32_t(p.tiles[i]); g.Y[i] = int32_t(p.Y[i]); }
     g.relu = (p.flags & WINO_RELU) ? 1 : 0;
-    hipLaunchKernelGGL((k_gemm_inv<N, MM, R, CONST, BLK, NW>), dim3(unsigned(nb)), dim3(NW * 64), 0,
-                       s, V, U, y, g, p.fm);
+    hipLaunchKernelGGL((k_gemm_inv<N, MM, R, CONST, BLK, NW, LOC, VEC, DEPTH>), dim3(unsigned(nb)),
+                       dim3(Geo::NT), 0, s, V, U, y, g, p.fm);
     return launch_status();
   }
 };
@@ -132,6 +145,14 @@ wino_status dispatch(const wino_plan_s& p, F&& f) {
   WINO_CASE(3, 4, 3)
 #undef WINO_CASE
   return WINO_EUNSUPPORTED;
+}
+
+int channel_group(int N, int m, int r) {
+  if (N == 2 && m == 2 && r == 3) return Blocking<2, 2, 3>::CG;
+  if (N == 3 && m == 2 && r == 3) return Blocking<3, 2, 3>::CG;
+  if (N == 2 && m == 4 && r == 3) return Blocking<2, 4, 3>::CG;
+  if (N == 3 && m == 4 && r == 3) return Blocking<3, 4, 3>::CG;
+  return 1;
 }
 
 int block_for(int N, int m, int r) {
@@ -176,12 +197,12 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   }
   p.T = T;
   p.blk = block_for(N, m, r);
-  p.nw = 4;
   p.T_pad = round_up(T, p.blk);
-  p.C_pad = int(round_up(C, p.blk == 32 ? 2 : 4));
+  p.cg = channel_group(N, m, r);
+  p.C_pad = int(round_up(C, p.cg));  // whole channel groups
   p.K_pad = int(round_up(K, p.blk));
   if (p.T_pad > kMaxI32) return WINO_EINVAL;
-  if (p.C_pad > 65535) return WINO_EINVAL;  // the input transform puts channels on grid.y
+  if (p.C_pad > (1 << 18)) return WINO_EINVAL;  // bounds the input-transform grid
   p.nxi = 1;
   for (int i = 0; i < N; ++i) p.nxi *= alpha;
   if ((p.T_pad / p.blk) * (p.K_pad / p.blk) > kMaxI32) return WINO_EINVAL;
@@ -234,6 +255,7 @@ wino_status wino_plan_describe(const wino_plan_t* p, wino_plan_desc* d) {
   for (int i = 0; i < 3; ++i) { d->X[i] = p->X[i]; d->Y[i] = p->Y[i]; d->tiles[i] = p->tiles[i]; }
   d->T = p->T; d->T_pad = p->T_pad;
   d->block_tiles = p->blk; d->block_kernels = p->blk;
+  d->channel_group = p->cg;
   d->default_points = p->const_mats ? 1 : 0;
   return WINO_OK;
 }

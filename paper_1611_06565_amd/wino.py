@@ -42,7 +42,7 @@ class _Desc(ctypes.Structure):
                 ("X", ctypes.c_int64 * 3), ("Y", ctypes.c_int64 * 3), ("tiles", ctypes.c_int64 * 3),
                 ("T", ctypes.c_int64), ("T_pad", ctypes.c_int64),
                 ("block_tiles", ctypes.c_int32), ("block_kernels", ctypes.c_int32),
-                ("default_points", ctypes.c_int32)]
+                ("default_points", ctypes.c_int32), ("channel_group", ctypes.c_int32)]
 
 
 _LIB = None
@@ -192,8 +192,24 @@ class Plan:
 
     def new_filter(self):
         import torch
+        return torch.empty(self.filter_bytes // 4, dtype=torch.float32, device="cuda")
+
+    def unpack_filter(self, U):
+        """U (device or host) -> numpy [alpha^N][C_pad][K_pad] in plain order."""
         d = self.desc
-        return torch.empty((d["n_xi"], d["C_pad"], d["K_pad"]), dtype=torch.float32, device="cuda")
+        cg = d["channel_group"]
+        u = U.detach().cpu().numpy() if hasattr(U, "detach") else np.asarray(U)
+        u = u.reshape(d["n_xi"], d["C_pad"] // cg, d["K_pad"], cg)
+        return u.transpose(0, 1, 3, 2).reshape(d["n_xi"], d["C_pad"], d["K_pad"])
+
+    def unpack_workspace(self, ws):
+        """V workspace (device or host) -> numpy [alpha^N][C_pad][T_pad] in plain order."""
+        d = self.desc
+        cg, b = d["channel_group"], d["block_tiles"]
+        v = ws.detach().cpu().numpy() if hasattr(ws, "detach") else np.asarray(ws)
+        v = v[: d["n_xi"] * d["C_pad"] * d["T_pad"]]
+        v = v.reshape(d["T_pad"] // b, d["n_xi"], d["C_pad"] // cg, b, cg)
+        return v.transpose(1, 2, 4, 0, 3).reshape(d["n_xi"], d["C_pad"], d["T_pad"])
 
     def new_workspace(self):
         import torch
