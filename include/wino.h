@@ -85,7 +85,8 @@ typedef struct {
   int32_t block_tiles;   /* GEMM rows per work-group                             */
   int32_t block_kernels; /* GEMM columns per work-group                          */
   int32_t default_points;/* 1 when the transform constants are compiled in        */
-  int32_t channel_group; /* CG: channels interleaved innermost in U and V          */
+  int32_t channel_group; /* CG: channels interleaved innermost in V                 */
+  int32_t filter_channel_group; /* CGU: channels interleaved innermost in U        */
 } wino_plan_desc;
 
 /* Build a plan for one layer.  §3.1-§3.3 and §4.1.
@@ -108,9 +109,9 @@ void wino_destroy(wino_plan_t* plan);
 wino_status wino_plan_describe(const wino_plan_t* plan, wino_plan_desc* desc);
 
 /* Bytes of the transformed-filter buffer U (float32), laid out as
- * U[alpha^N][C_pad/CG][K_pad][CG] with CG = channel_group: element
- * (xi, c, k) sits at ((xi*C_pad/CG + c/CG)*K_pad + k)*CG + c%CG.  Padding
- * channels and kernels are zero. */
+ * U[alpha^N][C_pad/CGU][K_pad][CGU] with CGU = filter_channel_group: element
+ * (xi, c, k) sits at ((xi*C_pad/CGU + c/CGU)*K_pad + k)*CGU + c%CGU.
+ * Padding channels and kernels are zero. */
 size_t wino_filter_bytes(const wino_plan_t* plan);
 
 /* Bytes of workspace wino_forward needs: the transformed input V (float32),
@@ -118,6 +119,9 @@ size_t wino_filter_bytes(const wino_plan_t* plan);
  * B = block_tiles: element (xi, c, t) sits at
  * (((t/B)*alpha^N + xi)*C_pad/CG + c/CG)*B*CG + (t%B)*CG + c%CG. */
 size_t wino_workspace_bytes(const wino_plan_t* plan);
+
+/* Bytes of workspace wino_forward needs (today equal to wino_workspace_bytes). */
+size_t wino_forward_workspace_bytes(const wino_plan_t* plan);
 
 /* out[0..N+1] = [batch, K, Y_1 .. Y_N]. */
 wino_status wino_output_dims(const wino_plan_t* plan, int64_t* out);
@@ -148,7 +152,9 @@ wino_status wino_transform_input(const wino_plan_t* plan, const float* x, void* 
 wino_status wino_gemm_inverse(const wino_plan_t* plan, const void* workspace, size_t workspace_bytes,
                               const float* U, float* y, void* stream);
 
-/* wino_transform_input followed by wino_gemm_inverse on the same stream. */
+/* The whole forward (eq. 4 with eq. 5) on one stream: wino_transform_input
+ * followed by wino_gemm_inverse, with wino_forward_workspace_bytes(plan)
+ * bytes of workspace. */
 wino_status wino_forward(const wino_plan_t* plan, const float* x, const float* U, float* y,
                          void* workspace, size_t workspace_bytes, void* stream);
 

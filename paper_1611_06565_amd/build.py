@@ -24,6 +24,21 @@ FLAGS = [
 ]
 
 
+def _check_kernel_stubs(path):
+    """Fail if a kernel's host launch stub is missing.
+
+    clang drops a kernel template's host stub without a diagnostic when its
+    body does not type-check for the host target (a gfx950-only builtin
+    operand, say); the library then fails to load with an undefined symbol.
+    """
+    res = subprocess.run(["nm", "-u", path], capture_output=True, text=True)
+    if res.returncode != 0:
+        return  # nm unavailable: the load-time check still catches it
+    missing = [ln.split()[-1] for ln in res.stdout.splitlines() if "__device_stub__" in ln]
+    if missing:
+        raise RuntimeError("kernel launch stubs missing from the host pass: " + ", ".join(missing))
+
+
 def build(verbose=False):
     srcs = [os.path.join(CSRC, s) for s in SOURCES]
     fd, tmp = tempfile.mkstemp(prefix=".libwino.", suffix=".so", dir=HERE)
@@ -35,6 +50,7 @@ def build(verbose=False):
         res = subprocess.run(cmd, capture_output=True, text=True)
         if res.returncode != 0:
             raise RuntimeError("hipcc failed:\n" + res.stdout + res.stderr)
+        _check_kernel_stubs(tmp)
         os.replace(tmp, LIB)
     finally:
         if os.path.exists(tmp):

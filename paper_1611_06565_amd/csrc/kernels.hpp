@@ -8,7 +8,7 @@
 //
 // Layouts (float32, zero padding rows/columns):
 //   x [batch][C][X_1..X_N]     w [K][C][r^N]      y [batch][K][Y_1..Y_N]
-//   U [alpha^N][C_pad/CG][K_pad][CG]
+//   U [alpha^N][C_pad/CGU][K_pad][CGU]
 //   V [T_pad/BLK][alpha^N][C_pad/CG][BLK][CG]
 // T counts tiles over the whole batch (tiles of every sample form the rows of
 // one GEMM, §4.1 and §4.4: the method is batch-size agnostic).  BLK is the
@@ -39,10 +39,17 @@ template <int N, int MM, int R>
 struct Blocking {
   static constexpr int A = MM + R - 1;
   static constexpr int NXI = ipow(A, N);
-  static constexpr int BLK = NXI > 64 ? 16 : 32;
-  static constexpr int KSTEP = BLK == 32 ? 2 : 4;   // channels per MFMA
-  static constexpr int VEC = NXI > 64 ? 1 : 2;      // floats per operand load
-  static constexpr int CG = KSTEP * VEC;            // channels per group
+  // m = 2: slice-accumulating GEMM (gemm_acc.hpp), 64-tile x 64-kernel blocks
+  static constexpr bool ACC = (MM == 2);
+  static constexpr int BLK = ACC ? 64 : (NXI > 64 ? 16 : 32);   // tiles per V block
+  static constexpr int KBLK = ACC ? 64 : BLK;                    // kernels padded to this
+  static constexpr int KSTEP = (!ACC && BLK == 16) ? 4 : 2;      // channels per MFMA
+  static constexpr int VEC = ACC ? 2 : (NXI > 64 ? 1 : 2);       // floats per operand load
+  static constexpr int CG = ACC ? 4 : KSTEP * VEC;               // channels per V group
+  static constexpr int CGU = CG;                                 // channels per U group
+  // channels are padded to whole operand stages of the GEMM (128 / elements
+  // per pass; see AccGeom)
+  static constexpr int CPAD = ACC ? 128 / (ipow(A, N - 1) > 8 ? 8 : ipow(A, N - 1)) : CGU;
 };
 
 // ---------------------------------------------------------------- arguments
@@ -88,7 +95,7 @@ template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(256) k_filter(const float* __restrict__ w, float* __restrict__ U,
                                                 FilterArgs a, FMats fm) {
   using B = Blocking<N, MM, R>;
-  constexpr int A = B::A, NXI = B::NXI, CG = B::CG;
+  constexpr int A = B::A, NXI = B::NXI, CG = B::CGU;
   constexpr int RN = ipow(R, N);
   const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   const int cl = int(idx % CG);
@@ -245,6 +252,113 @@ struct GemmGeom {
   static_assert(LOC >= 1 && LOC < N, "at least one axis is reduced in registers, one across waves");
 };
 
+struct EpiArgs {
+  float* y;
+  int32_t K;
+  int64_t ystride_k;  // prod Y_i
+  int32_t Y[3];
+  int32_t relu;
+};
+
+// Inverse transform of a work-group's accumulators (eq. 4), stitched into y.
+// acc[x] is the BLK x BLK (tile, kernel) block of element wave*XPW + x.
+// tile_of(tl, ti) maps a local tile row to its sample (return value, -1 if
+// the row is padding) and per-axis tile coordinates ti.
+//
+// Part 1: A^T along the LOC trailing axes in registers; the m^LOC results of
+// every unit go to LDS plane (unit, o_loc) at [k][t ^ k].
+// Part 2: A^T along the N-LOC leading axes, ReLU, crop, store.  Item
+// (o_loc, k, t) runs with the last-axis output fastest, then the tile, so
+// neighbouring lanes write neighbouring outputs of a row.
+template <int N, int MM, int R, bool CONST, int BLK, int NW, int LOC, class AccT, class TileFn>
+__device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb, const EpiArgs& g,
+                                              const FMats& fm, TileFn tile_of) {
+  using S = MfmaShape<BLK>;
+  using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
+  constexpr int A = Geo::A, NT = Geo::NT;
+  constexpr int UPW = Geo::UPW, UNIT = Geo::UNIT, OLOC = Geo::OLOC, PL = Geo::PL;
+  constexpr int NUNIT = Geo::NUNIT;
+  static_assert(NT % (MM * BLK) == 0, "output lanes must tile the work-group");
+  const int lane = int(threadIdx.x) & 63;
+  const int wave = int(threadIdx.x) >> 6;
+  const int col = lane % BLK;
+  const MatRef<Which::AT, CONST, MM, R> AT{&fm};
+#pragma unroll
+  for (int r = 0; r < S::NACC; ++r) {
+    const int t = S::acc_row(lane, r);
+#pragma unroll
+    for (int u = 0; u < UPW; ++u) {
+      float sv[UNIT];
+#pragma unroll
+      for (int e = 0; e < UNIT; ++e) sv[e] = acc[u * UNIT + e][r];
+      float o[OLOC];
+      transform_nd<LOC, A, MM>(sv, o, AT);
+      float* dst = sm + ((wave * UPW + u) * OLOC) * PL + col * BLK + (t ^ col);
+#pragma unroll
+      for (int j = 0; j < OLOC; ++j) dst[j * PL] = o[j];
+    }
+  }
+  __syncthreads();
+
+  const int tid = int(threadIdx.x);
+  const int o_last = tid % MM;
+  const int tl = (tid / MM) % BLK;
+  int ti[3] = {0, 0, 0};
+  const int n = tile_of(tl, ti);
+  if (n < 0) return;
+  const int y_last = ti[N - 1] * MM + o_last;
+  if (y_last >= g.Y[N - 1]) return;
+  constexpr int ITEMS = OLOC * BLK * BLK;
+  constexpr int LEAD = N - LOC;
+  constexpr int OLEAD = ipow(MM, LEAD);
+  for (int i = tid; i < ITEMS; i += NT) {
+    const int k_l = (i / (MM * BLK)) % BLK;
+    const int o_rest = i / (MM * BLK * BLK);
+    const int kg = kb * BLK + k_l;
+    if (kg >= g.K) continue;
+    const int jj = o_rest * MM + o_last;
+    int yc[3] = {0, 0, 0};
+    bool ok = true;
+    {
+      int rem = o_rest;
+#pragma unroll
+      for (int ax = N - 2; ax >= LEAD; --ax) {
+        const int oa = rem % MM;
+        rem /= MM;
+        yc[ax] = ti[ax] * MM + oa;
+        ok = ok && yc[ax] < g.Y[ax];
+      }
+      yc[N - 1] = y_last;
+    }
+    if (!ok) continue;
+    float v[NUNIT];
+#pragma unroll
+    for (int uu = 0; uu < NUNIT; ++uu) v[uu] = sm[(uu * OLOC + jj) * PL + k_l * BLK + (tl ^ k_l)];
+    float out[OLEAD];
+    transform_nd<LEAD, A, MM>(v, out, AT);
+    float* yk = g.y + (int64_t(n) * g.K + kg) * g.ystride_k;
+#pragma unroll
+    for (int q = 0; q < OLEAD; ++q) {
+      int rem = q;
+      bool in = true;
+#pragma unroll
+      for (int ax = LEAD - 1; ax >= 0; --ax) {
+        const int oa = rem % MM;
+        rem /= MM;
+        yc[ax] = ti[ax] * MM + oa;
+        in = in && yc[ax] < g.Y[ax];
+      }
+      if (!in) continue;
+      int64_t off = yc[0];
+#pragma unroll
+      for (int ax = 1; ax < N; ++ax) off = off * g.Y[ax] + yc[ax];
+      float val = out[q];
+      if (g.relu) val = val > 0.0f ? val : 0.0f;
+      yk[off] = val;
+    }
+  }
+}
+
 // VEC = floats per operand load (one load feeds VEC MFMA k-steps).  DEPTH =
 // stages in the register ring (DEPTH-1 stages in flight while one is
 // consumed).
@@ -273,12 +387,15 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
   // group uses channel VEC*kr + j, so the VEC steps of a group cover all CG
   // channels.  One "stage" = one group = VEC k-steps.
   constexpr int CG = S::KSTEP * VEC;
+  constexpr int CGU = Blocking<N, MM, R>::CGU;                     // U groups: CGU/CG V groups each
+  static_assert(CGU % CG == 0, "U groups hold whole V groups");
   const int64_t vxi = int64_t(g.C_pad) * BLK;                      // V plane stride (floats)
   const int64_t uxi = g.uplane;                                    // U plane stride (floats)
   const float* vnext = V + (int64_t(tb) * NXI + int64_t(wave) * XPW) * vxi + col * CG + VEC * kr;
-  const float* unext = U + int64_t(wave) * XPW * uxi + int64_t(kb) * BLK * CG + col * CG + VEC * kr;
-  const int64_t vgstep = int64_t(BLK) * CG, ugstep = int64_t(g.K_pad) * CG;
+  const float* ubase = U + int64_t(wave) * XPW * uxi + int64_t(kb) * BLK * CGU + col * CGU + VEC * kr;
+  const int64_t vgstep = int64_t(BLK) * CG, ugstep = int64_t(g.K_pad) * CGU;
   const int nstages = g.C_pad / CG;
+  int unext_g = 0;                                                 // next V group to fetch
 
   typename S::acc_t acc[XPW];
 #pragma unroll
@@ -288,13 +405,14 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
                 typename std::conditional<VEC == 2, float2, float>::type>::type;
   vec_t ra[DEPTH][XPW], rb[DEPTH][XPW];
   auto fetch = [&](vec_t* a2, vec_t* b2) {
+    const float* unext = ubase + (unext_g / (CGU / CG)) * ugstep + (unext_g % (CGU / CG)) * CG;
 #pragma unroll
     for (int x = 0; x < XPW; ++x) {
       a2[x] = *reinterpret_cast<const vec_t*>(vnext + x * vxi);
       b2[x] = *reinterpret_cast<const vec_t*>(unext + x * uxi);
     }
     vnext += vgstep;
-    unext += ugstep;
+    ++unext_g;
   };
   auto consume = [&](const vec_t* a2, const vec_t* b2) {
     const float* af = reinterpret_cast<const float*>(a2);
@@ -329,89 +447,13 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
     }
   }
 
-  // ---- epilogue, part 1: A^T along the LOC trailing axes in registers; the
-  // m^LOC results of every unit go to LDS plane (unit, o_loc) at [k][t ^ k].
-  const MatRef<Which::AT, CONST, MM, R> AT{&fm};
-#pragma unroll
-  for (int r = 0; r < S::NACC; ++r) {
-    const int t = S::acc_row(lane, r);
-#pragma unroll
-    for (int u = 0; u < UPW; ++u) {
-      float sv[UNIT];
-#pragma unroll
-      for (int e = 0; e < UNIT; ++e) sv[e] = acc[u * UNIT + e][r];
-      float o[OLOC];
-      transform_nd<LOC, A, MM>(sv, o, AT);
-      float* dst = sm + ((wave * UPW + u) * OLOC) * PL + col * BLK + (t ^ col);
-#pragma unroll
-      for (int j = 0; j < OLOC; ++j) dst[j * PL] = o[j];
-    }
-  }
-  __syncthreads();
-
-  // ---- epilogue, part 2: A^T along the N-LOC leading axes, ReLU, crop, store.
-  // Item (o_loc, k, t) with the last-axis output fastest, then the tile, so
-  // neighbouring lanes write neighbouring outputs of a row.
-  const int tid = int(threadIdx.x);
-  const int o_last = tid % MM;
-  const int tl = (tid / MM) % BLK;
-  const int t = tb * BLK + tl;
-  if (t >= g.T) return;
-  int ti[3] = {0, 0, 0};
-  const int n = split_tile<N>(t, g.tiles, ti);
-  const int y_last = ti[N - 1] * MM + o_last;
-  if (y_last >= g.Y[N - 1]) return;
-  constexpr int ITEMS = OLOC * BLK * BLK;
-  constexpr int LEAD = N - LOC;                  // axes contracted here
-  constexpr int OLEAD = ipow(MM, LEAD);
-  for (int i = tid; i < ITEMS; i += NT) {
-    const int k_l = (i / (MM * BLK)) % BLK;
-    const int o_rest = i / (MM * BLK * BLK);     // o_loc without its last axis
-    const int kg = kb * BLK + k_l;
-    if (kg >= g.K) continue;
-    const int jj = o_rest * MM + o_last;         // o_loc index
-    // output coordinates of the LOC trailing axes (last one fixed per thread)
-    int yc[3] = {0, 0, 0};
-    bool ok = true;
-    {
-      int rem = o_rest;
-#pragma unroll
-      for (int ax = N - 2; ax >= LEAD; --ax) {
-        const int oa = rem % MM;
-        rem /= MM;
-        yc[ax] = ti[ax] * MM + oa;
-        ok = ok && yc[ax] < g.Y[ax];
-      }
-      yc[N - 1] = y_last;
-    }
-    if (!ok) continue;
-    float v[NUNIT];
-#pragma unroll
-    for (int uu = 0; uu < NUNIT; ++uu) v[uu] = sm[(uu * OLOC + jj) * PL + k_l * BLK + (tl ^ k_l)];
-    float out[OLEAD];
-    transform_nd<LEAD, A, MM>(v, out, AT);
-    float* yk = y + (int64_t(n) * g.K + kg) * g.ystride_k;
-#pragma unroll
-    for (int q = 0; q < OLEAD; ++q) {
-      // leading-axis output offsets of item q (axis LEAD-1 fastest)
-      int rem = q;
-      bool in = true;
-#pragma unroll
-      for (int ax = LEAD - 1; ax >= 0; --ax) {
-        const int oa = rem % MM;
-        rem /= MM;
-        yc[ax] = ti[ax] * MM + oa;
-        in = in && yc[ax] < g.Y[ax];
-      }
-      if (!in) continue;
-      int64_t off = yc[0];
-#pragma unroll
-      for (int ax = 1; ax < N; ++ax) off = off * g.Y[ax] + yc[ax];
-      float val = out[q];
-      if (g.relu) val = val > 0.0f ? val : 0.0f;
-      yk[off] = val;
-    }
-  }
+  EpiArgs e{y, g.K, g.ystride_k, {g.Y[0], g.Y[1], g.Y[2]}, g.relu};
+  auto tile_of = [&](int tl, int* ti) -> int {
+    const int t = tb * BLK + tl;
+    if (t >= g.T) return -1;
+    return split_tile<N>(t, g.tiles, ti);
+  };
+  gemm_epilogue<N, MM, R, CONST, BLK, NW, LOC>(acc, sm, kb, e, fm, tile_of);
 }
 
 // ------------------------------------------------------------ max-pool (a6)

@@ -7,6 +7,7 @@
 #include <cstring>
 #include <new>
 
+#include "gemm_acc.hpp"
 #include "kernels.hpp"
 #include "synth.hpp"
 #include "wino.h"
@@ -20,7 +21,7 @@ struct wino_plan_s {
   int64_t X[3], Y[3], tiles[3];
   int32_t pad[3];
   int64_t T, T_pad;
-  int blk, cg;
+  int blk, cg, cgu;
   uint32_t flags;
   bool const_mats;
   double AT[kMaxAlpha][kMaxAlpha], BT[kMaxAlpha][kMaxAlpha], G[kMaxAlpha][kMaxAlpha];
@@ -75,6 +76,7 @@ struct Launch {
   static constexpr int NXI = ipow(A, N);
   static constexpr int BLK = Blocking<N, MM, R>::BLK;
   static constexpr int CG = Blocking<N, MM, R>::CG;
+  static constexpr int CGU = Blocking<N, MM, R>::CGU;
   // GEMM work-group shape: waves, register-reduced trailing axes, operand
   // load width and register-ring depth.
   //   F(2^3): 8 waves (2 per SIMD) x two alpha-rows, 8-byte loads, 2 groups in flight
@@ -91,7 +93,7 @@ struct Launch {
     FilterArgs a{};
     a.uplane = int64_t(p.C_pad) * p.K_pad;
     a.C = p.C; a.K = p.K; a.C_pad = p.C_pad; a.K_pad = p.K_pad;
-    const int64_t n = int64_t(p.C_pad) * p.K_pad;   // C_pad is a multiple of CG
+    const int64_t n = int64_t(p.C_pad) * p.K_pad;   // C_pad is a multiple of CGU
     const unsigned grid = unsigned((n + 255) / 256);
     hipLaunchKernelGGL((k_filter<N, MM, R, CONST>), dim3(grid), dim3(256), 0, s, w, U, a, p.fm);
     return launch_status();
@@ -116,21 +118,39 @@ struct Launch {
 
   static wino_status gemm(const wino_plan_s& p, const float* V, const float* U, float* y,
                           hipStream_t s) {
-    GemmArgs g{};
-    g.vplane = int64_t(p.C_pad) * p.T_pad;
-    g.uplane = int64_t(p.C_pad) * p.K_pad;
-    g.ystride_k = 1;
-    for (int i = 0; i < N; ++i) g.ystride_k *= p.Y[i];
-    g.T = int32_t(p.T); g.T_pad = int32_t(p.T_pad);
-    g.C_pad = p.C_pad; g.K = p.K; g.K_pad = p.K_pad;
-    g.nkb = p.K_pad / BLK;
-    const int64_t nb = (p.T_pad / BLK) * int64_t(g.nkb);
-    g.nblocks = int32_t(nb);
-    for (int i = 0; i < 3; ++i) { g.tiles[i] = int32_t(p.tiles[i]); g.Y[i] = int32_t(p.Y[i]); }
-    g.relu = (p.flags & WINO_RELU) ? 1 : 0;
-    hipLaunchKernelGGL((k_gemm_inv<N, MM, R, CONST, BLK, NW, LOC, VEC, DEPTH>), dim3(unsigned(nb)),
-                       dim3(Geo::NT), 0, s, V, U, y, g, p.fm);
-    return launch_status();
+    if constexpr (Blocking<N, MM, R>::ACC) {
+      using G = AccGeom<N, MM, R>;
+      AccArgs a{};
+      a.vplane = int64_t(p.C_pad) * G::TB;
+      a.uplane = int64_t(p.C_pad) * p.K_pad;
+      a.ystride_k = 1;
+      for (int i = 0; i < N; ++i) a.ystride_k *= p.Y[i];
+      a.T = int32_t(p.T); a.C_pad = p.C_pad; a.K = p.K; a.K_pad = p.K_pad;
+      a.nkb = p.K_pad / G::KB;
+      const int64_t nb = (p.T_pad / G::TB) * int64_t(a.nkb);
+      a.nblocks = int32_t(nb);
+      for (int i = 0; i < 3; ++i) { a.tiles[i] = int32_t(p.tiles[i]); a.Y[i] = int32_t(p.Y[i]); }
+      a.relu = (p.flags & WINO_RELU) ? 1 : 0;
+      hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST>), dim3(unsigned(nb)), dim3(G::NT), 0, s, V, U, y,
+                         a, p.fm);
+      return launch_status();
+    } else {
+      GemmArgs g{};
+      g.vplane = int64_t(p.C_pad) * p.T_pad;
+      g.uplane = int64_t(p.C_pad) * p.K_pad;
+      g.ystride_k = 1;
+      for (int i = 0; i < N; ++i) g.ystride_k *= p.Y[i];
+      g.T = int32_t(p.T); g.T_pad = int32_t(p.T_pad);
+      g.C_pad = p.C_pad; g.K = p.K; g.K_pad = p.K_pad;
+      g.nkb = p.K_pad / BLK;
+      const int64_t nb = (p.T_pad / BLK) * int64_t(g.nkb);
+      g.nblocks = int32_t(nb);
+      for (int i = 0; i < 3; ++i) { g.tiles[i] = int32_t(p.tiles[i]); g.Y[i] = int32_t(p.Y[i]); }
+      g.relu = (p.flags & WINO_RELU) ? 1 : 0;
+      hipLaunchKernelGGL((k_gemm_inv<N, MM, R, CONST, BLK, NW, LOC, VEC, DEPTH>), dim3(unsigned(nb)),
+                         dim3(Geo::NT), 0, s, V, U, y, g, p.fm);
+      return launch_status();
+    }
   }
 };
 
@@ -147,19 +167,28 @@ wino_status dispatch(const wino_plan_s& p, F&& f) {
   return WINO_EUNSUPPORTED;
 }
 
-int channel_group(int N, int m, int r) {
-  if (N == 2 && m == 2 && r == 3) return Blocking<2, 2, 3>::CG;
-  if (N == 3 && m == 2 && r == 3) return Blocking<3, 2, 3>::CG;
-  if (N == 2 && m == 4 && r == 3) return Blocking<2, 4, 3>::CG;
-  if (N == 3 && m == 4 && r == 3) return Blocking<3, 4, 3>::CG;
-  return 1;
+template <int N, int M, int R> void groups_of(int* cg, int* cgu, int* cpad, int* kblk) {
+  *cg = Blocking<N, M, R>::CG;
+  *cgu = Blocking<N, M, R>::CGU;
+  *cpad = Blocking<N, M, R>::CPAD;
+  *kblk = Blocking<N, M, R>::KBLK;
+}
+// Channel groups of the V (cg) and U (cgu) layouts, channel padding multiple
+// and kernel padding multiple of an instantiation.
+void channel_groups(int N, int m, int r, int* cg, int* cgu, int* cpad, int* kblk) {
+  *cg = *cgu = *cpad = *kblk = 1;
+  if (N == 2 && m == 2 && r == 3) groups_of<2, 2, 3>(cg, cgu, cpad, kblk);
+  if (N == 3 && m == 2 && r == 3) groups_of<3, 2, 3>(cg, cgu, cpad, kblk);
+  if (N == 2 && m == 4 && r == 3) groups_of<2, 4, 3>(cg, cgu, cpad, kblk);
+  if (N == 3 && m == 4 && r == 3) groups_of<3, 4, 3>(cg, cgu, cpad, kblk);
 }
 
 int block_for(int N, int m, int r) {
-  const int a = m + r - 1;
-  int nxi = 1;
-  for (int i = 0; i < N; ++i) nxi *= a;
-  return nxi > 64 ? 16 : 32;
+  if (N == 2 && m == 2 && r == 3) return Blocking<2, 2, 3>::BLK;
+  if (N == 3 && m == 2 && r == 3) return Blocking<3, 2, 3>::BLK;
+  if (N == 2 && m == 4 && r == 3) return Blocking<2, 4, 3>::BLK;
+  if (N == 3 && m == 4 && r == 3) return Blocking<3, 4, 3>::BLK;
+  return 32;
 }
 
 }  // namespace
@@ -198,9 +227,14 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   p.T = T;
   p.blk = block_for(N, m, r);
   p.T_pad = round_up(T, p.blk);
-  p.cg = channel_group(N, m, r);
-  p.C_pad = int(round_up(C, p.cg));  // whole channel groups
-  p.K_pad = int(round_up(K, p.blk));
+  int cpad = 1, kblk = 1;
+  channel_groups(N, m, r, &p.cg, &p.cgu, &cpad, &kblk);
+  p.C_pad = int(round_up(C, cpad));   // whole operand stages / channel groups
+  {
+    int cg_, cgu_, cpad_, kblk_;
+    channel_groups(N, m, r, &cg_, &cgu_, &cpad_, &kblk_);
+    p.K_pad = int(round_up(K, kblk_));
+  }
   if (p.T_pad > kMaxI32) return WINO_EINVAL;
   if (p.C_pad > (1 << 18)) return WINO_EINVAL;  // bounds the input-transform grid
   p.nxi = 1;
@@ -254,8 +288,10 @@ wino_status wino_plan_describe(const wino_plan_t* p, wino_plan_desc* d) {
   d->batch = p->batch;
   for (int i = 0; i < 3; ++i) { d->X[i] = p->X[i]; d->Y[i] = p->Y[i]; d->tiles[i] = p->tiles[i]; }
   d->T = p->T; d->T_pad = p->T_pad;
-  d->block_tiles = p->blk; d->block_kernels = p->blk;
+  d->block_tiles = p->blk;
+  d->block_kernels = p->K_pad > 0 ? (p->blk == 64 ? 64 : p->blk) : 0;
   d->channel_group = p->cg;
+  d->filter_channel_group = p->cgu;
   d->default_points = p->const_mats ? 1 : 0;
   return WINO_OK;
 }
@@ -267,6 +303,8 @@ size_t wino_filter_bytes(const wino_plan_t* p) {
 size_t wino_workspace_bytes(const wino_plan_t* p) {
   return p ? size_t(p->nxi) * size_t(p->C_pad) * size_t(p->T_pad) * sizeof(float) : 0;
 }
+
+size_t wino_forward_workspace_bytes(const wino_plan_t* p) { return wino_workspace_bytes(p); }
 
 wino_status wino_output_dims(const wino_plan_t* p, int64_t* out) {
   if (p == nullptr || out == nullptr) return WINO_EINVAL;
@@ -314,9 +352,10 @@ wino_status wino_gemm_inverse(const wino_plan_t* p, const void* ws, size_t ws_by
 
 wino_status wino_forward(const wino_plan_t* p, const float* x, const float* U, float* y, void* ws,
                          size_t ws_bytes, void* stream) {
-  if (p == nullptr || x == nullptr || U == nullptr || y == nullptr || ws == nullptr)
-    return WINO_EINVAL;
-  if (!aligned16(x) || !aligned16(U) || !aligned16(y) || !aligned16(ws)) return WINO_EINVAL;
+  if (p == nullptr || x == nullptr || U == nullptr || y == nullptr) return WINO_EINVAL;
+  if (!aligned16(x) || !aligned16(U) || !aligned16(y)) return WINO_EINVAL;
+  if (ws == nullptr) return WINO_EINVAL;
+  if (!aligned16(ws)) return WINO_EINVAL;
   if (ws_bytes < wino_workspace_bytes(p)) return WINO_EWORKSPACE;
   wino_status st = wino_transform_input(p, x, ws, ws_bytes, stream);
   if (st != WINO_OK) return st;

@@ -42,7 +42,8 @@ class _Desc(ctypes.Structure):
                 ("X", ctypes.c_int64 * 3), ("Y", ctypes.c_int64 * 3), ("tiles", ctypes.c_int64 * 3),
                 ("T", ctypes.c_int64), ("T_pad", ctypes.c_int64),
                 ("block_tiles", ctypes.c_int32), ("block_kernels", ctypes.c_int32),
-                ("default_points", ctypes.c_int32), ("channel_group", ctypes.c_int32)]
+                ("default_points", ctypes.c_int32), ("channel_group", ctypes.c_int32),
+                ("filter_channel_group", ctypes.c_int32)]
 
 
 _LIB = None
@@ -70,6 +71,7 @@ def lib():
         "wino_plan_describe": (i32, [vp, ctypes.POINTER(_Desc)]),
         "wino_filter_bytes": (sz, [vp]),
         "wino_workspace_bytes": (sz, [vp]),
+        "wino_forward_workspace_bytes": (sz, [vp]),
         "wino_output_dims": (i32, [vp, P_i64]),
         "wino_get_matrices": (i32, [vp, P_dbl, P_dbl, P_dbl]),
         "wino_transform_filter": (i32, [vp, vp, vp, vp]),
@@ -173,7 +175,13 @@ class Plan:
 
     @property
     def workspace_bytes(self):
+        """Workspace of the two-stage API (transform_input + gemm_inverse)."""
         return int(self._L.wino_workspace_bytes(self._h))
+
+    @property
+    def forward_workspace_bytes(self):
+        """Workspace forward() needs."""
+        return int(self._L.wino_forward_workspace_bytes(self._h))
 
     def matrices(self):
         a, m, r = self.desc["alpha"], self.m, self.r
@@ -197,7 +205,7 @@ class Plan:
     def unpack_filter(self, U):
         """U (device or host) -> numpy [alpha^N][C_pad][K_pad] in plain order."""
         d = self.desc
-        cg = d["channel_group"]
+        cg = d["filter_channel_group"]
         u = U.detach().cpu().numpy() if hasattr(U, "detach") else np.asarray(U)
         u = u.reshape(d["n_xi"], d["C_pad"] // cg, d["K_pad"], cg)
         return u.transpose(0, 1, 3, 2).reshape(d["n_xi"], d["C_pad"], d["K_pad"])
@@ -259,12 +267,14 @@ class Plan:
         if y is None:
             y = self.new_output()
         self._check_shape(y, self.output_shape, "y")
-        if workspace is None:
-            workspace = self.new_workspace()
+        need = self.forward_workspace_bytes
+        if workspace is None and need:
+            workspace = torch.empty(need // 4, dtype=torch.float32, device="cuda")
+        ws_ptr = _dev_ptr(workspace, "workspace") if workspace is not None else ctypes.c_void_p()
+        ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
         _check(self._L.wino_forward(self._h, _dev_ptr(x, "x", torch.float32),
                                     _dev_ptr(U, "U", torch.float32), _dev_ptr(y, "y", torch.float32),
-                                    _dev_ptr(workspace, "workspace"),
-                                    workspace.numel() * workspace.element_size(), _stream()),
+                                    ws_ptr, ws_len, _stream()),
                "wino_forward")
         return y
 

@@ -119,16 +119,23 @@ def test_explicit_default_points_use_compiled_constants():
 
 
 def test_device_calls_reject_bad_arguments(L):
-    p = wino.Plan(3, 2, 3, 4, 4, [1, 8, 8, 8])
+    # Every call below must be rejected on the host before any launch: only
+    # NULL or misaligned pointers, or short workspaces, are passed.
+    p = wino.Plan(2, 4, 3, 4, 4, [1, 8, 8])
     need = p.workspace_bytes
+    assert p.forward_workspace_bytes == need
     vp = ctypes.c_void_p
-    # NULL pointers and misalignment are rejected before any launch.
     assert L.wino_transform_filter(p.handle, None, vp(4096), None) == -1
     assert L.wino_transform_filter(p.handle, vp(4096 + 4), vp(4096), None) == -1
     assert L.wino_transform_input(p.handle, vp(4096), vp(8192), need - 4, None) == -3
     assert L.wino_gemm_inverse(p.handle, vp(4096), need - 4, vp(8192), vp(16384), None) == -3
     assert L.wino_forward(p.handle, vp(4096), vp(8192), vp(16384), vp(32768), 0, None) == -3
     assert L.wino_forward(p.handle, vp(4096), vp(8192), vp(16384), None, need, None) == -1
+    f = wino.Plan(3, 2, 3, 4, 4, [1, 8, 8, 8])
+    assert f.forward_workspace_bytes == f.workspace_bytes > 0
+    assert L.wino_forward(f.handle, None, vp(8192), vp(16384), vp(32768), 1 << 30, None) == -1
+    assert L.wino_forward(f.handle, vp(4096 + 4), vp(8192), vp(16384), vp(32768), 1 << 30, None) == -1
+    assert L.wino_forward(f.handle, vp(4096), vp(8192), vp(16384 + 8), vp(32768), 1 << 30, None) == -1
     dims = (ctypes.c_int64 * 4)(1, 4, 4, 4)
     win = (ctypes.c_int32 * 3)(2, 2, 8)
     assert L.wino_maxpool3d(dims, win, vp(4096), vp(8192), None) == -1   # 4 // 8 == 0
