@@ -23,6 +23,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "kernels.hpp"
 #include "synth.hpp"
@@ -45,9 +46,9 @@ template <int N, int MM, int R>
 struct AccGeom {
   static constexpr int A = MM + R - 1;
   static constexpr int NXI = ipow(A, N);
-  // elements per pass: whole rows of the last axis, at most 8 (128 accumulator
-  // registers, leaving room for the m^N output accumulators)
-  static constexpr int E = ipow(A, N - 1) > 8 ? 8 : ipow(A, N - 1);
+  // elements per pass: one row of the last axis (alpha accumulators of 16
+  // registers, leaving room for the m^N output accumulators and the operands)
+  static constexpr int E = A;
   static constexpr int RP = E / A;                // alpha-rows per pass
   static constexpr int NROW = ipow(A, N - 1);     // alpha-rows in all
   static constexpr int NPASS = NXI / E;
@@ -55,26 +56,52 @@ struct AccGeom {
   static constexpr int NLEAD = NOUT / MM;         // outputs of the leading axes
   static constexpr int TB = 64, KB = 64;          // tiles and kernels per work-group
   static constexpr int NW = 4, NT = 256;          // wave (tq, kq) owns a 32 x 32 quadrant
-  static constexpr int SC = 128 / E;              // channels per stage: 64 KB of operands
+  static constexpr int NBUF = 4;                  // stage buffers in LDS
+  static constexpr int DEPTH = 3;                 // stages in flight ahead of the one multiplied
+  static constexpr int SC = 64 / E;               // channels per stage: 32 KB of operands
   static constexpr int G4 = SC / 4;               // 4-channel groups per stage
-  static constexpr int GPW = G4 / NW;             // groups per wave in the copies
-  static constexpr int SA = E * G4 * TB * 4;      // floats of V per stage buffer
-  static constexpr int SB = E * G4 * KB * 4;      // floats of U per stage buffer
-  static constexpr int STAGE = SA + SB;
+  static constexpr int CH = E * G4;               // 1 KB chunks per operand per stage
+  static constexpr int CPW = CH / NW;             // chunks per operand per wave
+  static constexpr int SA = CH * 256;             // floats of V (and of U) per stage
+  static constexpr int STAGE = 2 * SA;
   static constexpr int PLANE = TB * KB;           // stitch plane of one output index
+  static constexpr int PPB = STAGE / PLANE;       // stitch planes per buffer
   static_assert(MM == 2, "m = 2 only: 2^N output accumulators per pair");
   static_assert(E % A == 0 && NXI % E == 0, "passes of whole alpha-rows");
   static_assert(SC % 8 == 0, "whole pairs of 4-channel groups per stage");
-  static_assert(G4 % NW == 0, "copies split evenly over the waves");
-  static_assert(NOUT % 2 == 0 && (NOUT / 2) * PLANE <= STAGE, "stitch fits the two buffers");
+  static_assert(CH % NW == 0, "copies split evenly over the waves");
+  static_assert(NOUT <= NBUF * PPB, "stitch fits the stage buffers");
+  static_assert(DEPTH < NBUF, "a buffer is refilled only after it was multiplied");
 };
 
 // One 16-byte direct-to-LDS copy per lane: lane l moves src[4l..4l+3] (its own
-// global address) to dst[4l..4l+3] (dst is wave-uniform).  A plain function,
-// not a template, so that the host pass never checks the builtin's gfx950-only
-// operand size against the host target.
+// global address) to dst[4l..4l+3] (dst is wave-uniform; M0 holds its LDS
+// byte address).  Written as inline assembly so that the compiler does not
+// track these copies: it would otherwise make LDS reads of other buffers wait
+// for them.  Every wait for the copies is explicit (s_waitcnt vmcnt), and the
+// stage barrier, which has a memory clobber, orders them against LDS reads.
 __device__ __forceinline__ void lds_copy16(const float* src, float* dst) {
-  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+  // the low 32 bits of a generic pointer into LDS are its LDS byte address
+  const uint32_t lds_addr =
+      __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst)));
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(src), "s"(lds_addr)
+      : "m0");
+}
+
+// Work-group barrier for the copy pipeline.  __syncthreads() carries a release
+// fence, which would wait for every copy still in flight (vmcnt(0)) and undo
+// the pipelining; here the waits are explicit: the caller waits for its own
+// copies of the step, and LDS reads are finished (lgkmcnt(0)) before any wave
+// may overwrite a buffer.  The memory clobber keeps the compiler from moving
+// memory accesses across it.
+__device__ __forceinline__ void stage_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);             // lgkmcnt(0), vmcnt and expcnt untouched
+  asm volatile("s_barrier" ::: "memory");
 }
 
 // Coefficient of alpha-row `row` (leading element indices, last axis
@@ -107,12 +134,22 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
   using G = AccGeom<N, MM, R>;
   using S = MfmaShape<32>;
   constexpr int A = G::A, E = G::E, NOUT = G::NOUT, G4 = G::G4, RP = G::RP;
-  constexpr int TB = G::TB, KB = G::KB, NW = G::NW;
+  constexpr int TB = G::TB, KB = G::KB, NW = G::NW, NBUF = G::NBUF, DEPTH = G::DEPTH;
 
-  // Two operand buffers as distinct LDS objects: the compiler can then tell
-  // that reads of one do not depend on the copies in flight into the other.
+  // The stage buffers are distinct LDS objects, always named with a
+  // compile-time index: the compiler can then tell that reads of one buffer
+  // do not depend on copies still in flight into another.
   __shared__ __attribute__((aligned(16))) float buf0[G::STAGE];
   __shared__ __attribute__((aligned(16))) float buf1[G::STAGE];
+  __shared__ __attribute__((aligned(16))) float buf2[G::STAGE];
+  __shared__ __attribute__((aligned(16))) float buf3[G::STAGE];
+  auto buf = [&](auto I) -> float* {
+    constexpr int b = decltype(I)::value % NBUF;
+    if constexpr (b == 0) return buf0;
+    else if constexpr (b == 1) return buf1;
+    else if constexpr (b == 2) return buf2;
+    else return buf3;
+  };
 
   const int tid = int(threadIdx.x);
   const int lane = tid & 63;
@@ -123,25 +160,34 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
   const int L = xcd_remap(int(blockIdx.x), g.nblocks);
   const int tb = L / g.nkb, kb = L % g.nkb;
   const int nstage = g.C_pad / G::SC;             // channel stages per pass
+  const int nsteps = G::NPASS * nstage;
 
-  // ---- direct-to-LDS copies of one (pass, stage) step.  Wave w copies the
-  // 4-channel groups gi = w + NW*j of every element of the pass: 1 KB chunks
-  // V[tb][xi][grp][0:64][0:4] and U[xi][grp][kb*64 : kb*64+64][0:4].
-  const float* vsrc = V + int64_t(tb) * G::NXI * g.vplane + wave * (TB * 4) + lane * 4;
-  const float* usrc = U + int64_t(kb) * (KB * 4) + int64_t(wave) * g.K_pad * 4 + lane * 4;
+  // ---- direct-to-LDS copies of one (pass, stage) step.  Chunk c of an
+  // operand is (element e, 4-channel group gi) = (c / G4, c % G4): 1 KB, either
+  // V[tb][xi][grp][0:64][0:4] or U[xi][grp][kb*64 : kb*64+64][0:4], landing at
+  // c * 256 floats of the V or U half of the buffer.  Wave w copies chunks
+  // w, w + NW, ...
+  const float* vsrc = V + int64_t(tb) * G::NXI * g.vplane + lane * 4;
+  const float* usrc = U + int64_t(kb) * (KB * 4) + lane * 4;
+  int64_t voff[G::CPW], uoff[G::CPW];
+#pragma unroll
+  for (int i = 0; i < G::CPW; ++i) {
+    const int c = wave + NW * i, e = c / G4, gi = c % G4;
+    voff[i] = e * g.vplane + gi * (TB * 4);
+    uoff[i] = e * g.uplane + int64_t(gi) * g.K_pad * 4;
+  }
   const int64_t vstage = int64_t(G4) * TB * 4, ustage = int64_t(G4) * g.K_pad * 4;
+  // copy q in [0, 2 * CPW) of a step: chunk q / 2 of V (q even) or of U (q odd)
+  auto copy_one = [&](const float* vs, const float* us, float* base, int q) {
+    const int i = q >> 1, c = wave + NW * i;
+    if ((q & 1) == 0) lds_copy16(vs + voff[i], base + c * 256);
+    else lds_copy16(us + uoff[i], base + G::SA + c * 256);
+  };
   auto issue = [&](float* base, int pass, int st) {
     const float* vs = vsrc + int64_t(pass) * E * g.vplane + st * vstage;
     const float* us = usrc + int64_t(pass) * E * g.uplane + st * ustage;
 #pragma unroll
-    for (int e = 0; e < E; ++e)
-#pragma unroll
-      for (int j = 0; j < G::GPW; ++j) {
-        const int gi = wave + NW * j;
-        lds_copy16(vs + e * g.vplane + j * (NW * TB * 4), base + (e * G4 + gi) * 256);
-        lds_copy16(us + e * g.uplane + int64_t(j) * NW * g.K_pad * 4,
-                   base + G::SA + (e * G4 + gi) * 256);
-      }
+    for (int q = 0; q < 2 * G::CPW; ++q) copy_one(vs, us, base, q);
   };
 
   typename S::acc_t acc[E];
@@ -155,78 +201,88 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
   const int aoff = (kr * TB + tq * 32 + col) * 4;
   const int boff = G::SA + (kr * KB + kq * 32 + col) * 4;
 
-  // One step: wait for this step's operands, free the other buffer, start the
-  // next step's copies into it, and multiply this one.
-  auto step = [&](const float* cur, float* nxt, bool more, int npass, int nst) {
-    __builtin_amdgcn_s_waitcnt(0x0f70);           // vmcnt(0), other counters untouched
-    __syncthreads();                              // everyone's copies landed; nxt is free
-    if (more) issue(nxt, npass, nst);
-    const float* sa = cur + aoff;
-    const float* sb = cur + boff;
-    // pair p of 4-channel groups: lane half kr reads group 2p + kr, so k-step
-    // j of the pair contracts channels 8p + j (kr = 0) and 8p + 4 + j (kr = 1).
-    // Operands go in groups of 4 elements; the next group is read from LDS
-    // while the MFMAs of this one run.
-    constexpr int NG = (G4 / 2) * (E / 4);        // (pair, element group) steps
-    float4 a4[2][4], b4[2][4];
-    auto read_group = [&](int gidx, int slot) {
-      const int p = gidx / (E / 4), e0 = (gidx % (E / 4)) * 4;
+  // copy cursor: the next step to copy, as (pass, stage)
+  int cpass = 0, cst = 0;
+  auto advance = [&]() {
+    if (++cst == nstage) { cst = 0; ++cpass; }
+  };
+
+  // Operands go in groups of 4 elements of one pair p of 4-channel groups:
+  // lane half kr reads group 2p + kr, so k-step j of the pair contracts
+  // channels 8p + j (kr = 0) and 8p + 4 + j (kr = 1).  Each group is read from
+  // LDS while the MFMAs of the previous one run, across step boundaries too.
+  constexpr int NG = (G4 / 2) * (E / 4);          // operand groups per step
+  static_assert(NG % 2 == 0, "a step's first group always uses slot 0");
+  float4 a4[2][4], b4[2][4];
+  auto read_one = [&](const float* base, int gidx, int slot, int q) {   // q: A of e = q/2 (even), B (odd)
+    const int p = gidx / (E / 4), e = (gidx % (E / 4)) * 4 + (q >> 1);
+    const int off = (e * G4 + 2 * p) * 256;
+    if ((q & 1) == 0) a4[slot][q >> 1] = *reinterpret_cast<const float4*>(base + aoff + off);
+    else b4[slot][q >> 1] = *reinterpret_cast<const float4*>(base + boff + off);
+  };
+  auto read_group = [&](const float* base, int gidx, int slot) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int off = ((e0 + e) * G4 + 2 * p) * 256;
-        a4[slot][e] = *reinterpret_cast<const float4*>(sa + off);
-        b4[slot][e] = *reinterpret_cast<const float4*>(sb + off);
-      }
-    };
-    read_group(0, 0);
+    for (int q = 0; q < 8; ++q) read_one(base, gidx, slot, q);
+  };
+  // The 16 MFMAs of group gidx from `slot`, in a fixed order with the reads of
+  // the next group (into the other slot) and, in a step's last group, the
+  // copies of a later step placed between them so that the matrix unit keeps
+  // being fed while they issue.
+  auto mma_group = [&](int gidx, int slot, const float* nbase, int ngidx, bool reading,
+                       bool copying, const float* vs, const float* us, float* cbase) {
+    const int e0 = (gidx % (E / 4)) * 4;
 #pragma unroll
-    for (int gi = 0; gi < NG; ++gi) {
-      const int slot = gi & 1;
-      if (gi + 1 < NG) read_group(gi + 1, slot ^ 1);
-      const int e0 = (gi % (E / 4)) * 4;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float4 av4 = a4[slot][e], bv4 = b4[slot][e];
-          const float av = j == 0 ? av4.x : j == 1 ? av4.y : j == 2 ? av4.z : av4.w;
-          const float bv = j == 0 ? bv4.x : j == 1 ? bv4.y : j == 2 ? bv4.z : bv4.w;
-          acc[e0 + e] = S::mma(av, bv, acc[e0 + e]);
-          if (gi + 1 < NG && j < 2) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        }
+    for (int m = 0; m < 16; ++m) {
+      const int j = m >> 2, e = m & 3;
+      const float4 av4 = a4[slot][e], bv4 = b4[slot][e];
+      const float av = j == 0 ? av4.x : j == 1 ? av4.y : j == 2 ? av4.z : av4.w;
+      const float bv = j == 0 ? bv4.x : j == 1 ? bv4.y : j == 2 ? bv4.z : bv4.w;
+      acc[e0 + e] = S::mma(av, bv, acc[e0 + e]);
+      if (reading && m < 8) read_one(nbase, ngidx, slot ^ 1, m);
+      if (copying && (m & 1)) copy_one(vs, us, cbase, m >> 1);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
+  static_assert(2 * G::CPW == 8, "one copy after every other MFMA of a group");
 
-  // The stages of one pass alternate between the buffers; which buffer comes
-  // first depends on the parity of the steps taken so far.  Both orders are
-  // inlined with constant buffer addresses.
-  auto run_pass = [&](float* b0, float* b1, int pass) __attribute__((always_inline)) {
-    const bool last_pass = pass + 1 == G::NPASS;
-    for (int st = 0; st < nstage; st += 2) {
-      {
-        const bool wrap = st + 1 == nstage;
-        step(b0, b1, !(wrap && last_pass), wrap ? pass + 1 : pass, wrap ? 0 : st + 1);
-      }
-      if (st + 1 < nstage) {
-        const bool wrap = st + 2 == nstage;
-        step(b1, b0, !(wrap && last_pass), wrap ? pass + 1 : pass, wrap ? 0 : st + 2);
+  // Step s multiplies buffer s % NBUF, whose first group is already in slot
+  // 0.  Before its last group it synchronises for step s + 1: wait for this
+  // wave's copies of s + 1 (those of s + 2 may stay in flight), barrier (all
+  // copies of s + 1 landed; nobody reads buffer (s - 1) % NBUF any more); the
+  // last group then refills that buffer with step s + DEPTH and reads the
+  // first group of s + 1.
+  auto step = [&](auto I, int s) {
+    constexpr int b = decltype(I)::value;
+    const float* cur = buf(I);
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi) {
+      const int slot = gi & 1;
+      if (gi + 1 < NG) {
+        mma_group(gi, slot, cur, gi + 1, true, false, nullptr, nullptr, nullptr);
+      } else if (s + 1 < nsteps) {
+        if (s + 2 < nsteps) {
+          __builtin_amdgcn_s_waitcnt(0x0f78);     // vmcnt(8): the copies of s + 2 may be in flight
+          static_assert(2 * G::CPW == 8, "wait count matches the copies per step");
+        } else {
+          __builtin_amdgcn_s_waitcnt(0x0f70);     // vmcnt(0)
+        }
+        stage_barrier();
+        const bool copying = s + DEPTH < nsteps;
+        const float* vs = vsrc + int64_t(cpass) * E * g.vplane + cst * vstage;
+        const float* us = usrc + int64_t(cpass) * E * g.uplane + cst * ustage;
+        if (copying) advance();
+        mma_group(gi, slot, buf(std::integral_constant<int, b + 1>{}), 0, true, copying, vs, us,
+                  buf(std::integral_constant<int, b + DEPTH>{}));
+      } else {
+        mma_group(gi, slot, nullptr, 0, false, false, nullptr, nullptr, nullptr);
       }
     }
   };
 
-  issue(buf0, 0, 0);
-#pragma unroll 1
-  for (int pass = 0; pass < G::NPASS; ++pass) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] = typename S::acc_t{};
-    if ((pass * nstage) & 1) run_pass(buf1, buf0, pass);
-    else run_pass(buf0, buf1, pass);
-
-    // pass complete: its elements are RP alpha-rows (leading indices fixed,
-    // last index free).  Reduce each row along the last axis with A^T, then add
-    // it to every output with the product of A^T over the leading indices.
+  // the pass epilogue: its elements are RP alpha-rows (leading indices fixed,
+  // last index free).  Reduce each row along the last axis with A^T, then add
+  // it to every output with the product of A^T over the leading indices.
+  auto epilogue = [&](int pass) {
     float c[G::NLEAD][RP];
 #pragma unroll
     for (int oo = 0; oo < G::NLEAD; ++oo)
@@ -248,13 +304,63 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
         for (int rp = 0; rp < RP; ++rp)
           yacc[o][r] = __builtin_fmaf(c[o / MM][rp], rows[rp][o % MM], yacc[o][r]);
     }
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = typename S::acc_t{};
+  };
+
+  // ---- prologue: copies of the first DEPTH steps, then the first group
+  issue(buf0, cpass, cst);
+  advance();
+  if (1 < nsteps) {
+    issue(buf1, cpass, cst);
+    advance();
+  }
+  if (2 < nsteps) {
+    issue(buf2, cpass, cst);
+    advance();
+  }
+  static_assert(DEPTH == 3, "prologue fills three buffers");
+  if (nsteps >= 3) __builtin_amdgcn_s_waitcnt(0x4f70);        // vmcnt(16)
+  else if (nsteps == 2) __builtin_amdgcn_s_waitcnt(0x0f78);   // vmcnt(8)
+  else __builtin_amdgcn_s_waitcnt(0x0f70);                    // vmcnt(0)
+  stage_barrier();
+  read_group(buf0, 0, 0);
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = typename S::acc_t{};
+
+  // ---- steps, four per trip so that every buffer is named at compile time
+  int s = 0, pass = 0, st = 0;
+  auto finish = [&]() {                           // after a step: true when all are done
+    ++s;
+    if (++st == nstage) {
+      epilogue(pass);
+      st = 0;
+      ++pass;
+    }
+    return s == nsteps;
+  };
+  static_assert(NBUF == 4, "the step loop unrolls four buffers");
+#pragma unroll 1
+  for (;;) {
+    step(std::integral_constant<int, 0>{}, s);
+    if (finish()) break;
+    step(std::integral_constant<int, 1>{}, s);
+    if (finish()) break;
+    step(std::integral_constant<int, 2>{}, s);
+    if (finish()) break;
+    step(std::integral_constant<int, 3>{}, s);
+    if (finish()) break;
   }
 
   // ---- stitch: outputs through LDS so that neighbouring lanes store
-  // neighbouring outputs of a row.  Plane o ([k][t], t XOR-swizzled by k) lives
-  // in buf0 for o < NOUT/2, else in buf1.
+  // neighbouring outputs of a row.  Plane o ([k][t], t XOR-swizzled by k) is
+  // plane o % PPB of buffer o / PPB.
   __syncthreads();
-  auto plane = [&](int o) { return (o < NOUT / 2 ? buf0 : buf1) + (o % (NOUT / 2)) * G::PLANE; };
+  auto plane = [&](int o) {
+    const int b = o / G::PPB;
+    float* base = b == 0 ? buf0 : b == 1 ? buf1 : b == 2 ? buf2 : buf3;
+    return base + (o % G::PPB) * G::PLANE;
+  };
 #pragma unroll
   for (int o = 0; o < NOUT; ++o)
 #pragma unroll
