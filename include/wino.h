@@ -115,9 +115,9 @@ wino_status wino_plan_describe(const wino_plan_t* plan, wino_plan_desc* desc);
 size_t wino_filter_bytes(const wino_plan_t* plan);
 
 /* Bytes of workspace wino_forward needs: the transformed input V (float32),
- * laid out tile-block major as V[T_pad/B][alpha^N][C_pad/CG][B][CG] with
+ * laid out tile-block major as V[T_pad/B][C_pad/CG][alpha^N][B][CG] with
  * B = block_tiles: element (xi, c, t) sits at
- * (((t/B)*alpha^N + xi)*C_pad/CG + c/CG)*B*CG + (t%B)*CG + c%CG. */
+ * (((t/B)*C_pad/CG + c/CG)*alpha^N + xi)*B*CG + (t%B)*CG + c%CG. */
 size_t wino_workspace_bytes(const wino_plan_t* plan);
 
 /* Bytes of workspace wino_forward needs (today equal to wino_workspace_bytes). */

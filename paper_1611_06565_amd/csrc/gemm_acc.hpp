@@ -16,7 +16,7 @@
 // double buffer, so the next stage streams in while this one is multiplied,
 // without holding registers.
 //
-// Layouts: V[T_pad/64][alpha^N][C_pad/4][64][4], U[alpha^N][C_pad/4][K_pad][4]
+// Layouts: V[T_pad/64][C_pad/4][alpha^N][64][4], U[alpha^N][C_pad/4][K_pad][4]
 // (channel groups of 4 innermost: a lane's 16-byte LDS read holds 4 channels).
 #pragma once
 
@@ -32,7 +32,7 @@
 namespace wino {
 
 struct AccArgs {
-  int64_t vplane;     // floats per (tile block, element): C_pad * 64
+  int64_t vblock;     // floats per tile block of V: alpha^N * C_pad * 64
   int64_t uplane;     // floats per element of U: C_pad * K_pad
   int64_t ystride_k;  // prod Y_i
   int32_t T, C_pad, K, K_pad;
@@ -80,17 +80,30 @@ struct AccGeom {
 // track these copies: it would otherwise make LDS reads of other buffers wait
 // for them.  Every wait for the copies is explicit (s_waitcnt vmcnt), and the
 // stage barrier, which has a memory clobber, orders them against LDS reads.
+// NT marks the load non-temporal (streamed operand rows that should not push
+// the shared transformed filter out of L2).
+template <bool NT>
 __device__ __forceinline__ void lds_copy16(const float* src, float* dst) {
   // the low 32 bits of a generic pointer into LDS are its LDS byte address
   const uint32_t lds_addr =
       __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst)));
-  asm volatile(
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, off"
-      :
-      : "v"(src), "s"(lds_addr)
-      : "m0");
+  if constexpr (NT) {
+    asm volatile(
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %0, off nt"
+        :
+        : "v"(src), "s"(lds_addr)
+        : "m0");
+  } else {
+    asm volatile(
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %0, off"
+        :
+        : "v"(src), "s"(lds_addr)
+        : "m0");
+  }
 }
 
 // Work-group barrier for the copy pipeline.  __syncthreads() carries a release
@@ -164,27 +177,28 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
 
   // ---- direct-to-LDS copies of one (pass, stage) step.  Chunk c of an
   // operand is (element e, 4-channel group gi) = (c / G4, c % G4): 1 KB, either
-  // V[tb][xi][grp][0:64][0:4] or U[xi][grp][kb*64 : kb*64+64][0:4], landing at
+  // V[tb][grp][xi][0:64][0:4] or U[xi][grp][kb*64 : kb*64+64][0:4], landing at
   // c * 256 floats of the V or U half of the buffer.  Wave w copies chunks
   // w, w + NW, ...
-  const float* vsrc = V + int64_t(tb) * G::NXI * g.vplane + lane * 4;
+  constexpr int64_t VX = TB * 4, VG = int64_t(G::NXI) * TB * 4;    // V element / group strides
+  const float* vsrc = V + int64_t(tb) * g.vblock + lane * 4;
   const float* usrc = U + int64_t(kb) * (KB * 4) + lane * 4;
   int64_t voff[G::CPW], uoff[G::CPW];
 #pragma unroll
   for (int i = 0; i < G::CPW; ++i) {
     const int c = wave + NW * i, e = c / G4, gi = c % G4;
-    voff[i] = e * g.vplane + gi * (TB * 4);
+    voff[i] = e * VX + gi * VG;
     uoff[i] = e * g.uplane + int64_t(gi) * g.K_pad * 4;
   }
-  const int64_t vstage = int64_t(G4) * TB * 4, ustage = int64_t(G4) * g.K_pad * 4;
+  const int64_t vstage = G4 * VG, ustage = int64_t(G4) * g.K_pad * 4;
   // copy q in [0, 2 * CPW) of a step: chunk q / 2 of V (q even) or of U (q odd)
   auto copy_one = [&](const float* vs, const float* us, float* base, int q) {
     const int i = q >> 1, c = wave + NW * i;
-    if ((q & 1) == 0) lds_copy16(vs + voff[i], base + c * 256);
-    else lds_copy16(us + uoff[i], base + G::SA + c * 256);
+    if ((q & 1) == 0) lds_copy16<true>(vs + voff[i], base + c * 256);
+    else lds_copy16<false>(us + uoff[i], base + G::SA + c * 256);
   };
   auto issue = [&](float* base, int pass, int st) {
-    const float* vs = vsrc + int64_t(pass) * E * g.vplane + st * vstage;
+    const float* vs = vsrc + int64_t(pass) * E * VX + st * vstage;
     const float* us = usrc + int64_t(pass) * E * g.uplane + st * ustage;
 #pragma unroll
     for (int q = 0; q < 2 * G::CPW; ++q) copy_one(vs, us, base, q);
@@ -268,7 +282,7 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
         }
         stage_barrier();
         const bool copying = s + DEPTH < nsteps;
-        const float* vs = vsrc + int64_t(cpass) * E * g.vplane + cst * vstage;
+        const float* vs = vsrc + int64_t(cpass) * E * VX + cst * vstage;
         const float* us = usrc + int64_t(cpass) * E * g.uplane + cst * ustage;
         if (copying) advance();
         mma_group(gi, slot, buf(std::integral_constant<int, b + 1>{}), 0, true, copying, vs, us,
@@ -403,7 +417,7 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
     for (int ax = 1; ax < N; ++ax) off = off * g.Y[ax] + yc[ax];
     float v = plane(orest * MM + ol)[kl * TB + (tl ^ (kl & 31))];
     if (g.relu) v = v > 0.0f ? v : 0.0f;
-    y[(int64_t(n) * g.K + kg) * g.ystride_k + off] = v;
+    __builtin_nontemporal_store(v, y + (int64_t(n) * g.K + kg) * g.ystride_k + off);
   }
 }
 

@@ -9,13 +9,15 @@
 // Layouts (float32, zero padding rows/columns):
 //   x [batch][C][X_1..X_N]     w [K][C][r^N]      y [batch][K][Y_1..Y_N]
 //   U [alpha^N][C_pad/CGU][K_pad][CGU]
-//   V [T_pad/BLK][alpha^N][C_pad/CG][BLK][CG]
+//   V [T_pad/BLK][C_pad/CG][alpha^N][BLK][CG]
 // T counts tiles over the whole batch (tiles of every sample form the rows of
 // one GEMM, §4.1 and §4.4: the method is batch-size agnostic).  BLK is the
-// GEMM block (32 or 16 tiles / kernels) and CG the channel group (see
-// Blocking): interleaving channel groups innermost lets every lane fetch
-// VEC k-steps of an MFMA operand with one load, and storing V tile-block
-// major keeps all of one work-group's operand rows in one contiguous region.
+// GEMM block of tiles and CG the channel group (see Blocking): interleaving
+// channel groups innermost lets every lane fetch VEC k-steps of an MFMA
+// operand with one load; storing V tile-block major keeps all of one
+// GEMM work-group's operand rows in one contiguous region, and putting the
+// elements inside the channel group makes the input transform of one (tile
+// block, channel group) write one contiguous run.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -59,15 +61,15 @@ struct FilterArgs {
 };
 
 struct InputArgs {
-  int64_t vplane;  // C_pad * T_pad
   int64_t xstride_c;  // prod X_i
   int32_t C, C_pad;
   int32_t T, T_pad;
+  int32_t ntb, nblocks;  // tile blocks; work-groups in the grid
   int32_t X[3], tiles[3], pad[3];
 };
 
 struct GemmArgs {
-  int64_t vplane, uplane;
+  int64_t uplane;     // C_pad * K_pad
   int64_t ystride_k;  // prod Y_i
   int32_t T, T_pad, C_pad, K, K_pad;
   int32_t nkb;        // K_pad / BLK
@@ -86,6 +88,16 @@ __device__ __forceinline__ int split_tile(int t, const int32_t* tiles, int* ti) 
     t /= tiles[a];
   }
   return t;
+}
+
+// Work-groups are dispatched round-robin over the 8 XCDs.  Renumber them so
+// that consecutive logical blocks (in the GEMM the K-blocks of one tile block,
+// which read the same V rows) land on the same XCD and share its L2.
+__device__ __forceinline__ int xcd_remap(int b, int nb) {
+  constexpr int NX = 8;
+  const int xcd = b % NX, j = b / NX;
+  const int per = nb / NX, rem = nb % NX;
+  return xcd < rem ? xcd * (per + 1) + j : rem * (per + 1) + (xcd - rem) * per + j;
 }
 
 // ------------------------------------------------------------ filter (a2)
@@ -121,57 +133,89 @@ __global__ void __launch_bounds__(256) k_filter(const float* __restrict__ w, flo
 
 // ------------------------------------------------------------- input (a3)
 // One thread per (tile, channel): gather the alpha^N window (zero outside the
-// input), transform along every axis, scatter to the alpha^N planes of V.
-// A work-group covers one GEMM tile block and 256 / (BLK * CG) channel
-// groups; lanes run over channels of a group fastest, then tiles, so each
-// plane store is one contiguous run.
+// input), transform along every axis (eq. 4, B^T on the data side), and write
+// the alpha^N values to V.
+//
+// A work-group covers one GEMM tile block (BLK tiles) and 256 / (BLK * CG)
+// channel groups; lanes run over the channels of a group fastest, then tiles,
+// so each plane store of a wave is one contiguous run.  Each window row (A
+// values along the last axis) is a single wide load from a start clamped into
+// the input row, shifted and zero-masked in registers; a row whose leading
+// coordinates fall outside the input loads a clamped row and is masked to
+// zero.  No branches depend on the tile, so edge tiles cost what inner ones do.
 template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, float* __restrict__ V,
                                                InputArgs a, FMats fm) {
   using B = Blocking<N, MM, R>;
   constexpr int A = B::A, NXI = B::NXI, BLK = B::BLK, CG = B::CG;
   constexpr int GPW = 256 / (BLK * CG);   // channel groups per work-group
+  constexpr int NROW = NXI / A;           // window rows (leading indices)
+  constexpr int XCH = NXI % 16 == 0 ? 16 : 12;   // planes staged through LDS at a time
   static_assert(GPW * BLK * CG == 256, "work-group shape");
+  static_assert(CG == 4 && NXI % XCH == 0 && XCH % 4 == 0, "store rounds of 4 planes");
   const int tid = int(threadIdx.x);
   const int cl = tid % CG;
   const int tl = (tid / CG) % BLK;
   const int gl = tid / (CG * BLK);
-  const int tb = int(blockIdx.x);
-  const int cg = int(blockIdx.y) * GPW + gl;
+  // consecutive tile blocks of one channel group run on the same XCD, so the
+  // input windows they share (neighbouring tiles overlap by r - 1) hit its L2
+  const int L = xcd_remap(int(blockIdx.x), a.nblocks);
+  const int tb = L % a.ntb;
+  const int cg = (L / a.ntb) * GPW + gl;
   const int c = cg * CG + cl;
-  if (c >= a.C_pad) return;
   const int t = tb * BLK + tl;
   float d[NXI];
   if (t < a.T && c < a.C) {
     int ti[3] = {0, 0, 0};
     const int n = split_tile<N>(t, a.tiles, ti);
     int o[3];
-    bool in[3][A];
 #pragma unroll
-    for (int ax = 0; ax < N; ++ax) {
-      o[ax] = ti[ax] * MM - a.pad[ax];
-#pragma unroll
-      for (int i = 0; i < A; ++i) in[ax][i] = (unsigned)(o[ax] + i) < (unsigned)a.X[ax];
-    }
+    for (int ax = 0; ax < N; ++ax) o[ax] = ti[ax] * MM - a.pad[ax];
     const float* xc = x + (int64_t(n) * a.C + c) * a.xstride_c;
-    if constexpr (N == 2) {
+    const int XL = a.X[N - 1];
+    // last axis: the window [oL, oL + A) is read as [sL, sL + A) inside the row
+    const int oL = o[N - 1];
+    const bool wide = XL >= A;            // uniform over the launch
+    const int sL = wide ? min(max(oL, 0), XL - A) : 0;
+    const int delta = oL - sL;            // window element i is loaded element i + delta
 #pragma unroll
-      for (int i0 = 0; i0 < A; ++i0)
+    for (int row = 0; row < NROW; ++row) {
+      int lead[2] = {0, 0};
+      int rem = row;
 #pragma unroll
-        for (int i1 = 0; i1 < A; ++i1)
-          d[i0 * A + i1] = (in[0][i0] && in[1][i1])
-                               ? xc[int64_t(o[0] + i0) * a.X[1] + (o[1] + i1)] : 0.0f;
-    } else {
+      for (int ax = N - 2; ax >= 0; --ax) {
+        lead[ax] = rem % A;
+        rem /= A;
+      }
+      int64_t off = 0;
+      bool valid = true;
 #pragma unroll
-      for (int i0 = 0; i0 < A; ++i0)
+      for (int ax = 0; ax < N - 1; ++ax) {
+        const int q = o[ax] + lead[ax];
+        valid = valid && (unsigned)q < (unsigned)a.X[ax];
+        off = off * a.X[ax] + min(max(q, 0), a.X[ax] - 1);
+      }
+      const float* xr = xc + off * XL;
+      float* dr = d + row * A;
+      if (wide) {
+        float ld[A];
+        __builtin_memcpy(ld, xr + sL, sizeof(ld));
 #pragma unroll
-        for (int i1 = 0; i1 < A; ++i1)
+        for (int i = 0; i < A; ++i) {
+          float v = 0.0f;
 #pragma unroll
-          for (int i2 = 0; i2 < A; ++i2)
-            d[(i0 * A + i1) * A + i2] =
-                (in[0][i0] && in[1][i1] && in[2][i2])
-                    ? xc[(int64_t(o[0] + i0) * a.X[1] + (o[1] + i1)) * a.X[2] + (o[2] + i2)]
-                    : 0.0f;
+          for (int j = 0; j < A; ++j) v = (j == i + delta) ? ld[j] : v;
+          dr[i] = valid ? v : 0.0f;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < A; ++i) {
+          const int q = oL + i;
+          const bool in = valid && (unsigned)q < (unsigned)XL;
+          const float v = xr[min(max(q, 0), XL - 1)];
+          dr[i] = in ? v : 0.0f;
+        }
+      }
     }
   } else {
 #pragma unroll
@@ -179,11 +223,35 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
   }
   float v[NXI];
   transform_nd<N, A, A>(d, v, MatRef<Which::BT, CONST, MM, R>{&fm});
-  // V[tb][xi][cg][tl][cl]; consecutive xi planes are C_pad * BLK floats apart
-  const int64_t xi_stride = int64_t(a.C_pad) * BLK;
-  float* dst = V + int64_t(tb) * NXI * xi_stride + (int64_t(cg) * BLK + tl) * CG + cl;
+  // V[tb][cg][xi][tl][cl]: the work-group's NXI planes of each of its channel
+  // groups are one contiguous run of NXI * 256 floats.  The values go through
+  // LDS XCH planes at a time so that each lane stores 16 bytes (one tile's 4
+  // channels) and a wave writes 1 KB contiguous per store.
+  __shared__ float4 stage[XCH][64];      // the work-group's 256 floats of a plane
+  float* const gbase = V + (int64_t(tb) * a.C_pad + int64_t(cg - gl) * CG) * NXI * BLK;
+  const int pr = tid >> 6, f = tid & 63;  // plane within a round of 4; float4 = (group, tile)
+  const int g = f / BLK;
+  const bool store = (cg - gl + g) * CG < a.C_pad;
 #pragma unroll
-  for (int xi = 0; xi < NXI; ++xi) dst[xi * xi_stride] = v[xi];
+  for (int x0 = 0; x0 < NXI; x0 += XCH) {
+    if (x0 > 0) __syncthreads();          // previous planes stored
+#pragma unroll
+    for (int i = 0; i < XCH; ++i) reinterpret_cast<float*>(stage[i])[(gl * BLK + tl) * CG + cl] = v[x0 + i];
+    __syncthreads();
+    if (store) {
+#pragma unroll
+      for (int i = 0; i < XCH; i += 4) {
+        // non-temporal: V streams to HBM without evicting the input windows
+        // that neighbouring work-groups still read from L2
+        const float4 val = stage[i + pr][f];
+        float* p = gbase + (int64_t(g) * NXI + x0 + i + pr) * (BLK * CG) + (f % BLK) * CG;
+        __builtin_nontemporal_store(val.x, p + 0);
+        __builtin_nontemporal_store(val.y, p + 1);
+        __builtin_nontemporal_store(val.z, p + 2);
+        __builtin_nontemporal_store(val.w, p + 3);
+      }
+    }
+  }
 }
 
 // ------------------------------------------------- batched GEMM (a4 + a5)
@@ -220,16 +288,6 @@ template <> struct MfmaShape<16> {
   // accumulator register r of a lane holds row 4*(lane/16) + r, column lane%16
   __device__ static __forceinline__ int acc_row(int lane, int r) { return 4 * (lane >> 4) + r; }
 };
-
-// Work-groups are dispatched round-robin over the 8 XCDs.  Renumber them so
-// that consecutive logical blocks (the K-blocks of one tile block, which read
-// the same V rows) land on the same XCD and share its L2.
-__device__ __forceinline__ int xcd_remap(int b, int nb) {
-  constexpr int NX = 8;
-  const int xcd = b % NX, j = b / NX;
-  const int per = nb / NX, rem = nb % NX;
-  return xcd < rem ? xcd * (per + 1) + j : rem * (per + 1) + (xcd - rem) * per + j;
-}
 
 // Shape of one GEMM work-group.  NW waves split the alpha^N elements evenly;
 // each wave's share is made of whole "units" of the LOC trailing axes
@@ -382,18 +440,18 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
   const int tb = L / g.nkb, kb = L % g.nkb;
   const int col = lane % BLK, kr = lane / BLK;
 
-  // Operand rows: V[tb][xi][cg][t][CG] and U[xi][cg][k][CG].  Lane (kr, col)
+  // Operand rows: V[tb][cg][xi][t][CG] and U[xi][cg][k][CG].  Lane (kr, col)
   // owns channels VEC*kr .. VEC*kr+VEC-1 of every group; MFMA k-step j of a
   // group uses channel VEC*kr + j, so the VEC steps of a group cover all CG
   // channels.  One "stage" = one group = VEC k-steps.
   constexpr int CG = S::KSTEP * VEC;
   constexpr int CGU = Blocking<N, MM, R>::CGU;                     // U groups: CGU/CG V groups each
   static_assert(CGU % CG == 0, "U groups hold whole V groups");
-  const int64_t vxi = int64_t(g.C_pad) * BLK;                      // V plane stride (floats)
+  const int64_t vxi = int64_t(BLK) * CG;                           // V element stride (floats)
   const int64_t uxi = g.uplane;                                    // U plane stride (floats)
-  const float* vnext = V + (int64_t(tb) * NXI + int64_t(wave) * XPW) * vxi + col * CG + VEC * kr;
+  const float* vnext = V + int64_t(tb) * NXI * g.C_pad * BLK + int64_t(wave) * XPW * vxi + col * CG + VEC * kr;
   const float* ubase = U + int64_t(wave) * XPW * uxi + int64_t(kb) * BLK * CGU + col * CGU + VEC * kr;
-  const int64_t vgstep = int64_t(BLK) * CG, ugstep = int64_t(g.K_pad) * CGU;
+  const int64_t vgstep = int64_t(NXI) * BLK * CG, ugstep = int64_t(g.K_pad) * CGU;
   const int nstages = g.C_pad / CG;
   int unext_g = 0;                                                 // next V group to fetch
 

@@ -101,7 +101,6 @@ struct Launch {
 
   static wino_status input(const wino_plan_s& p, const float* x, float* V, hipStream_t s) {
     InputArgs a{};
-    a.vplane = int64_t(p.C_pad) * p.T_pad;
     a.xstride_c = 1;
     for (int i = 0; i < N; ++i) a.xstride_c *= p.X[i];
     a.C = p.C; a.C_pad = p.C_pad;
@@ -111,8 +110,10 @@ struct Launch {
     }
     constexpr int GPW = 256 / (BLK * CG);
     const int64_t groups = p.C_pad / CG;
-    dim3 grid(unsigned(p.T_pad / BLK), unsigned((groups + GPW - 1) / GPW));
-    hipLaunchKernelGGL((k_input<N, MM, R, CONST>), grid, dim3(256), 0, s, x, V, a, p.fm);
+    const int64_t nb = (p.T_pad / BLK) * ((groups + GPW - 1) / GPW);
+    a.ntb = int32_t(p.T_pad / BLK);
+    a.nblocks = int32_t(nb);
+    hipLaunchKernelGGL((k_input<N, MM, R, CONST>), dim3(unsigned(nb)), dim3(256), 0, s, x, V, a, p.fm);
     return launch_status();
   }
 
@@ -121,7 +122,7 @@ struct Launch {
     if constexpr (Blocking<N, MM, R>::ACC) {
       using G = AccGeom<N, MM, R>;
       AccArgs a{};
-      a.vplane = int64_t(p.C_pad) * G::TB;
+      a.vblock = int64_t(p.nxi) * p.C_pad * G::TB;
       a.uplane = int64_t(p.C_pad) * p.K_pad;
       a.ystride_k = 1;
       for (int i = 0; i < N; ++i) a.ystride_k *= p.Y[i];
@@ -136,7 +137,6 @@ struct Launch {
       return launch_status();
     } else {
       GemmArgs g{};
-      g.vplane = int64_t(p.C_pad) * p.T_pad;
       g.uplane = int64_t(p.C_pad) * p.K_pad;
       g.ystride_k = 1;
       for (int i = 0; i < N; ++i) g.ystride_k *= p.Y[i];
@@ -239,7 +239,8 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   if (p.C_pad > (1 << 18)) return WINO_EINVAL;  // bounds the input-transform grid
   p.nxi = 1;
   for (int i = 0; i < N; ++i) p.nxi *= alpha;
-  if ((p.T_pad / p.blk) * (p.K_pad / p.blk) > kMaxI32) return WINO_EINVAL;
+  if ((p.T_pad / p.blk) * (p.K_pad / p.blk) > kMaxI32) return WINO_EINVAL;   // GEMM grid
+  if ((p.T_pad / p.blk) * (p.C_pad / p.cg) > kMaxI32) return WINO_EINVAL;     // input grid
 
   // Transform synthesis (a1): exact rationals, one rounding per entry.
   Rat pts[kMaxAlpha];

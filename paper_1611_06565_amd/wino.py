@@ -216,8 +216,8 @@ class Plan:
         cg, b = d["channel_group"], d["block_tiles"]
         v = ws.detach().cpu().numpy() if hasattr(ws, "detach") else np.asarray(ws)
         v = v[: d["n_xi"] * d["C_pad"] * d["T_pad"]]
-        v = v.reshape(d["T_pad"] // b, d["n_xi"], d["C_pad"] // cg, b, cg)
-        return v.transpose(1, 2, 4, 0, 3).reshape(d["n_xi"], d["C_pad"], d["T_pad"])
+        v = v.reshape(d["T_pad"] // b, d["C_pad"] // cg, d["n_xi"], b, cg)
+        return v.transpose(2, 1, 4, 0, 3).reshape(d["n_xi"], d["C_pad"], d["T_pad"])
 
     def new_workspace(self):
         import torch
