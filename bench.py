@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 PEAK_FP32_MFMA = 157.3      # TFLOP/s, MI355X dense fp32 matrix
 PEAK_HBM = 8000.0           # GB/s, MI355X HBM3E
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-TRAFFIC_FILE = os.path.join(PROFILE_DIR, "k_gemm_inv_f2x3_c64k128_traffic.txt")
+TRAFFIC_FILE = os.path.join(PROFILE_DIR, "k_gemm_acc_f2x3_c64k128_traffic.txt")
 KERNEL_SOURCES = ["paper_1611_06565_amd/csrc/kernels.hpp", "paper_1611_06565_amd/csrc/gemm_acc.hpp",
                   "paper_1611_06565_amd/csrc/transforms.hpp", "paper_1611_06565_amd/csrc/synth.hpp",
                   "paper_1611_06565_amd/csrc/wino.hip"]

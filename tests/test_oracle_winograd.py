@@ -9,6 +9,9 @@
   order gives the same tensor.
 * The 2-D special case of §3.2: A[(C g C^T) . (B d B^T)]A^T in matrix form.
 * The §2.2 worked example.
+* Exact invariants of a correlation that tiling and stitching must keep:
+  translation by shifts that are not multiples of m, linearity, batch
+  independence, and a one-hot kernel selecting the input window (no flip).
 """
 import itertools
 import random
@@ -125,3 +128,63 @@ def test_nonfinite_input_poisons_tile():
     y = winograd_forward(x, w, 2, 3)
     yd, _ = direct_blas(x, w, 0)
     assert np.isnan(y).sum() >= np.isnan(yd).sum()
+
+
+# ---- invariants of the correlation that the Winograd path must keep exactly
+def _exact(x, w, m, pad=0):
+    return winograd_forward(x, w, m, 3, pad=pad, exact=True)
+
+
+@pytest.mark.parametrize("N,m,axis,s", [(2, 2, 1, 1), (2, 4, 0, 3), (3, 2, 2, 1), (3, 4, 0, 1)])
+def test_translation_equivariance(N, m, axis, s):
+    """Shifting the input by s along an axis shifts the valid output by s:
+    the tile grid (stride m) must not leak into the result."""
+    rng = np.random.default_rng(7 + N + m + s)
+    X = (7, 6, 5)[:N] if N == 3 else (9, 8)
+    x = rng.integers(-3, 4, size=(1, 2) + X)
+    w = rng.integers(-3, 4, size=(2, 2) + (3,) * N)
+    xs = np.zeros_like(x)
+    src = [slice(None)] * (N + 2)
+    dst = [slice(None)] * (N + 2)
+    src[2 + axis] = slice(0, X[axis] - s)
+    dst[2 + axis] = slice(s, X[axis])
+    xs[tuple(dst)] = x[tuple(src)]
+    y, ys = _exact(x, w, m), _exact(xs, w, m)
+    keep_y = [slice(None)] * (N + 2)
+    keep_ys = [slice(None)] * (N + 2)
+    Y = y.shape[2 + axis]
+    keep_y[2 + axis] = slice(0, Y - s)
+    keep_ys[2 + axis] = slice(s, Y)
+    assert np.array_equal(ys[tuple(keep_ys)], y[tuple(keep_y)])
+
+
+def test_linearity_exact():
+    rng = np.random.default_rng(3)
+    x1 = rng.integers(-3, 4, size=(1, 2, 6, 5, 7))
+    x2 = rng.integers(-3, 4, size=(1, 2, 6, 5, 7))
+    w = rng.integers(-3, 4, size=(2, 2, 3, 3, 3))
+    lhs = _exact(2 * x1 - 3 * x2, w, 2, pad=1)
+    rhs = 2 * _exact(x1, w, 2, pad=1) - 3 * _exact(x2, w, 2, pad=1)
+    assert np.array_equal(lhs, rhs)
+
+
+def test_batch_independence_exact():
+    rng = np.random.default_rng(4)
+    x = rng.integers(-3, 4, size=(2, 2, 5, 6, 5))
+    w = rng.integers(-3, 4, size=(3, 2, 3, 3, 3))
+    both = _exact(x, w, 4, pad=1)
+    assert np.array_equal(both[:1], _exact(x[:1], w, 4, pad=1))
+    assert np.array_equal(both[1:], _exact(x[1:], w, 4, pad=1))
+
+
+@pytest.mark.parametrize("p", [(0, 0, 0), (2, 1, 0), (1, 2, 2)])
+def test_one_hot_kernel_selects_input(p):
+    """A kernel with a single 1 at offset p returns the input window at p: no flip."""
+    rng = np.random.default_rng(5)
+    x = rng.integers(-5, 6, size=(1, 1, 6, 7, 5))
+    w = np.zeros((1, 1, 3, 3, 3), dtype=np.int64)
+    w[(0, 0) + p] = 1
+    y = _exact(x, w, 2)
+    Y = y.shape[2:]
+    want = x[0, 0, p[0]:p[0] + Y[0], p[1]:p[1] + Y[1], p[2]:p[2] + Y[2]]
+    assert np.array_equal(y[0, 0], want)
