@@ -140,7 +140,7 @@ __device__ __forceinline__ float lead_coef(const MatRef<Which::AT, CONST, MM, R>
   return c;
 }
 
-template <int N, int MM, int R, bool CONST>
+template <int N, int MM, int R, bool CONST, bool OVL>
 __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
                                                   const float* __restrict__ U,
                                                   float* __restrict__ y, AccArgs g, FMats fm) {
@@ -156,6 +156,9 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
   __shared__ __attribute__((aligned(16))) float buf1[G::STAGE];
   __shared__ __attribute__((aligned(16))) float buf2[G::STAGE];
   __shared__ __attribute__((aligned(16))) float buf3[G::STAGE];
+  // copies past the last step land here, so every step issues the same copies
+  // and no branch splits the MFMA sequence
+  __shared__ __attribute__((aligned(16))) float dump[256];
   auto buf = [&](auto I) -> float* {
     constexpr int b = decltype(I)::value % NBUF;
     if constexpr (b == 0) return buf0;
@@ -191,25 +194,37 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
     uoff[i] = e * g.uplane + int64_t(gi) * g.K_pad * 4;
   }
   const int64_t vstage = G4 * VG, ustage = int64_t(G4) * g.K_pad * 4;
-  // copy q in [0, 2 * CPW) of a step: chunk q / 2 of V (q even) or of U (q odd)
-  auto copy_one = [&](const float* vs, const float* us, float* base, int q) {
+  // copy q in [0, 2 * CPW) of a step: chunk q / 2 of V (q even) or of U (q
+  // odd).  A step past the last one (real == false) copies the first chunk of
+  // the block again into the dump area instead.
+  auto copy_one = [&](const float* vs, const float* us, float* base, bool real, int q) {
     const int i = q >> 1, c = wave + NW * i;
-    if ((q & 1) == 0) lds_copy16<true>(vs + voff[i], base + c * 256);
-    else lds_copy16<false>(us + uoff[i], base + G::SA + c * 256);
+    if ((q & 1) == 0) {
+      lds_copy16<true>(real ? vs + voff[i] : vsrc, real ? base + c * 256 : dump);
+    } else {
+      lds_copy16<false>(real ? us + uoff[i] : usrc, real ? base + G::SA + c * 256 : dump);
+    }
   };
-  auto issue = [&](float* base, int pass, int st) {
+  auto issue = [&](float* base, bool real, int pass, int st) {
     const float* vs = vsrc + int64_t(pass) * E * VX + st * vstage;
     const float* us = usrc + int64_t(pass) * E * g.uplane + st * ustage;
 #pragma unroll
-    for (int q = 0; q < 2 * G::CPW; ++q) copy_one(vs, us, base, q);
+    for (int q = 0; q < 2 * G::CPW; ++q) copy_one(vs, us, base, real, q);
   };
 
-  typename S::acc_t acc[E];
+  // Two accumulator sets when the pass epilogue overlaps the next pass (OVL):
+  // pass p accumulates into set p % 2 while the epilogue of pass p - 1 reads
+  // and clears the other set between the MFMAs.
+  typename S::acc_t acc[OVL ? 2 : 1][E];
   float yacc[NOUT][S::NACC];
 #pragma unroll
   for (int o = 0; o < NOUT; ++o)
 #pragma unroll
     for (int r = 0; r < S::NACC; ++r) yacc[o][r] = 0.0f;
+#pragma unroll
+  for (int k = 0; k < (OVL ? 2 : 1); ++k)
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[k][e] = typename S::acc_t{};
 
   const MatRef<Which::AT, CONST, MM, R> AT{&fm};
   const int aoff = (kr * TB + tq * 32 + col) * 4;
@@ -218,7 +233,9 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
   // copy cursor: the next step to copy, as (pass, stage)
   int cpass = 0, cst = 0;
   auto advance = [&]() {
-    if (++cst == nstage) { cst = 0; ++cpass; }
+    const bool wrap = cst + 1 == nstage;
+    cst = wrap ? 0 : cst + 1;
+    cpass += wrap ? 1 : 0;
   };
 
   // Operands go in groups of 4 elements of one pair p of 4-channel groups:
@@ -238,12 +255,14 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
 #pragma unroll
     for (int q = 0; q < 8; ++q) read_one(base, gidx, slot, q);
   };
-  // The 16 MFMAs of group gidx from `slot`, in a fixed order with the reads of
-  // the next group (into the other slot) and, in a step's last group, the
-  // copies of a later step placed between them so that the matrix unit keeps
-  // being fed while they issue.
-  auto mma_group = [&](int gidx, int slot, const float* nbase, int ngidx, bool reading,
-                       bool copying, const float* vs, const float* us, float* cbase) {
+  // The 16 MFMAs of group gidx from `slot` into accumulator set AI, in a fixed
+  // order with the reads of the next group (into the other slot), in a step's
+  // last group the copies of a later step, and whatever `epi` adds after each
+  // MFMA, so that the matrix unit keeps being fed while they issue.
+  auto mma_group = [&](auto AI, auto COPY, int gidx, int slot, const float* nbase, int ngidx,
+                       const float* vs, const float* us, float* cbase, bool real, auto&& epi) {
+    constexpr int ai = decltype(AI)::value;
+    constexpr bool copying = decltype(COPY)::value;
     const int e0 = (gidx % (E / 4)) * 4;
 #pragma unroll
     for (int m = 0; m < 16; ++m) {
@@ -251,124 +270,173 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
       const float4 av4 = a4[slot][e], bv4 = b4[slot][e];
       const float av = j == 0 ? av4.x : j == 1 ? av4.y : j == 2 ? av4.z : av4.w;
       const float bv = j == 0 ? bv4.x : j == 1 ? bv4.y : j == 2 ? bv4.z : bv4.w;
-      acc[e0 + e] = S::mma(av, bv, acc[e0 + e]);
-      if (reading && m < 8) read_one(nbase, ngidx, slot ^ 1, m);
-      if (copying && (m & 1)) copy_one(vs, us, cbase, m >> 1);
+      acc[ai][e0 + e] = S::mma(av, bv, acc[ai][e0 + e]);
+      if (m < 8) read_one(nbase, ngidx, slot ^ 1, m);
+      if constexpr (copying) {
+        if (m & 1) copy_one(vs, us, cbase, real, m >> 1);
+      }
+      epi(gidx, m);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
   static_assert(2 * G::CPW == 8, "one copy after every other MFMA of a group");
+  auto no_epi = [](int, int) {};
 
   // Step s multiplies buffer s % NBUF, whose first group is already in slot
   // 0.  Before its last group it synchronises for step s + 1: wait for this
-  // wave's copies of s + 1 (those of s + 2 may stay in flight), barrier (all
-  // copies of s + 1 landed; nobody reads buffer (s - 1) % NBUF any more); the
-  // last group then refills that buffer with step s + DEPTH and reads the
-  // first group of s + 1.
-  auto step = [&](auto I, int s) {
+  // wave's copies of s + 1 (the copies of s + 2 may stay in flight: every step
+  // issues exactly 2 * CPW copies, real or dumped), barrier (all copies of s + 1
+  // landed; nobody reads buffer (s - 1) % NBUF any more); the last group then
+  // refills that buffer with step s + DEPTH and reads the first group of s + 1.
+  // The last step does the same on buffers nobody reads again.
+  using CopyOff = std::false_type;
+  using CopyOn = std::true_type;
+  auto step = [&](auto I, auto AI, int s, auto&& epi) {
     constexpr int b = decltype(I)::value;
     const float* cur = buf(I);
 #pragma unroll
-    for (int gi = 0; gi < NG; ++gi) {
-      const int slot = gi & 1;
-      if (gi + 1 < NG) {
-        mma_group(gi, slot, cur, gi + 1, true, false, nullptr, nullptr, nullptr);
-      } else if (s + 1 < nsteps) {
-        if (s + 2 < nsteps) {
-          __builtin_amdgcn_s_waitcnt(0x0f78);     // vmcnt(8): the copies of s + 2 may be in flight
-          static_assert(2 * G::CPW == 8, "wait count matches the copies per step");
-        } else {
-          __builtin_amdgcn_s_waitcnt(0x0f70);     // vmcnt(0)
-        }
-        stage_barrier();
-        const bool copying = s + DEPTH < nsteps;
-        const float* vs = vsrc + int64_t(cpass) * E * VX + cst * vstage;
-        const float* us = usrc + int64_t(cpass) * E * g.uplane + cst * ustage;
-        if (copying) advance();
-        mma_group(gi, slot, buf(std::integral_constant<int, b + 1>{}), 0, true, copying, vs, us,
-                  buf(std::integral_constant<int, b + DEPTH>{}));
-      } else {
-        mma_group(gi, slot, nullptr, 0, false, false, nullptr, nullptr, nullptr);
-      }
-    }
+    for (int gi = 0; gi + 1 < NG; ++gi)
+      mma_group(AI, CopyOff{}, gi, gi & 1, cur, gi + 1, nullptr, nullptr, nullptr, false, epi);
+    __builtin_amdgcn_s_waitcnt(0x0f78);           // vmcnt(8): the copies of s + 2 may be in flight
+    static_assert(2 * G::CPW == 8, "wait count matches the copies per step");
+    stage_barrier();
+    const bool real = s + DEPTH < nsteps;
+    const float* vs = vsrc + int64_t(cpass) * E * VX + cst * vstage;
+    const float* us = usrc + int64_t(cpass) * E * g.uplane + cst * ustage;
+    advance();
+    mma_group(AI, CopyOn{}, NG - 1, (NG - 1) & 1, buf(std::integral_constant<int, b + 1>{}), 0, vs, us,
+              buf(std::integral_constant<int, b + DEPTH>{}), real, epi);
   };
 
-  // the pass epilogue: its elements are RP alpha-rows (leading indices fixed,
-  // last index free).  Reduce each row along the last axis with A^T, then add
-  // it to every output with the product of A^T over the leading indices.
-  auto epilogue = [&](int pass) {
-    float c[G::NLEAD][RP];
+  // The pass epilogue.  A pass's elements are one alpha-row (leading indices
+  // fixed, last index free): reduce the row along the last axis with A^T, then
+  // add it to every output with the product of A^T over the leading indices
+  // (c[oo] for leading output index oo), and clear the accumulators.  Done
+  // per accumulator register r, in two halves.
+  static_assert(RP == 1, "one alpha-row per pass");
+  auto lead_coefs = [&](int row, float* c) {
 #pragma unroll
-    for (int oo = 0; oo < G::NLEAD; ++oo)
+    for (int oo = 0; oo < G::NLEAD; ++oo) c[oo] = lead_coef<N, MM, R, CONST>(AT, row, oo);
+  };
+  auto epi_half = [&](auto AP, const float* c, float* rowv, int r, int half) {
+    constexpr int ap = decltype(AP)::value;
+    if (half == 0) {
+      float sv[A];
 #pragma unroll
-      for (int rp = 0; rp < RP; ++rp) c[oo][rp] = lead_coef<N, MM, R, CONST>(AT, pass * RP + rp, oo);
+      for (int e = 0; e < A; ++e) sv[e] = acc[ap][e][r];
+      apply_axis<1, A, MM, 1>(sv, rowv, AT);
+#pragma unroll
+      for (int o = 0; o < NOUT / 2; ++o) yacc[o][r] = __builtin_fmaf(c[o / MM], rowv[o % MM], yacc[o][r]);
+    } else {
+#pragma unroll
+      for (int o = NOUT / 2; o < NOUT; ++o) yacc[o][r] = __builtin_fmaf(c[o / MM], rowv[o % MM], yacc[o][r]);
+#pragma unroll
+      for (int e = 0; e < A; ++e) acc[ap][e][r] = 0.0f;
+    }
+  };
+  auto epilogue = [&](auto AP, int pass) {
+    float c[G::NLEAD], rowv[MM];
+    lead_coefs(pass, c);
 #pragma unroll
     for (int r = 0; r < S::NACC; ++r) {
-      float rows[RP][MM];
-#pragma unroll
-      for (int rp = 0; rp < RP; ++rp) {
-        float sv[A];
-#pragma unroll
-        for (int e = 0; e < A; ++e) sv[e] = acc[rp * A + e][r];
-        apply_axis<1, A, MM, 1>(sv, rows[rp], AT);
-      }
-#pragma unroll
-      for (int o = 0; o < NOUT; ++o)
-#pragma unroll
-        for (int rp = 0; rp < RP; ++rp)
-          yacc[o][r] = __builtin_fmaf(c[o / MM][rp], rows[rp][o % MM], yacc[o][r]);
+      epi_half(AP, c, rowv, r, 0);
+      epi_half(AP, c, rowv, r, 1);
     }
-#pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] = typename S::acc_t{};
   };
 
   // ---- prologue: copies of the first DEPTH steps, then the first group
-  issue(buf0, cpass, cst);
+  issue(buf0, true, cpass, cst);
   advance();
-  if (1 < nsteps) {
-    issue(buf1, cpass, cst);
-    advance();
-  }
-  if (2 < nsteps) {
-    issue(buf2, cpass, cst);
-    advance();
-  }
+  issue(buf1, 1 < nsteps, cpass, cst);
+  advance();
+  issue(buf2, 2 < nsteps, cpass, cst);
+  advance();
   static_assert(DEPTH == 3, "prologue fills three buffers");
-  if (nsteps >= 3) __builtin_amdgcn_s_waitcnt(0x4f70);        // vmcnt(16)
-  else if (nsteps == 2) __builtin_amdgcn_s_waitcnt(0x0f78);   // vmcnt(8)
-  else __builtin_amdgcn_s_waitcnt(0x0f70);                    // vmcnt(0)
+  __builtin_amdgcn_s_waitcnt(0x4f70);             // vmcnt(16): step 0's copies landed
   stage_barrier();
   read_group(buf0, 0, 0);
-#pragma unroll
-  for (int e = 0; e < E; ++e) acc[e] = typename S::acc_t{};
 
-  // ---- steps, four per trip so that every buffer is named at compile time
-  int s = 0, pass = 0, st = 0;
-  auto finish = [&]() {                           // after a step: true when all are done
-    ++s;
-    if (++st == nstage) {
-      epilogue(pass);
-      st = 0;
-      ++pass;
-    }
-    return s == nsteps;
-  };
-  static_assert(NBUF == 4, "the step loop unrolls four buffers");
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  static_assert(NBUF == 4, "the step loops unroll four buffers");
+  if constexpr (OVL) {
+    // Every pass has a multiple of four steps, so each starts on buffer 0.
+    // Pass p's first two steps carry the epilogue of pass p - 1 (registers
+    // 0-7, then 8-15), one half-register after every other MFMA; pass 0
+    // carries a harmless epilogue of the still-zero other set.
+    static_assert(NG == 2 && S::NACC == 16, "16 half-registers per step of 32 MFMAs");
+    static_assert(G::NPASS % 2 == 0, "passes alternate between the two sets");
+    int s = 0;
+    auto run_pass = [&](auto AC, int pass) {
+      using AP = std::integral_constant<int, 1 - decltype(AC)::value>;
+      float c[G::NLEAD], rowv[MM];
+      lead_coefs(pass > 0 ? pass - 1 : 0, c);
+      auto epi_of = [&](int h) {
+        return [&, h](int gi, int m) {
+          if (m & 1) {
+            const int q = gi * 8 + (m >> 1);
+            epi_half(AP{}, c, rowv, 8 * h + (q >> 1), q & 1);
+          }
+        };
+      };
+      step(I0{}, AC, s, epi_of(0));
+      ++s;
+      step(I1{}, AC, s, epi_of(1));
+      ++s;
+      step(I2{}, AC, s, no_epi);
+      ++s;
+      step(I3{}, AC, s, no_epi);
+      ++s;
 #pragma unroll 1
-  for (;;) {
-    step(std::integral_constant<int, 0>{}, s);
-    if (finish()) break;
-    step(std::integral_constant<int, 1>{}, s);
-    if (finish()) break;
-    step(std::integral_constant<int, 2>{}, s);
-    if (finish()) break;
-    step(std::integral_constant<int, 3>{}, s);
-    if (finish()) break;
+      for (int st = 4; st < nstage; st += 4) {
+        step(I0{}, AC, s, no_epi);
+        ++s;
+        step(I1{}, AC, s, no_epi);
+        ++s;
+        step(I2{}, AC, s, no_epi);
+        ++s;
+        step(I3{}, AC, s, no_epi);
+        ++s;
+      }
+    };
+#pragma unroll 1
+    for (int pass = 0; pass < G::NPASS; pass += 2) {
+      run_pass(std::integral_constant<int, 0>{}, pass);
+      run_pass(std::integral_constant<int, 1>{}, pass + 1);
+    }
+    epilogue(std::integral_constant<int, 1>{}, G::NPASS - 1);
+  } else {
+    // ---- steps, four per trip so that every buffer is named at compile time
+    using A0 = std::integral_constant<int, 0>;
+    int s = 0, pass = 0, st = 0;
+    auto finish = [&]() {                         // after a step: true when all are done
+      ++s;
+      if (++st == nstage) {
+        epilogue(A0{}, pass);
+        st = 0;
+        ++pass;
+      }
+      return s == nsteps;
+    };
+#pragma unroll 1
+    for (;;) {
+      step(I0{}, A0{}, s, no_epi);
+      if (finish()) break;
+      step(I1{}, A0{}, s, no_epi);
+      if (finish()) break;
+      step(I2{}, A0{}, s, no_epi);
+      if (finish()) break;
+      step(I3{}, A0{}, s, no_epi);
+      if (finish()) break;
+    }
   }
 
   // ---- stitch: outputs through LDS so that neighbouring lanes store
   // neighbouring outputs of a row.  Plane o ([k][t], t XOR-swizzled by k) is
   // plane o % PPB of buffer o / PPB.
+  __builtin_amdgcn_s_waitcnt(0x0f70);             // vmcnt(0): no copy still writes LDS
   __syncthreads();
   auto plane = [&](int o) {
     const int b = o / G::PPB;
@@ -392,32 +460,34 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
   const int n = split_tile<N>(t, g.tiles, ti);
   const int ylast = ti[N - 1] * MM + ol;
   if (ylast >= g.Y[N - 1]) return;
-  constexpr int ITEMS = NOUT * TB * KB;
-  constexpr int NT = G::NT;
-  static_assert(NT % (MM * TB) == 0, "lanes tile the outputs");
-  for (int i = tid; i < ITEMS; i += NT) {
-    const int kl = (i / (MM * TB)) % KB;
-    const int orest = i / (MM * TB * KB);          // outputs of the leading axes
-    const int kg = kb * KB + kl;
-    if (kg >= g.K) continue;
-    int yc[3] = {0, 0, 0};
-    bool in = true;
-    int rem = orest;
+  // thread (ol, tl) stores its tile's outputs for kernels k0, k0 + KS, ...
+  constexpr int KS = G::NT / (MM * TB);
+  static_assert(G::NT % (MM * TB) == 0, "lanes tile the outputs");
+  const int k0 = tid / (MM * TB);
+  float* const yn = y + int64_t(n) * g.K * g.ystride_k;
 #pragma unroll
-    for (int ax = N - 2; ax >= 0; --ax) {
-      const int oa = rem % MM;
-      rem /= MM;
-      yc[ax] = ti[ax] * MM + oa;
-      in = in && yc[ax] < g.Y[ax];
+  for (int orest = 0; orest < G::NLEAD; ++orest) {   // output index of the leading axes
+    int64_t off = 0;
+    bool in = true;
+#pragma unroll
+    for (int ax = 0; ax < N - 1; ++ax) {
+      const int oa = (orest / ipow(MM, N - 2 - ax)) % MM;
+      const int yc = ti[ax] * MM + oa;
+      in = in && yc < g.Y[ax];
+      off = off * g.Y[ax] + yc;
     }
     if (!in) continue;
-    yc[N - 1] = ylast;
-    int64_t off = yc[0];
-#pragma unroll
-    for (int ax = 1; ax < N; ++ax) off = off * g.Y[ax] + yc[ax];
-    float v = plane(orest * MM + ol)[kl * TB + (tl ^ (kl & 31))];
-    if (g.relu) v = v > 0.0f ? v : 0.0f;
-    __builtin_nontemporal_store(v, y + (int64_t(n) * g.K + kg) * g.ystride_k + off);
+    off = off * g.Y[N - 1] + ylast;
+    const float* pl = plane(orest * MM + ol);
+    float* yo = yn + off;
+#pragma unroll 8
+    for (int kl = k0; kl < KB; kl += KS) {
+      const int kg = kb * KB + kl;
+      if (kg >= g.K) break;
+      float v = pl[kl * TB + (tl ^ (kl & 31))];
+      if (g.relu) v = v > 0.0f ? v : 0.0f;
+      __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
+    }
   }
 }
 

@@ -36,6 +36,17 @@ SMALL = [
               x_dist="normal", w_dist="he", relu=True),
 ]
 
+# C_pad a multiple of 64: the m = 2 GEMM overlaps each pass's epilogue with
+# the next pass (one or two rotations of the four stage buffers per pass)
+OVERLAP = [
+    LayerSpec("f2x3_3d_c64_ovl", N=3, m=2, r=3, batch=1, C=64, K=70, X=(6, 9, 10), pad=1,
+              x_dist="relu_normal", w_dist="he"),
+    LayerSpec("f2x3_3d_c128_ovl", N=3, m=2, r=3, batch=2, C=128, K=64, X=(5, 7, 6), pad=1,
+              x_dist="normal", w_dist="he", relu=True),
+    LayerSpec("f2x3_2d_c64_ovl", N=2, m=2, r=3, batch=3, C=60, K=130, X=(21, 17), pad=1,
+              x_dist="uniform", w_dist="he"),
+]
+
 EDGE = [
     LayerSpec("one_output", N=3, m=2, r=3, batch=1, C=3, K=2, X=(3, 3, 3), pad=0),
     LayerSpec("one_output_m4", N=3, m=4, r=3, batch=1, C=3, K=2, X=(3, 3, 3), pad=0),
@@ -51,7 +62,7 @@ EDGE = [
 ]
 
 
-@pytest.mark.parametrize("spec", SMALL + EDGE, ids=lambda s: s.name)
+@pytest.mark.parametrize("spec", SMALL + OVERLAP + EDGE, ids=lambda s: s.name)
 def test_small_layers_full_output(spec):
     x, w = draw_layer(spec, seed=11)
     y, _ = run_layer(spec, x, w, guard=1024)
