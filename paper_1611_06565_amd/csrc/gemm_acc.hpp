@@ -4,17 +4,18 @@
 // The inverse transform of eq. (4) is linear: every output is a sum over the
 // alpha^N elements xi of a coefficient (a product of A^T entries, one per
 // axis) times M_xi.  So the products of one (tile, kernel) pair need not be
-// live at once: a pass computes a few whole alpha-rows of elements (leading
-// indices fixed, last index free), reduces each row by A^T along the last
-// axis and adds it into the m^N outputs with the leading coefficients.  A
-// work-group keeps one pass of accumulators and covers a 64-tile x 64-kernel
-// block (twice the MFMA operand reuse of keeping all alpha^N elements
-// resident), plus m^N output accumulators per pair.
+// live at once: a pass computes two elements (half a row of the last axis),
+// reduces them by the matching columns of A^T along the last axis and adds
+// the result into the m^N outputs with the product of A^T over the leading
+// axes.  A work-group keeps one pass of accumulators and covers a 64-tile x
+// 64-kernel block (twice the MFMA operand reuse of keeping all alpha^N
+// elements resident); with two elements per pass a wave needs at most 256
+// registers, so two work-groups share a CU and each one's barriers, copies
+// and epilogues run under the other's MFMAs.
 //
 // Operands (V tile rows and U kernel columns of one pass and one channel
-// stage) are copied global -> LDS with 16-byte direct-to-LDS loads into a
-// double buffer, so the next stage streams in while this one is multiplied,
-// without holding registers.
+// stage) are copied global -> LDS with 16-byte direct-to-LDS loads into four
+// stage buffers, three steps ahead, without holding registers.
 //
 // Layouts: V[T_pad/64][C_pad/4][alpha^N][64][4], U[alpha^N][C_pad/4][K_pad][4]
 // (channel groups of 4 innermost: a lane's 16-byte LDS read holds 4 channels).
@@ -46,31 +47,30 @@ template <int N, int MM, int R>
 struct AccGeom {
   static constexpr int A = MM + R - 1;
   static constexpr int NXI = ipow(A, N);
-  // elements per pass: one row of the last axis (alpha accumulators of 16
-  // registers, leaving room for the m^N output accumulators and the operands)
-  static constexpr int E = A;
-  static constexpr int RP = E / A;                // alpha-rows per pass
-  static constexpr int NROW = ipow(A, N - 1);     // alpha-rows in all
+  static constexpr int E = 2;                     // elements per pass: half a row of the last axis
+  static constexpr int HALVES = A / E;            // passes per row
+  static constexpr int NROW = ipow(A, N - 1);     // rows of the last axis
   static constexpr int NPASS = NXI / E;
   static constexpr int NOUT = ipow(MM, N);        // outputs per (tile, kernel)
   static constexpr int NLEAD = NOUT / MM;         // outputs of the leading axes
   static constexpr int TB = 64, KB = 64;          // tiles and kernels per work-group
   static constexpr int NW = 4, NT = 256;          // wave (tq, kq) owns a 32 x 32 quadrant
   static constexpr int NBUF = 4;                  // stage buffers in LDS
-  static constexpr int DEPTH = 3;                 // stages in flight ahead of the one multiplied
-  static constexpr int SC = 64 / E;               // channels per stage: 32 KB of operands
+  static constexpr int DEPTH = 3;                 // steps in flight ahead of the one multiplied
+  static constexpr int SC = 16;                   // channels per stage
   static constexpr int G4 = SC / 4;               // 4-channel groups per stage
+  static constexpr int NG = G4 / 2;               // operand groups (channel pairs) per step
   static constexpr int CH = E * G4;               // 1 KB chunks per operand per stage
   static constexpr int CPW = CH / NW;             // chunks per operand per wave
+  static constexpr int CPS = 2 * CPW;             // copies per wave per step
   static constexpr int SA = CH * 256;             // floats of V (and of U) per stage
-  static constexpr int STAGE = 2 * SA;
+  static constexpr int STAGE = 2 * SA;            // 16 KB
   static constexpr int PLANE = TB * KB;           // stitch plane of one output index
-  static constexpr int PPB = STAGE / PLANE;       // stitch planes per buffer
+  static constexpr int PPR = NBUF * (STAGE / PLANE);   // stitch planes per round
   static_assert(MM == 2, "m = 2 only: 2^N output accumulators per pair");
-  static_assert(E % A == 0 && NXI % E == 0, "passes of whole alpha-rows");
-  static_assert(SC % 8 == 0, "whole pairs of 4-channel groups per stage");
-  static_assert(CH % NW == 0, "copies split evenly over the waves");
-  static_assert(NOUT <= NBUF * PPB, "stitch fits the stage buffers");
+  static_assert(A % E == 0, "passes of half rows");
+  static_assert(CH % NW == 0 && CPS == 4, "four copies per wave per step");
+  static_assert(STAGE == PLANE && NOUT % PPR == 0, "stitch rounds of whole buffers");
   static_assert(DEPTH < NBUF, "a buffer is refilled only after it was multiplied");
 };
 
@@ -140,18 +140,17 @@ __device__ __forceinline__ float lead_coef(const MatRef<Which::AT, CONST, MM, R>
   return c;
 }
 
-template <int N, int MM, int R, bool CONST, bool OVL>
-__global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
-                                                  const float* __restrict__ U,
-                                                  float* __restrict__ y, AccArgs g, FMats fm) {
+template <int N, int MM, int R, bool CONST>
+__global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V,
+                                                     const float* __restrict__ U,
+                                                     float* __restrict__ y, AccArgs g, FMats fm) {
   using G = AccGeom<N, MM, R>;
   using S = MfmaShape<32>;
-  constexpr int A = G::A, E = G::E, NOUT = G::NOUT, G4 = G::G4, RP = G::RP;
+  constexpr int A = G::A, E = G::E, NOUT = G::NOUT, G4 = G::G4, NG = G::NG;
   constexpr int TB = G::TB, KB = G::KB, NW = G::NW, NBUF = G::NBUF, DEPTH = G::DEPTH;
 
   // The stage buffers are distinct LDS objects, always named with a
-  // compile-time index: the compiler can then tell that reads of one buffer
-  // do not depend on copies still in flight into another.
+  // compile-time index.
   __shared__ __attribute__((aligned(16))) float buf0[G::STAGE];
   __shared__ __attribute__((aligned(16))) float buf1[G::STAGE];
   __shared__ __attribute__((aligned(16))) float buf2[G::STAGE];
@@ -166,6 +165,7 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
     else if constexpr (b == 2) return buf2;
     else return buf3;
   };
+  auto bufi = [&](int b) -> float* { return b == 0 ? buf0 : b == 1 ? buf1 : b == 2 ? buf2 : buf3; };
 
   const int tid = int(threadIdx.x);
   const int lane = tid & 63;
@@ -194,9 +194,9 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
     uoff[i] = e * g.uplane + int64_t(gi) * g.K_pad * 4;
   }
   const int64_t vstage = G4 * VG, ustage = int64_t(G4) * g.K_pad * 4;
-  // copy q in [0, 2 * CPW) of a step: chunk q / 2 of V (q even) or of U (q
-  // odd).  A step past the last one (real == false) copies the first chunk of
-  // the block again into the dump area instead.
+  // copy q of a step: chunk q / 2 of V (q even) or of U (q odd).  A step past
+  // the last one (real == false) copies the block's first chunk again into
+  // the dump area instead.
   auto copy_one = [&](const float* vs, const float* us, float* base, bool real, int q) {
     const int i = q >> 1, c = wave + NW * i;
     if ((q & 1) == 0) {
@@ -205,288 +205,226 @@ __global__ void __launch_bounds__(256) k_gemm_acc(const float* __restrict__ V,
       lds_copy16<false>(real ? us + uoff[i] : usrc, real ? base + G::SA + c * 256 : dump);
     }
   };
-  auto issue = [&](float* base, bool real, int pass, int st) {
-    const float* vs = vsrc + int64_t(pass) * E * VX + st * vstage;
-    const float* us = usrc + int64_t(pass) * E * g.uplane + st * ustage;
+  // copy cursor: the next step to copy, as (pass, stage)
+  int cpass = 0, cst = 0;
+  auto cursor_src = [&](const float*& vs, const float*& us) {
+    vs = vsrc + int64_t(cpass) * E * VX + cst * vstage;
+    us = usrc + int64_t(cpass) * E * g.uplane + cst * ustage;
+  };
+  auto advance = [&]() {
+    const bool wrap = cst + 1 == nstage;
+    cst = wrap ? 0 : cst + 1;
+    cpass += wrap ? 1 : 0;
+  };
+  auto issue = [&](float* base, bool real) {
+    const float* vs;
+    const float* us;
+    cursor_src(vs, us);
 #pragma unroll
-    for (int q = 0; q < 2 * G::CPW; ++q) copy_one(vs, us, base, real, q);
+    for (int q = 0; q < G::CPS; ++q) copy_one(vs, us, base, real, q);
+    advance();
   };
 
-  // Two accumulator sets when the pass epilogue overlaps the next pass (OVL):
-  // pass p accumulates into set p % 2 while the epilogue of pass p - 1 reads
-  // and clears the other set between the MFMAs.
-  typename S::acc_t acc[OVL ? 2 : 1][E];
+  typename S::acc_t acc[E];
   float yacc[NOUT][S::NACC];
 #pragma unroll
   for (int o = 0; o < NOUT; ++o)
 #pragma unroll
     for (int r = 0; r < S::NACC; ++r) yacc[o][r] = 0.0f;
 #pragma unroll
-  for (int k = 0; k < (OVL ? 2 : 1); ++k)
-#pragma unroll
-    for (int e = 0; e < E; ++e) acc[k][e] = typename S::acc_t{};
+  for (int e = 0; e < E; ++e) acc[e] = typename S::acc_t{};
 
   const MatRef<Which::AT, CONST, MM, R> AT{&fm};
   const int aoff = (kr * TB + tq * 32 + col) * 4;
   const int boff = G::SA + (kr * KB + kq * 32 + col) * 4;
 
-  // copy cursor: the next step to copy, as (pass, stage)
-  int cpass = 0, cst = 0;
-  auto advance = [&]() {
-    const bool wrap = cst + 1 == nstage;
-    cst = wrap ? 0 : cst + 1;
-    cpass += wrap ? 1 : 0;
-  };
-
-  // Operands go in groups of 4 elements of one pair p of 4-channel groups:
-  // lane half kr reads group 2p + kr, so k-step j of the pair contracts
-  // channels 8p + j (kr = 0) and 8p + 4 + j (kr = 1).  Each group is read from
-  // LDS while the MFMAs of the previous one run, across step boundaries too.
-  constexpr int NG = (G4 / 2) * (E / 4);          // operand groups per step
-  static_assert(NG % 2 == 0, "a step's first group always uses slot 0");
-  float4 a4[2][4], b4[2][4];
-  auto read_one = [&](const float* base, int gidx, int slot, int q) {   // q: A of e = q/2 (even), B (odd)
-    const int p = gidx / (E / 4), e = (gidx % (E / 4)) * 4 + (q >> 1);
+  // Operand group p (a pair of 4-channel groups) of a step: lane half kr reads
+  // group 2p + kr, so k-step j contracts channels 8p + j (kr = 0) and 8p + 4 + j
+  // (kr = 1), for both elements of the pass.  Each group is read from LDS while
+  // the MFMAs of the previous one run, across step boundaries too.
+  float4 a4[2][E], b4[2][E];
+  auto read_one = [&](const float* base, int p, int slot, int q) {   // q: A of e = q/2 (even), B (odd)
+    const int e = q >> 1;
     const int off = (e * G4 + 2 * p) * 256;
-    if ((q & 1) == 0) a4[slot][q >> 1] = *reinterpret_cast<const float4*>(base + aoff + off);
-    else b4[slot][q >> 1] = *reinterpret_cast<const float4*>(base + boff + off);
+    if ((q & 1) == 0) a4[slot][e] = *reinterpret_cast<const float4*>(base + aoff + off);
+    else b4[slot][e] = *reinterpret_cast<const float4*>(base + boff + off);
   };
-  auto read_group = [&](const float* base, int gidx, int slot) {
-#pragma unroll
-    for (int q = 0; q < 8; ++q) read_one(base, gidx, slot, q);
-  };
-  // The 16 MFMAs of group gidx from `slot` into accumulator set AI, in a fixed
-  // order with the reads of the next group (into the other slot), in a step's
-  // last group the copies of a later step, and whatever `epi` adds after each
-  // MFMA, so that the matrix unit keeps being fed while they issue.
-  auto mma_group = [&](auto AI, auto COPY, int gidx, int slot, const float* nbase, int ngidx,
-                       const float* vs, const float* us, float* cbase, bool real, auto&& epi) {
-    constexpr int ai = decltype(AI)::value;
+  // The 4 * E MFMAs of group p from `slot`, in a fixed order with the reads of
+  // the next group (into the other slot) and, in a step's last group, the
+  // copies of a later step.
+  auto mma_group = [&](auto COPY, int slot, const float* nbase, int np, const float* vs,
+                       const float* us, float* cbase, bool real) {
     constexpr bool copying = decltype(COPY)::value;
-    const int e0 = (gidx % (E / 4)) * 4;
 #pragma unroll
-    for (int m = 0; m < 16; ++m) {
-      const int j = m >> 2, e = m & 3;
+    for (int m = 0; m < 4 * E; ++m) {
+      const int j = m / E, e = m % E;
       const float4 av4 = a4[slot][e], bv4 = b4[slot][e];
       const float av = j == 0 ? av4.x : j == 1 ? av4.y : j == 2 ? av4.z : av4.w;
       const float bv = j == 0 ? bv4.x : j == 1 ? bv4.y : j == 2 ? bv4.z : bv4.w;
-      acc[ai][e0 + e] = S::mma(av, bv, acc[ai][e0 + e]);
-      if (m < 8) read_one(nbase, ngidx, slot ^ 1, m);
+      acc[e] = S::mma(av, bv, acc[e]);
+      if (m < 2 * E) read_one(nbase, np, slot ^ 1, m);
       if constexpr (copying) {
         if (m & 1) copy_one(vs, us, cbase, real, m >> 1);
       }
-      epi(gidx, m);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  static_assert(2 * G::CPW == 8, "one copy after every other MFMA of a group");
-  auto no_epi = [](int, int) {};
+  static_assert(4 * E == 2 * G::CPS, "one copy after every other MFMA of a group");
 
   // Step s multiplies buffer s % NBUF, whose first group is already in slot
   // 0.  Before its last group it synchronises for step s + 1: wait for this
-  // wave's copies of s + 1 (the copies of s + 2 may stay in flight: every step
-  // issues exactly 2 * CPW copies, real or dumped), barrier (all copies of s + 1
-  // landed; nobody reads buffer (s - 1) % NBUF any more); the last group then
-  // refills that buffer with step s + DEPTH and reads the first group of s + 1.
-  // The last step does the same on buffers nobody reads again.
+  // wave's copies of s + 1 (the CPS copies of s + 2 may stay in flight: every
+  // step issues exactly CPS copies, real or dumped), barrier (all copies of
+  // s + 1 landed; nobody reads buffer (s - 1) % NBUF any more); the last group
+  // then refills that buffer with step s + DEPTH and reads the first group of
+  // s + 1.  The last step does the same on buffers nobody reads again.
   using CopyOff = std::false_type;
   using CopyOn = std::true_type;
-  auto step = [&](auto I, auto AI, int s, auto&& epi) {
+  static_assert(NG % 2 == 0, "a step's first group always uses slot 0");
+  auto step = [&](auto I, int s) {
     constexpr int b = decltype(I)::value;
     const float* cur = buf(I);
 #pragma unroll
-    for (int gi = 0; gi + 1 < NG; ++gi)
-      mma_group(AI, CopyOff{}, gi, gi & 1, cur, gi + 1, nullptr, nullptr, nullptr, false, epi);
-    __builtin_amdgcn_s_waitcnt(0x0f78);           // vmcnt(8): the copies of s + 2 may be in flight
-    static_assert(2 * G::CPW == 8, "wait count matches the copies per step");
+    for (int p = 0; p + 1 < NG; ++p) mma_group(CopyOff{}, p & 1, cur, p + 1, nullptr, nullptr, nullptr, false);
+    __builtin_amdgcn_s_waitcnt(0x0f74);           // vmcnt(4): the copies of s + 2 may be in flight
+    static_assert(G::CPS == 4, "wait count matches the copies per step");
     stage_barrier();
     const bool real = s + DEPTH < nsteps;
-    const float* vs = vsrc + int64_t(cpass) * E * VX + cst * vstage;
-    const float* us = usrc + int64_t(cpass) * E * g.uplane + cst * ustage;
+    const float* vs;
+    const float* us;
+    cursor_src(vs, us);
     advance();
-    mma_group(AI, CopyOn{}, NG - 1, (NG - 1) & 1, buf(std::integral_constant<int, b + 1>{}), 0, vs, us,
-              buf(std::integral_constant<int, b + DEPTH>{}), real, epi);
+    mma_group(CopyOn{}, (NG - 1) & 1, buf(std::integral_constant<int, b + 1>{}), 0, vs, us,
+              buf(std::integral_constant<int, b + DEPTH>{}), real);
   };
 
-  // The pass epilogue.  A pass's elements are one alpha-row (leading indices
-  // fixed, last index free): reduce the row along the last axis with A^T, then
-  // add it to every output with the product of A^T over the leading indices
-  // (c[oo] for leading output index oo), and clear the accumulators.  Done
-  // per accumulator register r, in two halves.
-  static_assert(RP == 1, "one alpha-row per pass");
-  auto lead_coefs = [&](int row, float* c) {
+  // Pass epilogue for pass p = (row, half h): the two elements xi_last = 2h,
+  // 2h + 1 of the row are reduced by the matching columns of A^T along the last
+  // axis, then added to every output with the product of A^T over the leading
+  // axes; the accumulators are cleared for the next pass.
+  auto epilogue = [&](int pass) {
+    const int row = pass / G::HALVES, h = pass % G::HALVES;
+    float c[G::NLEAD], at[MM][E];
 #pragma unroll
     for (int oo = 0; oo < G::NLEAD; ++oo) c[oo] = lead_coef<N, MM, R, CONST>(AT, row, oo);
-  };
-  auto epi_half = [&](auto AP, const float* c, float* rowv, int r, int half) {
-    constexpr int ap = decltype(AP)::value;
-    if (half == 0) {
-      float sv[A];
 #pragma unroll
-      for (int e = 0; e < A; ++e) sv[e] = acc[ap][e][r];
-      apply_axis<1, A, MM, 1>(sv, rowv, AT);
+    for (int ol = 0; ol < MM; ++ol)
 #pragma unroll
-      for (int o = 0; o < NOUT / 2; ++o) yacc[o][r] = __builtin_fmaf(c[o / MM], rowv[o % MM], yacc[o][r]);
-    } else {
+      for (int e = 0; e < E; ++e) {
+        float v = AT(ol, e);
 #pragma unroll
-      for (int o = NOUT / 2; o < NOUT; ++o) yacc[o][r] = __builtin_fmaf(c[o / MM], rowv[o % MM], yacc[o][r]);
-#pragma unroll
-      for (int e = 0; e < A; ++e) acc[ap][e][r] = 0.0f;
-    }
-  };
-  auto epilogue = [&](auto AP, int pass) {
-    float c[G::NLEAD], rowv[MM];
-    lead_coefs(pass, c);
+        for (int hh = 1; hh < G::HALVES; ++hh) v = (h == hh) ? AT(ol, hh * E + e) : v;
+        at[ol][e] = v;
+      }
 #pragma unroll
     for (int r = 0; r < S::NACC; ++r) {
-      epi_half(AP, c, rowv, r, 0);
-      epi_half(AP, c, rowv, r, 1);
+      float rv[MM];
+#pragma unroll
+      for (int ol = 0; ol < MM; ++ol) {
+        float v = at[ol][0] * acc[0][r];
+#pragma unroll
+        for (int e = 1; e < E; ++e) v = __builtin_fmaf(at[ol][e], acc[e][r], v);
+        rv[ol] = v;
+      }
+#pragma unroll
+      for (int o = 0; o < NOUT; ++o) yacc[o][r] = __builtin_fmaf(c[o / MM], rv[o % MM], yacc[o][r]);
     }
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = typename S::acc_t{};
   };
 
   // ---- prologue: copies of the first DEPTH steps, then the first group
-  issue(buf0, true, cpass, cst);
-  advance();
-  issue(buf1, 1 < nsteps, cpass, cst);
-  advance();
-  issue(buf2, 2 < nsteps, cpass, cst);
-  advance();
+  issue(buf0, true);
+  issue(buf1, 1 < nsteps);
+  issue(buf2, 2 < nsteps);
   static_assert(DEPTH == 3, "prologue fills three buffers");
-  __builtin_amdgcn_s_waitcnt(0x4f70);             // vmcnt(16): step 0's copies landed
+  __builtin_amdgcn_s_waitcnt(0x0f78);             // vmcnt(8): step 0's copies landed
+  static_assert(2 * G::CPS == 8, "prologue wait count");
   stage_barrier();
-  read_group(buf0, 0, 0);
+#pragma unroll
+  for (int q = 0; q < 2 * E; ++q) read_one(buf0, 0, 0, q);
 
+  // ---- steps, four per trip so that every buffer is named at compile time
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
   using I3 = std::integral_constant<int, 3>;
-  static_assert(NBUF == 4, "the step loops unroll four buffers");
-  if constexpr (OVL) {
-    // Every pass has a multiple of four steps, so each starts on buffer 0.
-    // Pass p's first two steps carry the epilogue of pass p - 1 (registers
-    // 0-7, then 8-15), one half-register after every other MFMA; pass 0
-    // carries a harmless epilogue of the still-zero other set.
-    static_assert(NG == 2 && S::NACC == 16, "16 half-registers per step of 32 MFMAs");
-    static_assert(G::NPASS % 2 == 0, "passes alternate between the two sets");
-    int s = 0;
-    auto run_pass = [&](auto AC, int pass) {
-      using AP = std::integral_constant<int, 1 - decltype(AC)::value>;
-      float c[G::NLEAD], rowv[MM];
-      lead_coefs(pass > 0 ? pass - 1 : 0, c);
-      auto epi_of = [&](int h) {
-        return [&, h](int gi, int m) {
-          if (m & 1) {
-            const int q = gi * 8 + (m >> 1);
-            epi_half(AP{}, c, rowv, 8 * h + (q >> 1), q & 1);
-          }
-        };
-      };
-      step(I0{}, AC, s, epi_of(0));
-      ++s;
-      step(I1{}, AC, s, epi_of(1));
-      ++s;
-      step(I2{}, AC, s, no_epi);
-      ++s;
-      step(I3{}, AC, s, no_epi);
-      ++s;
-#pragma unroll 1
-      for (int st = 4; st < nstage; st += 4) {
-        step(I0{}, AC, s, no_epi);
-        ++s;
-        step(I1{}, AC, s, no_epi);
-        ++s;
-        step(I2{}, AC, s, no_epi);
-        ++s;
-        step(I3{}, AC, s, no_epi);
-        ++s;
-      }
-    };
-#pragma unroll 1
-    for (int pass = 0; pass < G::NPASS; pass += 2) {
-      run_pass(std::integral_constant<int, 0>{}, pass);
-      run_pass(std::integral_constant<int, 1>{}, pass + 1);
+  static_assert(NBUF == 4, "the step loop unrolls four buffers");
+  int s = 0, pass = 0, st = 0;
+  auto finish = [&]() {                           // after a step: true when all are done
+    ++s;
+    if (++st == nstage) {
+      epilogue(pass);
+      st = 0;
+      ++pass;
     }
-    epilogue(std::integral_constant<int, 1>{}, G::NPASS - 1);
-  } else {
-    // ---- steps, four per trip so that every buffer is named at compile time
-    using A0 = std::integral_constant<int, 0>;
-    int s = 0, pass = 0, st = 0;
-    auto finish = [&]() {                         // after a step: true when all are done
-      ++s;
-      if (++st == nstage) {
-        epilogue(A0{}, pass);
-        st = 0;
-        ++pass;
-      }
-      return s == nsteps;
-    };
+    return s == nsteps;
+  };
 #pragma unroll 1
-    for (;;) {
-      step(I0{}, A0{}, s, no_epi);
-      if (finish()) break;
-      step(I1{}, A0{}, s, no_epi);
-      if (finish()) break;
-      step(I2{}, A0{}, s, no_epi);
-      if (finish()) break;
-      step(I3{}, A0{}, s, no_epi);
-      if (finish()) break;
-    }
+  for (;;) {
+    step(I0{}, s);
+    if (finish()) break;
+    step(I1{}, s);
+    if (finish()) break;
+    step(I2{}, s);
+    if (finish()) break;
+    step(I3{}, s);
+    if (finish()) break;
   }
 
   // ---- stitch: outputs through LDS so that neighbouring lanes store
-  // neighbouring outputs of a row.  Plane o ([k][t], t XOR-swizzled by k) is
-  // plane o % PPB of buffer o / PPB.
+  // neighbouring outputs of a row, PPR output planes per round.  Plane o
+  // ([k][t], t XOR-swizzled by k) of a round lives in buffer o % PPR.
   __builtin_amdgcn_s_waitcnt(0x0f70);             // vmcnt(0): no copy still writes LDS
-  __syncthreads();
-  auto plane = [&](int o) {
-    const int b = o / G::PPB;
-    float* base = b == 0 ? buf0 : b == 1 ? buf1 : b == 2 ? buf2 : buf3;
-    return base + (o % G::PPB) * G::PLANE;
-  };
-#pragma unroll
-  for (int o = 0; o < NOUT; ++o)
-#pragma unroll
-    for (int r = 0; r < S::NACC; ++r) {
-      const int t = tq * 32 + S::acc_row(lane, r), k = kq * 32 + col;
-      plane(o)[k * TB + (t ^ (k & 31))] = yacc[o][r];
-    }
-  __syncthreads();
-  // item i: last-axis output fastest, then tile, then kernel, then the others
   const int ol = tid % MM;
   const int tl = (tid / MM) % TB;
   const int t = tb * TB + tl;
-  if (t >= g.T) return;
   int ti[3] = {0, 0, 0};
-  const int n = split_tile<N>(t, g.tiles, ti);
+  const int n = split_tile<N>(t < g.T ? t : 0, g.tiles, ti);
   const int ylast = ti[N - 1] * MM + ol;
-  if (ylast >= g.Y[N - 1]) return;
+  const bool mine = t < g.T && ylast < g.Y[N - 1];
   // thread (ol, tl) stores its tile's outputs for kernels k0, k0 + KS, ...
   constexpr int KS = G::NT / (MM * TB);
   static_assert(G::NT % (MM * TB) == 0, "lanes tile the outputs");
   const int k0 = tid / (MM * TB);
   float* const yn = y + int64_t(n) * g.K * g.ystride_k;
+  constexpr int LPR = G::PPR / MM;                // leading output indices per round
 #pragma unroll
-  for (int orest = 0; orest < G::NLEAD; ++orest) {   // output index of the leading axes
-    int64_t off = 0;
-    bool in = true;
+  for (int o0 = 0; o0 < NOUT; o0 += G::PPR) {
+    __syncthreads();                              // buffers free (last MFMA reads / previous round)
 #pragma unroll
-    for (int ax = 0; ax < N - 1; ++ax) {
-      const int oa = (orest / ipow(MM, N - 2 - ax)) % MM;
-      const int yc = ti[ax] * MM + oa;
-      in = in && yc < g.Y[ax];
-      off = off * g.Y[ax] + yc;
-    }
-    if (!in) continue;
-    off = off * g.Y[N - 1] + ylast;
-    const float* pl = plane(orest * MM + ol);
-    float* yo = yn + off;
+    for (int o = o0; o < o0 + G::PPR; ++o)
+#pragma unroll
+      for (int r = 0; r < S::NACC; ++r) {
+        const int tt = tq * 32 + S::acc_row(lane, r), k = kq * 32 + col;
+        bufi(o - o0)[k * TB + (tt ^ (k & 31))] = yacc[o][r];
+      }
+    __syncthreads();
+    if (mine) {
+#pragma unroll
+      for (int orest = o0 / MM; orest < o0 / MM + LPR; ++orest) {   // leading output index
+        int64_t off = 0;
+        bool in = true;
+#pragma unroll
+        for (int ax = 0; ax < N - 1; ++ax) {
+          const int oa = (orest / ipow(MM, N - 2 - ax)) % MM;
+          const int yc = ti[ax] * MM + oa;
+          in = in && yc < g.Y[ax];
+          off = off * g.Y[ax] + yc;
+        }
+        if (!in) continue;
+        off = off * g.Y[N - 1] + ylast;
+        const float* pl = bufi(orest * MM + ol - o0);
+        float* yo = yn + off;
 #pragma unroll 8
-    for (int kl = k0; kl < KB; kl += KS) {
-      const int kg = kb * KB + kl;
-      if (kg >= g.K) break;
-      float v = pl[kl * TB + (tl ^ (kl & 31))];
-      if (g.relu) v = v > 0.0f ? v : 0.0f;
-      __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
+        for (int kl = k0; kl < KB; kl += KS) {
+          const int kg = kb * KB + kl;
+          if (kg >= g.K) break;
+          float v = pl[kl * TB + (tl ^ (kl & 31))];
+          if (g.relu) v = v > 0.0f ? v : 0.0f;
+          __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
+        }
+      }
     }
   }
 }

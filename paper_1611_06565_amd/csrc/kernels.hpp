@@ -49,9 +49,9 @@ struct Blocking {
   static constexpr int VEC = ACC ? 2 : (NXI > 64 ? 1 : 2);       // floats per operand load
   static constexpr int CG = ACC ? 4 : KSTEP * VEC;               // channels per V group
   static constexpr int CGU = CG;                                 // channels per U group
-  // channels are padded to whole operand stages of the GEMM (32 KB stages of
-  // alpha elements; see AccGeom)
-  static constexpr int CPAD = ACC ? 64 / A : CGU;
+  // channels are padded to whole operand stages of the GEMM (16 channels;
+  // see AccGeom)
+  static constexpr int CPAD = ACC ? 16 : CGU;
 };
 
 // ---------------------------------------------------------------- arguments

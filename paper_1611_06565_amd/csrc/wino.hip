@@ -132,15 +132,8 @@ struct Launch {
       a.nblocks = int32_t(nb);
       for (int i = 0; i < 3; ++i) { a.tiles[i] = int32_t(p.tiles[i]); a.Y[i] = int32_t(p.Y[i]); }
       a.relu = (p.flags & WINO_RELU) ? 1 : 0;
-      // the overlapped-epilogue variant needs every pass to start on the same
-      // stage buffer (a multiple of NBUF channel stages per pass), and the
-      // compile-time matrices (with run-time ones it runs out of registers)
-      if (CONST && (p.C_pad / G::SC) % G::NBUF == 0)
-        hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST, true>), dim3(unsigned(nb)), dim3(G::NT), 0, s, V,
-                           U, y, a, p.fm);
-      else
-        hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST, false>), dim3(unsigned(nb)), dim3(G::NT), 0, s, V,
-                           U, y, a, p.fm);
+      hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST>), dim3(unsigned(nb)), dim3(G::NT), 0, s, V, U, y,
+                         a, p.fm);
       return launch_status();
     } else {
       GemmArgs g{};
