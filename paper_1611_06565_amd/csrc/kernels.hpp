@@ -254,6 +254,111 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
   }
 }
 
+// Input transform for large windows (alpha^N = 216, F(4^3, 3^3)): one
+// (tile, channel)'s window is too big for one thread's registers at a useful
+// occupancy, so it is split over A threads along axis 0.  Thread (i0, q)
+// loads plane i0 of the window of pair q (A rows of A values, loaded and
+// masked as in k_input) and transforms it along the other two axes; the
+// planes meet in LDS; then thread (x0, q) forms output plane x0 =
+// sum_i0 B^T[x0][i0] * plane_i0 (axis 0 of eq. 4) and writes its A^2 values.
+// A work-group covers one tile block (BLK tiles) and one channel group: the
+// BLK * CG pairs q, with channels fastest.
+template <int N, int MM, int R, bool CONST>
+__global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x, float* __restrict__ V, InputArgs a, FMats fm) {
+  using B = Blocking<N, MM, R>;
+  constexpr int A = B::A, NXI = B::NXI, BLK = B::BLK, CG = B::CG;
+  constexpr int NQ = BLK * CG;            // (tile, channel) pairs per work-group
+  constexpr int PL = NXI / A;             // values per plane
+  static_assert(N == 3 && NQ == 64 && A * 64 == 384, "one wave per plane, six planes");
+  __shared__ float planes[A][PL][NQ];
+
+  const int tid = int(threadIdx.x);
+  const int q = tid % NQ;
+  const int i0 = __builtin_amdgcn_readfirstlane(tid / NQ);   // plane of this wave
+  const int cl = q % CG, tl = q / CG;
+  const int L = xcd_remap(int(blockIdx.x), a.nblocks);
+  const int tb = L % a.ntb;
+  const int cg = L / a.ntb;
+  const int c = cg * CG + cl;
+  const int t = tb * BLK + tl;
+
+  float d[PL];
+  if (t < a.T && c < a.C) {
+    int ti[3] = {0, 0, 0};
+    const int n = split_tile<N>(t, a.tiles, ti);
+    int o[3];
+#pragma unroll
+    for (int ax = 0; ax < N; ++ax) o[ax] = ti[ax] * MM - a.pad[ax];
+    const float* xc = x + (int64_t(n) * a.C + c) * a.xstride_c;
+    const int XL = a.X[N - 1];
+    const int oL = o[N - 1];
+    const bool wide = XL >= A;
+    const int sL = wide ? min(max(oL, 0), XL - A) : 0;
+    const int delta = oL - sL;
+    const int q0 = o[0] + i0;
+    const bool valid0 = (unsigned)q0 < (unsigned)a.X[0];
+    const int64_t off0 = min(max(q0, 0), a.X[0] - 1);
+#pragma unroll
+    for (int i1 = 0; i1 < A; ++i1) {
+      const int q1 = o[1] + i1;
+      const bool valid = valid0 && (unsigned)q1 < (unsigned)a.X[1];
+      const float* xr = xc + (off0 * a.X[1] + min(max(q1, 0), a.X[1] - 1)) * XL;
+      float* dr = d + i1 * A;
+      if (wide) {
+        float ld[A];
+        __builtin_memcpy(ld, xr + sL, sizeof(ld));
+#pragma unroll
+        for (int i = 0; i < A; ++i) {
+          float v = 0.0f;
+#pragma unroll
+          for (int j = 0; j < A; ++j) v = (j == i + delta) ? ld[j] : v;
+          dr[i] = valid ? v : 0.0f;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < A; ++i) {
+          const int qq = oL + i;
+          const bool in = valid && (unsigned)qq < (unsigned)XL;
+          const float v = xr[min(max(qq, 0), XL - 1)];
+          dr[i] = in ? v : 0.0f;
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < PL; ++i) d[i] = 0.0f;
+  }
+  const MatRef<Which::BT, CONST, MM, R> BT{&fm};
+  float p2[PL];
+  transform_nd<2, A, A>(d, p2, BT);       // axes 1 and 2 of the plane
+#pragma unroll
+  for (int j = 0; j < PL; ++j) planes[i0][j][q] = p2[j];
+  __syncthreads();
+
+  // output plane x0 = i0 of this wave; V[tb][cg][xi][tl][cl], xi = x0 * PL + j
+  const int x0 = i0;
+  float* dst = V + (int64_t(tb) * a.C_pad + int64_t(cg) * CG) * NXI * BLK + int64_t(x0) * PL * (BLK * CG) + q;
+  auto combine = [&](auto X0) {
+    constexpr int xr = decltype(X0)::value;
+#pragma unroll
+    for (int j = 0; j < PL; ++j) {
+      float col[A];
+#pragma unroll
+      for (int i = 0; i < A; ++i) col[i] = planes[i][j][q];
+      __builtin_nontemporal_store(dot_row<A>(BT, xr, col, 1), dst + j * (BLK * CG));
+    }
+  };
+  static_assert(A == 6, "six output planes");
+  switch (x0) {
+    case 0: combine(std::integral_constant<int, 0>{}); break;
+    case 1: combine(std::integral_constant<int, 1>{}); break;
+    case 2: combine(std::integral_constant<int, 2>{}); break;
+    case 3: combine(std::integral_constant<int, 3>{}); break;
+    case 4: combine(std::integral_constant<int, 4>{}); break;
+    default: combine(std::integral_constant<int, 5>{}); break;
+  }
+}
+
 // ------------------------------------------------- batched GEMM (a4 + a5)
 // Work-group = BLK tiles x BLK kernels x all alpha^N elements.  Wave w owns
 // the elements with xi_0 = w (an alpha^(N-1) slice) and keeps one BLK x BLK

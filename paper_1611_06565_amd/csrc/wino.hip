@@ -108,12 +108,22 @@ struct Launch {
     for (int i = 0; i < 3; ++i) {
       a.X[i] = int32_t(p.X[i]); a.tiles[i] = int32_t(p.tiles[i]); a.pad[i] = p.pad[i];
     }
-    constexpr int GPW = 256 / (BLK * CG);
     const int64_t groups = p.C_pad / CG;
-    const int64_t nb = (p.T_pad / BLK) * ((groups + GPW - 1) / GPW);
     a.ntb = int32_t(p.T_pad / BLK);
-    a.nblocks = int32_t(nb);
-    hipLaunchKernelGGL((k_input<N, MM, R, CONST>), dim3(unsigned(nb)), dim3(256), 0, s, x, V, a, p.fm);
+    if constexpr (Blocking<N, MM, R>::NXI > 64) {
+      // large windows: A threads per (tile, channel), one tile block and one
+      // channel group per work-group
+      constexpr int A = Blocking<N, MM, R>::A;
+      const int64_t nb = (p.T_pad / BLK) * groups;
+      a.nblocks = int32_t(nb);
+      hipLaunchKernelGGL((k_input_split<N, MM, R, CONST>), dim3(unsigned(nb)), dim3(A * 64), 0, s, x, V,
+                         a, p.fm);
+    } else {
+      constexpr int GPW = 256 / (BLK * CG);
+      const int64_t nb = (p.T_pad / BLK) * ((groups + GPW - 1) / GPW);
+      a.nblocks = int32_t(nb);
+      hipLaunchKernelGGL((k_input<N, MM, R, CONST>), dim3(unsigned(nb)), dim3(256), 0, s, x, V, a, p.fm);
+    }
     return launch_status();
   }
 
