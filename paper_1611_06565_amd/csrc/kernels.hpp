@@ -46,7 +46,7 @@ struct Blocking {
   static constexpr int BLK = ACC ? 64 : (NXI > 64 ? 16 : 32);   // tiles per V block
   static constexpr int KBLK = ACC ? 64 : BLK;                    // kernels padded to this
   static constexpr int KSTEP = (!ACC && BLK == 16) ? 4 : 2;      // channels per MFMA
-  static constexpr int VEC = ACC ? 2 : (NXI > 64 ? 1 : 2);       // floats per operand load
+  static constexpr int VEC = ACC ? 2 : (NXI > 64 ? 1 : 4);       // floats per operand load
   static constexpr int CG = ACC ? 4 : KSTEP * VEC;               // channels per V group
   static constexpr int CGU = CG;                                 // channels per U group
   // channels are padded to whole operand stages of the GEMM (16 channels;
@@ -152,7 +152,7 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
   constexpr int NROW = NXI / A;           // window rows (leading indices)
   constexpr int XCH = NXI % 16 == 0 ? 16 : 12;   // planes staged through LDS at a time
   static_assert(GPW * BLK * CG == 256, "work-group shape");
-  static_assert(CG == 4 && NXI % XCH == 0 && XCH % 4 == 0, "store rounds of 4 planes");
+  static_assert(CG % 4 == 0 && NXI % XCH == 0 && XCH % 4 == 0, "store rounds of 4 planes");
   const int tid = int(threadIdx.x);
   const int cl = tid % CG;
   const int tl = (tid / CG) % BLK;
@@ -224,13 +224,14 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
   float v[NXI];
   transform_nd<N, A, A>(d, v, MatRef<Which::BT, CONST, MM, R>{&fm});
   // V[tb][cg][xi][tl][cl]: the work-group's NXI planes of each of its channel
-  // groups are one contiguous run of NXI * 256 floats.  The values go through
-  // LDS XCH planes at a time so that each lane stores 16 bytes (one tile's 4
-  // channels) and a wave writes 1 KB contiguous per store.
+  // groups are one contiguous run.  The values go through LDS XCH planes at a
+  // time so that each lane stores 16 bytes (4 channels of a tile) and a wave
+  // writes 1 KB contiguous per store.
   __shared__ float4 stage[XCH][64];      // the work-group's 256 floats of a plane
   float* const gbase = V + (int64_t(tb) * a.C_pad + int64_t(cg - gl) * CG) * NXI * BLK;
-  const int pr = tid >> 6, f = tid & 63;  // plane within a round of 4; float4 = (group, tile)
-  const int g = f / BLK;
+  constexpr int C4 = CG / 4;              // float4s per tile row of a group
+  const int pr = tid >> 6, f = tid & 63;  // plane within a round of 4; float4 = (group, tile, quarter)
+  const int g = f / (BLK * C4), ft = (f / C4) % BLK, f4 = f % C4;
   const bool store = (cg - gl + g) * CG < a.C_pad;
 #pragma unroll
   for (int x0 = 0; x0 < NXI; x0 += XCH) {
@@ -243,8 +244,9 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
       for (int i = 0; i < XCH; i += 4) {
         // non-temporal: V streams to HBM without evicting the input windows
         // that neighbouring work-groups still read from L2
-        const float4 val = stage[i + pr][f];
-        float* p = gbase + (int64_t(g) * NXI + x0 + i + pr) * (BLK * CG) + (f % BLK) * CG;
+        // stage plane layout [group][tile][channel]: one float4 = 4 channels of a tile
+        const float4 val = reinterpret_cast<const float4*>(stage[i + pr])[((g * BLK + ft) * CG) / 4 + f4];
+        float* p = gbase + (int64_t(g) * NXI + x0 + i + pr) * (BLK * CG) + ft * CG + f4 * 4;
         __builtin_nontemporal_store(val.x, p + 0);
         __builtin_nontemporal_store(val.y, p + 1);
         __builtin_nontemporal_store(val.z, p + 2);

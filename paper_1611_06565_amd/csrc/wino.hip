@@ -86,7 +86,7 @@ struct Launch {
   static constexpr int NW = (N == 3 && A == 6) ? 12 : (N == 3 ? 8 : A);
   static constexpr int LOC = 1;
   static constexpr int VEC = Blocking<N, MM, R>::VEC;
-  static constexpr int DEPTH = (N == 3 && A == 6) ? 2 : 3;
+  static constexpr int DEPTH = (A == 6) ? 2 : 3;
   using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
 
   static wino_status filter(const wino_plan_s& p, const float* w, float* U, hipStream_t s) {
