@@ -38,7 +38,10 @@ struct AccArgs {
   int64_t ystride_k;  // prod Y_i
   int32_t T, C_pad, K, K_pad;
   int32_t nkb;        // K_pad / 64
-  int32_t nblocks;    // work-groups in the grid
+  // Work per XCD (work-group b runs on XCD b % 8 as its unit b / 8): XCD x
+  // owns blocks xb0[x] .. xb0[x] + xn[x] - 1; its last xs[x] blocks are done
+  // as two halves each (by passes), so its last round is half as long.
+  int32_t xb0[8], xn[8], xs[8];
   int32_t tiles[3], Y[3];
   int32_t relu;
 };
@@ -173,10 +176,23 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
   const int tq = wave >> 1, kq = wave & 1;        // quadrant of the 64 x 64 block
   const int col = lane & 31, kr = lane >> 5;
 
-  const int L = xcd_remap(int(blockIdx.x), g.nblocks);
-  const int tb = L / g.nkb, kb = L % g.nkb;
+  // Work unit -> (block, passes).  Each XCD runs its own contiguous range of
+  // blocks (consecutive blocks share V rows in its L2), whole blocks first,
+  // then the two halves of its last few blocks, which would otherwise run
+  // alone after the XCD's last full round of resident work-groups.  Halves
+  // add their partial outputs into zeroed y.  Surplus units exit at once.
+  const int xcd = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3;
+  const int xn = g.xn[xcd], xs = g.xs[xcd];
+  if (j >= xn + xs) return;
+  const int nwhole = xn - xs;
+  const bool split = j >= nwhole;
+  const int blk = g.xb0[xcd] + (split ? nwhole + (j - nwhole) / 2 : j);
+  const int p0 = split ? ((j - nwhole) & 1) * (G::NPASS / 2) : 0;
+  const int npass = split ? G::NPASS / 2 : G::NPASS;
+  static_assert(G::NPASS % 2 == 0, "halves of whole passes");
+  const int tb = blk / g.nkb, kb = blk % g.nkb;
   const int nstage = g.C_pad / G::SC;             // channel stages per pass
-  const int nsteps = G::NPASS * nstage;
+  const int nsteps = npass * nstage;
 
   // ---- direct-to-LDS copies of one (pass, stage) step.  Chunk c of an
   // operand is (element e, 4-channel group gi) = (c / G4, c % G4): 1 KB, either
@@ -206,7 +222,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
     }
   };
   // copy cursor: the next step to copy, as (pass, stage)
-  int cpass = 0, cst = 0;
+  int cpass = p0, cst = 0;
   auto cursor_src = [&](const float*& vs, const float*& us) {
     vs = vsrc + int64_t(cpass) * E * VX + cst * vstage;
     us = usrc + int64_t(cpass) * E * g.uplane + cst * ustage;
@@ -350,7 +366,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
   using I2 = std::integral_constant<int, 2>;
   using I3 = std::integral_constant<int, 3>;
   static_assert(NBUF == 4, "the step loop unrolls four buffers");
-  int s = 0, pass = 0, st = 0;
+  int s = 0, pass = p0, st = 0;
   auto finish = [&]() {                           // after a step: true when all are done
     ++s;
     if (++st == nstage) {
@@ -421,11 +437,53 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
           const int kg = kb * KB + kl;
           if (kg >= g.K) break;
           float v = pl[kl * TB + (tl ^ (kl & 31))];
-          if (g.relu) v = v > 0.0f ? v : 0.0f;
-          __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
+          if (split) {
+            // two partials onto zero: 0 + a + b rounds the same in either order
+            unsafeAtomicAdd(yo + int64_t(kg) * g.ystride_k, v);
+          } else {
+            if (g.relu) v = v > 0.0f ? v : 0.0f;
+            __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
+          }
         }
       }
     }
+  }
+}
+
+// Zero the outputs of the blocks done in two halves (the last xs[x] blocks of
+// each XCD's range): a block covers the 64 tiles of tile block tb and the 64
+// kernels of kernel block kb, every output of a tile (m^N) inside the output
+// extent.
+template <int N, int MM>
+__global__ void __launch_bounds__(256) k_zero_split(float* __restrict__ y, AccArgs g) {
+  constexpr int NOUT = ipow(MM, N), TB = 64, KB = 64;
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;   // (split block j, tile, output)
+  const int o = int(i % NOUT), tl = int((i / NOUT) % TB);
+  int j = int(i / (NOUT * TB)), blk = -1;
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    if (blk < 0 && j < g.xs[x]) blk = g.xb0[x] + g.xn[x] - g.xs[x] + j;
+    else if (blk < 0) j -= g.xs[x];
+  }
+  if (blk < 0) return;
+  const int tb = blk / g.nkb, kb = blk % g.nkb;
+  const int t = tb * TB + tl;
+  if (t >= g.T) return;
+  int ti[3] = {0, 0, 0};
+  const int n = split_tile<N>(t, g.tiles, ti);
+  int64_t off = 0;
+#pragma unroll
+  for (int ax = 0; ax < N; ++ax) {
+    const int oa = (o / ipow(MM, N - 1 - ax)) % MM;
+    const int yc = ti[ax] * MM + oa;
+    if (yc >= g.Y[ax]) return;
+    off = off * g.Y[ax] + yc;
+  }
+  float* yo = y + int64_t(n) * g.K * g.ystride_k + off;
+  for (int kl = 0; kl < KB; ++kl) {
+    const int kg = kb * KB + kl;
+    if (kg >= g.K) break;
+    yo[int64_t(kg) * g.ystride_k] = 0.0f;
   }
 }
 

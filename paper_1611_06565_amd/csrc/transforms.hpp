@@ -16,7 +16,12 @@
 
 namespace wino {
 
-constexpr int ipow(int b, int e) { return e == 0 ? 1 : b * ipow(b, e - 1); }
+// Iterative (not recursive) so that device code can always inline it.
+__host__ __device__ constexpr int ipow(int b, int e) {
+  int r = 1;
+  for (int i = 0; i < e; ++i) r *= b;
+  return r;
+}
 
 // Which matrix of the triple a transform reads.
 enum class Which { AT, BT, G };

@@ -30,6 +30,20 @@ struct wino_plan_s {
 
 namespace {
 
+// Compute units of the current device (cached per device).
+int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+
 constexpr int64_t kMaxI32 = 0x7fffffff;
 
 int64_t round_up(int64_t v, int64_t b) { return (v + b - 1) / b * b; }
@@ -139,11 +153,31 @@ struct Launch {
       a.T = int32_t(p.T); a.C_pad = p.C_pad; a.K = p.K; a.K_pad = p.K_pad;
       a.nkb = p.K_pad / G::KB;
       const int64_t nb = (p.T_pad / G::TB) * int64_t(a.nkb);
-      a.nblocks = int32_t(nb);
       for (int i = 0; i < 3; ++i) { a.tiles[i] = int32_t(p.tiles[i]); a.Y[i] = int32_t(p.Y[i]); }
       a.relu = (p.flags & WINO_RELU) ? 1 : 0;
-      hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST>), dim3(unsigned(nb)), dim3(G::NT), 0, s, V, U, y,
-                         a, p.fm);
+      // Work-groups go to the 8 XCDs round-robin; each XCD takes a contiguous
+      // range of blocks.  On an XCD, the blocks past its last full round of
+      // resident work-groups (two per CU) are done as two halves each, so the
+      // last round is half as long.  Not with a fused ReLU, which needs the
+      // whole sum.
+      constexpr int NX = 8;
+      const int64_t slots = 2 * int64_t(cu_count() / NX);
+      int64_t maxu = 0, nsplit = 0;
+      for (int x = 0; x < NX; ++x) {
+        const int64_t n = nb / NX + (x < nb % NX ? 1 : 0);
+        const int64_t b0 = x * (nb / NX) + (x < nb % NX ? x : nb % NX);
+        int64_t sx = 0;
+        if (!a.relu && slots > 0) sx = n < slots ? n : n % slots;
+        a.xb0[x] = int32_t(b0); a.xn[x] = int32_t(n); a.xs[x] = int32_t(sx);
+        maxu = maxu > n + sx ? maxu : n + sx;
+        nsplit += sx;
+      }
+      if (nsplit > 0) {
+        const int64_t items = nsplit * G::TB * G::NOUT;
+        hipLaunchKernelGGL((k_zero_split<N, MM>), dim3(unsigned((items + 255) / 256)), dim3(256), 0, s, y, a);
+      }
+      hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST>), dim3(unsigned(NX * maxu)), dim3(G::NT), 0, s, V, U,
+                         y, a, p.fm);
       return launch_status();
     } else {
       GemmArgs g{};
