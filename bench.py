@@ -182,7 +182,15 @@ def main():
     nxi = d["n_xi"]
     gemm_flops = 2.0 * nxi * d["T"] * spec.C * spec.K
     in_bytes = 4.0 * (spec.batch * spec.C * float(np.prod(spec.X)) + nxi * d["T"] * spec.C)
-    achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
+    # The GEMM's algorithmic bytes: V read once, U read once, y written once.
+    # Below the ridge point (peak FLOP/s over peak bytes/s) it is bound by HBM.
+    gemm_bytes = 4.0 * (nxi * d["T"] * spec.C + nxi * spec.C * spec.K
+                        + spec.batch * spec.K * float(np.prod(spec.out_spatial)))
+    hbm_bound = gemm_flops / gemm_bytes < PEAK_FP32_MFMA * 1e12 / (PEAK_HBM * 1e9)
+    if hbm_bound:
+        achieved = gemm_bytes / (gemm_ms * 1e-3) / 1e9
+    else:
+        achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
     traffic = read_traffic(kernel_hash())
 
     check = None
@@ -221,16 +229,18 @@ def main():
             "tiles": d["T"], "direct_gflop_per_step": flops / 1e9,
         },
         "roofline": {
-            "kernel": ("k_gemm_acc (batched fp32-MFMA GEMM, inverse transform accumulated per slice)"
+            "kernel": ("k_gemm_acc (batched fp32-MFMA GEMM, inverse transform accumulated per pass)"
                        if spec.m == 2 else
                        "k_gemm_inv (batched fp32-MFMA GEMM + fused inverse transform)"),
-            "bound": "mfma",
+            "bound": "hbm" if hbm_bound else "mfma",
             "achieved": achieved,
-            "peak": PEAK_FP32_MFMA,
-            "unit": "TFLOP/s",
-            "frac": achieved / PEAK_FP32_MFMA,
+            "peak": PEAK_HBM if hbm_bound else PEAK_FP32_MFMA,
+            "unit": "GB/s" if hbm_bound else "TFLOP/s",
+            "frac": achieved / (PEAK_HBM if hbm_bound else PEAK_FP32_MFMA),
             "traffic": traffic,
-            "algorithmic": "2*alpha^N*T*C*K = %.4g FLOP per launch" % gemm_flops,
+            "algorithmic": ("4*(alpha^N*T*C + alpha^N*C*K + n*K*prod(Y)) = %.4g bytes per launch" % gemm_bytes
+                            if hbm_bound else "2*alpha^N*T*C*K = %.4g FLOP per launch" % gemm_flops),
+            "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,
         },
         "stages_ms": {"filter_transform": filt_ms, "input_transform": inp_ms,
                       "gemm_inverse": gemm_ms},
