@@ -43,9 +43,10 @@ def kernel_hash():
     return h.hexdigest()[:16]
 
 
-def read_traffic(expected_hash):
+def read_traffic(expected_hash, config):
     """HBM bytes per launch of the GEMM kernel from the committed counter
-    summary, or None if absent or taken on different kernel sources."""
+    summary, or None if absent, taken on another workload or on different
+    kernel sources."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     vals = {}
@@ -54,7 +55,7 @@ def read_traffic(expected_hash):
             m = re.match(r"\s*(\w+)\s*[:=]\s*(\S+)", line)
             if m:
                 vals[m.group(1)] = m.group(2)
-    if vals.get("kernel_sources_sha256_16") != expected_hash:
+    if vals.get("kernel_sources_sha256_16") != expected_hash or vals.get("config") != str(config):
         return None
     try:
         return float(vals["traffic_bytes_per_launch"])
@@ -191,7 +192,7 @@ def main():
         achieved = gemm_bytes / (gemm_ms * 1e-3) / 1e9
     else:
         achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
-    traffic = read_traffic(kernel_hash())
+    traffic = read_traffic(kernel_hash(), args.config)
 
     check = None
     if not args.no_check:
