@@ -1,10 +1,12 @@
 // gfx950 kernels of the N-D Winograd forward.
 //
-//   k_filter     U[xi][c][k]  = (w[k][c] x_n G)[xi]            eq. (4), kernel side
-//   k_input      V[xi][c][t]  = (d_{t,c} x_n B^T)[xi]          eq. (4), data side
-//   k_gemm_inv   M_xi = V_xi . U_xi on fp32 MFMA (eq. 5), then
-//                y tile = M[:, t, k] x_n A^T, stitched and cropped (eq. 4)
-//   k_maxpool3d  pooling for the C3D stack (not part of the method)
+//   k_filter       U[xi][c][k]  = (w[k][c] x_n G)[xi]            eq. (4), kernel side
+//   k_input        V[xi][c][t]  = (d_{t,c} x_n B^T)[xi]          eq. (4), data side
+//   k_input_split  the same for alpha^N = 216, split over A threads per (t, c)
+//   k_gemm_inv     M_xi = V_xi . U_xi on fp32 MFMA (eq. 5), then
+//                  y tile = M[:, t, k] x_n A^T, stitched and cropped (eq. 4);
+//                  m = 4 (m = 2 uses k_gemm_acc in gemm_acc.hpp)
+//   k_maxpool3d    pooling for the C3D stack (not part of the method)
 //
 // Layouts (float32, zero padding rows/columns):
 //   x [batch][C][X_1..X_N]     w [K][C][r^N]      y [batch][K][Y_1..Y_N]
@@ -41,7 +43,7 @@ template <int N, int MM, int R>
 struct Blocking {
   static constexpr int A = MM + R - 1;
   static constexpr int NXI = ipow(A, N);
-  // m = 2: slice-accumulating GEMM (gemm_acc.hpp), 64-tile x 64-kernel blocks
+  // m = 2: pass-accumulating GEMM (gemm_acc.hpp), 64-tile x 64-kernel blocks
   static constexpr bool ACC = (MM == 2);
   static constexpr int BLK = ACC ? 64 : (NXI > 64 ? 16 : 32);   // tiles per V block
   static constexpr int KBLK = ACC ? 64 : BLK;                    // kernels padded to this
@@ -362,18 +364,19 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
 }
 
 // ------------------------------------------------- batched GEMM (a4 + a5)
-// Work-group = BLK tiles x BLK kernels x all alpha^N elements.  Wave w owns
-// the elements with xi_0 = w (an alpha^(N-1) slice) and keeps one BLK x BLK
-// fp32 MFMA accumulator per element for the whole channel reduction.  MFMA
-// operands stream straight from global memory (V from HBM/L2, U from L2)
+// (m = 4; m = 2 uses k_gemm_acc.)  Work-group = BLK tiles x BLK kernels x all
+// alpha^N elements.  The NW waves split the elements evenly in whole units of
+// the LOC trailing axes (alpha^LOC consecutive elements) and keep one BLK x
+// BLK fp32 MFMA accumulator per element for the whole channel reduction.
+// MFMA operands stream straight from global memory (V from HBM/L2, U from L2)
 // through a DEPTH-stage register ring, DEPTH-1 channel steps ahead.
 //
 // Epilogue (eq. 4's inverse transform, separable): each lane holds, for every
 // (tile, kernel) of its accumulator registers, all elements of its wave's
-// slice, so A^T is applied along axes 1..N-1 in registers; the m^(N-1)
-// partial results per wave go through LDS once, and the last step (A^T along
-// axis 0) is done by threads laid out so that neighbouring lanes write
-// neighbouring outputs of a row.
+// units, so A^T is applied along the LOC trailing axes in registers; the
+// partial results go through LDS, and A^T along the leading axes is done by
+// threads laid out so that neighbouring lanes write neighbouring outputs of
+// a row.
 template <int BLK> struct MfmaShape;
 template <> struct MfmaShape<32> {
   static constexpr int KSTEP = 2, NACC = 16;
