@@ -48,7 +48,7 @@ struct Blocking {
   static constexpr int BLK = ACC ? 64 : (NXI > 64 ? 16 : 32);   // tiles per V block
   static constexpr int KBLK = ACC ? 64 : BLK;                    // kernels padded to this
   static constexpr int KSTEP = (!ACC && BLK == 16) ? 4 : 2;      // channels per MFMA
-  static constexpr int VEC = ACC ? 2 : (NXI > 64 ? 1 : 4);       // floats per operand load
+  static constexpr int VEC = ACC ? 2 : 4;                        // floats per operand load
   static constexpr int CG = ACC ? 4 : KSTEP * VEC;               // channels per V group
   static constexpr int CGU = CG;                                 // channels per U group
   // channels are padded to whole operand stages of the GEMM (16 channels;
@@ -265,24 +265,27 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
 // masked as in k_input) and transforms it along the other two axes; the
 // planes meet in LDS; then thread (x0, q) forms output plane x0 =
 // sum_i0 B^T[x0][i0] * plane_i0 (axis 0 of eq. 4) and writes its A^2 values.
-// A work-group covers one tile block (BLK tiles) and one channel group: the
-// BLK * CG pairs q, with channels fastest.
+// A work-group covers 64 pairs q, channels fastest: 64 / CG tiles of one tile
+// block times a whole channel group, so each plane write is 256 contiguous
+// bytes of V.
 template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x, float* __restrict__ V, InputArgs a, FMats fm) {
   using B = Blocking<N, MM, R>;
   constexpr int A = B::A, NXI = B::NXI, BLK = B::BLK, CG = B::CG;
-  constexpr int NQ = BLK * CG;            // (tile, channel) pairs per work-group
+  constexpr int NQ = 64;                  // (tile, channel) pairs per work-group, channels fastest
+  constexpr int TPW = NQ / CG;            // tiles per work-group: a whole channel group each
+  constexpr int QG = BLK / TPW;           // work-groups per (tile block, channel group)
   constexpr int PL = NXI / A;             // values per plane
-  static_assert(N == 3 && NQ == 64 && A * 64 == 384, "one wave per plane, six planes");
+  static_assert(N == 3 && A * 64 == 384 && NQ % CG == 0 && BLK % TPW == 0, "one wave per plane, six planes");
   __shared__ float planes[A][PL][NQ];
 
   const int tid = int(threadIdx.x);
   const int q = tid % NQ;
   const int i0 = __builtin_amdgcn_readfirstlane(tid / NQ);   // plane of this wave
-  const int cl = q % CG, tl = q / CG;
   const int L = xcd_remap(int(blockIdx.x), a.nblocks);
-  const int tb = L % a.ntb;
-  const int cg = L / a.ntb;
+  const int tb = (L / QG) % a.ntb, tq = L % QG;
+  const int cg = (L / QG) / a.ntb;
+  const int cl = q % CG, tl = tq * TPW + q / CG;
   const int c = cg * CG + cl;
   const int t = tb * BLK + tl;
 
@@ -341,7 +344,8 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
 
   // output plane x0 = i0 of this wave; V[tb][cg][xi][tl][cl], xi = x0 * PL + j
   const int x0 = i0;
-  float* dst = V + (int64_t(tb) * a.C_pad + int64_t(cg) * CG) * NXI * BLK + int64_t(x0) * PL * (BLK * CG) + q;
+  float* dst = V + (int64_t(tb) * a.C_pad + int64_t(cg) * CG) * NXI * BLK + int64_t(x0) * PL * (BLK * CG) +
+               tl * CG + cl;
   auto combine = [&](auto X0) {
     constexpr int xr = decltype(X0)::value;
 #pragma unroll

@@ -100,7 +100,9 @@ struct Launch {
   static constexpr int NW = (N == 3 && A == 6) ? 12 : (N == 3 ? 8 : A);
   static constexpr int LOC = 1;
   static constexpr int VEC = Blocking<N, MM, R>::VEC;
-  static constexpr int DEPTH = (A == 6) ? 2 : 3;
+  // F(4^3): no register ring (16-byte loads of 18 elements per wave leave no
+  // room for one); the other waves of the SIMD hide the load latency
+  static constexpr int DEPTH = (N == 3 && A == 6) ? 1 : (A == 6) ? 2 : 3;
   using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
 
   static wino_status filter(const wino_plan_s& p, const float* w, float* U, hipStream_t s) {
@@ -125,10 +127,10 @@ struct Launch {
     const int64_t groups = p.C_pad / CG;
     a.ntb = int32_t(p.T_pad / BLK);
     if constexpr (Blocking<N, MM, R>::NXI > 64) {
-      // large windows: A threads per (tile, channel), one tile block and one
+      // large windows: A threads per (tile, channel), 64 / CG tiles and one
       // channel group per work-group
       constexpr int A = Blocking<N, MM, R>::A;
-      const int64_t nb = (p.T_pad / BLK) * groups;
+      const int64_t nb = (p.T_pad / BLK) * groups * (BLK * CG / 64);
       a.nblocks = int32_t(nb);
       hipLaunchKernelGGL((k_input_split<N, MM, R, CONST>), dim3(unsigned(nb)), dim3(A * 64), 0, s, x, V,
                          a, p.fm);
