@@ -277,7 +277,9 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
   constexpr int QG = BLK / TPW;           // work-groups per (tile block, channel group)
   constexpr int PL = NXI / A;             // values per plane
   static_assert(N == 3 && A * 64 == 384 && NQ % CG == 0 && BLK % TPW == 0, "one wave per plane, six planes");
-  __shared__ float planes[A][PL][NQ];
+  constexpr int HALF = PL / 2;            // the planes meet in LDS in two halves (occupancy)
+  static_assert(PL % 2 == 0, "even plane size");
+  __shared__ float planes[A][HALF][NQ];
 
   const int tid = int(threadIdx.x);
   const int q = tid % NQ;
@@ -338,32 +340,35 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
   const MatRef<Which::BT, CONST, MM, R> BT{&fm};
   float p2[PL];
   transform_nd<2, A, A>(d, p2, BT);       // axes 1 and 2 of the plane
-#pragma unroll
-  for (int j = 0; j < PL; ++j) planes[i0][j][q] = p2[j];
-  __syncthreads();
-
   // output plane x0 = i0 of this wave; V[tb][cg][xi][tl][cl], xi = x0 * PL + j
   const int x0 = i0;
   float* dst = V + (int64_t(tb) * a.C_pad + int64_t(cg) * CG) * NXI * BLK + int64_t(x0) * PL * (BLK * CG) +
                tl * CG + cl;
-  auto combine = [&](auto X0) {
+  auto combine = [&](auto X0, int h) {
     constexpr int xr = decltype(X0)::value;
 #pragma unroll
-    for (int j = 0; j < PL; ++j) {
+    for (int j = 0; j < HALF; ++j) {
       float col[A];
 #pragma unroll
       for (int i = 0; i < A; ++i) col[i] = planes[i][j][q];
-      __builtin_nontemporal_store(dot_row<A>(BT, xr, col, 1), dst + j * (BLK * CG));
+      __builtin_nontemporal_store(dot_row<A>(BT, xr, col, 1), dst + (h * HALF + j) * (BLK * CG));
     }
   };
   static_assert(A == 6, "six output planes");
-  switch (x0) {
-    case 0: combine(std::integral_constant<int, 0>{}); break;
-    case 1: combine(std::integral_constant<int, 1>{}); break;
-    case 2: combine(std::integral_constant<int, 2>{}); break;
-    case 3: combine(std::integral_constant<int, 3>{}); break;
-    case 4: combine(std::integral_constant<int, 4>{}); break;
-    default: combine(std::integral_constant<int, 5>{}); break;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (h > 0) __syncthreads();           // the first half has been read
+#pragma unroll
+    for (int j = 0; j < HALF; ++j) planes[i0][j][q] = p2[h * HALF + j];
+    __syncthreads();
+    switch (x0) {
+      case 0: combine(std::integral_constant<int, 0>{}, h); break;
+      case 1: combine(std::integral_constant<int, 1>{}, h); break;
+      case 2: combine(std::integral_constant<int, 2>{}, h); break;
+      case 3: combine(std::integral_constant<int, 3>{}, h); break;
+      case 4: combine(std::integral_constant<int, 4>{}, h); break;
+      default: combine(std::integral_constant<int, 5>{}, h); break;
+    }
   }
 }
 
