@@ -144,7 +144,8 @@ __global__ void __launch_bounds__(256) k_filter(const float* __restrict__ w, flo
 // values along the last axis) is a single wide load from a start clamped into
 // the input row, shifted and zero-masked in registers; a row whose leading
 // coordinates fall outside the input loads a clamped row and is masked to
-// zero.  No branches depend on the tile, so edge tiles cost what inner ones do.
+// zero.  A wave whose windows all lie inside the input loads the rows as they
+// are and skips the shifts and masks (a wave-uniform branch).
 template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, float* __restrict__ V,
                                                InputArgs a, FMats fm) {
@@ -166,20 +167,27 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
   const int cg = (L / a.ntb) * GPW + gl;
   const int c = cg * CG + cl;
   const int t = tb * BLK + tl;
-  float d[NXI];
-  if (t < a.T && c < a.C) {
-    int ti[3] = {0, 0, 0};
-    const int n = split_tile<N>(t, a.tiles, ti);
-    int o[3];
+  const bool live = t < a.T && c < a.C;
+  int ti[3] = {0, 0, 0};
+  const int n = split_tile<N>(live ? t : 0, a.tiles, ti);
+  int o[3];
 #pragma unroll
-    for (int ax = 0; ax < N; ++ax) o[ax] = ti[ax] * MM - a.pad[ax];
+  for (int ax = 0; ax < N; ++ax) o[ax] = ti[ax] * MM - a.pad[ax];
+  const int XL = a.X[N - 1];
+  // last axis: the window [oL, oL + A) is read as [sL, sL + A) inside the row
+  const int oL = o[N - 1];
+  const bool wide = XL >= A;              // uniform over the launch
+  const int sL = wide ? min(max(oL, 0), XL - A) : 0;
+  const int delta = oL - sL;              // window element i is loaded element i + delta
+  // a wave whose windows all lie inside the input skips the shift and masks
+  bool inner = wide && delta == 0;
+#pragma unroll
+  for (int ax = 0; ax < N - 1; ++ax) inner = inner && o[ax] >= 0 && o[ax] + A <= a.X[ax];
+  const bool plain = __all(!live || inner);
+  float d[NXI];
+  auto gather = [&](auto PLAIN) {
+    constexpr bool P = decltype(PLAIN)::value;
     const float* xc = x + (int64_t(n) * a.C + c) * a.xstride_c;
-    const int XL = a.X[N - 1];
-    // last axis: the window [oL, oL + A) is read as [sL, sL + A) inside the row
-    const int oL = o[N - 1];
-    const bool wide = XL >= A;            // uniform over the launch
-    const int sL = wide ? min(max(oL, 0), XL - A) : 0;
-    const int delta = oL - sL;            // window element i is loaded element i + delta
 #pragma unroll
     for (int row = 0; row < NROW; ++row) {
       int lead[2] = {0, 0};
@@ -199,7 +207,9 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
       }
       const float* xr = xc + off * XL;
       float* dr = d + row * A;
-      if (wide) {
+      if constexpr (P) {
+        __builtin_memcpy(dr, xr + oL, A * sizeof(float));
+      } else if (wide) {
         float ld[A];
         __builtin_memcpy(ld, xr + sL, sizeof(ld));
 #pragma unroll
@@ -219,6 +229,10 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
         }
       }
     }
+  };
+  if (live) {
+    if (plain) gather(std::true_type{});
+    else gather(std::false_type{});
   } else {
 #pragma unroll
     for (int i = 0; i < NXI; ++i) d[i] = 0.0f;
@@ -291,21 +305,26 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
   const int c = cg * CG + cl;
   const int t = tb * BLK + tl;
 
-  float d[PL];
-  if (t < a.T && c < a.C) {
-    int ti[3] = {0, 0, 0};
-    const int n = split_tile<N>(t, a.tiles, ti);
-    int o[3];
+  const bool live = t < a.T && c < a.C;
+  int ti[3] = {0, 0, 0};
+  const int n = split_tile<N>(live ? t : 0, a.tiles, ti);
+  int o[3];
 #pragma unroll
-    for (int ax = 0; ax < N; ++ax) o[ax] = ti[ax] * MM - a.pad[ax];
+  for (int ax = 0; ax < N; ++ax) o[ax] = ti[ax] * MM - a.pad[ax];
+  const int XL = a.X[N - 1];
+  const int oL = o[N - 1];
+  const bool wide = XL >= A;
+  const int sL = wide ? min(max(oL, 0), XL - A) : 0;
+  const int delta = oL - sL;
+  const int q0 = o[0] + i0;
+  const bool valid0 = (unsigned)q0 < (unsigned)a.X[0];
+  // a wave whose plane windows all lie inside the input skips the shift and masks
+  const bool inner = wide && delta == 0 && valid0 && o[1] >= 0 && o[1] + A <= a.X[1];
+  const bool plain = __all(!live || inner);
+  float d[PL];
+  auto gather = [&](auto PLAIN) {
+    constexpr bool P = decltype(PLAIN)::value;
     const float* xc = x + (int64_t(n) * a.C + c) * a.xstride_c;
-    const int XL = a.X[N - 1];
-    const int oL = o[N - 1];
-    const bool wide = XL >= A;
-    const int sL = wide ? min(max(oL, 0), XL - A) : 0;
-    const int delta = oL - sL;
-    const int q0 = o[0] + i0;
-    const bool valid0 = (unsigned)q0 < (unsigned)a.X[0];
     const int64_t off0 = min(max(q0, 0), a.X[0] - 1);
 #pragma unroll
     for (int i1 = 0; i1 < A; ++i1) {
@@ -313,7 +332,9 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
       const bool valid = valid0 && (unsigned)q1 < (unsigned)a.X[1];
       const float* xr = xc + (off0 * a.X[1] + min(max(q1, 0), a.X[1] - 1)) * XL;
       float* dr = d + i1 * A;
-      if (wide) {
+      if constexpr (P) {
+        __builtin_memcpy(dr, xr + oL, A * sizeof(float));
+      } else if (wide) {
         float ld[A];
         __builtin_memcpy(ld, xr + sL, sizeof(ld));
 #pragma unroll
@@ -333,6 +354,10 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
         }
       }
     }
+  };
+  if (live) {
+    if (plain) gather(std::true_type{});
+    else gather(std::false_type{});
   } else {
 #pragma unroll
     for (int i = 0; i < PL; ++i) d[i] = 0.0f;
