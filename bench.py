@@ -16,6 +16,7 @@ the stream the kernels run on; the roofline object reports the dominant
 kernel against the MI355X fp32 MFMA peak.
 """
 import argparse
+import glob
 import hashlib
 import json
 import os
@@ -29,7 +30,6 @@ sys.path.insert(0, ROOT)
 PEAK_FP32_MFMA = 157.3      # TFLOP/s, MI355X dense fp32 matrix
 PEAK_HBM = 8000.0           # GB/s, MI355X HBM3E
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-TRAFFIC_FILE = os.path.join(PROFILE_DIR, "k_gemm_acc_f2x3_c64k128_traffic.txt")
 KERNEL_SOURCES = ["paper_1611_06565_amd/csrc/kernels.hpp", "paper_1611_06565_amd/csrc/gemm_acc.hpp",
                   "paper_1611_06565_amd/csrc/transforms.hpp", "paper_1611_06565_amd/csrc/synth.hpp",
                   "paper_1611_06565_amd/csrc/wino.hip"]
@@ -45,22 +45,22 @@ def kernel_hash():
 
 def read_traffic(expected_hash, config):
     """HBM bytes per launch of the GEMM kernel from the committed counter
-    summary, or None if absent, taken on another workload or on different
-    kernel sources."""
-    if not os.path.exists(TRAFFIC_FILE):
-        return None
-    vals = {}
-    with open(TRAFFIC_FILE) as f:
-        for line in f:
-            m = re.match(r"\s*(\w+)\s*[:=]\s*(\S+)", line)
-            if m:
-                vals[m.group(1)] = m.group(2)
-    if vals.get("kernel_sources_sha256_16") != expected_hash or vals.get("config") != str(config):
-        return None
-    try:
-        return float(vals["traffic_bytes_per_launch"])
-    except (KeyError, ValueError):
-        return None
+    summary (profiles/*_traffic.txt) taken on this workload with these kernel
+    sources, or None if there is none."""
+    for path in sorted(glob.glob(os.path.join(PROFILE_DIR, "*_traffic.txt"))):
+        vals = {}
+        with open(path) as f:
+            for line in f:
+                m = re.match(r"\s*(\w+)\s*[:=]\s*(\S+)", line)
+                if m:
+                    vals[m.group(1)] = m.group(2)
+        if vals.get("kernel_sources_sha256_16") != expected_hash or vals.get("config") != str(config):
+            continue
+        try:
+            return float(vals["traffic_bytes_per_launch"])
+        except (KeyError, ValueError):
+            continue
+    return None
 
 
 def cpu_baseline(spec, x, w, budget_s=10.0):
