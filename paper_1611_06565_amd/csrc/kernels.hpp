@@ -36,9 +36,12 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // GEMM block (tiles and kernels per work-group), operand load width and
-// channel group per (N, m, r).  A lane loads VEC consecutive channels of a
-// group per operand; MFMA k-step j of the group uses the j-th of them, so a
-// group holds KSTEP * VEC channels.
+// channel group per (N, m, r).  For m = 4 a GEMM "stage" covers KSTEP * VEC
+// channels: lane group kr of an MFMA operand loads channels VEC*kr ..
+// VEC*kr+VEC-1 of the stage, and k-step j uses the j-th of them.  The stage
+// is one channel group (CG = KSTEP * VEC) or, for alpha^N = 216, KSTEP groups
+// of VEC channels (CG = VEC), so that one input-transform work-group (16
+// tiles x one group) writes 256 contiguous bytes per element.
 template <int N, int MM, int R>
 struct Blocking {
   static constexpr int A = MM + R - 1;
@@ -49,11 +52,12 @@ struct Blocking {
   static constexpr int KBLK = ACC ? 64 : BLK;                    // kernels padded to this
   static constexpr int KSTEP = (!ACC && BLK == 16) ? 4 : 2;      // channels per MFMA
   static constexpr int VEC = ACC ? 2 : 4;                        // floats per operand load
-  static constexpr int CG = ACC ? 4 : KSTEP * VEC;               // channels per V group
+  static constexpr int STAGE = KSTEP * VEC;                      // channels per GEMM stage (m = 4)
+  static constexpr int CG = ACC ? 4 : (NXI > 64 ? VEC : STAGE);  // channels per V group
   static constexpr int CGU = CG;                                 // channels per U group
   // channels are padded to whole operand stages of the GEMM (16 channels;
   // see AccGeom)
-  static constexpr int CPAD = ACC ? 16 : CGU;
+  static constexpr int CPAD = ACC ? 16 : STAGE;
 };
 
 // ---------------------------------------------------------------- arguments
@@ -68,6 +72,7 @@ struct InputArgs {
   int32_t T, T_pad;
   int32_t ntb, nblocks;  // tile blocks; work-groups in the grid
   int32_t X[3], tiles[3], pad[3];
+  int32_t rowfast;       // k_input_split: every tile block is 16 tiles of one row (see there)
 };
 
 struct GemmArgs {
@@ -275,66 +280,116 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
 // Input transform for large windows (alpha^N = 216, F(4^3, 3^3)): one
 // (tile, channel)'s window is too big for one thread's registers at a useful
 // occupancy, so it is split over A threads along axis 0.  Thread (i0, q)
-// loads plane i0 of the window of pair q (A rows of A values, loaded and
-// masked as in k_input) and transforms it along the other two axes; the
-// planes meet in LDS; then thread (x0, q) forms output plane x0 =
-// sum_i0 B^T[x0][i0] * plane_i0 (axis 0 of eq. 4) and writes its A^2 values.
-// A work-group covers 64 pairs q, channels fastest: 64 / CG tiles of one tile
-// block times a whole channel group, so each plane write is 256 contiguous
-// bytes of V.
+// loads plane i0 of the window of pair q (A rows of A values) and transforms
+// it along the other two axes; the planes meet in LDS; then the wave of
+// output plane x0 forms sum_i0 B^T[x0][i0] * plane_i0 (axis 0 of eq. 4) and
+// writes its A^2 values.
+//
+// A work-group covers one V block: 16 tiles x one group of 4 channels.  On
+// the loading side lanes run over the tiles fastest (lane = 16 * channel +
+// tile), so when the 16 tiles are consecutive along the last axis of one
+// input row (rowfast: the plan checks it once) every lane fetches the four
+// inputs at 4 * its tile coordinate with one aligned 16-byte load, the two
+// values on each side of its window come from the neighbouring lanes of its
+// 16-lane row (DPP row shifts), and the two row ends of the block from one
+// extra 8-byte load.  Otherwise each lane gathers its own window rows as in
+// k_input.  On the storing side lane (j, tile) writes the 4 channels of one
+// tile as 16 bytes, so a wave writes 4 runs of 256 contiguous bytes of V.
+__device__ __forceinline__ float dpp_from_prev(float old, float v) {
+  // lane i of each 16-lane row takes lane i-1's v; lane 0 keeps old
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), 0x111, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float dpp_from_next(float old, float v) {
+  // lane i of each 16-lane row takes lane i+1's v; lane 15 keeps old
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), 0x101, 0xf, 0xf, false));
+}
+
 template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x, float* __restrict__ V, InputArgs a, FMats fm) {
   using B = Blocking<N, MM, R>;
   constexpr int A = B::A, NXI = B::NXI, BLK = B::BLK, CG = B::CG;
-  constexpr int NQ = 64;                  // (tile, channel) pairs per work-group, channels fastest
-  constexpr int TPW = NQ / CG;            // tiles per work-group: a whole channel group each
-  constexpr int QG = BLK / TPW;           // work-groups per (tile block, channel group)
+  constexpr int NQ = BLK * CG;            // (tile, channel) pairs per work-group: one V block
   constexpr int PL = NXI / A;             // values per plane
-  static_assert(N == 3 && A * 64 == 384 && NQ % CG == 0 && BLK % TPW == 0, "one wave per plane, six planes");
+  static_assert(N == 3 && MM == 4 && A == 6 && BLK == 16 && CG == 4 && NQ == 64, "one wave per plane, six planes");
   constexpr int HALF = PL / 2;            // the planes meet in LDS in two halves (occupancy)
   static_assert(PL % 2 == 0, "even plane size");
-  __shared__ float planes[A][HALF][NQ];
+  __shared__ float4 planes[A][HALF][BLK];   // [plane][value][tile] -> the CG channels
 
-  const int tid = int(threadIdx.x);
-  const int q = tid % NQ;
-  const int i0 = __builtin_amdgcn_readfirstlane(tid / NQ);   // plane of this wave
+  const int lane = int(threadIdx.x) & 63;
+  const int i0 = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);   // plane of this wave
   const int L = xcd_remap(int(blockIdx.x), a.nblocks);
-  const int tb = (L / QG) % a.ntb, tq = L % QG;
-  const int cg = (L / QG) / a.ntb;
-  const int cl = q % CG, tl = tq * TPW + q / CG;
+  const int tb = L % a.ntb, cg = L / a.ntb;
+  const int tl = lane % BLK, cl = lane / BLK;
   const int c = cg * CG + cl;
   const int t = tb * BLK + tl;
-
-  const bool live = t < a.T && c < a.C;
-  int ti[3] = {0, 0, 0};
-  const int n = split_tile<N>(live ? t : 0, a.tiles, ti);
-  int o[3];
-#pragma unroll
-  for (int ax = 0; ax < N; ++ax) o[ax] = ti[ax] * MM - a.pad[ax];
   const int XL = a.X[N - 1];
-  const int oL = o[N - 1];
-  const bool wide = XL >= A;
-  const int sL = wide ? min(max(oL, 0), XL - A) : 0;
-  const int delta = oL - sL;
-  const int q0 = o[0] + i0;
-  const bool valid0 = (unsigned)q0 < (unsigned)a.X[0];
-  // a wave whose plane windows all lie inside the input skips the shift and masks
-  const bool inner = wide && delta == 0 && valid0 && o[1] >= 0 && o[1] + A <= a.X[1];
-  const bool plain = __all(!live || inner);
+  const int cc = min(c, a.C - 1);
+  const float* xc = x + int64_t(cc) * a.xstride_c;          // channel c of sample 0
   float d[PL];
-  auto gather = [&](auto PLAIN) {
-    constexpr bool P = decltype(PLAIN)::value;
-    const float* xc = x + (int64_t(n) * a.C + c) * a.xstride_c;
+
+  if (a.rowfast) {
+    // the 16 tiles share sample and leading tile coordinates; lane tl's
+    // window row starts at 4 * (tW0 + tl) - pad
+    int ti[3] = {0, 0, 0};
+    const int n = split_tile<N>(tb * BLK, a.tiles, ti);
+    const float* xn = xc + int64_t(n) * a.C * a.xstride_c;
+    const int tW = ti[2] + tl;
+    const int q0 = ti[0] * MM - a.pad[0] + i0;
+    const bool valid0 = c < a.C && (unsigned)q0 < (unsigned)a.X[0];
+    const int p = a.pad[2];
+    const int wo = min(MM * tW, XL - 4);
+    const bool own_in = MM * tW < XL;
+    // row ends: lanes 0..7 fetch the two values left of the block, 8..15 the
+    // two right of it
+    const int wl = MM * ti[2] - 2, wr = MM * ti[2] + MM * BLK;
+    const bool left = tl < BLK / 2;
+    const int wh = left ? max(wl, 0) : min(wr, XL - 2);
+    const bool h_in = left ? wl >= 0 : wr < XL;
+#pragma unroll
+    for (int i1 = 0; i1 < A; ++i1) {
+      const int q1 = ti[1] * MM - a.pad[1] + i1;
+      const bool valid = valid0 && (unsigned)q1 < (unsigned)a.X[1];
+      const float* xr = xn + (int64_t(min(max(q0, 0), a.X[0] - 1)) * a.X[1] + min(max(q1, 0), a.X[1] - 1)) * XL;
+      float4 o = *reinterpret_cast<const float4*>(xr + wo);
+      float2 h = *reinterpret_cast<const float2*>(xr + wh);
+      if (!own_in) o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      if (!h_in) h = make_float2(0.0f, 0.0f);
+      // e = offset from 4 * tW: -2, -1 from the previous lane, 0..3 own, 4, 5 from the next
+      float e[8];
+      e[0] = dpp_from_prev(h.x, o.z);
+      e[1] = dpp_from_prev(h.y, o.w);
+      e[2] = o.x; e[3] = o.y; e[4] = o.z; e[5] = o.w;
+      e[6] = dpp_from_next(h.x, o.x);
+      e[7] = dpp_from_next(h.y, o.y);
+#pragma unroll
+      for (int i = 0; i < A; ++i) {
+        // window value i sits at offset i - p
+        const float v = p == 0 ? e[i + 2] : (p == 1 ? e[i + 1] : e[i]);
+        d[i1 * A + i] = valid ? v : 0.0f;
+      }
+    }
+  } else {
+    const bool live = t < a.T && c < a.C;
+    int ti[3] = {0, 0, 0};
+    const int n = split_tile<N>(live ? t : 0, a.tiles, ti);
+    const float* xn = xc + int64_t(n) * a.C * a.xstride_c;
+    int o[3];
+#pragma unroll
+    for (int ax = 0; ax < N; ++ax) o[ax] = ti[ax] * MM - a.pad[ax];
+    const int oL = o[N - 1];
+    const bool wide = XL >= A;
+    const int sL = wide ? min(max(oL, 0), XL - A) : 0;
+    const int delta = oL - sL;
+    const int q0 = o[0] + i0;
+    const bool valid0 = live && (unsigned)q0 < (unsigned)a.X[0];
     const int64_t off0 = min(max(q0, 0), a.X[0] - 1);
 #pragma unroll
     for (int i1 = 0; i1 < A; ++i1) {
       const int q1 = o[1] + i1;
       const bool valid = valid0 && (unsigned)q1 < (unsigned)a.X[1];
-      const float* xr = xc + (off0 * a.X[1] + min(max(q1, 0), a.X[1] - 1)) * XL;
+      const float* xr = xn + (off0 * a.X[1] + min(max(q1, 0), a.X[1] - 1)) * XL;
       float* dr = d + i1 * A;
-      if constexpr (P) {
-        __builtin_memcpy(dr, xr + oL, A * sizeof(float));
-      } else if (wide) {
+      if (wide) {
         float ld[A];
         __builtin_memcpy(ld, xr + sL, sizeof(ld));
 #pragma unroll
@@ -354,37 +409,41 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
         }
       }
     }
-  };
-  if (live) {
-    if (plain) gather(std::true_type{});
-    else gather(std::false_type{});
-  } else {
-#pragma unroll
-    for (int i = 0; i < PL; ++i) d[i] = 0.0f;
   }
   const MatRef<Which::BT, CONST, MM, R> BT{&fm};
   float p2[PL];
   transform_nd<2, A, A>(d, p2, BT);       // axes 1 and 2 of the plane
-  // output plane x0 = i0 of this wave; V[tb][cg][xi][tl][cl], xi = x0 * PL + j
+
+  // output plane x0 = i0 of this wave: V[tb][cg][xi][tile][CG], xi = x0 * PL + j
   const int x0 = i0;
-  float* dst = V + (int64_t(tb) * a.C_pad + int64_t(cg) * CG) * NXI * BLK + int64_t(x0) * PL * (BLK * CG) +
-               tl * CG + cl;
+  const int sj = lane / BLK;              // storing lane: value j = sj + 4 * k of the half, tile tl
+  float* dst = V + (int64_t(tb) * a.C_pad + int64_t(cg) * CG) * NXI * BLK + int64_t(x0) * PL * NQ + tl * CG;
   auto combine = [&](auto X0, int h) {
     constexpr int xr = decltype(X0)::value;
 #pragma unroll
-    for (int j = 0; j < HALF; ++j) {
-      float col[A];
+    for (int k = 0; k < (HALF + 3) / 4; ++k) {
+      const int j = sj + 4 * k;
+      if (j < HALF) {
+        float4 col[A];
 #pragma unroll
-      for (int i = 0; i < A; ++i) col[i] = planes[i][j][q];
-      __builtin_nontemporal_store(dot_row<A>(BT, xr, col, 1), dst + (h * HALF + j) * (BLK * CG));
+        for (int i = 0; i < A; ++i) col[i] = planes[i][j][tl];
+        const float* cf = reinterpret_cast<const float*>(col);
+        f32x4 out;
+        out[0] = dot_row<A>(BT, xr, cf + 0, 4);
+        out[1] = dot_row<A>(BT, xr, cf + 1, 4);
+        out[2] = dot_row<A>(BT, xr, cf + 2, 4);
+        out[3] = dot_row<A>(BT, xr, cf + 3, 4);
+        __builtin_nontemporal_store(out, reinterpret_cast<f32x4*>(dst + (h * HALF + j) * NQ));
+      }
     }
   };
   static_assert(A == 6, "six output planes");
+  float* pl = reinterpret_cast<float*>(&planes[i0][0][tl]) + cl;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     if (h > 0) __syncthreads();           // the first half has been read
 #pragma unroll
-    for (int j = 0; j < HALF; ++j) planes[i0][j][q] = p2[h * HALF + j];
+    for (int j = 0; j < HALF; ++j) pl[j * BLK * CG] = p2[h * HALF + j];
     __syncthreads();
     switch (x0) {
       case 0: combine(std::integral_constant<int, 0>{}, h); break;
@@ -584,20 +643,24 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
   const int tb = L / g.nkb, kb = L % g.nkb;
   const int col = lane % BLK, kr = lane / BLK;
 
-  // Operand rows: V[tb][cg][xi][t][CG] and U[xi][cg][k][CG].  Lane (kr, col)
-  // owns channels VEC*kr .. VEC*kr+VEC-1 of every group; MFMA k-step j of a
-  // group uses channel VEC*kr + j, so the VEC steps of a group cover all CG
-  // channels.  One "stage" = one group = VEC k-steps.
-  constexpr int CG = S::KSTEP * VEC;
-  constexpr int CGU = Blocking<N, MM, R>::CGU;                     // U groups: CGU/CG V groups each
-  static_assert(CGU % CG == 0, "U groups hold whole V groups");
+  // Operand rows: V[tb][cg][xi][t][CG] and U[xi][cg][k][CG].  A "stage" is
+  // SC = KSTEP * VEC channels: lane (kr, col) owns channels VEC*kr ..
+  // VEC*kr+VEC-1 of every stage (channel c0 = SC*s + VEC*kr of stage s sits
+  // in group c0 / CG at offset c0 % CG); MFMA k-step j of the stage uses
+  // channel c0 + j, so the VEC steps cover all SC channels.
+  constexpr int SC = S::KSTEP * VEC;
+  constexpr int CG = Blocking<N, MM, R>::CG;
+  static_assert(Blocking<N, MM, R>::CGU == CG && Blocking<N, MM, R>::STAGE == SC, "U and V share the groups");
+  static_assert(SC % CG == 0 && CG % VEC == 0, "a stage holds whole groups; a load stays in one group");
   const int64_t vxi = int64_t(BLK) * CG;                           // V element stride (floats)
   const int64_t uxi = g.uplane;                                    // U plane stride (floats)
-  const float* vnext = V + int64_t(tb) * NXI * g.C_pad * BLK + int64_t(wave) * XPW * vxi + col * CG + VEC * kr;
-  const float* ubase = U + int64_t(wave) * XPW * uxi + int64_t(kb) * BLK * CGU + col * CGU + VEC * kr;
-  const int64_t vgstep = int64_t(NXI) * BLK * CG, ugstep = int64_t(g.K_pad) * CGU;
-  const int nstages = g.C_pad / CG;
-  int unext_g = 0;                                                 // next V group to fetch
+  const int c0 = VEC * kr;                                         // this lane's channel in a stage
+  const float* vnext = V + int64_t(tb) * NXI * g.C_pad * BLK + int64_t(c0 / CG) * NXI * BLK * CG +
+                       int64_t(wave) * XPW * vxi + col * CG + c0 % CG;
+  const float* unext = U + int64_t(wave) * XPW * uxi + (int64_t(c0 / CG) * g.K_pad + int64_t(kb) * BLK + col) * CG +
+                       c0 % CG;
+  const int64_t vgstep = int64_t(NXI) * BLK * SC, ugstep = int64_t(g.K_pad) * SC;
+  const int nstages = g.C_pad / SC;
 
   typename S::acc_t acc[XPW];
 #pragma unroll
@@ -607,14 +670,13 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
                 typename std::conditional<VEC == 2, float2, float>::type>::type;
   vec_t ra[DEPTH][XPW], rb[DEPTH][XPW];
   auto fetch = [&](vec_t* a2, vec_t* b2) {
-    const float* unext = ubase + (unext_g / (CGU / CG)) * ugstep + (unext_g % (CGU / CG)) * CG;
 #pragma unroll
     for (int x = 0; x < XPW; ++x) {
       a2[x] = *reinterpret_cast<const vec_t*>(vnext + x * vxi);
       b2[x] = *reinterpret_cast<const vec_t*>(unext + x * uxi);
     }
     vnext += vgstep;
-    ++unext_g;
+    unext += ugstep;
   };
   auto consume = [&](const vec_t* a2, const vec_t* b2) {
     const float* af = reinterpret_cast<const float*>(a2);

@@ -127,11 +127,16 @@ struct Launch {
     const int64_t groups = p.C_pad / CG;
     a.ntb = int32_t(p.T_pad / BLK);
     if constexpr (Blocking<N, MM, R>::NXI > 64) {
-      // large windows: A threads per (tile, channel), 64 / CG tiles and one
-      // channel group per work-group
+      // large windows: A threads per (tile, channel), one V block (BLK tiles
+      // x one channel group) per work-group.  Row-aligned loads when every
+      // block is BLK tiles of one input row, rows are whole 16-byte units and
+      // a window starts at most 2 values left of its tile.
       constexpr int A = Blocking<N, MM, R>::A;
-      const int64_t nb = (p.T_pad / BLK) * groups * (BLK * CG / 64);
+      static_assert(BLK * CG == 64, "one pair per lane");
+      const int64_t nb = (p.T_pad / BLK) * groups;
       a.nblocks = int32_t(nb);
+      // (x is 16-byte aligned: the entry points check it)
+      a.rowfast = (p.tiles[N - 1] % BLK == 0 && p.X[N - 1] % 4 == 0 && p.pad[N - 1] <= 2) ? 1 : 0;
       hipLaunchKernelGGL((k_input_split<N, MM, R, CONST>), dim3(unsigned(nb)), dim3(A * 64), 0, s, x, V,
                          a, p.fm);
     } else {

@@ -61,8 +61,23 @@ EDGE = [
     LayerSpec("odd_c_3d_m4", N=3, m=4, r=3, batch=1, C=5, K=17, X=(8, 6, 10), pad=1),
 ]
 
+# F(4^3) with whole rows of 16 tiles along the last axis: the input transform
+# loads each block's rows with one aligned 16-byte load per lane and takes the
+# window halo from neighbouring lanes (pads 0, 1, 2; one and two blocks per
+# row; padding channel groups)
+ROWFAST = [
+    LayerSpec("f4x3_row1_pad1", N=3, m=4, r=3, batch=2, C=9, K=20, X=(5, 6, 64), pad=1,
+              x_dist="normal", w_dist="he"),
+    LayerSpec("f4x3_row2_pad1", N=3, m=4, r=3, batch=1, C=4, K=16, X=(3, 4, 128), pad=1,
+              x_dist="uniform", w_dist="he", relu=True),
+    LayerSpec("f4x3_row1_pad0", N=3, m=4, r=3, batch=1, C=6, K=7, X=(6, 7, 64), pad=0,
+              x_dist="normal", w_dist="normal"),
+    LayerSpec("f4x3_row1_pad2", N=3, m=4, r=3, batch=1, C=17, K=5, X=(4, 5, 60), pad=2,
+              x_dist="normal", w_dist="he"),
+]
 
-@pytest.mark.parametrize("spec", SMALL + OVERLAP + EDGE, ids=lambda s: s.name)
+
+@pytest.mark.parametrize("spec", SMALL + OVERLAP + EDGE + ROWFAST, ids=lambda s: s.name)
 def test_small_layers_full_output(spec):
     x, w = draw_layer(spec, seed=11)
     y, _ = run_layer(spec, x, w, guard=1024)
