@@ -336,7 +336,6 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
     const int tW = ti[2] + tl;
     const int q0 = ti[0] * MM - a.pad[0] + i0;
     const bool valid0 = c < a.C && (unsigned)q0 < (unsigned)a.X[0];
-    const int p = a.pad[2];
     const int wo = min(MM * tW, XL - 4);
     const bool own_in = MM * tW < XL;
     // row ends: lanes 0..7 fetch the two values left of the block, 8..15 the
@@ -345,28 +344,34 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
     const bool left = tl < BLK / 2;
     const int wh = left ? max(wl, 0) : min(wr, XL - 2);
     const bool h_in = left ? wl >= 0 : wr < XL;
+    // the rows of one pad (window value i sits at offset i - P from 4 * tW)
+    auto rows = [&](auto PP) {
+      constexpr int P = decltype(PP)::value;
 #pragma unroll
-    for (int i1 = 0; i1 < A; ++i1) {
-      const int q1 = ti[1] * MM - a.pad[1] + i1;
-      const bool valid = valid0 && (unsigned)q1 < (unsigned)a.X[1];
-      const float* xr = xn + (int64_t(min(max(q0, 0), a.X[0] - 1)) * a.X[1] + min(max(q1, 0), a.X[1] - 1)) * XL;
-      float4 o = *reinterpret_cast<const float4*>(xr + wo);
-      float2 h = *reinterpret_cast<const float2*>(xr + wh);
-      if (!own_in) o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-      if (!h_in) h = make_float2(0.0f, 0.0f);
-      // e = offset from 4 * tW: -2, -1 from the previous lane, 0..3 own, 4, 5 from the next
-      float e[8];
-      e[0] = dpp_from_prev(h.x, o.z);
-      e[1] = dpp_from_prev(h.y, o.w);
-      e[2] = o.x; e[3] = o.y; e[4] = o.z; e[5] = o.w;
-      e[6] = dpp_from_next(h.x, o.x);
-      e[7] = dpp_from_next(h.y, o.y);
+      for (int i1 = 0; i1 < A; ++i1) {
+        const int q1 = ti[1] * MM - a.pad[1] + i1;
+        const bool valid = valid0 && (unsigned)q1 < (unsigned)a.X[1];
+        const float* xr = xn + (int64_t(min(max(q0, 0), a.X[0] - 1)) * a.X[1] + min(max(q1, 0), a.X[1] - 1)) * XL;
+        float4 o = *reinterpret_cast<const float4*>(xr + wo);
+        float2 h = *reinterpret_cast<const float2*>(xr + wh);
+        // the lanes of a DPP row share the channel, hence the row's validity
+        if (!(own_in && valid)) o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (!(h_in && valid)) h = make_float2(0.0f, 0.0f);
+        // e = offset from 4 * tW: -2, -1 from the previous lane, 0..3 own, 4, 5 from the next
+        float e[8];
+        e[0] = dpp_from_prev(h.x, o.z);
+        e[1] = dpp_from_prev(h.y, o.w);
+        e[2] = o.x; e[3] = o.y; e[4] = o.z; e[5] = o.w;
+        e[6] = dpp_from_next(h.x, o.x);
+        e[7] = dpp_from_next(h.y, o.y);
 #pragma unroll
-      for (int i = 0; i < A; ++i) {
-        // window value i sits at offset i - p
-        const float v = p == 0 ? e[i + 2] : (p == 1 ? e[i + 1] : e[i]);
-        d[i1 * A + i] = valid ? v : 0.0f;
+        for (int i = 0; i < A; ++i) d[i1 * A + i] = e[i + 2 - P];
       }
+    };
+    switch (a.pad[2]) {
+      case 0: rows(std::integral_constant<int, 0>{}); break;
+      case 1: rows(std::integral_constant<int, 1>{}); break;
+      default: rows(std::integral_constant<int, 2>{}); break;
     }
   } else {
     const bool live = t < a.T && c < a.C;
@@ -429,10 +434,10 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
         for (int i = 0; i < A; ++i) col[i] = planes[i][j][tl];
         const float* cf = reinterpret_cast<const float*>(col);
         f32x4 out;
-        out[0] = dot_row<A>(BT, xr, cf + 0, 4);
-        out[1] = dot_row<A>(BT, xr, cf + 1, 4);
-        out[2] = dot_row<A>(BT, xr, cf + 2, 4);
-        out[3] = dot_row<A>(BT, xr, cf + 3, 4);
+        out[0] = row_dot<A, xr>(BT, cf + 0, 4);
+        out[1] = row_dot<A, xr>(BT, cf + 1, 4);
+        out[2] = row_dot<A, xr>(BT, cf + 2, 4);
+        out[3] = row_dot<A, xr>(BT, cf + 3, 4);
         __builtin_nontemporal_store(out, reinterpret_cast<f32x4*>(dst + (h * HALF + j) * NQ));
       }
     }
