@@ -451,12 +451,12 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
 }
 
 // Zero the outputs of the blocks done in two halves (the last xs[x] blocks of
-// each XCD's range): a block covers the 64 tiles of tile block tb and the 64
+// each XCD's range): a block covers the TB tiles of tile block tb and the KB
 // kernels of kernel block kb, every output of a tile (m^N) inside the output
 // extent.
-template <int N, int MM>
+template <int N, int MM, int TB, int KB>
 __global__ void __launch_bounds__(256) k_zero_split(float* __restrict__ y, AccArgs g) {
-  constexpr int NOUT = ipow(MM, N), TB = 64, KB = 64;
+  constexpr int NOUT = ipow(MM, N);
   const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;   // (split block j, tile, output)
   const int o = int(i % NOUT), tl = int((i / NOUT) % TB);
   int j = int(i / (NOUT * TB)), blk = -1;

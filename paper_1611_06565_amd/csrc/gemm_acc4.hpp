@@ -1,0 +1,363 @@
+// Batched GEMM with the inverse transform accumulated pass by pass, for 2-D
+// output tiles of extent m = 4 (F(4^2, r^2)).
+//
+// The same scheme as k_gemm_acc (gemm_acc.hpp): a pass computes M_xi for two
+// elements (a third of a row of the last axis), reduces them by the matching
+// columns of A^T along the last axis and adds the result into the m^2 = 16
+// outputs with A^T of the leading axis (eq. 4 is linear).  With 16 outputs
+// per (tile, kernel) a wave owns 32 tiles x 16 kernels, as two 16 x 16 blocks
+// of v_mfma_f32_16x16x4f32, so its output accumulators take 128 registers; a
+// work-group of four waves covers 64 tiles x 32 kernels, twice the operand
+// reuse of keeping all alpha^2 elements resident in registers, and two
+// work-groups share a CU so that each one's barriers, copies and epilogues
+// run under the other's MFMAs.
+//
+// Operands of one (pass, channel stage) step, V rows of 64 tiles and U columns
+// of 32 kernels for 16 channels of two elements (12 KB), are copied global ->
+// LDS with 16-byte direct-to-LDS loads into four stage buffers, three steps
+// ahead.  A lane group kr (lanes 16 kr .. 16 kr + 15) of an MFMA operand reads
+// 4-channel group kr of the stage as one float4 and k-step j uses its j-th
+// channel, so the four k-steps of a step contract all 16 channels.
+//
+// Layouts: V[T_pad/64][C_pad/4][alpha^2][64][4], U[alpha^2][C_pad/4][K_pad][4].
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <type_traits>
+
+#include "gemm_acc.hpp"
+#include "kernels.hpp"
+#include "synth.hpp"
+#include "transforms.hpp"
+
+namespace wino {
+
+template <int N, int MM, int R>
+struct Acc4Geom {
+  static constexpr int A = MM + R - 1;
+  static constexpr int NXI = ipow(A, N);
+  static constexpr int E = 2;                     // elements per pass
+  static constexpr int HALVES = A / E;            // passes per row of the last axis
+  static constexpr int NROW = ipow(A, N - 1);     // rows of the last axis
+  static constexpr int NPASS = NXI / E;
+  static constexpr int NOUT = ipow(MM, N);        // outputs per (tile, kernel)
+  static constexpr int NLEAD = NOUT / MM;         // outputs of the leading axis
+  static constexpr int TB = 64, KB = 32;          // tiles and kernels per work-group
+  static constexpr int NW = 4, NT = 256;          // wave (tq, kq) owns 32 tiles x 16 kernels
+  static constexpr int NH = 2;                    // 16 x 16 MFMA blocks per wave (tile halves)
+  static constexpr int NACC = 4;                  // accumulator registers per block
+  static constexpr int NBUF = 4;                  // stage buffers in LDS
+  static constexpr int DEPTH = 3;                 // steps in flight ahead of the one multiplied
+  static constexpr int SC = 16;                   // channels per stage
+  static constexpr int G4 = SC / 4;               // 4-channel groups per stage (= MFMA lane groups)
+  static constexpr int SAV = E * G4 * TB * 4;     // floats of V per stage (1 KB chunks)
+  static constexpr int SAU = E * G4 * KB * 4;     // floats of U per stage (512 B chunks)
+  static constexpr int STAGE = SAV + SAU;         // 12 KB
+  static constexpr int NCOPY = SAV / 256 + SAU / 256;   // 1 KB copies per step
+  static constexpr int CPS = NCOPY / NW;          // copies per wave per step
+  static constexpr int PLANE = TB * KB;           // stitch plane of one output index
+  static constexpr int PPR = NBUF;                // stitch planes per round (one per buffer)
+  static_assert(N == 2 && MM == 4, "2-D, m = 4");
+  static_assert(A % E == 0, "passes of whole thirds of a row");
+  static_assert(NCOPY % NW == 0 && CPS == 3, "three copies per wave per step");
+  static_assert(PLANE <= STAGE && NOUT % PPR == 0 && PPR % MM == 0, "stitch rounds of whole output rows");
+  static_assert(DEPTH < NBUF, "a buffer is refilled only after it was multiplied");
+  static_assert(KB * 4 * 2 == 256, "a U copy moves two 512 B chunks");
+};
+
+template <int N, int MM, int R, bool CONST>
+__global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ V,
+                                                      const float* __restrict__ U,
+                                                      float* __restrict__ y, AccArgs g, FMats fm) {
+  using G = Acc4Geom<N, MM, R>;
+  using S = MfmaShape<16>;
+  constexpr int A = G::A, E = G::E, NOUT = G::NOUT, G4 = G::G4, NH = G::NH, NACC = G::NACC;
+  constexpr int TB = G::TB, KB = G::KB, NW = G::NW, NBUF = G::NBUF, DEPTH = G::DEPTH;
+  static_assert(S::KSTEP == G4 && S::NACC == NACC, "lane groups = 4-channel groups");
+
+  __shared__ __attribute__((aligned(16))) float buf0[G::STAGE];
+  __shared__ __attribute__((aligned(16))) float buf1[G::STAGE];
+  __shared__ __attribute__((aligned(16))) float buf2[G::STAGE];
+  __shared__ __attribute__((aligned(16))) float buf3[G::STAGE];
+  // copies past the last step land here, so every step issues the same copies
+  __shared__ __attribute__((aligned(16))) float dump[256];
+  auto buf = [&](auto I) -> float* {
+    constexpr int b = decltype(I)::value % NBUF;
+    if constexpr (b == 0) return buf0;
+    else if constexpr (b == 1) return buf1;
+    else if constexpr (b == 2) return buf2;
+    else return buf3;
+  };
+  auto bufi = [&](int b) -> float* { return b == 0 ? buf0 : b == 1 ? buf1 : b == 2 ? buf2 : buf3; };
+
+  const int tid = int(threadIdx.x);
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tq = wave >> 1, kq = wave & 1;        // 32-tile half and 16-kernel half of the block
+  const int row = lane & 15, kr = lane >> 4;      // MFMA operand row / column and lane group
+
+  // Work unit -> (block, passes), as in k_gemm_acc.
+  const int xcd = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3;
+  const int xn = g.xn[xcd], xs = g.xs[xcd];
+  if (j >= xn + xs) return;
+  const int nwhole = xn - xs;
+  const bool split = j >= nwhole;
+  const int blk = g.xb0[xcd] + (split ? nwhole + (j - nwhole) / 2 : j);
+  const int p0 = split ? ((j - nwhole) & 1) * (G::NPASS / 2) : 0;
+  const int npass = split ? G::NPASS / 2 : G::NPASS;
+  static_assert(G::NPASS % 2 == 0, "halves of whole passes");
+  const int tb = blk / g.nkb, kb = blk % g.nkb;
+  const int nstage = g.C_pad / G::SC;             // channel stages per pass
+  const int nsteps = npass * nstage;
+
+  // ---- direct-to-LDS copies of one (pass, stage) step.  Copy c < 8: V chunk
+  // (e, gi) = (c / G4, c % G4), V[tb][grp][xi][0:64][0:4], to c * 256.  Copy
+  // c >= 8: U chunks (e, gi) and (e, gi + 1), gi = 2 (u % 2), u = c - 8, e = u / 2:
+  // lanes 0..31 move U[xi][grp][kb*32 + lane][0:4], lanes 32..63 the same of
+  // group grp + 1, to SAV + (e * G4 + gi) * 128 (the two chunks are adjacent).
+  // Wave w does copies w, w + 4, w + 8.
+  constexpr int64_t VX = TB * 4, VG = int64_t(G::NXI) * TB * 4;    // V element / group strides
+  const float* vsrc = V + int64_t(tb) * g.vblock + lane * 4;
+  const float* usrc = U + int64_t(kb) * (KB * 4) + (lane & 31) * 4 + int64_t(lane >> 5) * g.K_pad * 4;
+  int64_t off[G::CPS];
+  int dsto[G::CPS];
+#pragma unroll
+  for (int i = 0; i < G::CPS; ++i) {
+    const int c = wave + NW * i;
+    if (c < 8) {
+      const int e = c / G4, gi = c % G4;
+      off[i] = e * VX + gi * VG;
+      dsto[i] = c * 256;
+    } else {
+      const int u = c - 8, e = u / 2, gi = 2 * (u % 2);
+      off[i] = e * g.uplane + int64_t(gi) * g.K_pad * 4;
+      dsto[i] = G::SAV + (e * G4 + gi) * 128;
+    }
+  }
+  const int64_t vstage = G4 * VG, ustage = int64_t(G4) * g.K_pad * 4;
+  // copy i of a step; a step past the last one (real == false) copies the
+  // block's first V chunk again into the dump area instead
+  auto copy_one = [&](const float* vs, const float* us, float* base, bool real, int i) {
+    const int c = wave + NW * i;                 // wave-uniform: V or U is a uniform choice
+    if (c < 8) lds_copy16<true>(real ? vs + off[i] : vsrc, real ? base + dsto[i] : dump);
+    else lds_copy16<false>(real ? us + off[i] : vsrc, real ? base + dsto[i] : dump);
+  };
+  int cpass = p0, cst = 0;
+  auto cursor_src = [&](const float*& vs, const float*& us) {
+    vs = vsrc + int64_t(cpass) * E * VX + cst * vstage;
+    us = usrc + int64_t(cpass) * E * g.uplane + cst * ustage;
+  };
+  auto advance = [&]() {
+    const bool wrap = cst + 1 == nstage;
+    cst = wrap ? 0 : cst + 1;
+    cpass += wrap ? 1 : 0;
+  };
+  auto issue = [&](float* base, bool real) {
+    const float* vs;
+    const float* us;
+    cursor_src(vs, us);
+#pragma unroll
+    for (int i = 0; i < G::CPS; ++i) copy_one(vs, us, base, real, i);
+    advance();
+  };
+
+  typename S::acc_t acc[E][NH];
+  float yacc[NOUT][NH][NACC];
+#pragma unroll
+  for (int o = 0; o < NOUT; ++o)
+#pragma unroll
+    for (int h = 0; h < NH; ++h)
+#pragma unroll
+      for (int r = 0; r < NACC; ++r) yacc[o][h][r] = 0.0f;
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+#pragma unroll
+    for (int h = 0; h < NH; ++h) acc[e][h] = typename S::acc_t{};
+
+  const MatRef<Which::AT, CONST, MM, R> AT{&fm};
+  // lane group kr reads 4-channel group kr: V tile tq*32 + h*16 + row, U kernel kq*16 + row
+  const int aoff = kr * TB * 4 + (tq * 32 + row) * 4;
+  const int boff = G::SAV + kr * KB * 4 + (kq * 16 + row) * 4;
+
+  // operands of one step in `slot`: A of element e, half h; B of element e
+  float4 a4[2][E][NH], b4[2][E];
+  constexpr int NREAD = E * (NH + 1);
+  auto read_one = [&](const float* base, int slot, int q) {
+    const int e = q / (NH + 1), w = q % (NH + 1);
+    if (w < NH) a4[slot][e][w] = *reinterpret_cast<const float4*>(base + e * G4 * TB * 4 + aoff + w * 64);
+    else b4[slot][e] = *reinterpret_cast<const float4*>(base + e * G4 * KB * 4 + boff);
+  };
+  // the 4 * E * NH MFMAs of a step from `slot`, with the reads of the next
+  // step (other slot) and the copies of a later step in a fixed order
+  constexpr int NMMA = G4 * E * NH;
+  static_assert(NMMA == 16 && NREAD <= NMMA && G::CPS <= NMMA / 4, "placement of reads and copies");
+  auto mma_step = [&](int slot, const float* nbase, const float* vs, const float* us, float* cbase, bool real) {
+#pragma unroll
+    for (int m = 0; m < NMMA; ++m) {
+      const int jk = m / (E * NH), e = (m / NH) % E, h = m % NH;
+      const float4 av4 = a4[slot][e][h], bv4 = b4[slot][e];
+      const float av = jk == 0 ? av4.x : jk == 1 ? av4.y : jk == 2 ? av4.z : av4.w;
+      const float bv = jk == 0 ? bv4.x : jk == 1 ? bv4.y : jk == 2 ? bv4.z : bv4.w;
+      acc[e][h] = S::mma(av, bv, acc[e][h]);
+      if (m < NREAD) read_one(nbase, slot ^ 1, m);
+      if (m % 4 == 3 && m / 4 < G::CPS) copy_one(vs, us, cbase, real, m / 4);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // Step s multiplies buffer s % NBUF from slot s % 2 (read during step s - 1).
+  // At its start it waits for this wave's copies of s + 1 (those of s + 2 may
+  // stay in flight: every step issues exactly CPS copies, real or dumped) and
+  // synchronises (all copies of s + 1 landed; nobody reads buffer
+  // (s - 1) % NBUF any more); its MFMAs then run with the reads of step s + 1
+  // and the copies of step s + DEPTH into buffer (s + DEPTH) % NBUF.
+  auto step = [&](auto I, int s) {
+    constexpr int b = decltype(I)::value;
+    __builtin_amdgcn_s_waitcnt(0x0f73);           // vmcnt(3): the copies of s + 2 may be in flight
+    stage_barrier();
+    const bool real = s + DEPTH < nsteps;
+    const float* vs;
+    const float* us;
+    cursor_src(vs, us);
+    advance();
+    mma_step(b & 1, buf(std::integral_constant<int, b + 1>{}), vs, us, buf(std::integral_constant<int, b + DEPTH>{}),
+             real);
+  };
+
+  // Pass epilogue, pass p = (row xi_0, third h): elements xi_1 = 2h, 2h + 1 of
+  // the row are reduced by the matching columns of A^T, then added to every
+  // output (o_0, o_1) with A^T[o_0][xi_0]; the accumulators are cleared.
+  auto epilogue = [&](int pass) {
+    const int xr = pass / G::HALVES, h3 = pass % G::HALVES;
+    float c[G::NLEAD], at[MM][E];
+#pragma unroll
+    for (int o0 = 0; o0 < G::NLEAD; ++o0) {
+      float v = AT(o0, 0);
+#pragma unroll
+      for (int q = 1; q < A; ++q) v = (xr == q) ? AT(o0, q) : v;
+      c[o0] = v;
+    }
+#pragma unroll
+    for (int ol = 0; ol < MM; ++ol)
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        float v = AT(ol, e);
+#pragma unroll
+        for (int hh = 1; hh < G::HALVES; ++hh) v = (h3 == hh) ? AT(ol, hh * E + e) : v;
+        at[ol][e] = v;
+      }
+#pragma unroll
+    for (int h = 0; h < NH; ++h)
+#pragma unroll
+      for (int r = 0; r < NACC; ++r) {
+        float rv[MM];
+#pragma unroll
+        for (int ol = 0; ol < MM; ++ol) {
+          float v = at[ol][0] * acc[0][h][r];
+#pragma unroll
+          for (int e = 1; e < E; ++e) v = __builtin_fmaf(at[ol][e], acc[e][h][r], v);
+          rv[ol] = v;
+        }
+#pragma unroll
+        for (int o = 0; o < NOUT; ++o) yacc[o][h][r] = __builtin_fmaf(c[o / MM], rv[o % MM], yacc[o][h][r]);
+      }
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+#pragma unroll
+      for (int h = 0; h < NH; ++h) acc[e][h] = typename S::acc_t{};
+  };
+
+  // ---- prologue: copies of the first DEPTH steps, then step 0's operands
+  issue(buf0, true);
+  issue(buf1, 1 < nsteps);
+  issue(buf2, 2 < nsteps);
+  static_assert(DEPTH == 3, "prologue fills three buffers");
+  __builtin_amdgcn_s_waitcnt(0x0f76);             // vmcnt(6): step 0's copies landed
+  static_assert(2 * G::CPS == 6, "prologue wait count");
+  stage_barrier();
+#pragma unroll
+  for (int q = 0; q < NREAD; ++q) read_one(buf0, 0, q);
+
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  static_assert(NBUF == 4, "the step loop unrolls four buffers");
+  int s = 0, pass = p0, st = 0;
+  auto finish = [&]() {
+    ++s;
+    if (++st == nstage) {
+      epilogue(pass);
+      st = 0;
+      ++pass;
+    }
+    return s == nsteps;
+  };
+#pragma unroll 1
+  for (;;) {
+    step(I0{}, s);
+    if (finish()) break;
+    step(I1{}, s);
+    if (finish()) break;
+    step(I2{}, s);
+    if (finish()) break;
+    step(I3{}, s);
+    if (finish()) break;
+  }
+
+  // ---- stitch: outputs through LDS, one output plane ([k][t], t XOR-swizzled
+  // by k) per buffer, a whole leading output index (MM planes of the last
+  // axis) per round; thread (ol, tl) stores its tile's output ol of the last
+  // axis for every kernel, so neighbouring lanes store neighbouring outputs.
+  __builtin_amdgcn_s_waitcnt(0x0f70);             // vmcnt(0): no copy still writes LDS
+  const int ol = tid % MM;
+  const int tl = (tid / MM) % TB;
+  static_assert(G::NT == MM * TB, "one thread per (output of the last axis, tile)");
+  const int t = tb * TB + tl;
+  int ti[3] = {0, 0, 0};
+  const int n = split_tile<N>(t < g.T ? t : 0, g.tiles, ti);
+  const int ylast = ti[N - 1] * MM + ol;
+  const bool mine = t < g.T && ylast < g.Y[N - 1];
+  float* const yn = y + int64_t(n) * g.K * g.ystride_k;
+#pragma unroll
+  for (int o0 = 0; o0 < NOUT; o0 += G::PPR) {
+    __syncthreads();                              // buffers free (last MFMA reads / previous round)
+#pragma unroll
+    for (int o = o0; o < o0 + G::PPR; ++o)
+#pragma unroll
+      for (int h = 0; h < NH; ++h)
+#pragma unroll
+        for (int r = 0; r < NACC; ++r) {
+          const int tt = tq * 32 + h * 16 + S::acc_row(lane, r), k = kq * 16 + row;
+          bufi(o - o0)[k * TB + (tt ^ (k & 31))] = yacc[o][h][r];
+        }
+    __syncthreads();
+    if (mine) {
+#pragma unroll
+      for (int orest = o0 / MM; orest < (o0 + G::PPR) / MM; ++orest) {   // leading output index
+        const int yc = ti[0] * MM + orest;
+        if (yc >= g.Y[0]) continue;
+        const int64_t off2 = int64_t(yc) * g.Y[N - 1] + ylast;
+        const float* pl = bufi(orest * MM + ol - o0);
+        float* yo = yn + off2;
+#pragma unroll 8
+        for (int kl = 0; kl < KB; ++kl) {
+          const int kg = kb * KB + kl;
+          if (kg >= g.K) break;
+          float v = pl[kl * TB + (tl ^ (kl & 31))];
+          if (split) {
+            // two partials onto zero: 0 + a + b rounds the same in either order
+            unsafeAtomicAdd(yo + int64_t(kg) * g.ystride_k, v);
+          } else {
+            if (g.relu) v = v > 0.0f ? v : 0.0f;
+            __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
+          }
+        }
+      }
+    }
+  }
+}
+
+}  // namespace wino

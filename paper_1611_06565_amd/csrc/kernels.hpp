@@ -5,7 +5,8 @@
 //   k_input_split  the same for alpha^N = 216, split over A threads per (t, c)
 //   k_gemm_inv     M_xi = V_xi . U_xi on fp32 MFMA (eq. 5), then
 //                  y tile = M[:, t, k] x_n A^T, stitched and cropped (eq. 4);
-//                  m = 4 (m = 2 uses k_gemm_acc in gemm_acc.hpp)
+//                  F(4^3) (m = 2 uses k_gemm_acc in gemm_acc.hpp, F(4^2)
+//                  k_gemm_acc4 in gemm_acc4.hpp)
 //   k_maxpool3d    pooling for the C3D stack (not part of the method)
 //
 // Layouts (float32, zero padding rows/columns):
@@ -35,29 +36,33 @@ namespace wino {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// GEMM block (tiles and kernels per work-group), operand load width and
-// channel group per (N, m, r).  For m = 4 a GEMM "stage" covers KSTEP * VEC
-// channels: lane group kr of an MFMA operand loads channels VEC*kr ..
-// VEC*kr+VEC-1 of the stage, and k-step j uses the j-th of them.  The stage
-// is one channel group (CG = KSTEP * VEC) or, for alpha^N = 216, KSTEP groups
-// of VEC channels (CG = VEC), so that one input-transform work-group (16
-// tiles x one group) writes 256 contiguous bytes per element.
+// GEMM kind, block (tiles and kernels per work-group), operand load width
+// and channel group per (N, m, r).
+//   KIND 0 (m = 2) and 1 (2-D, m = 4): pass-accumulating GEMMs (gemm_acc.hpp,
+//     gemm_acc4.hpp) on 64-tile blocks of V with channel groups of 4.
+//   KIND 2 (3-D, m = 4): k_gemm_inv, all alpha^N elements resident.  A GEMM
+//     "stage" covers KSTEP * VEC channels: lane group kr of an MFMA operand
+//     loads channels VEC*kr .. VEC*kr+VEC-1 of the stage, and k-step j uses
+//     the j-th of them; the stage is KSTEP groups of VEC channels (CG = VEC),
+//     so that one input-transform work-group (16 tiles x one group) writes
+//     256 contiguous bytes per element.
 template <int N, int MM, int R>
 struct Blocking {
   static constexpr int A = MM + R - 1;
   static constexpr int NXI = ipow(A, N);
-  // m = 2: pass-accumulating GEMM (gemm_acc.hpp), 64-tile x 64-kernel blocks
-  static constexpr bool ACC = (MM == 2);
-  static constexpr int BLK = ACC ? 64 : (NXI > 64 ? 16 : 32);   // tiles per V block
-  static constexpr int KBLK = ACC ? 64 : BLK;                    // kernels padded to this
-  static constexpr int KSTEP = (!ACC && BLK == 16) ? 4 : 2;      // channels per MFMA
-  static constexpr int VEC = ACC ? 2 : 4;                        // floats per operand load
-  static constexpr int STAGE = KSTEP * VEC;                      // channels per GEMM stage (m = 4)
-  static constexpr int CG = ACC ? 4 : (NXI > 64 ? VEC : STAGE);  // channels per V group
+  static constexpr int KIND = MM == 2 ? 0 : (N == 2 ? 1 : 2);
+  static constexpr bool ACC = KIND == 0;                         // k_gemm_acc
+  static constexpr bool PASS = KIND != 2;                        // k_gemm_acc or k_gemm_acc4
+  static constexpr int BLK = PASS ? 64 : 16;                     // tiles per V block
+  static constexpr int KBLK = KIND == 0 ? 64 : (KIND == 1 ? 32 : 16);   // kernels padded to this
+  static constexpr int KSTEP = 4;                                // channels per MFMA (k_gemm_inv)
+  static constexpr int VEC = 4;                                  // floats per operand load (k_gemm_inv)
+  static constexpr int STAGE = KSTEP * VEC;                      // channels per GEMM stage (k_gemm_inv)
+  static constexpr int CG = 4;                                   // channels per V group
   static constexpr int CGU = CG;                                 // channels per U group
-  // channels are padded to whole operand stages of the GEMM (16 channels;
-  // see AccGeom)
-  static constexpr int CPAD = ACC ? 16 : STAGE;
+  // channels are padded to whole operand stages of the GEMM (16 channels)
+  static constexpr int CPAD = 16;
+  static_assert(KIND != 2 || NXI > 64, "k_gemm_inv serves F(4^3) only");
 };
 
 // ---------------------------------------------------------------- arguments
@@ -462,7 +467,7 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
 }
 
 // ------------------------------------------------- batched GEMM (a4 + a5)
-// (m = 4; m = 2 uses k_gemm_acc.)  Work-group = BLK tiles x BLK kernels x all
+// (F(4^3); m = 2 uses k_gemm_acc, F(4^2) k_gemm_acc4.)  Work-group = BLK tiles x BLK kernels x all
 // alpha^N elements.  The NW waves split the elements evenly in whole units of
 // the LOC trailing axes (alpha^LOC consecutive elements) and keep one BLK x
 // BLK fp32 MFMA accumulator per element for the whole channel reduction.

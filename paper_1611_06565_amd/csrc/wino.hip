@@ -8,6 +8,7 @@
 #include <new>
 
 #include "gemm_acc.hpp"
+#include "gemm_acc4.hpp"
 #include "kernels.hpp"
 #include "synth.hpp"
 #include "wino.h"
@@ -21,7 +22,7 @@ struct wino_plan_s {
   int64_t X[3], Y[3], tiles[3];
   int32_t pad[3];
   int64_t T, T_pad;
-  int blk, cg, cgu;
+  int blk, kblk, cg, cgu;
   uint32_t flags;
   bool const_mats;
   double AT[kMaxAlpha][kMaxAlpha], BT[kMaxAlpha][kMaxAlpha], G[kMaxAlpha][kMaxAlpha];
@@ -91,19 +92,14 @@ struct Launch {
   static constexpr int BLK = Blocking<N, MM, R>::BLK;
   static constexpr int CG = Blocking<N, MM, R>::CG;
   static constexpr int CGU = Blocking<N, MM, R>::CGU;
-  // GEMM work-group shape: waves, register-reduced trailing axes, operand
-  // load width and register-ring depth.
-  //   F(2^3): 8 waves (2 per SIMD) x two alpha-rows, 8-byte loads, 2 groups in flight
-  //   F(4^3): 12 waves x three alpha-rows, 4-byte loads (register budget)
-  //   (VEC and the channel group CG come from Blocking and fix the U/V layout)
-  //   2-D   : one alpha-row per wave
-  static constexpr int NW = (N == 3 && A == 6) ? 12 : (N == 3 ? 8 : A);
+  // k_gemm_inv (F(4^3)) work-group shape: 12 waves x three alpha-rows,
+  // no register-reduced trailing axes beyond the last, 16-byte operand loads
+  // and no register ring (18 elements per wave leave no room for one; the
+  // other waves of the SIMD hide the load latency).
+  static constexpr int NW = 12;
   static constexpr int LOC = 1;
   static constexpr int VEC = Blocking<N, MM, R>::VEC;
-  // F(4^3): no register ring (16-byte loads of 18 elements per wave leave no
-  // room for one); the other waves of the SIMD hide the load latency
-  static constexpr int DEPTH = (N == 3 && A == 6) ? 1 : (A == 6) ? 2 : 3;
-  using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
+  static constexpr int DEPTH = 1;
 
   static wino_status filter(const wino_plan_s& p, const float* w, float* U, hipStream_t s) {
     FilterArgs a{};
@@ -148,45 +144,61 @@ struct Launch {
     return launch_status();
   }
 
+  // Per-XCD work ranges of a pass-accumulating GEMM (k_gemm_acc, k_gemm_acc4):
+  // work-groups go to the 8 XCDs round-robin; each XCD takes a contiguous
+  // range of blocks.  On an XCD, the blocks past its last full round of
+  // resident work-groups (two per CU) are done as two halves each, so the last
+  // round is half as long.  Not with a fused ReLU, which needs the whole sum.
+  // Returns the grid size; zeroes the outputs of split blocks first.
+  template <int TB, int KB>
+  static int64_t acc_setup(const wino_plan_s& p, AccArgs& a, float* y, hipStream_t s) {
+    a.vblock = int64_t(p.nxi) * p.C_pad * TB;
+    a.uplane = int64_t(p.C_pad) * p.K_pad;
+    a.ystride_k = 1;
+    for (int i = 0; i < N; ++i) a.ystride_k *= p.Y[i];
+    a.T = int32_t(p.T); a.C_pad = p.C_pad; a.K = p.K; a.K_pad = p.K_pad;
+    a.nkb = p.K_pad / KB;
+    const int64_t nb = (p.T_pad / TB) * int64_t(a.nkb);
+    for (int i = 0; i < 3; ++i) { a.tiles[i] = int32_t(p.tiles[i]); a.Y[i] = int32_t(p.Y[i]); }
+    a.relu = (p.flags & WINO_RELU) ? 1 : 0;
+    constexpr int NX = 8;
+    const int64_t slots = 2 * int64_t(cu_count() / NX);
+    int64_t maxu = 0, nsplit = 0;
+    for (int x = 0; x < NX; ++x) {
+      const int64_t n = nb / NX + (x < nb % NX ? 1 : 0);
+      const int64_t b0 = x * (nb / NX) + (x < nb % NX ? x : nb % NX);
+      int64_t sx = 0;
+      if (!a.relu && slots > 0) sx = n < slots ? n : n % slots;
+      a.xb0[x] = int32_t(b0); a.xn[x] = int32_t(n); a.xs[x] = int32_t(sx);
+      maxu = maxu > n + sx ? maxu : n + sx;
+      nsplit += sx;
+    }
+    if (nsplit > 0) {
+      const int64_t items = nsplit * TB * ipow(MM, N);
+      hipLaunchKernelGGL((k_zero_split<N, MM, TB, KB>), dim3(unsigned((items + 255) / 256)), dim3(256), 0, s, y, a);
+    }
+    return NX * maxu;
+  }
+
   static wino_status gemm(const wino_plan_s& p, const float* V, const float* U, float* y,
                           hipStream_t s) {
-    if constexpr (Blocking<N, MM, R>::ACC) {
+    constexpr int KIND = Blocking<N, MM, R>::KIND;
+    if constexpr (KIND == 0) {
       using G = AccGeom<N, MM, R>;
       AccArgs a{};
-      a.vblock = int64_t(p.nxi) * p.C_pad * G::TB;
-      a.uplane = int64_t(p.C_pad) * p.K_pad;
-      a.ystride_k = 1;
-      for (int i = 0; i < N; ++i) a.ystride_k *= p.Y[i];
-      a.T = int32_t(p.T); a.C_pad = p.C_pad; a.K = p.K; a.K_pad = p.K_pad;
-      a.nkb = p.K_pad / G::KB;
-      const int64_t nb = (p.T_pad / G::TB) * int64_t(a.nkb);
-      for (int i = 0; i < 3; ++i) { a.tiles[i] = int32_t(p.tiles[i]); a.Y[i] = int32_t(p.Y[i]); }
-      a.relu = (p.flags & WINO_RELU) ? 1 : 0;
-      // Work-groups go to the 8 XCDs round-robin; each XCD takes a contiguous
-      // range of blocks.  On an XCD, the blocks past its last full round of
-      // resident work-groups (two per CU) are done as two halves each, so the
-      // last round is half as long.  Not with a fused ReLU, which needs the
-      // whole sum.
-      constexpr int NX = 8;
-      const int64_t slots = 2 * int64_t(cu_count() / NX);
-      int64_t maxu = 0, nsplit = 0;
-      for (int x = 0; x < NX; ++x) {
-        const int64_t n = nb / NX + (x < nb % NX ? 1 : 0);
-        const int64_t b0 = x * (nb / NX) + (x < nb % NX ? x : nb % NX);
-        int64_t sx = 0;
-        if (!a.relu && slots > 0) sx = n < slots ? n : n % slots;
-        a.xb0[x] = int32_t(b0); a.xn[x] = int32_t(n); a.xs[x] = int32_t(sx);
-        maxu = maxu > n + sx ? maxu : n + sx;
-        nsplit += sx;
-      }
-      if (nsplit > 0) {
-        const int64_t items = nsplit * G::TB * G::NOUT;
-        hipLaunchKernelGGL((k_zero_split<N, MM>), dim3(unsigned((items + 255) / 256)), dim3(256), 0, s, y, a);
-      }
-      hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST>), dim3(unsigned(NX * maxu)), dim3(G::NT), 0, s, V, U,
-                         y, a, p.fm);
+      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, y, s);
+      hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST>), dim3(unsigned(grid)), dim3(G::NT), 0, s, V, U, y, a,
+                         p.fm);
+      return launch_status();
+    } else if constexpr (KIND == 1) {
+      using G = Acc4Geom<N, MM, R>;
+      AccArgs a{};
+      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, y, s);
+      hipLaunchKernelGGL((k_gemm_acc4<N, MM, R, CONST>), dim3(unsigned(grid)), dim3(G::NT), 0, s, V, U, y, a,
+                         p.fm);
       return launch_status();
     } else {
+      using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
       GemmArgs g{};
       g.uplane = int64_t(p.C_pad) * p.K_pad;
       g.ystride_k = 1;
@@ -284,6 +296,7 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   {
     int cg_, cgu_, cpad_, kblk_;
     channel_groups(N, m, r, &cg_, &cgu_, &cpad_, &kblk_);
+    p.kblk = kblk_;
     p.K_pad = int(round_up(K, kblk_));
   }
   if (p.T_pad > kMaxI32) return WINO_EINVAL;
@@ -341,7 +354,7 @@ wino_status wino_plan_describe(const wino_plan_t* p, wino_plan_desc* d) {
   for (int i = 0; i < 3; ++i) { d->X[i] = p->X[i]; d->Y[i] = p->Y[i]; d->tiles[i] = p->tiles[i]; }
   d->T = p->T; d->T_pad = p->T_pad;
   d->block_tiles = p->blk;
-  d->block_kernels = p->K_pad > 0 ? (p->blk == 64 ? 64 : p->blk) : 0;
+  d->block_kernels = p->K_pad > 0 ? p->kblk : 0;
   d->channel_group = p->cg;
   d->filter_channel_group = p->cgu;
   d->default_points = p->const_mats ? 1 : 0;
