@@ -83,8 +83,11 @@ struct AccGeom {
 // track these copies: it would otherwise make LDS reads of other buffers wait
 // for them.  Every wait for the copies is explicit (s_waitcnt vmcnt), and the
 // stage barrier, which has a memory clobber, orders them against LDS reads.
-// NT marks the load non-temporal (streamed operand rows that should not push
-// the shared transformed filter out of L2).
+// NT marks the load non-temporal.  V rows are copied that way although the
+// other kernel blocks of a tile block read them too: temporal copies make the
+// GEMM a little faster on its own but leave V in the caches (L2 and the
+// memory-side cache) in place of the input x that the next input transform
+// reads, which costs more than they gain.
 template <bool NT>
 __device__ __forceinline__ void lds_copy16(const float* src, float* dst) {
   // the low 32 bits of a generic pointer into LDS are its LDS byte address
@@ -115,6 +118,10 @@ __device__ __forceinline__ void lds_copy16(const float* src, float* dst) {
 // copies of the step, and LDS reads are finished (lgkmcnt(0)) before any wave
 // may overwrite a buffer.  The memory clobber keeps the compiler from moving
 // memory accesses across it.
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// this wave are outstanding (expcnt and lgkmcnt untouched).
+constexpr int vmcnt_imm(int n) { return 0x0f70 | (n & 15) | (((n >> 4) & 3) << 14); }
+
 __device__ __forceinline__ void stage_barrier() {
   __builtin_amdgcn_s_waitcnt(0xc07f);             // lgkmcnt(0), vmcnt and expcnt untouched
   asm volatile("s_barrier" ::: "memory");

@@ -48,8 +48,11 @@ struct Acc4Geom {
   static constexpr int NW = 4, NT = 256;          // wave (tq, kq) owns 32 tiles x 16 kernels
   static constexpr int NH = 2;                    // 16 x 16 MFMA blocks per wave (tile halves)
   static constexpr int NACC = 4;                  // accumulator registers per block
-  static constexpr int NBUF = 4;                  // stage buffers in LDS
-  static constexpr int DEPTH = 3;                 // steps in flight ahead of the one multiplied
+  static constexpr int NBUF = 6;                  // stage buffers in LDS
+  // steps copied ahead of the one multiplied: a step's buffer is refilled as
+  // soon as its operands are in registers (all reads of it precede the step's
+  // barrier), so all NBUF buffers are in flight
+  static constexpr int DEPTH = NBUF;
   static constexpr int SC = 16;                   // channels per stage
   static constexpr int G4 = SC / 4;               // 4-channel groups per stage (= MFMA lane groups)
   static constexpr int SAV = E * G4 * TB * 4;     // floats of V per stage (1 KB chunks)
@@ -58,12 +61,12 @@ struct Acc4Geom {
   static constexpr int NCOPY = SAV / 256 + SAU / 256;   // 1 KB copies per step
   static constexpr int CPS = NCOPY / NW;          // copies per wave per step
   static constexpr int PLANE = TB * KB;           // stitch plane of one output index
-  static constexpr int PPR = NBUF;                // stitch planes per round (one per buffer)
+  static constexpr int PPR = 4;                   // stitch planes per round (one per buffer)
   static_assert(N == 2 && MM == 4, "2-D, m = 4");
   static_assert(A % E == 0, "passes of whole thirds of a row");
   static_assert(NCOPY % NW == 0 && CPS == 3, "three copies per wave per step");
-  static_assert(PLANE <= STAGE && NOUT % PPR == 0 && PPR % MM == 0, "stitch rounds of whole output rows");
-  static_assert(DEPTH < NBUF, "a buffer is refilled only after it was multiplied");
+  static_assert(PLANE <= STAGE && NOUT % PPR == 0 && PPR % MM == 0 && PPR <= NBUF, "stitch rounds of whole output rows");
+  static_assert(DEPTH <= NBUF && NBUF % 2 == 0, "a buffer is refilled once its operands are read; slots alternate");
   static_assert(KB * 4 * 2 == 256, "a U copy moves two 512 B chunks");
 };
 
@@ -81,6 +84,9 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
   __shared__ __attribute__((aligned(16))) float buf1[G::STAGE];
   __shared__ __attribute__((aligned(16))) float buf2[G::STAGE];
   __shared__ __attribute__((aligned(16))) float buf3[G::STAGE];
+  __shared__ __attribute__((aligned(16))) float buf4[G::STAGE];
+  __shared__ __attribute__((aligned(16))) float buf5[G::STAGE];
+  static_assert(NBUF == 6, "six stage buffers");
   // copies past the last step land here, so every step issues the same copies
   __shared__ __attribute__((aligned(16))) float dump[256];
   auto buf = [&](auto I) -> float* {
@@ -88,9 +94,11 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
     if constexpr (b == 0) return buf0;
     else if constexpr (b == 1) return buf1;
     else if constexpr (b == 2) return buf2;
-    else return buf3;
+    else if constexpr (b == 3) return buf3;
+    else if constexpr (b == 4) return buf4;
+    else return buf5;
   };
-  auto bufi = [&](int b) -> float* { return b == 0 ? buf0 : b == 1 ? buf1 : b == 2 ? buf2 : buf3; };
+  auto bufi = [&](int b) -> float* { return b == 0 ? buf0 : b == 1 ? buf1 : b == 2 ? buf2 : buf3; };   // stitch
 
   const int tid = int(threadIdx.x);
   const int lane = tid & 63;
@@ -117,21 +125,24 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
   // c >= 8: U chunks (e, gi) and (e, gi + 1), gi = 2 (u % 2), u = c - 8, e = u / 2:
   // lanes 0..31 move U[xi][grp][kb*32 + lane][0:4], lanes 32..63 the same of
   // group grp + 1, to SAV + (e * G4 + gi) * 128 (the two chunks are adjacent).
-  // Wave w does copies w, w + 4, w + 8.
+  // Wave w does copies w, w + 4 (V) and w + 8 (U), so whether a wave's copy
+  // i is V or U is known at compile time.
   constexpr int64_t VX = TB * 4, VG = int64_t(G::NXI) * TB * 4;    // V element / group strides
   const float* vsrc = V + int64_t(tb) * g.vblock + lane * 4;
   const float* usrc = U + int64_t(kb) * (KB * 4) + (lane & 31) * 4 + int64_t(lane >> 5) * g.K_pad * 4;
   int64_t off[G::CPS];
   int dsto[G::CPS];
+  constexpr int NVC = G::SAV / 256 / NW;           // V copies per wave
+  static_assert(NW == 4 && NVC == 2 && G::CPS == NVC + 1, "copies w, w + 4 of V and w + 8 of U");
 #pragma unroll
   for (int i = 0; i < G::CPS; ++i) {
     const int c = wave + NW * i;
-    if (c < 8) {
+    if (i < NVC) {
       const int e = c / G4, gi = c % G4;
       off[i] = e * VX + gi * VG;
       dsto[i] = c * 256;
     } else {
-      const int u = c - 8, e = u / 2, gi = 2 * (u % 2);
+      const int u = c - NW * NVC, e = u / 2, gi = 2 * (u % 2);
       off[i] = e * g.uplane + int64_t(gi) * g.K_pad * 4;
       dsto[i] = G::SAV + (e * G4 + gi) * 128;
     }
@@ -139,9 +150,10 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
   const int64_t vstage = G4 * VG, ustage = int64_t(G4) * g.K_pad * 4;
   // copy i of a step; a step past the last one (real == false) copies the
   // block's first V chunk again into the dump area instead
-  auto copy_one = [&](const float* vs, const float* us, float* base, bool real, int i) {
-    const int c = wave + NW * i;                 // wave-uniform: V or U is a uniform choice
-    if (c < 8) lds_copy16<true>(real ? vs + off[i] : vsrc, real ? base + dsto[i] : dump);
+  auto copy_one = [&](auto I, const float* vs, const float* us, float* base, bool real) {
+    constexpr int i = decltype(I)::value;
+    // non-temporal V rows: see lds_copy16
+    if constexpr (i < NVC) lds_copy16<true>(real ? vs + off[i] : vsrc, real ? base + dsto[i] : dump);
     else lds_copy16<false>(real ? us + off[i] : vsrc, real ? base + dsto[i] : dump);
   };
   int cpass = p0, cst = 0;
@@ -158,8 +170,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
     const float* vs;
     const float* us;
     cursor_src(vs, us);
-#pragma unroll
-    for (int i = 0; i < G::CPS; ++i) copy_one(vs, us, base, real, i);
+    unroll<G::CPS>([&](auto I) { copy_one(I, vs, us, base, real); });
     advance();
   };
 
@@ -194,28 +205,29 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
   constexpr int NMMA = G4 * E * NH;
   static_assert(NMMA == 16 && NREAD <= NMMA && G::CPS <= NMMA / 4, "placement of reads and copies");
   auto mma_step = [&](int slot, const float* nbase, const float* vs, const float* us, float* cbase, bool real) {
-#pragma unroll
-    for (int m = 0; m < NMMA; ++m) {
-      const int jk = m / (E * NH), e = (m / NH) % E, h = m % NH;
+    unroll<NMMA>([&](auto M) {
+      constexpr int m = decltype(M)::value;
+      constexpr int jk = m / (E * NH), e = (m / NH) % E, h = m % NH;
       const float4 av4 = a4[slot][e][h], bv4 = b4[slot][e];
       const float av = jk == 0 ? av4.x : jk == 1 ? av4.y : jk == 2 ? av4.z : av4.w;
       const float bv = jk == 0 ? bv4.x : jk == 1 ? bv4.y : jk == 2 ? bv4.z : bv4.w;
       acc[e][h] = S::mma(av, bv, acc[e][h]);
-      if (m < NREAD) read_one(nbase, slot ^ 1, m);
-      if (m % 4 == 3 && m / 4 < G::CPS) copy_one(vs, us, cbase, real, m / 4);
+      if constexpr (m < NREAD) read_one(nbase, slot ^ 1, m);
+      if constexpr (m % 4 == 3 && m / 4 < G::CPS) copy_one(std::integral_constant<int, m / 4>{}, vs, us, cbase, real);
       __builtin_amdgcn_sched_barrier(0);
-    }
+    });
   };
 
   // Step s multiplies buffer s % NBUF from slot s % 2 (read during step s - 1).
-  // At its start it waits for this wave's copies of s + 1 (those of s + 2 may
-  // stay in flight: every step issues exactly CPS copies, real or dumped) and
-  // synchronises (all copies of s + 1 landed; nobody reads buffer
-  // (s - 1) % NBUF any more); its MFMAs then run with the reads of step s + 1
-  // and the copies of step s + DEPTH into buffer (s + DEPTH) % NBUF.
+  // At its start it waits for this wave's copies of s + 1 (those of s + 2 ..
+  // s + DEPTH - 1 may stay in flight: every step issues exactly CPS copies,
+  // real or dumped) and synchronises: all copies of s + 1 landed, and every
+  // wave has finished reading buffer s % NBUF into registers.  Its MFMAs then
+  // run with the reads of step s + 1 and the copies of step s + DEPTH into
+  // buffer (s + DEPTH) % NBUF = s % NBUF.
   auto step = [&](auto I, int s) {
     constexpr int b = decltype(I)::value;
-    __builtin_amdgcn_s_waitcnt(0x0f73);           // vmcnt(3): the copies of s + 2 may be in flight
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm((DEPTH - 2) * G::CPS));
     stage_barrier();
     const bool real = s + DEPTH < nsteps;
     const float* vs;
@@ -270,21 +282,12 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
   };
 
   // ---- prologue: copies of the first DEPTH steps, then step 0's operands
-  issue(buf0, true);
-  issue(buf1, 1 < nsteps);
-  issue(buf2, 2 < nsteps);
-  static_assert(DEPTH == 3, "prologue fills three buffers");
-  __builtin_amdgcn_s_waitcnt(0x0f76);             // vmcnt(6): step 0's copies landed
-  static_assert(2 * G::CPS == 6, "prologue wait count");
+  unroll<DEPTH>([&](auto I) { issue(buf(I), decltype(I)::value < nsteps); });
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm((DEPTH - 1) * G::CPS));   // step 0's copies landed
   stage_barrier();
 #pragma unroll
   for (int q = 0; q < NREAD; ++q) read_one(buf0, 0, q);
 
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I3 = std::integral_constant<int, 3>;
-  static_assert(NBUF == 4, "the step loop unrolls four buffers");
   int s = 0, pass = p0, st = 0;
   auto finish = [&]() {
     ++s;
@@ -295,16 +298,16 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
     }
     return s == nsteps;
   };
+  // NBUF steps per trip so that every buffer is named at compile time
+  bool done = false;
 #pragma unroll 1
-  for (;;) {
-    step(I0{}, s);
-    if (finish()) break;
-    step(I1{}, s);
-    if (finish()) break;
-    step(I2{}, s);
-    if (finish()) break;
-    step(I3{}, s);
-    if (finish()) break;
+  while (!done) {
+    unroll<NBUF>([&](auto I) {
+      if (!done) {
+        step(I, s);
+        done = finish();
+      }
+    });
   }
 
   // ---- stitch: outputs through LDS, one output plane ([k][t], t XOR-swizzled
