@@ -34,6 +34,10 @@ SMALL = [
               x_dist="normal", w_dist="he", relu=True),
     LayerSpec("f4x3_3d_relu", N=3, m=4, r=3, batch=2, C=8, K=16, X=(7, 9, 6), pad=1,
               x_dist="normal", w_dist="he", relu=True),
+    # F(4^2) with a fused ReLU: whole blocks only (no split tail), several
+    # channel stages and kernel blocks
+    LayerSpec("f4x2_2d_relu", N=2, m=4, r=3, batch=3, C=40, K=75, X=(22, 29), pad=1,
+              x_dist="normal", w_dist="he", relu=True),
 ]
 
 # C_pad a multiple of 64: the m = 2 GEMM overlaps each pass's epilogue with
