@@ -158,6 +158,16 @@ wino_status wino_gemm_inverse(const wino_plan_t* plan, const void* workspace, si
 wino_status wino_forward(const wino_plan_t* plan, const float* x, const float* U, float* y,
                          void* workspace, size_t workspace_bytes, void* stream);
 
+/* wino_gemm_inverse and wino_forward with the per-kernel bias b of eq. (2)
+ * (§3.1): y[n][k][...] = sum + bias[k], then the optional ReLU.
+ *   bias  device, [K] float32, 4-byte aligned, read only; NULL = no bias
+ *         (then identical to the calls above).
+ * Errors as for the calls above; a misaligned bias is WINO_EINVAL. */
+wino_status wino_gemm_inverse_ex(const wino_plan_t* plan, const void* workspace, size_t workspace_bytes,
+                                 const float* U, const float* bias, float* y, void* stream);
+wino_status wino_forward_ex(const wino_plan_t* plan, const float* x, const float* U, const float* bias,
+                            float* y, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Max-pool with window = stride and floor rounding over the trailing 3 axes
  * of x [lead][X_1][X_2][X_3] -> y [lead][X_1/p_1][X_2/p_2][X_3/p_3]
  * (the C3D stack's pooling layers; not part of the Winograd method).

@@ -9,7 +9,8 @@ valid extent Y = X + 2 pad - r + 1 (§2.2 gives S = D - G + 1 unpadded), with
 x zero-extended outside [0, X).
 
 Each function returns (y, den) where den = sum |w| |x| over the same
-receptive field, the denominator of the normalised error metric.  All
+receptive field (plus |b_k| with a bias), the denominator of the normalised
+error metric.  All
 arithmetic is fp64 on the exact float32 input values.
 
 Pins (tests/test_oracle_direct.py): the naive loop nest, the per-offset BLAS
@@ -46,7 +47,7 @@ def direct_naive(x, w, pad=0, relu=False, bias=None):
         for k in range(K):
             for o in itertools.product(*[range(v) for v in Y]):
                 acc = 0.0 if bias is None else float(bias[k])
-                mag = 0.0
+                mag = 0.0 if bias is None else abs(float(bias[k]))
                 for c in range(C):
                     for p in itertools.product(range(r), repeat=N):
                         src = tuple(oi + pi - pad for oi, pi in zip(o, p))
@@ -88,16 +89,19 @@ def direct_blas(x, w, pad=0, relu=False, bias=None, with_den=True):
         if with_den:
             den += np.tensordot(aw[(slice(None), slice(None)) + p], axp[sl], axes=([1], [1]))
     y = np.moveaxis(y, 0, 1)
-    if bias is not None:
-        y = y + np.asarray(bias, dtype=np.float64).reshape((1, K) + (1,) * N)
-    if relu:
-        y = np.maximum(y, 0.0)
     if with_den:
         den = np.moveaxis(den, 0, 1)
+    if bias is not None:
+        b = np.asarray(bias, dtype=np.float64).reshape((1, K) + (1,) * N)
+        y = y + b
+        if with_den:
+            den = den + np.abs(b)
+    if relu:
+        y = np.maximum(y, 0.0)
     return y, den
 
 
-def direct_sampled(x, w, pad, coords, relu=False, chunk=2048):
+def direct_sampled(x, w, pad, coords, relu=False, chunk=2048, bias=None):
     """O3: outputs at selected positions only, one receptive field at a time.
 
     coords: int array [S][2+N] of (n, k, o_1..o_N).  Returns (y [S], den [S])."""
@@ -120,6 +124,10 @@ def direct_sampled(x, w, pad, coords, relu=False, chunk=2048):
         wv = w.reshape(w.shape[0], w.shape[1], -1)[cc[:, 1]].astype(np.float64)     # [S][C][P]
         yv = np.einsum("scp,scp->s", xv, wv)
         dv = np.einsum("scp,scp->s", np.abs(xv), np.abs(wv))
+        if bias is not None:
+            bv = np.asarray(bias, dtype=np.float64)[cc[:, 1]]
+            yv = yv + bv
+            dv = dv + np.abs(bv)
         ys.append(np.maximum(yv, 0.0) if relu else yv)
         dens.append(dv)
     return np.concatenate(ys), np.concatenate(dens)

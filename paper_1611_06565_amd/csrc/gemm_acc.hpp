@@ -44,6 +44,8 @@ struct AccArgs {
   int32_t xb0[8], xn[8], xs[8];
   int32_t tiles[3], Y[3];
   int32_t relu;
+  const float* bias;  // [K] or null: b_k of eq. (2), added before the ReLU (by the
+                      // first half of a split block only, so it is added once)
 };
 
 template <int N, int MM, int R>
@@ -445,9 +447,12 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
           if (kg >= g.K) break;
           float v = pl[kl * TB + (tl ^ (kl & 31))];
           if (split) {
-            // two partials onto zero: 0 + a + b rounds the same in either order
+            // two partials onto zero: 0 + a + b rounds the same in either
+            // order; the bias joins the first half's partial
+            if (g.bias != nullptr && p0 == 0) v += g.bias[kg];
             unsafeAtomicAdd(yo + int64_t(kg) * g.ystride_k, v);
           } else {
+            if (g.bias != nullptr) v += g.bias[kg];
             if (g.relu) v = v > 0.0f ? v : 0.0f;
             __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
           }

@@ -351,9 +351,12 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
           if (kg >= g.K) break;
           float v = pl[kl * TB + (tl ^ (kl & 31))];
           if (split) {
-            // two partials onto zero: 0 + a + b rounds the same in either order
+            // two partials onto zero: 0 + a + b rounds the same in either
+            // order; the bias joins the first half's partial
+            if (g.bias != nullptr && p0 == 0) v += g.bias[kg];
             unsafeAtomicAdd(yo + int64_t(kg) * g.ystride_k, v);
           } else {
+            if (g.bias != nullptr) v += g.bias[kg];
             if (g.relu) v = v > 0.0f ? v : 0.0f;
             __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
           }

@@ -88,6 +88,7 @@ struct GemmArgs {
   int32_t nblocks;    // work-groups in the grid
   int32_t tiles[3], Y[3];
   int32_t relu;
+  const float* bias;  // [K] or null: b_k of eq. (2), added before the ReLU
 };
 
 // Tile t (linear over batch and the tile grid, last axis fastest) -> sample
@@ -529,6 +530,7 @@ struct EpiArgs {
   int64_t ystride_k;  // prod Y_i
   int32_t Y[3];
   int32_t relu;
+  const float* bias;  // [K] or null
 };
 
 // Inverse transform of a work-group's accumulators (eq. 4), stitched into y.
@@ -608,6 +610,7 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
     float out[OLEAD];
     transform_nd<LEAD, A, MM>(v, out, AT);
     float* yk = g.y + (int64_t(n) * g.K + kg) * g.ystride_k;
+    const float bk = g.bias != nullptr ? g.bias[kg] : 0.0f;
 #pragma unroll
     for (int q = 0; q < OLEAD; ++q) {
       int rem = q;
@@ -624,6 +627,7 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
 #pragma unroll
       for (int ax = 1; ax < N; ++ax) off = off * g.Y[ax] + yc[ax];
       float val = out[q];
+      if (g.bias != nullptr) val += bk;
       if (g.relu) val = val > 0.0f ? val : 0.0f;
       yk[off] = val;
     }
@@ -721,7 +725,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
     }
   }
 
-  EpiArgs e{y, g.K, g.ystride_k, {g.Y[0], g.Y[1], g.Y[2]}, g.relu};
+  EpiArgs e{y, g.K, g.ystride_k, {g.Y[0], g.Y[1], g.Y[2]}, g.relu, g.bias};
   auto tile_of = [&](int tl, int* ti) -> int {
     const int t = tb * BLK + tl;
     if (t >= g.T) return -1;

@@ -151,7 +151,7 @@ struct Launch {
   // round is half as long.  Not with a fused ReLU, which needs the whole sum.
   // Returns the grid size; zeroes the outputs of split blocks first.
   template <int TB, int KB>
-  static int64_t acc_setup(const wino_plan_s& p, AccArgs& a, float* y, hipStream_t s) {
+  static int64_t acc_setup(const wino_plan_s& p, AccArgs& a, const float* bias, float* y, hipStream_t s) {
     a.vblock = int64_t(p.nxi) * p.C_pad * TB;
     a.uplane = int64_t(p.C_pad) * p.K_pad;
     a.ystride_k = 1;
@@ -161,6 +161,7 @@ struct Launch {
     const int64_t nb = (p.T_pad / TB) * int64_t(a.nkb);
     for (int i = 0; i < 3; ++i) { a.tiles[i] = int32_t(p.tiles[i]); a.Y[i] = int32_t(p.Y[i]); }
     a.relu = (p.flags & WINO_RELU) ? 1 : 0;
+    a.bias = bias;
     constexpr int NX = 8;
     const int64_t slots = 2 * int64_t(cu_count() / NX);
     int64_t maxu = 0, nsplit = 0;
@@ -180,20 +181,20 @@ struct Launch {
     return NX * maxu;
   }
 
-  static wino_status gemm(const wino_plan_s& p, const float* V, const float* U, float* y,
+  static wino_status gemm(const wino_plan_s& p, const float* V, const float* U, const float* bias, float* y,
                           hipStream_t s) {
     constexpr int KIND = Blocking<N, MM, R>::KIND;
     if constexpr (KIND == 0) {
       using G = AccGeom<N, MM, R>;
       AccArgs a{};
-      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, y, s);
+      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, bias, y, s);
       hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST>), dim3(unsigned(grid)), dim3(G::NT), 0, s, V, U, y, a,
                          p.fm);
       return launch_status();
     } else if constexpr (KIND == 1) {
       using G = Acc4Geom<N, MM, R>;
       AccArgs a{};
-      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, y, s);
+      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, bias, y, s);
       hipLaunchKernelGGL((k_gemm_acc4<N, MM, R, CONST>), dim3(unsigned(grid)), dim3(G::NT), 0, s, V, U, y, a,
                          p.fm);
       return launch_status();
@@ -210,6 +211,7 @@ struct Launch {
       g.nblocks = int32_t(nb);
       for (int i = 0; i < 3; ++i) { g.tiles[i] = int32_t(p.tiles[i]); g.Y[i] = int32_t(p.Y[i]); }
       g.relu = (p.flags & WINO_RELU) ? 1 : 0;
+      g.bias = bias;
       hipLaunchKernelGGL((k_gemm_inv<N, MM, R, CONST, BLK, NW, LOC, VEC, DEPTH>), dim3(unsigned(nb)),
                          dim3(Geo::NT), 0, s, V, U, y, g, p.fm);
       return launch_status();
@@ -405,26 +407,38 @@ wino_status wino_transform_input(const wino_plan_t* p, const float* x, void* ws,
   return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::input(*p, x, V, s); });
 }
 
-wino_status wino_gemm_inverse(const wino_plan_t* p, const void* ws, size_t ws_bytes, const float* U,
-                              float* y, void* stream) {
+wino_status wino_gemm_inverse_ex(const wino_plan_t* p, const void* ws, size_t ws_bytes, const float* U,
+                                 const float* bias, float* y, void* stream) {
   if (p == nullptr || ws == nullptr || U == nullptr || y == nullptr) return WINO_EINVAL;
   if (!aligned16(ws) || !aligned16(U) || !aligned16(y)) return WINO_EINVAL;
+  if (bias != nullptr && (reinterpret_cast<uintptr_t>(bias) & 3u) != 0) return WINO_EINVAL;
   if (ws_bytes < wino_workspace_bytes(p)) return WINO_EWORKSPACE;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const float* V = static_cast<const float*>(ws);
-  return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::gemm(*p, V, U, y, s); });
+  return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::gemm(*p, V, U, bias, y, s); });
 }
 
-wino_status wino_forward(const wino_plan_t* p, const float* x, const float* U, float* y, void* ws,
-                         size_t ws_bytes, void* stream) {
+wino_status wino_gemm_inverse(const wino_plan_t* p, const void* ws, size_t ws_bytes, const float* U,
+                              float* y, void* stream) {
+  return wino_gemm_inverse_ex(p, ws, ws_bytes, U, nullptr, y, stream);
+}
+
+wino_status wino_forward_ex(const wino_plan_t* p, const float* x, const float* U, const float* bias,
+                            float* y, void* ws, size_t ws_bytes, void* stream) {
   if (p == nullptr || x == nullptr || U == nullptr || y == nullptr) return WINO_EINVAL;
   if (!aligned16(x) || !aligned16(U) || !aligned16(y)) return WINO_EINVAL;
+  if (bias != nullptr && (reinterpret_cast<uintptr_t>(bias) & 3u) != 0) return WINO_EINVAL;
   if (ws == nullptr) return WINO_EINVAL;
   if (!aligned16(ws)) return WINO_EINVAL;
   if (ws_bytes < wino_workspace_bytes(p)) return WINO_EWORKSPACE;
   wino_status st = wino_transform_input(p, x, ws, ws_bytes, stream);
   if (st != WINO_OK) return st;
-  return wino_gemm_inverse(p, ws, ws_bytes, U, y, stream);
+  return wino_gemm_inverse_ex(p, ws, ws_bytes, U, bias, y, stream);
+}
+
+wino_status wino_forward(const wino_plan_t* p, const float* x, const float* U, float* y, void* ws,
+                         size_t ws_bytes, void* stream) {
+  return wino_forward_ex(p, x, U, nullptr, y, ws, ws_bytes, stream);
 }
 
 wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const float* x, float* y,

@@ -78,6 +78,8 @@ def lib():
         "wino_transform_input": (i32, [vp, vp, vp, sz, vp]),
         "wino_gemm_inverse": (i32, [vp, vp, sz, vp, vp, vp]),
         "wino_forward": (i32, [vp, vp, vp, vp, vp, sz, vp]),
+        "wino_gemm_inverse_ex": (i32, [vp, vp, sz, vp, vp, vp, vp]),
+        "wino_forward_ex": (i32, [vp, vp, vp, vp, vp, vp, sz, vp]),
         "wino_maxpool3d": (i32, [P_i64, ctypes.POINTER(i32), vp, vp, vp]),
         "wino_status_string": (ctypes.c_char_p, [i32]),
     }
@@ -249,19 +251,28 @@ class Plan:
                                             _stream()), "wino_transform_input")
         return ws
 
-    def gemm_inverse(self, ws, U, y=None):
+    def _bias_ptr(self, bias):
+        import torch
+        if bias is None:
+            return ctypes.c_void_p()
+        self._check_shape(bias, (self.K,), "bias")
+        return _dev_ptr(bias, "bias", torch.float32)
+
+    def gemm_inverse(self, ws, U, y=None, bias=None):
+        """bias: optional device [K] float32, b of eq. (2), added before the ReLU."""
         import torch
         if y is None:
             y = self.new_output()
         self._check_shape(y, self.output_shape, "y")
-        _check(self._L.wino_gemm_inverse(self._h, _dev_ptr(ws, "workspace"),
-                                         ws.numel() * ws.element_size(),
-                                         _dev_ptr(U, "U", torch.float32),
-                                         _dev_ptr(y, "y", torch.float32), _stream()),
-               "wino_gemm_inverse")
+        _check(self._L.wino_gemm_inverse_ex(self._h, _dev_ptr(ws, "workspace"),
+                                            ws.numel() * ws.element_size(),
+                                            _dev_ptr(U, "U", torch.float32), self._bias_ptr(bias),
+                                            _dev_ptr(y, "y", torch.float32), _stream()),
+               "wino_gemm_inverse_ex")
         return y
 
-    def forward(self, x, U, y=None, workspace=None):
+    def forward(self, x, U, y=None, workspace=None, bias=None):
+        """bias: optional device [K] float32, b of eq. (2), added before the ReLU."""
         import torch
         self._check_shape(x, self.input_shape, "x")
         if y is None:
@@ -272,10 +283,10 @@ class Plan:
             workspace = torch.empty(need // 4, dtype=torch.float32, device="cuda")
         ws_ptr = _dev_ptr(workspace, "workspace") if workspace is not None else ctypes.c_void_p()
         ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
-        _check(self._L.wino_forward(self._h, _dev_ptr(x, "x", torch.float32),
-                                    _dev_ptr(U, "U", torch.float32), _dev_ptr(y, "y", torch.float32),
-                                    ws_ptr, ws_len, _stream()),
-               "wino_forward")
+        _check(self._L.wino_forward_ex(self._h, _dev_ptr(x, "x", torch.float32),
+                                       _dev_ptr(U, "U", torch.float32), self._bias_ptr(bias),
+                                       _dev_ptr(y, "y", torch.float32), ws_ptr, ws_len, _stream()),
+               "wino_forward_ex")
         return y
 
 

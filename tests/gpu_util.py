@@ -23,7 +23,7 @@ def require_gpu():
     return torch
 
 
-def run_layer(spec, x, w, points=None, guard=0):
+def run_layer(spec, x, w, points=None, guard=0, bias=None):
     """Plan, transform the filter and run the forward.  Returns (y numpy, plan).
 
     With guard > 0 the output is a view inside a larger buffer whose guard
@@ -44,7 +44,8 @@ def run_layer(spec, x, w, points=None, guard=0):
         y = buf[guard:guard + n_out].view(plan.output_shape)
     else:
         y = plan.new_output()
-    plan.forward(xd, U, y=y, workspace=ws)
+    bd = torch.from_numpy(np.ascontiguousarray(bias)).cuda() if bias is not None else None
+    plan.forward(xd, U, y=y, workspace=ws, bias=bd)
     torch.cuda.synchronize()
     if guard:
         b = buf.cpu().numpy()
@@ -52,8 +53,8 @@ def run_layer(spec, x, w, points=None, guard=0):
     return y.cpu().numpy(), plan
 
 
-def check_full(spec, y, x, w):
-    y_ref, den = direct_blas(x, w, spec.pad, relu=spec.relu)
+def check_full(spec, y, x, w, bias=None):
+    y_ref, den = direct_blas(x, w, spec.pad, relu=spec.relu, bias=bias)
     err = normalised_error(y, y_ref, den)
     log(f"  max err {err['max']:.3e} p99.99 {err['p9999']:.3e} at {err['argmax']} "
         f"clamped {err['clamped']}")
@@ -78,10 +79,10 @@ def sample_coords(shape, n, rng, edges=True):
     return out
 
 
-def check_sampled(spec, y, x, w, n=4000, seed=0):
+def check_sampled(spec, y, x, w, n=4000, seed=0, bias=None):
     rng = np.random.default_rng(seed)
     coords = sample_coords(y.shape, n, rng)
-    ys, dens = direct_sampled(x, w, spec.pad, coords, relu=spec.relu)
+    ys, dens = direct_sampled(x, w, spec.pad, coords, relu=spec.relu, bias=bias)
     got = y[tuple(coords.T)]
     err = normalised_error(got, ys, dens)
     log(f"  sampled {len(coords)}: max err {err['max']:.3e} p99.99 {err['p9999']:.3e}")

@@ -136,6 +136,13 @@ def test_device_calls_reject_bad_arguments(L):
     assert L.wino_forward(f.handle, None, vp(8192), vp(16384), vp(32768), 1 << 30, None) == -1
     assert L.wino_forward(f.handle, vp(4096 + 4), vp(8192), vp(16384), vp(32768), 1 << 30, None) == -1
     assert L.wino_forward(f.handle, vp(4096), vp(8192), vp(16384 + 8), vp(32768), 1 << 30, None) == -1
+    # the bias variants: a misaligned bias, then the checks of the plain calls
+    assert L.wino_forward_ex(f.handle, vp(4096), vp(8192), vp(512 + 2), vp(16384), vp(32768), 1 << 30,
+                             None) == -1
+    assert L.wino_gemm_inverse_ex(f.handle, vp(4096), 1 << 30, vp(8192), vp(512 + 1), vp(16384), None) == -1
+    assert L.wino_forward_ex(f.handle, vp(4096), vp(8192), vp(512), vp(16384), vp(32768), 0, None) == -3
+    assert L.wino_gemm_inverse_ex(p.handle, vp(4096), need - 4, vp(8192), None, vp(16384), None) == -3
+    assert L.wino_forward_ex(f.handle, None, vp(8192), None, vp(16384), vp(32768), 1 << 30, None) == -1
     dims = (ctypes.c_int64 * 4)(1, 4, 4, 4)
     win = (ctypes.c_int32 * 3)(2, 2, 8)
     assert L.wino_maxpool3d(dims, win, vp(4096), vp(8192), None) == -1   # 4 // 8 == 0

@@ -89,6 +89,28 @@ def test_small_layers_full_output(spec):
     check_full(spec, y, x, w)
 
 
+# eq. (2)'s bias: every GEMM kernel, split-tail blocks (small layers split every
+# block into halves; the bias joins one half) and whole blocks (ReLU layers)
+BIAS = [SMALL[1], SMALL[5], SMALL[2], SMALL[7], SMALL[3], SMALL[6]]
+
+
+@pytest.mark.parametrize("spec", BIAS, ids=lambda s: s.name)
+def test_bias(spec):
+    x, w = draw_layer(spec, seed=13)
+    b = (np.random.default_rng(4).standard_normal(spec.K) * 0.5).astype(np.float32)
+    y, _ = run_layer(spec, x, w, bias=b, guard=256)
+    check_full(spec, y, x, w, bias=b)
+
+
+def test_bias_determinism_bitwise():
+    spec = SMALL[1]
+    x, w = draw_layer(spec, seed=2)
+    b = np.linspace(-1, 1, spec.K).astype(np.float32)
+    y1, _ = run_layer(spec, x, w, bias=b)
+    y2, _ = run_layer(spec, x, w, bias=b)
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+
+
 @pytest.mark.parametrize("spec,points", [
     (SMALL[3], PAPER_F43_POINTS), (SMALL[2], PAPER_F43_POINTS),
     (SMALL[1], (0, 0.5, -0.5)), (SMALL[2], (0, -1, 1, 0.5, -2)),
@@ -198,6 +220,17 @@ def test_full_size_configs_sampled(cfg):
     assert y.shape == (spec.batch, spec.K) + spec.out_spatial
     assert np.all(np.isfinite(y))
     check_sampled(spec, y, x, w, n=6000, seed=cfg)
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_full_size_bias_sampled(cfg):
+    """The bench layers with a bias: whole blocks and split-tail halves in one launch."""
+    spec = CONFIGS[cfg]
+    x, w = draw_layer(spec, seed=cfg + 20)
+    b = np.random.default_rng(cfg).standard_normal(spec.K).astype(np.float32)
+    y, _ = run_layer(spec, x, w, bias=b)
+    assert np.all(np.isfinite(y))
+    check_sampled(spec, y, x, w, n=3000, seed=cfg, bias=b)
 
 
 def test_full_size_c3d_stack_sampled():

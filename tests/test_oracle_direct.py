@@ -72,6 +72,35 @@ def test_sampled_equals_blas():
     np.testing.assert_allclose(ds, den[tuple(coords.T)], rtol=1e-13, atol=1e-13)
 
 
+@pytest.mark.parametrize("N,n,C,K,X,r,pad", SHAPES[::2])
+def test_bias_all_forms_and_torch(N, n, C, K, X, r, pad):
+    """eq. (2)'s bias b_k: the three forms agree, torch's convNd with its bias
+    argument agrees, the ReLU applies after the bias, and the denominator
+    counts |b_k|."""
+    rng = np.random.default_rng(N * 7 + K)
+    x = _rand(rng, (n, C) + X)
+    w = _rand(rng, (K, C) + (r,) * N)
+    b = (3.0 * rng.standard_normal(K)).astype(np.float32)
+    conv = {1: torch.nn.functional.conv1d, 2: torch.nn.functional.conv2d,
+            3: torch.nn.functional.conv3d}[N]
+    ref = conv(torch.from_numpy(x).double(), torch.from_numpy(w).double(),
+               bias=torch.from_numpy(b).double(), padding=pad).numpy()
+    y0, d0 = direct_blas(x, w, pad)
+    for relu in (False, True):
+        want = np.maximum(ref, 0.0) if relu else ref
+        y1, d1 = direct_naive(x, w, pad, relu=relu, bias=b)
+        y2, d2 = direct_blas(x, w, pad, relu=relu, bias=b)
+        np.testing.assert_allclose(y1, want, rtol=1e-12, atol=1e-12 * np.abs(ref).max())
+        np.testing.assert_allclose(y2, want, rtol=1e-12, atol=1e-12 * np.abs(ref).max())
+        dwant = d0 + np.abs(b).reshape((1, K) + (1,) * N)
+        np.testing.assert_allclose(d1, dwant, rtol=1e-13, atol=1e-13)
+        np.testing.assert_allclose(d2, dwant, rtol=1e-13, atol=1e-13)
+        coords = np.stack(np.meshgrid(*[np.arange(v) for v in y2.shape], indexing="ij"), -1).reshape(-1, 2 + N)
+        ys, ds = direct_sampled(x, w, pad, coords, relu=relu, bias=b, chunk=13)
+        np.testing.assert_allclose(ys, y2[tuple(coords.T)], rtol=1e-13, atol=1e-13)
+        np.testing.assert_allclose(ds, d2[tuple(coords.T)], rtol=1e-13, atol=1e-13)
+
+
 def test_hand_example():
     ex = read_kv("f23_hand_example.txt")
     d = np.array([[[float(v) for v in ex["d"]]]], dtype=np.float32)
