@@ -103,6 +103,82 @@ def calib_copy(nbytes=1 << 30, reps=5):
     print(json.dumps({"calib_copy_bytes_each_way": nbytes, "reps": reps}), flush=True)
 
 
+def bench_fig4(args):
+    """The paper's 2-D benchmark (§4.4, Fig. 4) on synthetic stand-ins: a batch of
+    224 x 224 images through three unpadded 4 x 4 layers of 32 channels and 32
+    kernels with F(5^2, 4^2), transformed kernels cached; throughput in
+    megavoxels (input pixels) per second, as the paper reports it."""
+    import numpy as np
+    import torch
+
+    from paper_1611_06565_amd.wino import Plan
+    from workloads import direct_flops, draw_layer, fig4_layers
+
+    layers = fig4_layers(batch=args.fig4)
+    plans, Us, wss, ys = [], [], [], []
+    x0 = None
+    for i, spec in enumerate(layers):
+        x, w = draw_layer(spec, seed=100 + i)
+        if i == 0:
+            x0 = torch.from_numpy(x).cuda()
+        plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X), pad=spec.pad)
+        plans.append(plan)
+        Us.append(plan.transform_filter(torch.from_numpy(w).cuda()))
+        wss.append(plan.new_workspace())
+        ys.append(plan.new_output())
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        src = x0
+        for i, plan in enumerate(plans):
+            if ev is not None:
+                ev[2 * i].record()
+            plan.transform_input(src, wss[i])
+            if ev is not None:
+                ev[2 * i + 1].record()
+            plan.gemm_inverse(wss[i], Us[i], ys[i])
+            src = ys[i]
+        if ev is not None:
+            ev[2 * len(plans)].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    nev = 2 * len(plans) + 1
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    st = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(nev - 1)] for e in evs]).mean(axis=0)
+    batch = layers[0].batch
+    mvox = batch * layers[0].X[0] * layers[0].X[1] / (ms_step * 1e-3) / 1e6
+    flops = sum(direct_flops(s) for s in layers)
+    per_layer = []
+    for i, (spec, plan) in enumerate(zip(layers, plans)):
+        d = plan.desc
+        g_bytes = 4.0 * (d["n_xi"] * d["T"] * spec.C + d["n_xi"] * spec.C * spec.K
+                         + spec.batch * spec.K * float(np.prod(spec.out_spatial)))
+        in_bytes = 4.0 * (spec.batch * spec.C * float(np.prod(spec.X)) + d["n_xi"] * d["T"] * spec.C)
+        per_layer.append({"X": list(spec.X), "input_transform_us": float(st[2 * i]) * 1e3,
+                          "gemm_inverse_us": float(st[2 * i + 1]) * 1e3,
+                          "input_hbm_frac": in_bytes / (float(st[2 * i]) * 1e-3) / 1e9 / PEAK_HBM,
+                          "gemm_hbm_frac": g_bytes / (float(st[2 * i + 1]) * 1e-3) / 1e9 / PEAK_HBM})
+    out = {
+        "metric": "MVox/s: 224x224 images through three 4x4 conv layers (C=K=32), F(5^2,4^2)",
+        "value": mvox, "unit": "MVox/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"paper 2-D benchmark stand-in: batch {batch}, 224x224, 3 layers of 4x4, "
+                               "C=K=32, unpadded, kernels transformed once", "batch": batch},
+        "effective_tflops": flops / (ms_step * 1e-3) / 1e12,
+        "layers": per_layer,
+        "paper_cpu_MVox_s": 10.9,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -115,6 +191,8 @@ def main():
     ap.add_argument("--no-check", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
                     help="only run a 1 GiB device copy (for HBM counter scaling)")
+    ap.add_argument("--fig4", type=int, default=0, metavar="BATCH",
+                    help="run the paper's 2-D benchmark stand-in (three 4x4 layers, 224x224) at this batch")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -129,6 +207,9 @@ def main():
 
     if args.calib_copy:
         calib_copy()
+        return
+    if args.fig4:
+        bench_fig4(args)
         return
 
     from paper_1611_06565_amd.wino import Plan

@@ -40,7 +40,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // and channel group per (N, m, r).
 //   KIND 0 (m = 2) and 1 (2-D, m = 4): pass-accumulating GEMMs (gemm_acc.hpp,
 //     gemm_acc4.hpp) on 64-tile blocks of V with channel groups of 4.
-//   KIND 2 (3-D, m = 4): k_gemm_inv, all alpha^N elements resident.  A GEMM
+//   KIND 2 (F(4^3), F(5^2, 4^2)): k_gemm_inv, all alpha^N elements resident.  A GEMM
 //     "stage" covers KSTEP * VEC channels: lane group kr of an MFMA operand
 //     loads channels VEC*kr .. VEC*kr+VEC-1 of the stage, and k-step j uses
 //     the j-th of them; the stage is KSTEP groups of VEC channels (CG = VEC),
@@ -50,7 +50,7 @@ template <int N, int MM, int R>
 struct Blocking {
   static constexpr int A = MM + R - 1;
   static constexpr int NXI = ipow(A, N);
-  static constexpr int KIND = MM == 2 ? 0 : (N == 2 ? 1 : 2);
+  static constexpr int KIND = MM == 2 ? 0 : ((N == 2 && MM == 4 && R == 3) ? 1 : 2);
   static constexpr bool ACC = KIND == 0;                         // k_gemm_acc
   static constexpr bool PASS = KIND != 2;                        // k_gemm_acc or k_gemm_acc4
   static constexpr int BLK = PASS ? 64 : 16;                     // tiles per V block
@@ -62,7 +62,7 @@ struct Blocking {
   static constexpr int CGU = CG;                                 // channels per U group
   // channels are padded to whole operand stages of the GEMM (16 channels)
   static constexpr int CPAD = 16;
-  static_assert(KIND != 2 || NXI > 64, "k_gemm_inv serves F(4^3) only");
+  static_assert(KIND != 2 || NXI >= 64, "k_gemm_inv serves F(4^3) and F(5^2, 4^2)");
 };
 
 // ---------------------------------------------------------------- arguments
@@ -551,7 +551,10 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
   constexpr int A = Geo::A, NT = Geo::NT;
   constexpr int UPW = Geo::UPW, UNIT = Geo::UNIT, OLOC = Geo::OLOC, PL = Geo::PL;
   constexpr int NUNIT = Geo::NUNIT;
-  static_assert(NT % (MM * BLK) == 0, "output lanes must tile the work-group");
+  // Part 2 runs on the first NTE threads, a whole number of (output of the
+  // last axis, tile) rows
+  constexpr int NTE = (NT / (MM * BLK)) * (MM * BLK);
+  static_assert(NTE > 0, "at least one row of output lanes");
   const int lane = int(threadIdx.x) & 63;
   const int wave = int(threadIdx.x) >> 6;
   const int col = lane % BLK;
@@ -574,6 +577,7 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
   __syncthreads();
 
   const int tid = int(threadIdx.x);
+  if (tid >= NTE) return;
   const int o_last = tid % MM;
   const int tl = (tid / MM) % BLK;
   int ti[3] = {0, 0, 0};
@@ -584,7 +588,7 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
   constexpr int ITEMS = OLOC * BLK * BLK;
   constexpr int LEAD = N - LOC;
   constexpr int OLEAD = ipow(MM, LEAD);
-  for (int i = tid; i < ITEMS; i += NT) {
+  for (int i = tid; i < ITEMS; i += NTE) {
     const int k_l = (i / (MM * BLK)) % BLK;
     const int o_rest = i / (MM * BLK * BLK);
     const int kg = kb * BLK + k_l;
@@ -646,7 +650,6 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
   constexpr int A = Geo::A, NXI = Geo::NXI, NT = Geo::NT, XPW = Geo::XPW;
   constexpr int UPW = Geo::UPW, UNIT = Geo::UNIT, OLOC = Geo::OLOC, PL = Geo::PL;
   constexpr int NUNIT = Geo::NUNIT;
-  static_assert(NT % (MM * BLK) == 0, "output lanes must tile the work-group");
   static_assert(VEC == 1 || VEC == 2 || VEC == 4, "operand load width");
 
   __shared__ float sm[Geo::LDS_FLOATS];

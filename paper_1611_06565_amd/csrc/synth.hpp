@@ -194,6 +194,11 @@ template <> struct DefaultPoints<2, 3> {
 template <> struct DefaultPoints<4, 3> {
   static constexpr Rat pts[5] = {{0, 1}, {1, 1}, {-1, 1}, {2, 1}, {-2, 1}};
 };
+// F(5,4) (alpha = 8, one of Table 1's sizes; r = 4 is the kernel of the
+// paper's 2-D benchmark, §4.4): {0, 1, -1, 2, -2, 1/2, -1/2}.
+template <> struct DefaultPoints<5, 4> {
+  static constexpr Rat pts[7] = {{0, 1}, {1, 1}, {-1, 1}, {2, 1}, {-2, 1}, {1, 2}, {-1, 2}};
+};
 
 template <int M, int R>
 inline constexpr RatMats kDefaultRat = synthesize(M, R, DefaultPoints<M, R>::pts);
@@ -205,6 +210,7 @@ inline constexpr FMats kDefaultF = to_fmats(kDefaultRat<M, R>);
 inline const Rat* default_points(int m, int r, int* count) {
   if (m == 2 && r == 3) { *count = 3; return DefaultPoints<2, 3>::pts; }
   if (m == 4 && r == 3) { *count = 5; return DefaultPoints<4, 3>::pts; }
+  if (m == 5 && r == 4) { *count = 7; return DefaultPoints<5, 4>::pts; }
   *count = 0;
   return nullptr;
 }

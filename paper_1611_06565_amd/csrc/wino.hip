@@ -75,7 +75,7 @@ bool rationalize(double v, Rat* out) {
 }
 
 bool supported(int N, int m, int r) {
-  return (N == 2 || N == 3) && r == 3 && (m == 2 || m == 4);
+  return ((N == 2 || N == 3) && r == 3 && (m == 2 || m == 4)) || (N == 2 && m == 5 && r == 4);
 }
 
 wino_status launch_status() {
@@ -92,11 +92,11 @@ struct Launch {
   static constexpr int BLK = Blocking<N, MM, R>::BLK;
   static constexpr int CG = Blocking<N, MM, R>::CG;
   static constexpr int CGU = Blocking<N, MM, R>::CGU;
-  // k_gemm_inv (F(4^3)) work-group shape: 12 waves x three alpha-rows,
-  // no register-reduced trailing axes beyond the last, 16-byte operand loads
-  // and no register ring (18 elements per wave leave no room for one; the
-  // other waves of the SIMD hide the load latency).
-  static constexpr int NW = 12;
+  // k_gemm_inv work-group shape: F(4^3): 12 waves x three alpha-rows (18
+  // elements); F(5^2, 4^2): 8 waves x one alpha-row (8 elements).  The last
+  // axis is reduced in registers, 16-byte operand loads, no register ring
+  // (the other waves of the SIMD hide the load latency).
+  static constexpr int NW = (N == 3 && A == 6) ? 12 : 8;
   static constexpr int LOC = 1;
   static constexpr int VEC = Blocking<N, MM, R>::VEC;
   static constexpr int DEPTH = 1;
@@ -228,6 +228,7 @@ wino_status dispatch(const wino_plan_s& p, F&& f) {
   WINO_CASE(3, 2, 3)
   WINO_CASE(2, 4, 3)
   WINO_CASE(3, 4, 3)
+  WINO_CASE(2, 5, 4)
 #undef WINO_CASE
   return WINO_EUNSUPPORTED;
 }
@@ -246,6 +247,7 @@ void channel_groups(int N, int m, int r, int* cg, int* cgu, int* cpad, int* kblk
   if (N == 3 && m == 2 && r == 3) groups_of<3, 2, 3>(cg, cgu, cpad, kblk);
   if (N == 2 && m == 4 && r == 3) groups_of<2, 4, 3>(cg, cgu, cpad, kblk);
   if (N == 3 && m == 4 && r == 3) groups_of<3, 4, 3>(cg, cgu, cpad, kblk);
+  if (N == 2 && m == 5 && r == 4) groups_of<2, 5, 4>(cg, cgu, cpad, kblk);
 }
 
 int block_for(int N, int m, int r) {
@@ -253,6 +255,7 @@ int block_for(int N, int m, int r) {
   if (N == 3 && m == 2 && r == 3) return Blocking<3, 2, 3>::BLK;
   if (N == 2 && m == 4 && r == 3) return Blocking<2, 4, 3>::BLK;
   if (N == 3 && m == 4 && r == 3) return Blocking<3, 4, 3>::BLK;
+  if (N == 2 && m == 5 && r == 4) return Blocking<2, 5, 4>::BLK;
   return 32;
 }
 

@@ -113,6 +113,18 @@ def test_matrices_bitwise_equal_oracle(N, m, pts):
     assert plan.desc["default_points"] == (1 if pts is None else 0)
 
 
+@pytest.mark.parametrize("pts", [None, (0, 1, -1, 2, -2, 0.5, -0.5), (0, 1, -1, 3, -3, 2, -2)])
+def test_matrices_bitwise_equal_oracle_f54(pts):
+    """F(5,4) (alpha = 8, 2-D): compiled default constants and caller points."""
+    plan = wino.Plan(2, 5, 4, 2, 2, [1, 12, 12], pad=0, points=pts)
+    AT, BT, G = plan.matrices()
+    oAT, oBT, oG = _oracle_f64(5, 4, pts if pts is not None else default_points(5, 4))
+    for a, b in ((AT, oAT), (BT, oBT), (G, oG)):
+        assert a.shape == b.shape
+        assert np.array_equal(a.view(np.uint64), b.view(np.uint64))
+    assert plan.desc["default_points"] == (0 if pts is not None and pts[3] == 3 else 1)
+
+
 def test_explicit_default_points_use_compiled_constants():
     plan = wino.Plan(3, 2, 3, 2, 2, [1, 8, 8, 8], points=(0, 1, -1))
     assert plan.desc["default_points"] == 1

@@ -16,7 +16,7 @@ from oracle.pool import maxpool
 from oracle.toomcook import PAPER_F43_POINTS
 from oracle.winograd import transform_filter as o_filter
 from oracle.winograd import transform_input as o_input
-from workloads import C3D_STACK, CONFIGS, LayerSpec, draw_layer, draw_stack
+from workloads import C3D_STACK, CONFIGS, LayerSpec, draw_layer, draw_stack, fig4_layers
 
 pytestmark = pytest.mark.gpu
 
@@ -89,9 +89,30 @@ def test_small_layers_full_output(spec):
     check_full(spec, y, x, w)
 
 
+# F(5^2, 4^2): alpha = 8, 4 x 4 kernels (the kernel size of the paper's 2-D
+# benchmark, §4.4); k_gemm_inv with 64 elements and 25 outputs per (tile, kernel)
+F54 = [
+    LayerSpec("f5x4_2d_ragged", N=2, m=5, r=4, batch=2, C=9, K=20, X=(23, 31), pad=0,
+              x_dist="normal", w_dist="he"),
+    LayerSpec("f5x4_2d_pad1_relu", N=2, m=5, r=4, batch=3, C=33, K=17, X=(19, 26), pad=1,
+              x_dist="uniform", w_dist="he", relu=True),
+    LayerSpec("f5x4_2d_one_tile", N=2, m=5, r=4, batch=1, C=2, K=3, X=(8, 8), pad=0),
+    LayerSpec("f5x4_2d_wide", N=2, m=5, r=4, batch=1, C=40, K=70, X=(40, 57), pad=2,
+              x_dist="relu_normal", w_dist="he"),
+]
+
+
+@pytest.mark.parametrize("spec", F54, ids=lambda s: s.name)
+def test_f54_layers_full_output(spec):
+    x, w = draw_layer(spec, seed=17)
+    y, _ = run_layer(spec, x, w, guard=512)
+    assert y.shape == (spec.batch, spec.K) + spec.out_spatial
+    check_full(spec, y, x, w)
+
+
 # eq. (2)'s bias: every GEMM kernel, split-tail blocks (small layers split every
 # block into halves; the bias joins one half) and whole blocks (ReLU layers)
-BIAS = [SMALL[1], SMALL[5], SMALL[2], SMALL[7], SMALL[3], SMALL[6]]
+BIAS = [SMALL[1], SMALL[5], SMALL[2], SMALL[7], SMALL[3], SMALL[6], F54[0]]
 
 
 @pytest.mark.parametrize("spec", BIAS, ids=lambda s: s.name)
@@ -231,6 +252,17 @@ def test_full_size_bias_sampled(cfg):
     y, _ = run_layer(spec, x, w, bias=b)
     assert np.all(np.isfinite(y))
     check_sampled(spec, y, x, w, n=3000, seed=cfg, bias=b)
+
+
+def test_full_size_fig4_layer_sampled():
+    """First layer of the paper's 2-D benchmark stand-in (F(5^2, 4^2), 224 x 224,
+    C = K = 32) at batch 20, sampled against the oracle."""
+    spec = fig4_layers(batch=20)[0]
+    x, w = draw_layer(spec, seed=100)
+    y, _ = run_layer(spec, x, w)
+    assert y.shape == (20, 32, 221, 221)
+    assert np.all(np.isfinite(y))
+    check_sampled(spec, y, x, w, n=4000, seed=6)
 
 
 def test_full_size_c3d_stack_sampled():

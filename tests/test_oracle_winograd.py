@@ -39,6 +39,9 @@ EXACT_CASES = [
     (3, 2, 3, None, 2, 3, 2, (4, 4, 4), 0),
     (3, 4, 3, None, 1, 2, 2, (5, 6, 4), 1),
     (3, 4, 3, PAPER_F43_POINTS, 1, 2, 2, (6, 6, 6), 0),
+    (1, 5, 4, None, 1, 2, 2, (17,), 1),
+    (2, 5, 4, None, 1, 2, 2, (12, 9), 0),
+    (2, 5, 4, None, 1, 1, 2, (8, 13), 1),
 ]
 
 
@@ -74,7 +77,7 @@ def _kron_all(M, N):
     return K
 
 
-@pytest.mark.parametrize("N,m,r", [(2, 2, 3), (3, 2, 3), (2, 4, 3), (3, 4, 3)])
+@pytest.mark.parametrize("N,m,r", [(2, 2, 3), (3, 2, 3), (2, 4, 3), (3, 4, 3), (2, 5, 4)])
 def test_separability(N, m, r):
     AT, BT, G = matrices(m, r, exact=True)
     alpha = m + r - 1

@@ -120,6 +120,19 @@ C3D_STACK = StackSpec(
     m=2, x_dist="uniform")
 
 
+def fig4_layers(batch=200, X=224, depth=3):
+    """Stand-in for the paper's 2-D benchmark (§4.4, Fig. 4): a 224 x 224 image
+    through three unpadded 4 x 4 layers of 32 channels and 32 kernels (no
+    activation is stated; none is applied), here with F(5^2, 4^2).  Layer i + 1
+    takes layer i's output; random inputs stand in for the ImageNet images."""
+    out = []
+    for i in range(depth):
+        out.append(LayerSpec(f"fig4_l{i + 1}_b{batch}", N=2, m=5, r=4, batch=batch, C=32, K=32,
+                             X=(X, X), pad=0, x_dist="uniform", w_dist="he"))
+        X -= 3
+    return out
+
+
 def _gen(seed):
     import torch
     return torch.Generator("cpu").manual_seed(int(seed))
