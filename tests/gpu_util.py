@@ -8,9 +8,9 @@ from oracle.direct import direct_blas, direct_sampled
 from oracle.metric import normalised_error
 
 # normalised max error per output-tile extent m: the stated bars for m = 2
-# and 4; for F(5,4) (alpha = 8, points up to +-2 and +-1/2, entries of A^T up
-# to 32 and of B^T up to 21/4) one decade above m = 4
-TOL = {2: 1e-5, 4: 1e-4, 5: 1e-3}
+# and 4; F(5,4) (2-D, alpha = 8) takes the m = 4 bar (measured max errors about
+# 3e-6, a margin of 30 like F(4^3)'s)
+TOL = {2: 1e-5, 4: 1e-4, 5: 1e-4}
 
 
 def log(msg):
