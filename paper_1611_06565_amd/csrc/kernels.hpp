@@ -40,7 +40,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // and channel group per (N, m, r).
 //   KIND 0 (m = 2) and 1 (2-D, m = 4): pass-accumulating GEMMs (gemm_acc.hpp,
 //     gemm_acc4.hpp) on 64-tile blocks of V with channel groups of 4.
-//   KIND 2 (F(4^3), F(5^2, 4^2)): k_gemm_inv, all alpha^N elements resident.  A GEMM
+//   KIND 2 (F(4^3) and the other 2-D sizes): k_gemm_inv, all alpha^N elements resident.  A GEMM
 //     "stage" covers KSTEP * VEC channels: lane group kr of an MFMA operand
 //     loads channels VEC*kr .. VEC*kr+VEC-1 of the stage, and k-step j uses
 //     the j-th of them; the stage is KSTEP groups of VEC channels (CG = VEC),
@@ -62,7 +62,6 @@ struct Blocking {
   static constexpr int CGU = CG;                                 // channels per U group
   // channels are padded to whole operand stages of the GEMM (16 channels)
   static constexpr int CPAD = 16;
-  static_assert(KIND != 2 || NXI >= 64, "k_gemm_inv serves F(4^3) and F(5^2, 4^2)");
 };
 
 // ---------------------------------------------------------------- arguments

@@ -24,6 +24,7 @@
 #pragma once
 
 #include <cstdint>
+#include <utility>
 
 namespace wino {
 
@@ -183,22 +184,20 @@ constexpr FMats to_fmats(const RatMats& R) {
   return F;
 }
 
-// Default interpolation points per (m, r).  F(2,3): the §2.2 set {0, 1, -1}.
-// F(4,3): {0, 1, -1, 2, -2}; the §3.3 set {0, 1, -1, 1/3, -1/3} is accepted
-// as an explicit choice but loses about an order of magnitude of fp32
-// accuracy in 3-D.
-template <int M, int R> struct DefaultPoints;
-template <> struct DefaultPoints<2, 3> {
-  static constexpr Rat pts[3] = {{0, 1}, {1, 1}, {-1, 1}};
+// Default interpolation points per (m, r): the first m + r - 2 entries of
+// the ladder {0, 1, -1, 2, -2, 1/2, -1/2} (infinity implied).  F(2,3) gets
+// the §2.2 set {0, 1, -1}; F(4,3) gets {0, 1, -1, 2, -2} (the §3.3 set
+// {0, 1, -1, 1/3, -1/3} is accepted as an explicit choice but loses about an
+// order of magnitude of fp32 accuracy in 3-D); F(5,4) and the other alpha = 8
+// sizes of Table 1 get all seven.
+constexpr int kLadderLen = kMaxAlpha - 1;
+constexpr Rat kLadder[kLadderLen] = {{0, 1}, {1, 1}, {-1, 1}, {2, 1}, {-2, 1}, {1, 2}, {-1, 2}};
+template <int K, class Seq = std::make_integer_sequence<int, K>> struct LadderPrefix;
+template <int K, int... I> struct LadderPrefix<K, std::integer_sequence<int, I...>> {
+  static_assert(K >= 1 && K <= kLadderLen, "alpha in 2..8");
+  static constexpr Rat pts[K] = {kLadder[I]...};
 };
-template <> struct DefaultPoints<4, 3> {
-  static constexpr Rat pts[5] = {{0, 1}, {1, 1}, {-1, 1}, {2, 1}, {-2, 1}};
-};
-// F(5,4) (alpha = 8, one of Table 1's sizes; r = 4 is the kernel of the
-// paper's 2-D benchmark, §4.4): {0, 1, -1, 2, -2, 1/2, -1/2}.
-template <> struct DefaultPoints<5, 4> {
-  static constexpr Rat pts[7] = {{0, 1}, {1, 1}, {-1, 1}, {2, 1}, {-2, 1}, {1, 2}, {-1, 2}};
-};
+template <int M, int R> struct DefaultPoints : LadderPrefix<M + R - 2> {};
 
 template <int M, int R>
 inline constexpr RatMats kDefaultRat = synthesize(M, R, DefaultPoints<M, R>::pts);
@@ -208,11 +207,13 @@ inline constexpr FMats kDefaultF = to_fmats(kDefaultRat<M, R>);
 
 // Host helper: the default points for (m, r), or nullptr.
 inline const Rat* default_points(int m, int r, int* count) {
-  if (m == 2 && r == 3) { *count = 3; return DefaultPoints<2, 3>::pts; }
-  if (m == 4 && r == 3) { *count = 5; return DefaultPoints<4, 3>::pts; }
-  if (m == 5 && r == 4) { *count = 7; return DefaultPoints<5, 4>::pts; }
-  *count = 0;
-  return nullptr;
+  const int k = m + r - 2;
+  if (m < 1 || r < 1 || k < 1 || k > kLadderLen) {
+    *count = 0;
+    return nullptr;
+  }
+  *count = k;
+  return kLadder;
 }
 
 }  // namespace wino

@@ -74,8 +74,18 @@ bool rationalize(double v, Rat* out) {
   return false;
 }
 
+// The (N, m, r) with compiled kernels: F(2,3) and F(4,3) in 2-D and 3-D;
+// in 2-D also the other sizes of Table 1, F(3,2) (alpha = 4) and F(5,4),
+// F(4,5), F(3,6) (alpha = 8).
+#define WINO_SIZES(X) \
+  X(2, 2, 3) X(3, 2, 3) X(2, 4, 3) X(3, 4, 3) X(2, 5, 4) X(2, 4, 5) X(2, 3, 6) X(2, 3, 2)
+
 bool supported(int N, int m, int r) {
-  return ((N == 2 || N == 3) && r == 3 && (m == 2 || m == 4)) || (N == 2 && m == 5 && r == 4);
+#define WINO_SUPPORTED(N_, M_, R_) \
+  if (N == N_ && m == M_ && r == R_) return true;
+  WINO_SIZES(WINO_SUPPORTED)
+#undef WINO_SUPPORTED
+  return false;
 }
 
 wino_status launch_status() {
@@ -93,10 +103,10 @@ struct Launch {
   static constexpr int CG = Blocking<N, MM, R>::CG;
   static constexpr int CGU = Blocking<N, MM, R>::CGU;
   // k_gemm_inv work-group shape: F(4^3): 12 waves x three alpha-rows (18
-  // elements); F(5^2, 4^2): 8 waves x one alpha-row (8 elements).  The last
+  // elements); 2-D sizes: alpha waves x one alpha-row (alpha elements).  The last
   // axis is reduced in registers, 16-byte operand loads, no register ring
   // (the other waves of the SIMD hide the load latency).
-  static constexpr int NW = (N == 3 && A == 6) ? 12 : 8;
+  static constexpr int NW = (N == 3 && A == 6) ? 12 : ipow(A, N - 1);
   static constexpr int LOC = 1;
   static constexpr int VEC = Blocking<N, MM, R>::VEC;
   static constexpr int DEPTH = 1;
@@ -224,11 +234,7 @@ wino_status dispatch(const wino_plan_s& p, F&& f) {
 #define WINO_CASE(N_, M_, R_)                                            \
   if (p.N == N_ && p.m == M_ && p.r == R_)                               \
     return p.const_mats ? f(L<N_, M_, R_, true>{}) : f(L<N_, M_, R_, false>{});
-  WINO_CASE(2, 2, 3)
-  WINO_CASE(3, 2, 3)
-  WINO_CASE(2, 4, 3)
-  WINO_CASE(3, 4, 3)
-  WINO_CASE(2, 5, 4)
+  WINO_SIZES(WINO_CASE)
 #undef WINO_CASE
   return WINO_EUNSUPPORTED;
 }
@@ -243,19 +249,17 @@ template <int N, int M, int R> void groups_of(int* cg, int* cgu, int* cpad, int*
 // and kernel padding multiple of an instantiation.
 void channel_groups(int N, int m, int r, int* cg, int* cgu, int* cpad, int* kblk) {
   *cg = *cgu = *cpad = *kblk = 1;
-  if (N == 2 && m == 2 && r == 3) groups_of<2, 2, 3>(cg, cgu, cpad, kblk);
-  if (N == 3 && m == 2 && r == 3) groups_of<3, 2, 3>(cg, cgu, cpad, kblk);
-  if (N == 2 && m == 4 && r == 3) groups_of<2, 4, 3>(cg, cgu, cpad, kblk);
-  if (N == 3 && m == 4 && r == 3) groups_of<3, 4, 3>(cg, cgu, cpad, kblk);
-  if (N == 2 && m == 5 && r == 4) groups_of<2, 5, 4>(cg, cgu, cpad, kblk);
+#define WINO_GROUPS(N_, M_, R_) \
+  if (N == N_ && m == M_ && r == R_) groups_of<N_, M_, R_>(cg, cgu, cpad, kblk);
+  WINO_SIZES(WINO_GROUPS)
+#undef WINO_GROUPS
 }
 
 int block_for(int N, int m, int r) {
-  if (N == 2 && m == 2 && r == 3) return Blocking<2, 2, 3>::BLK;
-  if (N == 3 && m == 2 && r == 3) return Blocking<3, 2, 3>::BLK;
-  if (N == 2 && m == 4 && r == 3) return Blocking<2, 4, 3>::BLK;
-  if (N == 3 && m == 4 && r == 3) return Blocking<3, 4, 3>::BLK;
-  if (N == 2 && m == 5 && r == 4) return Blocking<2, 5, 4>::BLK;
+#define WINO_BLOCK(N_, M_, R_) \
+  if (N == N_ && m == M_ && r == R_) return Blocking<N_, M_, R_>::BLK;
+  WINO_SIZES(WINO_BLOCK)
+#undef WINO_BLOCK
   return 32;
 }
 

@@ -113,16 +113,19 @@ def test_matrices_bitwise_equal_oracle(N, m, pts):
     assert plan.desc["default_points"] == (1 if pts is None else 0)
 
 
-@pytest.mark.parametrize("pts", [None, (0, 1, -1, 2, -2, 0.5, -0.5), (0, 1, -1, 3, -3, 2, -2)])
-def test_matrices_bitwise_equal_oracle_f54(pts):
-    """F(5,4) (alpha = 8, 2-D): compiled default constants and caller points."""
-    plan = wino.Plan(2, 5, 4, 2, 2, [1, 12, 12], pad=0, points=pts)
+@pytest.mark.parametrize("m,r,pts", [
+    (5, 4, None), (5, 4, (0, 1, -1, 2, -2, 0.5, -0.5)), (5, 4, (0, 1, -1, 3, -3, 2, -2)),
+    (4, 5, None), (3, 6, None), (3, 2, None), (3, 2, (0, 2, -1)),
+])
+def test_matrices_bitwise_equal_oracle_2d_sizes(m, r, pts):
+    """The other 2-D sizes of Table 1: compiled default constants and caller points."""
+    plan = wino.Plan(2, m, r, 2, 2, [1, 12, 12], pad=0, points=pts)
     AT, BT, G = plan.matrices()
-    oAT, oBT, oG = _oracle_f64(5, 4, pts if pts is not None else default_points(5, 4))
+    oAT, oBT, oG = _oracle_f64(m, r, pts if pts is not None else default_points(m, r))
     for a, b in ((AT, oAT), (BT, oBT), (G, oG)):
         assert a.shape == b.shape
         assert np.array_equal(a.view(np.uint64), b.view(np.uint64))
-    assert plan.desc["default_points"] == (0 if pts is not None and pts[3] == 3 else 1)
+    assert plan.desc["default_points"] == (1 if pts is None or tuple(pts) == tuple(default_points(m, r)) else 0)
 
 
 def test_explicit_default_points_use_compiled_constants():

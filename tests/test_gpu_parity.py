@@ -99,6 +99,13 @@ F54 = [
     LayerSpec("f5x4_2d_one_tile", N=2, m=5, r=4, batch=1, C=2, K=3, X=(8, 8), pad=0),
     LayerSpec("f5x4_2d_wide", N=2, m=5, r=4, batch=1, C=40, K=70, X=(40, 57), pad=2,
               x_dist="relu_normal", w_dist="he"),
+    # the other 2-D sizes of Table 1
+    LayerSpec("f4x5_2d", N=2, m=4, r=5, batch=2, C=12, K=19, X=(21, 26), pad=2,
+              x_dist="normal", w_dist="he"),
+    LayerSpec("f3x6_2d", N=2, m=3, r=6, batch=1, C=20, K=33, X=(25, 19), pad=0,
+              x_dist="uniform", w_dist="he", relu=True),
+    LayerSpec("f3x2_2d", N=2, m=3, r=2, batch=3, C=17, K=40, X=(20, 23), pad=1,
+              x_dist="normal", w_dist="normal"),
 ]
 
 

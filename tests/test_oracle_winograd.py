@@ -42,6 +42,9 @@ EXACT_CASES = [
     (1, 5, 4, None, 1, 2, 2, (17,), 1),
     (2, 5, 4, None, 1, 2, 2, (12, 9), 0),
     (2, 5, 4, None, 1, 1, 2, (8, 13), 1),
+    (2, 4, 5, None, 1, 2, 2, (11, 12), 0),
+    (2, 3, 6, None, 1, 2, 1, (13, 10), 1),
+    (2, 3, 2, None, 2, 2, 2, (7, 8), 1),
 ]
 
 
