@@ -315,6 +315,13 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
   // axis) per round; thread (ol, tl) stores its tile's output ol of the last
   // axis for every kernel, so neighbouring lanes store neighbouring outputs.
   __builtin_amdgcn_s_waitcnt(0x0f70);             // vmcnt(0): no copy still writes LDS
+  // the block's bias values go through LDS: a global load inside the store
+  // loop would make its stores wait for each other (vmcnt counts both)
+  __shared__ float bsm[KB];
+  if (g.bias != nullptr && tid < KB) {
+    const int kg = kb * KB + tid;
+    bsm[tid] = kg < g.K ? g.bias[kg] : 0.0f;
+  }
   const int ol = tid % MM;
   const int tl = (tid / MM) % TB;
   static_assert(G::NT == MM * TB, "one thread per (output of the last axis, tile)");
@@ -353,10 +360,10 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
           if (split) {
             // two partials onto zero: 0 + a + b rounds the same in either
             // order; the bias joins the first half's partial
-            if (g.bias != nullptr && p0 == 0) v += g.bias[kg];
+            if (g.bias != nullptr && p0 == 0) v += bsm[kl];
             unsafeAtomicAdd(yo + int64_t(kg) * g.ystride_k, v);
           } else {
-            if (g.bias != nullptr) v += g.bias[kg];
+            if (g.bias != nullptr) v += bsm[kl];
             if (g.relu) v = v > 0.0f ? v : 0.0f;
             __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
           }

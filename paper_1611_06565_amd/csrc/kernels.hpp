@@ -542,7 +542,7 @@ struct EpiArgs {
 // Part 2: A^T along the N-LOC leading axes, ReLU, crop, store.  Item
 // (o_loc, k, t) runs with the last-axis output fastest, then the tile, so
 // neighbouring lanes write neighbouring outputs of a row.
-template <int N, int MM, int R, bool CONST, int BLK, int NW, int LOC, class AccT, class TileFn>
+template <int N, int MM, int R, bool CONST, int BLK, int NW, int LOC, bool BIAS, class AccT, class TileFn>
 __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb, const EpiArgs& g,
                                               const FMats& fm, TileFn tile_of) {
   using S = MfmaShape<BLK>;
@@ -558,6 +558,17 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
   const int wave = int(threadIdx.x) >> 6;
   const int col = lane % BLK;
   const MatRef<Which::AT, CONST, MM, R> AT{&fm};
+  // BIAS (a separate instance, so that layers without a bias run the same
+  // code as before it existed): the block's bias values go through LDS, as a
+  // global load inside the store loop would make its stores wait for each
+  // other (vmcnt counts both)
+  __shared__ float bsm[BLK];
+  if constexpr (BIAS) {
+    if (int(threadIdx.x) < BLK) {
+      const int kg = kb * BLK + int(threadIdx.x);
+      bsm[threadIdx.x] = kg < g.K ? g.bias[kg] : 0.0f;
+    }
+  }
 #pragma unroll
   for (int r = 0; r < S::NACC; ++r) {
     const int t = S::acc_row(lane, r);
@@ -613,7 +624,11 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
     float out[OLEAD];
     transform_nd<LEAD, A, MM>(v, out, AT);
     float* yk = g.y + (int64_t(n) * g.K + kg) * g.ystride_k;
-    const float bk = g.bias != nullptr ? g.bias[kg] : 0.0f;
+    if constexpr (BIAS) {
+      const float bk = bsm[k_l];
+#pragma unroll
+      for (int q = 0; q < OLEAD; ++q) out[q] += bk;
+    }
 #pragma unroll
     for (int q = 0; q < OLEAD; ++q) {
       int rem = q;
@@ -630,7 +645,6 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
 #pragma unroll
       for (int ax = 1; ax < N; ++ax) off = off * g.Y[ax] + yc[ax];
       float val = out[q];
-      if (g.bias != nullptr) val += bk;
       if (g.relu) val = val > 0.0f ? val : 0.0f;
       yk[off] = val;
     }
@@ -733,7 +747,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
     if (t >= g.T) return -1;
     return split_tile<N>(t, g.tiles, ti);
   };
-  gemm_epilogue<N, MM, R, CONST, BLK, NW, LOC>(acc, sm, kb, e, fm, tile_of);
+  if (g.bias != nullptr) gemm_epilogue<N, MM, R, CONST, BLK, NW, LOC, true>(acc, sm, kb, e, fm, tile_of);
+  else gemm_epilogue<N, MM, R, CONST, BLK, NW, LOC, false>(acc, sm, kb, e, fm, tile_of);
 }
 
 // ------------------------------------------------------------ max-pool (a6)
