@@ -401,13 +401,6 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
   // neighbouring outputs of a row, PPR output planes per round.  Plane o
   // ([k][t], t XOR-swizzled by k) of a round lives in buffer o % PPR.
   __builtin_amdgcn_s_waitcnt(0x0f70);             // vmcnt(0): no copy still writes LDS
-  // the block's bias values go through LDS: a global load inside the store
-  // loop would make its stores wait for each other (vmcnt counts both)
-  __shared__ float bsm[KB];
-  if (g.bias != nullptr && tid < KB) {
-    const int kg = kb * KB + tid;
-    bsm[tid] = kg < g.K ? g.bias[kg] : 0.0f;
-  }
   const int ol = tid % MM;
   const int tl = (tid / MM) % TB;
   const int t = tb * TB + tl;
@@ -456,10 +449,10 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
           if (split) {
             // two partials onto zero: 0 + a + b rounds the same in either
             // order; the bias joins the first half's partial
-            if (g.bias != nullptr && p0 == 0) v += bsm[kl];
+            if (g.bias != nullptr && p0 == 0) v += g.bias[kg];
             unsafeAtomicAdd(yo + int64_t(kg) * g.ystride_k, v);
           } else {
-            if (g.bias != nullptr) v += bsm[kl];
+            if (g.bias != nullptr) v += g.bias[kg];
             if (g.relu) v = v > 0.0f ? v : 0.0f;
             __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
           }
