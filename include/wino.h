@@ -175,6 +175,25 @@ wino_status wino_forward_ex(const wino_plan_t* plan, const float* x, const float
 wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const float* x, float* y,
                            void* stream);
 
+/* Accuracy of a point set (§2.2, §3.3: the points trade fp32 accuracy).
+ * wino_points_error_growth: kappa = kappa_1^N, where kappa_1 is the largest
+ * over outputs i of sum_xi |A^T[i][xi]| |G[xi,:]|_1 |B^T[xi,:]|_1 / r, the
+ * first-order bound on the rounding error of the 1-D algorithm relative to the
+ * direct sum's magnitude for inputs of magnitude <= 1 (the N-D transforms are
+ * products over the axes).  Computed on the host from the exact rational
+ * matrices of Theorem 1 / Algorithm 1.
+ *   points  the alpha - 1 finite points (infinity implied), or NULL for the
+ *           default set; n_points = m + r - 2 when given
+ *   growth  out: kappa
+ * wino_search_points: the symmetric set {0 (if m + r - 2 is odd), +-p_1,
+ * +-p_2, ...} with p_i from {1, 2, 1/2, 3, 1/3, 3/2, 2/3, 4, 1/4} that
+ * minimises kappa (ties: earlier in that order); points[m + r - 2] and growth
+ * are written.  Host only, no device work; WINO_EINVAL for bad sizes or
+ * points (coincident, or not small rationals). */
+wino_status wino_points_error_growth(int N, int m, int r, const double* points, int n_points,
+                                     double* growth);
+wino_status wino_search_points(int N, int m, int r, double* points, double* growth);
+
 const char* wino_status_string(wino_status s);
 
 #ifdef __cplusplus

@@ -470,6 +470,89 @@ wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const flo
   return launch_status();
 }
 
+// Growth of fp32 rounding error through the transforms of a point set
+// (§2.2 and §3.3 note that the choice of points trades accuracy): for
+// |g|, |d| <= 1 the first-order error of output i of the 1-D algorithm
+// A^T [(G g) . (B^T d)] is at most u sum_xi |A^T[i][xi]| |G[xi]|_1 |B^T[xi]|_1,
+// against at most r for the direct sum; kappa_1 = max_i of that sum / r, and
+// the N-D transforms, products over the axes, give kappa_1^N.
+static bool growth_of(int N, int m, int r, const Rat* pts, double* out) {
+  const RatMats R = synthesize(m, r, pts);
+  if (!R.ok) return false;
+  const int a = m + r - 1;
+  double k1 = 0.0;
+  for (int i = 0; i < m; ++i) {
+    double sum = 0.0;
+    for (int x = 0; x < a; ++x) {
+      double gn = 0.0, bn = 0.0;
+      for (int k = 0; k < r; ++k) gn += std::fabs(to_f64(R.G[x][k]));
+      for (int j = 0; j < a; ++j) bn += std::fabs(to_f64(R.BT[x][j]));
+      sum += std::fabs(to_f64(R.AT[i][x])) * gn * bn;
+    }
+    k1 = std::fmax(k1, sum / r);
+  }
+  *out = std::pow(k1, N);
+  return true;
+}
+
+wino_status wino_points_error_growth(int N, int m, int r, const double* points, int n_points,
+                                     double* growth) {
+  if (growth == nullptr || N < 1 || N > 3 || m < 1 || r < 1 || m + r - 1 > kMaxAlpha) return WINO_EINVAL;
+  const int np = m + r - 2;
+  Rat pts[kMaxAlpha];
+  if (points == nullptr) {
+    int cnt = 0;
+    const Rat* d = default_points(m, r, &cnt);
+    if (d == nullptr || cnt != np) return WINO_EINVAL;
+    for (int i = 0; i < np; ++i) pts[i] = d[i];
+  } else {
+    if (n_points != np) return WINO_EINVAL;
+    for (int i = 0; i < np; ++i)
+      if (!rationalize(points[i], &pts[i])) return WINO_EINVAL;
+  }
+  return growth_of(N, m, r, pts, growth) ? WINO_OK : WINO_EINVAL;
+}
+
+wino_status wino_search_points(int N, int m, int r, double* points, double* growth) {
+  if (points == nullptr || growth == nullptr || N < 1 || N > 3 || m < 1 || r < 1 ||
+      m + r - 1 > kMaxAlpha)
+    return WINO_EINVAL;
+  const int np = m + r - 2;
+  // candidates: 0 (when the count is odd) and pairs +-p, p from a pool of
+  // small rationals; every subset of pairs of the right size is tried
+  static const Rat pool[] = {{1, 1}, {2, 1}, {1, 2}, {3, 1}, {1, 3}, {3, 2}, {2, 3}, {4, 1}, {1, 4}};
+  constexpr int NP = int(sizeof(pool) / sizeof(pool[0]));
+  const int pairs = np / 2;
+  const bool zero = (np % 2) == 1;
+  if (pairs > NP) return WINO_EUNSUPPORTED;
+  double best = 0.0;
+  bool found = false;
+  Rat best_pts[kMaxAlpha];
+  for (uint32_t mask = 0; mask < (1u << NP); ++mask) {
+    if (__builtin_popcount(mask) != pairs) continue;
+    Rat pts[kMaxAlpha];
+    int n = 0;
+    if (zero) pts[n++] = rat(0);
+    for (int i = 0; i < NP; ++i)
+      if (mask & (1u << i)) {
+        pts[n++] = pool[i];
+        pts[n++] = neg(pool[i]);
+      }
+    double g = 0.0;
+    if (!growth_of(N, m, r, pts, &g)) continue;
+    // ties go to the earlier subset: pool order prefers small integers
+    if (!found || g < best * (1.0 - 1e-12)) {
+      best = g;
+      found = true;
+      for (int i = 0; i < np; ++i) best_pts[i] = pts[i];
+    }
+  }
+  if (!found) return WINO_EUNSUPPORTED;
+  for (int i = 0; i < np; ++i) points[i] = to_f64(best_pts[i]);
+  *growth = best;
+  return WINO_OK;
+}
+
 const char* wino_status_string(wino_status s) {
   switch (s) {
     case WINO_OK: return "ok";

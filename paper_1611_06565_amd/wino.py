@@ -82,6 +82,8 @@ def lib():
         "wino_forward_ex": (i32, [vp, vp, vp, vp, vp, vp, sz, vp]),
         "wino_maxpool3d": (i32, [P_i64, ctypes.POINTER(i32), vp, vp, vp]),
         "wino_status_string": (ctypes.c_char_p, [i32]),
+        "wino_points_error_growth": (i32, [i32, i32, i32, P_dbl, i32, P_dbl]),
+        "wino_search_points": (i32, [i32, i32, i32, P_dbl, P_dbl]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -288,6 +290,29 @@ class Plan:
                                        _dev_ptr(y, "y", torch.float32), ws_ptr, ws_len, _stream()),
                "wino_forward_ex")
         return y
+
+
+def points_error_growth(N, m, r, points=None):
+    """kappa of a point set (None: the default set); see include/wino.h."""
+    L = lib()
+    g = ctypes.c_double()
+    if points is None:
+        _check(L.wino_points_error_growth(N, m, r, None, 0, ctypes.byref(g)), "wino_points_error_growth")
+    else:
+        arr = (ctypes.c_double * len(points))(*[_point(p) for p in points])
+        _check(L.wino_points_error_growth(N, m, r, arr, len(points), ctypes.byref(g)),
+               "wino_points_error_growth")
+    return g.value
+
+
+def search_points(N, m, r):
+    """The symmetric point set with the smallest kappa; returns (points, kappa)."""
+    L = lib()
+    n = m + r - 2
+    arr = (ctypes.c_double * n)()
+    g = ctypes.c_double()
+    _check(L.wino_search_points(N, m, r, arr, ctypes.byref(g)), "wino_search_points")
+    return tuple(arr), g.value
 
 
 def maxpool3d(x, window, y=None):

@@ -10,6 +10,7 @@
 """
 import ctypes
 import math
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -161,3 +162,46 @@ def test_device_calls_reject_bad_arguments(L):
     dims = (ctypes.c_int64 * 4)(1, 4, 4, 4)
     win = (ctypes.c_int32 * 3)(2, 2, 8)
     assert L.wino_maxpool3d(dims, win, vp(4096), vp(8192), None) == -1   # 4 // 8 == 0
+
+
+def _kappa_from_oracle(N, m, r, pts):
+    """kappa of include/wino.h from the oracle's exact matrices (Fractions)."""
+    AT, BT, G = winograd_matrices(m, r, pts)
+    a = m + r - 1
+    gn = [sum(abs(v) for v in G[x]) for x in range(a)]
+    bn = [sum(abs(v) for v in BT[x]) for x in range(a)]
+    k1 = max(sum(abs(AT[i][x]) * gn[x] * bn[x] for x in range(a)) for i in range(m)) / r
+    return float(k1) ** N
+
+
+@pytest.mark.parametrize("N,m,r,pts", [
+    (3, 2, 3, None), (3, 4, 3, None), (3, 4, 3, PAPER_F43_POINTS), (2, 5, 4, None),
+    (2, 4, 3, (0, 2, -2, 0.5, -0.5)), (2, 3, 6, (0, 1, -1, 3, -3, Fraction(1, 3), Fraction(-1, 3))),
+])
+def test_points_error_growth_matches_oracle_matrices(N, m, r, pts):
+    got = wino.points_error_growth(N, m, r, pts)
+    want = _kappa_from_oracle(N, m, r, pts if pts is not None else default_points(m, r))
+    assert abs(got - want) <= 1e-9 * want
+
+
+@pytest.mark.parametrize("N,m,r", [(3, 2, 3), (3, 4, 3), (2, 4, 3), (2, 5, 4), (2, 4, 5), (2, 3, 6), (2, 3, 2)])
+def test_search_points(N, m, r):
+    pts, g = wino.search_points(N, m, r)
+    assert len(pts) == m + r - 2 and len(set(pts)) == len(pts)
+    assert sorted(pts) == sorted(-p for p in pts)                 # symmetric
+    assert abs(g - _kappa_from_oracle(N, m, r, [Fraction(p).limit_denominator(64) for p in pts])) <= 1e-9 * g
+    assert g <= wino.points_error_growth(N, m, r) * (1 + 1e-12)  # no worse than the default set
+    if (m, r) == (4, 3):
+        assert g < wino.points_error_growth(N, m, r, PAPER_F43_POINTS)
+
+
+def test_points_error_growth_rejects(L):
+    g = ctypes.c_double()
+    two = (ctypes.c_double * 2)(0.0, 1.0)
+    assert L.wino_points_error_growth(3, 4, 3, two, 2, ctypes.byref(g)) == -1   # wrong count
+    same = (ctypes.c_double * 5)(0.0, 1.0, 1.0, 2.0, -2.0)
+    assert L.wino_points_error_growth(3, 4, 3, same, 5, ctypes.byref(g)) == -1  # coincident
+    assert L.wino_points_error_growth(0, 4, 3, None, 0, ctypes.byref(g)) == -1
+    assert L.wino_points_error_growth(2, 6, 4, None, 0, ctypes.byref(g)) == -1  # alpha 9
+    out = (ctypes.c_double * 5)()
+    assert L.wino_search_points(3, 4, 3, out, None) == -1

@@ -150,6 +150,24 @@ def test_caller_points(spec, points):
     check_full(spec, y, x, w)
 
 
+def test_searched_points_accuracy():
+    """The point set wino_search_points picks for F(4^3, 3^3) (smallest error
+    growth estimate) measures no less accurate than the paper's printed set,
+    whose estimate is 27 times larger; every set stays within the m = 4 bar."""
+    from paper_1611_06565_amd.wino import points_error_growth, search_points
+    spec = LayerSpec("f4x3_3d_points", N=3, m=4, r=3, batch=1, C=32, K=24, X=(18, 17, 20), pad=1,
+                     x_dist="uniform", w_dist="he")
+    x, w = draw_layer(spec, seed=9)
+    searched, g = search_points(3, 4, 3)
+    errs = {}
+    for name, pts in [("default", None), ("paper", PAPER_F43_POINTS), ("searched", searched)]:
+        y, _ = run_layer(spec, x, w, points=pts)
+        errs[name] = check_full(spec, y, x, w)["max"]
+        log(f"  {name}: points {pts} growth {points_error_growth(3, 4, 3, pts):.1f} max err {errs[name]:.3e}")
+    assert g < points_error_growth(3, 4, 3, PAPER_F43_POINTS)
+    assert errs["searched"] <= errs["paper"]
+
+
 @pytest.mark.parametrize("N,C", [(3, 16), (3, 5), (2, 16)])
 def test_integer_inputs_bitwise_exact(N, C):
     spec = LayerSpec(f"int_f2x3_{N}d", N=N, m=2, r=3, batch=2, C=C, K=37,
