@@ -3,13 +3,15 @@
  * F(m^N, r^N) for 2-D and 3-D ConvNet layers on AMD MI355X (gfx950).
  *
  * Method: Budden et al., "Deep Tensor Convolution on Multicores" (arXiv
- * 1611.06565).  The layer is eq. (2) of §3.1 without bias: for every sample n,
- * kernel k and output position o,
+ * 1611.06565).  The layer is eq. (2) of §3.1: for every sample n, kernel k and
+ * output position o,
  *
- *     y[n][k][o] = f( sum_c sum_{p in [0,r)^N} w[k][c][p] * x~[n][c][o + p - pad] )
+ *     y[n][k][o] = f( b[k] + sum_c sum_{p in [0,r)^N} w[k][c][p] * x~[n][c][o + p - pad] )
  *
- * a cross-correlation (no kernel flip) with f = identity or ReLU and x~ equal
- * to x zero-extended outside [0, X).  It is computed by eq. (4),
+ * a cross-correlation (no kernel flip) with f = identity or ReLU, b = 0 unless
+ * given (wino_forward_ex) and x~ equal to x zero-extended outside [0, X).
+ * Sizes (N, m, r): F(2,3) and F(4,3) in 2-D and 3-D; F(3,2), F(5,4), F(4,5)
+ * and F(3,6) (Table 1) in 2-D.  It is computed by eq. (4),
  *
  *     S = [ (g x_n G) (.) (d x_n B^T) ] x_n A^T      over each axis n,
  *
@@ -92,7 +94,9 @@ typedef struct {
 /* Build a plan for one layer.  §3.1-§3.3 and §4.1.
  *   N      number of spatial axes: 2 or 3
  *   m, r   output-tile and kernel extent per axis; supported (m, r) pairs are
- *          (2, 3) and (4, 3) for N = 2 and 3 (alpha = 4 or 6)
+ *          (2, 3) and (4, 3) for N = 2 and 3 (alpha = 4 or 6), and (3, 2),
+ *          (5, 4), (4, 5), (3, 6) for N = 2 (alpha = 4 or 8); others give
+ *          WINO_EUNSUPPORTED
  *   C, K   input channels and kernels, each >= 1
  *   dims   [batch, X_1 .. X_N], each >= 1; the output extent per axis
  *          Y_i = X_i + 2 pad_i - r + 1 must be >= 1

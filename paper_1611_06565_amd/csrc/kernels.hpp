@@ -5,7 +5,8 @@
 //   k_input_split  the same for alpha^N = 216, split over A threads per (t, c)
 //   k_gemm_inv     M_xi = V_xi . U_xi on fp32 MFMA (eq. 5), then
 //                  y tile = M[:, t, k] x_n A^T, stitched and cropped (eq. 4);
-//                  F(4^3) (m = 2 uses k_gemm_acc in gemm_acc.hpp, F(4^2)
+//                  F(4^3) and the 2-D sizes F(3,2), F(5,4), F(4,5), F(3,6)
+//                  (m = 2 uses k_gemm_acc in gemm_acc.hpp, F(4^2)
 //                  k_gemm_acc4 in gemm_acc4.hpp)
 //   k_maxpool3d    pooling for the C3D stack (not part of the method)
 //
@@ -38,9 +39,10 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // GEMM kind, block (tiles and kernels per work-group), operand load width
 // and channel group per (N, m, r).
-//   KIND 0 (m = 2) and 1 (2-D, m = 4): pass-accumulating GEMMs (gemm_acc.hpp,
+//   KIND 0 (m = 2) and 1 (F(4^2)): pass-accumulating GEMMs (gemm_acc.hpp,
 //     gemm_acc4.hpp) on 64-tile blocks of V with channel groups of 4.
-//   KIND 2 (F(4^3) and the other 2-D sizes): k_gemm_inv, all alpha^N elements resident.  A GEMM
+//   KIND 2 (F(4^3) and the other 2-D sizes): k_gemm_inv, all alpha^N
+//     elements resident, 16-tile blocks.  A GEMM
 //     "stage" covers KSTEP * VEC channels: lane group kr of an MFMA operand
 //     loads channels VEC*kr .. VEC*kr+VEC-1 of the stage, and k-step j uses
 //     the j-th of them; the stage is KSTEP groups of VEC channels (CG = VEC),
@@ -467,7 +469,8 @@ __global__ void __launch_bounds__(384) k_input_split(const float* __restrict__ x
 }
 
 // ------------------------------------------------- batched GEMM (a4 + a5)
-// (F(4^3); m = 2 uses k_gemm_acc, F(4^2) k_gemm_acc4.)  Work-group = BLK tiles x BLK kernels x all
+// (F(4^3) and the other 2-D sizes; m = 2 uses k_gemm_acc, F(4^2)
+// k_gemm_acc4.)  Work-group = BLK tiles x BLK kernels x all
 // alpha^N elements.  The NW waves split the elements evenly in whole units of
 // the LOC trailing axes (alpha^LOC consecutive elements) and keep one BLK x
 // BLK fp32 MFMA accumulator per element for the whole channel reduction.
