@@ -151,13 +151,33 @@ __global__ void __launch_bounds__(256) k_filter(const float* __restrict__ w, flo
 // the alpha^N values to V.
 //
 // A work-group covers one GEMM tile block (BLK tiles) and 256 / (BLK * CG)
-// channel groups; lanes run over the channels of a group fastest, then tiles,
-// so each plane store of a wave is one contiguous run.  Each window row (A
-// values along the last axis) is a single wide load from a start clamped into
-// the input row, shifted and zero-masked in registers; a row whose leading
-// coordinates fall outside the input loads a clamped row and is masked to
-// zero.  A wave whose windows all lie inside the input loads the rows as they
-// are and skips the shifts and masks (a wave-uniform branch).
+// channel groups.  Each window row (A values along the last axis) is a single
+// wide load from a start clamped into the input row, shifted and zero-masked
+// in registers; a row whose leading coordinates fall outside the input loads
+// a clamped row and is masked to zero.  A wave whose windows all lie inside
+// the input loads the rows as they are and skips the shifts and masks (a
+// wave-uniform branch).
+//
+// m = 2: lanes run over the tiles fastest (a wave is 64 consecutive tiles of
+// one channel).  With pad 1 on the last axis and an even row length (rowfast)
+// a lane's window row x[2t - 1 .. 2t + 2] is its own aligned pair
+// x[2t .. 2t + 1], the last value of the previous lane's pair and the first of
+// the next lane's (DPP wave shifts); lanes 0 and 63 load the missing end.  A
+// neighbour whose tile lies in another row of tiles only supplies positions
+// outside the input, which are masked.  Other m: lanes run over the channels
+// of a group fastest, then tiles.
+//
+// Outputs go through LDS so that each lane stores 16 bytes (4 channels of a
+// tile) and a wave writes 1 KB contiguous per store.
+__device__ __forceinline__ float dpp_wave_prev(float old, float v) {
+  // lane i takes lane i-1's v (wave_shr:1); lane 0 keeps old
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), 0x138, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float dpp_wave_next(float old, float v) {
+  // lane i takes lane i+1's v (wave_shl:1); lane 63 keeps old
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), 0x130, 0xf, 0xf, false));
+}
+
 template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, float* __restrict__ V,
                                                InputArgs a, FMats fm) {
@@ -166,11 +186,13 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
   constexpr int GPW = 256 / (BLK * CG);   // channel groups per work-group
   constexpr int NROW = NXI / A;           // window rows (leading indices)
   constexpr int XCH = NXI % 16 == 0 ? 16 : 12;   // planes staged through LDS at a time
+  constexpr bool TILEFAST = MM == 2;      // lanes over tiles fastest
   static_assert(GPW * BLK * CG == 256, "work-group shape");
   static_assert(CG % 4 == 0 && NXI % XCH == 0 && XCH % 4 == 0, "store rounds of 4 planes");
+  static_assert(!TILEFAST || (BLK == 64 && A == 4), "m = 2: a wave is 64 tiles of one channel");
   const int tid = int(threadIdx.x);
-  const int cl = tid % CG;
-  const int tl = (tid / CG) % BLK;
+  const int cl = TILEFAST ? (tid / BLK) % CG : tid % CG;
+  const int tl = TILEFAST ? tid % BLK : (tid / CG) % BLK;
   const int gl = tid / (CG * BLK);
   // consecutive tile blocks of one channel group run on the same XCD, so the
   // input windows they share (neighbouring tiles overlap by r - 1) hit its L2
@@ -196,27 +218,34 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
 #pragma unroll
   for (int ax = 0; ax < N - 1; ++ax) inner = inner && o[ax] >= 0 && o[ax] + A <= a.X[ax];
   const bool plain = __all(!live || inner);
+  const float* xc = x + (int64_t(n) * a.C + min(c, a.C - 1)) * a.xstride_c;
   float d[NXI];
+  // leading coordinates of window row `row`: offset of the clamped input row
+  // and whether it lies inside the input
+  auto row_at = [&](int row, int64_t& off) {
+    int lead[2] = {0, 0};
+    int rem = row;
+#pragma unroll
+    for (int ax = N - 2; ax >= 0; --ax) {
+      lead[ax] = rem % A;
+      rem /= A;
+    }
+    off = 0;
+    bool valid = live;
+#pragma unroll
+    for (int ax = 0; ax < N - 1; ++ax) {
+      const int q = o[ax] + lead[ax];
+      valid = valid && (unsigned)q < (unsigned)a.X[ax];
+      off = off * a.X[ax] + min(max(q, 0), a.X[ax] - 1);
+    }
+    return valid;
+  };
   auto gather = [&](auto PLAIN) {
     constexpr bool P = decltype(PLAIN)::value;
-    const float* xc = x + (int64_t(n) * a.C + c) * a.xstride_c;
 #pragma unroll
     for (int row = 0; row < NROW; ++row) {
-      int lead[2] = {0, 0};
-      int rem = row;
-#pragma unroll
-      for (int ax = N - 2; ax >= 0; --ax) {
-        lead[ax] = rem % A;
-        rem /= A;
-      }
-      int64_t off = 0;
-      bool valid = true;
-#pragma unroll
-      for (int ax = 0; ax < N - 1; ++ax) {
-        const int q = o[ax] + lead[ax];
-        valid = valid && (unsigned)q < (unsigned)a.X[ax];
-        off = off * a.X[ax] + min(max(q, 0), a.X[ax] - 1);
-      }
+      int64_t off;
+      const bool valid = row_at(row, off);
       const float* xr = xc + off * XL;
       float* dr = d + row * A;
       if constexpr (P) {
@@ -242,39 +271,79 @@ __global__ void __launch_bounds__(256) k_input(const float* __restrict__ x, floa
       }
     }
   };
-  if (live) {
-    if (plain) gather(std::true_type{});
-    else gather(std::false_type{});
-  } else {
+  if constexpr (TILEFAST) {
+    if (a.rowfast) {
+      // window row (pad 1) = x[2tW - 1], x[2tW], x[2tW + 1], x[2tW + 2]
+      const int lane = tid & 63;
+      const int tW = ti[N - 1];
+      const bool own_in = 2 * tW < XL;            // the pair lies inside the row (XL even)
+      const bool prev_in = tW > 0;
+      const bool next_in = 2 * tW + 2 < XL;
+      const int wo = min(2 * tW, XL - 2);
 #pragma unroll
-    for (int i = 0; i < NXI; ++i) d[i] = 0.0f;
+      for (int row = 0; row < NROW; ++row) {
+        int64_t off;
+        const bool valid = row_at(row, off);
+        const float* xr = xc + off * XL;
+        float2 pr = *reinterpret_cast<const float2*>(xr + wo);
+        if (!(valid && own_in)) pr = make_float2(0.0f, 0.0f);
+        // the wave's two ends: lane 0's left value, lane 63's right value
+        float h = 0.0f;
+        if (lane == 0 && valid && prev_in) h = xr[2 * tW - 1];
+        if (lane == 63 && valid && next_in) h = xr[2 * tW + 2];
+        const float lv = dpp_wave_prev(h, pr.y);
+        const float rv = dpp_wave_next(h, pr.x);
+        float* dr = d + row * A;
+        dr[0] = (valid && prev_in) ? lv : 0.0f;
+        dr[1] = pr.x;
+        dr[2] = pr.y;
+        dr[3] = (valid && next_in) ? rv : 0.0f;
+      }
+    } else {
+      gather(std::false_type{});
+    }
+  } else {
+    if (live) {
+      if (plain) gather(std::true_type{});
+      else gather(std::false_type{});
+    } else {
+#pragma unroll
+      for (int i = 0; i < NXI; ++i) d[i] = 0.0f;
+    }
   }
   float v[NXI];
   transform_nd<N, A, A>(d, v, MatRef<Which::BT, CONST, MM, R>{&fm});
   // V[tb][cg][xi][tl][cl]: the work-group's NXI planes of each of its channel
   // groups are one contiguous run.  The values go through LDS XCH planes at a
-  // time so that each lane stores 16 bytes (4 channels of a tile) and a wave
-  // writes 1 KB contiguous per store.
-  __shared__ float4 stage[XCH][64];      // the work-group's 256 floats of a plane
+  // time; a plane holds the work-group's 256 values as [group][tile][channel]
+  // (TILEFAST: [group][channel][tile], so that the lanes of a wave write
+  // consecutive words).
+  __shared__ float stage[XCH][256];
   float* const gbase = V + (int64_t(tb) * a.C_pad + int64_t(cg - gl) * CG) * NXI * BLK;
   constexpr int C4 = CG / 4;              // float4s per tile row of a group
-  const int pr = tid >> 6, f = tid & 63;  // plane within a round of 4; float4 = (group, tile, quarter)
+  const int pr4 = tid >> 6, f = tid & 63; // plane within a round of 4; float4 = (group, tile, quarter)
   const int g = f / (BLK * C4), ft = (f / C4) % BLK, f4 = f % C4;
   const bool store = (cg - gl + g) * CG < a.C_pad;
+  const int widx = TILEFAST ? (gl * CG + cl) * BLK + tl : (gl * BLK + tl) * CG + cl;
 #pragma unroll
   for (int x0 = 0; x0 < NXI; x0 += XCH) {
     if (x0 > 0) __syncthreads();          // previous planes stored
 #pragma unroll
-    for (int i = 0; i < XCH; ++i) reinterpret_cast<float*>(stage[i])[(gl * BLK + tl) * CG + cl] = v[x0 + i];
+    for (int i = 0; i < XCH; ++i) stage[i][widx] = v[x0 + i];
     __syncthreads();
     if (store) {
 #pragma unroll
       for (int i = 0; i < XCH; i += 4) {
         // non-temporal: V streams to HBM without evicting the input windows
         // that neighbouring work-groups still read from L2
-        // stage plane layout [group][tile][channel]: one float4 = 4 channels of a tile
-        const float4 val = reinterpret_cast<const float4*>(stage[i + pr])[((g * BLK + ft) * CG) / 4 + f4];
-        float* p = gbase + (int64_t(g) * NXI + x0 + i + pr) * (BLK * CG) + ft * CG + f4 * 4;
+        float4 val;
+        if constexpr (TILEFAST) {
+          const float* sp = stage[i + pr4] + (g * CG + f4 * 4) * BLK + ft;
+          val = make_float4(sp[0], sp[BLK], sp[2 * BLK], sp[3 * BLK]);
+        } else {
+          val = reinterpret_cast<const float4*>(stage[i + pr4])[((g * BLK + ft) * CG) / 4 + f4];
+        }
+        float* p = gbase + (int64_t(g) * NXI + x0 + i + pr4) * (BLK * CG) + ft * CG + f4 * 4;
         __builtin_nontemporal_store(val.x, p + 0);
         __builtin_nontemporal_store(val.y, p + 1);
         __builtin_nontemporal_store(val.z, p + 2);

@@ -149,6 +149,9 @@ struct Launch {
       constexpr int GPW = 256 / (BLK * CG);
       const int64_t nb = (p.T_pad / BLK) * ((groups + GPW - 1) / GPW);
       a.nblocks = int32_t(nb);
+      // m = 2: aligned pairs plus neighbouring lanes when the last axis has
+      // pad 1 and an even length (x is 16-byte aligned: the entry points check it)
+      a.rowfast = (MM == 2 && p.pad[N - 1] == 1 && p.X[N - 1] % 2 == 0) ? 1 : 0;
       hipLaunchKernelGGL((k_input<N, MM, R, CONST>), dim3(unsigned(nb)), dim3(256), 0, s, x, V, a, p.fm);
     }
     return launch_status();
