@@ -43,10 +43,9 @@ def kernel_hash():
     return h.hexdigest()[:16]
 
 
-def read_traffic(expected_hash, config):
-    """HBM bytes per launch of the GEMM kernel from the committed counter
-    summary (profiles/*_traffic.txt) taken on this workload with these kernel
-    sources, or None if there is none."""
+def read_counters(expected_hash, config):
+    """The GEMM kernel's counter summary (profiles/*_traffic.txt) taken on this
+    workload with these kernel sources, as a dict, or {} if there is none."""
     for path in sorted(glob.glob(os.path.join(PROFILE_DIR, "*_traffic.txt"))):
         vals = {}
         with open(path) as f:
@@ -54,13 +53,19 @@ def read_traffic(expected_hash, config):
                 m = re.match(r"\s*(\w+)\s*[:=]\s*(\S+)", line)
                 if m:
                     vals[m.group(1)] = m.group(2)
-        if vals.get("kernel_sources_sha256_16") != expected_hash or vals.get("config") != str(config):
-            continue
-        try:
-            return float(vals["traffic_bytes_per_launch"])
-        except (KeyError, ValueError):
-            continue
-    return None
+        if vals.get("kernel_sources_sha256_16") == expected_hash and vals.get("config") == str(config):
+            return vals
+    return {}
+
+
+def read_traffic(expected_hash, config):
+    """HBM bytes per launch of the GEMM kernel from the committed counter
+    summary, or None if absent, taken on another workload or on different
+    kernel sources."""
+    try:
+        return float(read_counters(expected_hash, config)["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(spec, x, w, budget_s=10.0):
@@ -273,7 +278,12 @@ def main():
         achieved = gemm_bytes / (gemm_ms * 1e-3) / 1e9
     else:
         achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
+    counters = read_counters(kernel_hash(), args.config)
     traffic = read_traffic(kernel_hash(), args.config)
+    try:
+        mfma_counted = float(counters["mfma_flops_per_launch"])
+    except (KeyError, ValueError):
+        mfma_counted = None
 
     check = None
     if not args.no_check:
@@ -313,6 +323,8 @@ def main():
         "roofline": {
             "kernel": ("k_gemm_acc (batched fp32-MFMA GEMM, inverse transform accumulated per pass)"
                        if spec.m == 2 else
+                       "k_gemm_acc4 (batched fp32-MFMA GEMM, inverse transform accumulated per pass)"
+                       if (spec.N, spec.m, spec.r) == (2, 4, 3) else
                        "k_gemm_inv (batched fp32-MFMA GEMM + fused inverse transform)"),
             "bound": "hbm" if hbm_bound else "mfma",
             "achieved": achieved,
@@ -323,6 +335,11 @@ def main():
             "algorithmic": ("4*(alpha^N*T*C + alpha^N*C*K + n*K*prod(Y)) = %.4g bytes per launch" % gemm_bytes
                             if hbm_bound else "2*alpha^N*T*C*K = %.4g FLOP per launch" % gemm_flops),
             "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,
+            # MFMA work counted by rocprofv3 (SQ_INSTS_VALU_MFMA_MOPS_F32 x 512)
+            # on these kernel sources, and the MFMA fraction it gives here
+            "mfma_flops_counted": mfma_counted,
+            "mfma_frac_counted": (mfma_counted / (gemm_ms * 1e-3) / 1e12 / PEAK_FP32_MFMA
+                                  if mfma_counted is not None else None),
         },
         "stages_ms": {"filter_transform": filt_ms, "input_transform": inp_ms,
                       "gemm_inverse": gemm_ms},
