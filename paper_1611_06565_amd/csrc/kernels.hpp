@@ -118,7 +118,7 @@ __device__ __forceinline__ int xcd_remap(int b, int nb) {
 // One thread per (channel, kernel); lanes run over the channel group fastest
 // so each plane store is contiguous.
 template <int N, int MM, int R, bool CONST>
-__global__ void __launch_bounds__(256) k_filter(const float* __restrict__ w, float* __restrict__ U,
+__global__ void __launch_bounds__(64) k_filter(const float* __restrict__ w, float* __restrict__ U,
                                                 FilterArgs a, FMats fm) {
   using B = Blocking<N, MM, R>;
   constexpr int A = B::A, NXI = B::NXI, CG = B::CGU;

@@ -116,8 +116,10 @@ struct Launch {
     a.uplane = int64_t(p.C_pad) * p.K_pad;
     a.C = p.C; a.K = p.K; a.C_pad = p.C_pad; a.K_pad = p.K_pad;
     const int64_t n = int64_t(p.C_pad) * p.K_pad;   // C_pad is a multiple of CGU
-    const unsigned grid = unsigned((n + 255) / 256);
-    hipLaunchKernelGGL((k_filter<N, MM, R, CONST>), dim3(grid), dim3(256), 0, s, w, U, a, p.fm);
+    // one thread per (channel, kernel): small work-groups spread the few
+    // threads of a layer (8192 for C = 64, K = 128) over more CUs
+    const unsigned grid = unsigned((n + 63) / 64);
+    hipLaunchKernelGGL((k_filter<N, MM, R, CONST>), dim3(grid), dim3(64), 0, s, w, U, a, p.fm);
     return launch_status();
   }
 
