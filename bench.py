@@ -184,14 +184,80 @@ def bench_fig4(args):
     print(json.dumps(out), flush=True)
 
 
+def bench_stack(args):
+    """The C3D-style stack (eight 3x3x3 pad-1 layers with fused ReLU, max-pools
+    between them) forward with the transformed kernels cached: effective
+    TFLOP/s over the direct FLOPs of all layers."""
+    import numpy as np
+    import torch
+
+    from paper_1611_06565_amd.wino import Plan, maxpool3d
+    from workloads import C3D_STACK, direct_flops, draw_stack
+
+    x, ws = draw_stack(C3D_STACK, seed=5 if args.seed is None else args.seed)
+    x0 = torch.from_numpy(x).cuda()
+    layers = []
+    for (spec, pool), w in zip(C3D_STACK.layers(), ws):
+        plan = Plan(3, spec.m, 3, spec.C, spec.K, [spec.batch] + list(spec.X), pad=1, relu=True)
+        U = plan.transform_filter(torch.from_numpy(w).cuda())
+        wsp = plan.new_workspace()
+        y = plan.new_output()
+        py = None
+        if pool is not None:
+            Y = spec.out_spatial
+            py = torch.empty((spec.batch, spec.K) + tuple(yy // p for yy, p in zip(Y, pool.window)),
+                             dtype=torch.float32, device="cuda")
+        layers.append((spec, pool, plan, U, wsp, y, py))
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        cur = x0
+        for i, (spec, pool, plan, U, wsp, y, py) in enumerate(layers):
+            if ev is not None:
+                ev[i].record()
+            plan.forward(cur, U, y=y, workspace=wsp)
+            cur = y
+            if pool is not None:
+                maxpool3d(y, pool.window, py)
+                cur = py
+        if ev is not None:
+            ev[len(layers)].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    nev = len(layers) + 1
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    st = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(nev - 1)] for e in evs]).mean(axis=0)
+    flops = [direct_flops(spec) for spec, *_ in layers]
+    out = {
+        "metric": "effective TFLOP/s of the C3D-style 3-D stack forward (direct FLOPs; kernels transformed once)",
+        "value": sum(flops) / (ms_step * 1e-3) / 1e12, "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "C3D-style stack: batch 4, 3x16x112x112, eight 3x3x3 pad-1 layers "
+                               "(64, 128, 256, 256, 512 x4), ReLU, max-pools; F(2^3,3^3)"},
+        "layers": [{"name": spec.name, "C": spec.C, "K": spec.K, "X": list(spec.X), "pool": bool(pool),
+                    "ms": float(st[i]), "tflops": flops[i] / (float(st[i]) * 1e-3) / 1e12}
+                   for i, (spec, pool, *_) in enumerate(layers)],
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--seed", type=int, default=None)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4],
-                    help="layer family (default 2, the F(2^3,3^3) C=64 K=128 video layer)")
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5],
+                    help="layer family (default 2, the F(2^3,3^3) C=64 K=128 video layer; "
+                         "5 = the C3D-style stack)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
@@ -215,6 +281,9 @@ def main():
         return
     if args.fig4:
         bench_fig4(args)
+        return
+    if args.config == 5:
+        bench_stack(args)
         return
 
     from paper_1611_06565_amd.wino import Plan

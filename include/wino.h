@@ -59,6 +59,10 @@ typedef struct wino_plan_s wino_plan_t; /* opaque, immutable after creation */
 /* Apply max(0, .) to every output in the output-transform epilogue
  * (the activation f of eq. 2). */
 #define WINO_RELU 1u
+/* Never split the channel-element passes of a product block over several
+ * work-groups (no partials scratch in the workspace; see
+ * wino_workspace_bytes). */
+#define WINO_NO_SPLIT 2u
 
 typedef struct {
   /* Symmetric zero padding per spatial axis, outer to inner.  0 is the
@@ -71,7 +75,7 @@ typedef struct {
    * from these points is the only input of transform synthesis. */
   const double* points;
   int32_t n_points;
-  uint32_t flags; /* WINO_RELU or 0 */
+  uint32_t flags; /* WINO_RELU | WINO_NO_SPLIT, or 0 */
 } wino_opts;
 
 /* Plan summary (host-side numbers only). */
@@ -89,6 +93,7 @@ typedef struct {
   int32_t default_points;/* 1 when the transform constants are compiled in        */
   int32_t channel_group; /* CG: channels interleaved innermost in V                 */
   int32_t filter_channel_group; /* CGU: channels interleaved innermost in U        */
+  int32_t gemm_parts;    /* work-groups each product block's passes are split over */
 } wino_plan_desc;
 
 /* Build a plan for one layer.  §3.1-§3.3 and §4.1.
@@ -118,10 +123,17 @@ wino_status wino_plan_describe(const wino_plan_t* plan, wino_plan_desc* desc);
  * Padding channels and kernels are zero. */
 size_t wino_filter_bytes(const wino_plan_t* plan);
 
-/* Bytes of workspace wino_forward needs: the transformed input V (float32),
- * laid out tile-block major as V[T_pad/B][C_pad/CG][alpha^N][B][CG] with
- * B = block_tiles: element (xi, c, t) sits at
- * (((t/B)*C_pad/CG + c/CG)*alpha^N + xi)*B*CG + (t%B)*CG + c%CG. */
+/* Bytes of workspace wino_forward needs.  It starts with the transformed
+ * input V (float32), laid out tile-block major as
+ * V[T_pad/B][C_pad/CG][alpha^N][B][CG] with B = block_tiles: element
+ * (xi, c, t) sits at (((t/B)*C_pad/CG + c/CG)*alpha^N + xi)*B*CG + (t%B)*CG
+ * + c%CG.  For F(2^N, 3^N) layers whose product has at most half as many
+ * 64 x 64 blocks as the device current at wino_plan has compute units, the
+ * product's element passes are split over up to 32 work-groups per block,
+ * and a scratch area for their partial outputs follows V (at V's size rounded
+ * up to 256 bytes); wino_gemm_inverse overwrites it.  The split is fixed when
+ * the plan is made and the partials are summed in a fixed order, so a plan's
+ * results are bitwise reproducible. */
 size_t wino_workspace_bytes(const wino_plan_t* plan);
 
 /* Bytes of workspace wino_forward needs (today equal to wino_workspace_bytes). */
@@ -150,10 +162,10 @@ wino_status wino_transform_input(const wino_plan_t* plan, const float* x, void* 
 
 /* Batched product M_xi = V_xi . U_xi over all xi (eq. 5) with the inverse
  * transform S = M x_n A^T, tile stitching, cropping and the optional ReLU
- * fused into its epilogue (eq. 4).  Reads the workspace written by
- * wino_transform_input.
+ * fused into its epilogue (eq. 4).  Reads the V part of the workspace written
+ * by wino_transform_input (and may overwrite the scratch area after it).
  *   y  device, [batch][K][Y_1..Y_N] float32, fully overwritten */
-wino_status wino_gemm_inverse(const wino_plan_t* plan, const void* workspace, size_t workspace_bytes,
+wino_status wino_gemm_inverse(const wino_plan_t* plan, void* workspace, size_t workspace_bytes,
                               const float* U, float* y, void* stream);
 
 /* The whole forward (eq. 4 with eq. 5) on one stream: wino_transform_input
@@ -167,7 +179,7 @@ wino_status wino_forward(const wino_plan_t* plan, const float* x, const float* U
  *   bias  device, [K] float32, 4-byte aligned, read only; NULL = no bias
  *         (then identical to the calls above).
  * Errors as for the calls above; a misaligned bias is WINO_EINVAL. */
-wino_status wino_gemm_inverse_ex(const wino_plan_t* plan, const void* workspace, size_t workspace_bytes,
+wino_status wino_gemm_inverse_ex(const wino_plan_t* plan, void* workspace, size_t workspace_bytes,
                                  const float* U, const float* bias, float* y, void* stream);
 wino_status wino_forward_ex(const wino_plan_t* plan, const float* x, const float* U, const float* bias,
                             float* y, void* workspace, size_t workspace_bytes, void* stream);

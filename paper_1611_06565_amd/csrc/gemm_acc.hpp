@@ -46,6 +46,12 @@ struct AccArgs {
   int32_t relu;
   const float* bias;  // [K] or null: b_k of eq. (2), added before the ReLU (by the
                       // first half of a split block only, so it is added once)
+  // Pass-split mode for grids much smaller than the resident slots (nparts >
+  // 1): unit u of the per-XCD ranges is part u % nparts of block u / nparts,
+  // a contiguous 1/nparts of the passes, and its partial outputs go to
+  // part[u][o][t][k] (64 x 64 per output index); k_part_reduce sums them.
+  float* part;
+  int32_t nparts;
 };
 
 template <int N, int MM, int R>
@@ -195,9 +201,12 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
   if (j >= xn + xs) return;
   const int nwhole = xn - xs;
   const bool split = j >= nwhole;
-  const int blk = g.xb0[xcd] + (split ? nwhole + (j - nwhole) / 2 : j);
-  const int p0 = split ? ((j - nwhole) & 1) * (G::NPASS / 2) : 0;
-  const int npass = split ? G::NPASS / 2 : G::NPASS;
+  const bool parts = g.nparts > 1;                // pass-split mode (then xs = 0)
+  const int unit = g.xb0[xcd] + (split ? nwhole + (j - nwhole) / 2 : j);
+  const int blk = parts ? unit / g.nparts : unit;
+  const int prt = parts ? unit % g.nparts : 0;
+  const int p0 = parts ? prt * (G::NPASS / g.nparts) : split ? ((j - nwhole) & 1) * (G::NPASS / 2) : 0;
+  const int npass = parts ? G::NPASS / g.nparts : split ? G::NPASS / 2 : G::NPASS;
   static_assert(G::NPASS % 2 == 0, "halves of whole passes");
   const int tb = blk / g.nkb, kb = blk % g.nkb;
   const int nstage = g.C_pad / G::SC;             // channel stages per pass
@@ -397,6 +406,20 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
     if (finish()) break;
   }
 
+  if (parts) {
+    // partial outputs of this unit: part[unit][o][t][k], lanes over k
+    __builtin_amdgcn_s_waitcnt(0x0f70);           // vmcnt(0): no copy still writes LDS
+    float* pp = g.part + int64_t(unit) * NOUT * (TB * KB);
+#pragma unroll
+    for (int o = 0; o < NOUT; ++o)
+#pragma unroll
+      for (int r = 0; r < S::NACC; ++r) {
+        const int tt = tq * 32 + S::acc_row(lane, r), k = kq * 32 + col;
+        pp[(o * TB + tt) * KB + k] = yacc[o][r];
+      }
+    return;
+  }
+
   // ---- stitch: outputs through LDS so that neighbouring lanes store
   // neighbouring outputs of a row, PPR output planes per round.  Plane o
   // ([k][t], t XOR-swizzled by k) of a round lives in buffer o % PPR.
@@ -459,6 +482,45 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
         }
       }
     }
+  }
+}
+
+// Pass-split mode: y = ReLU(sum over the parts, in part order + bias) for
+// every output of every block.  One thread per (block, tile, kernel); lanes
+// over kernels read the partials contiguously.  The fixed order keeps the
+// results bitwise reproducible.
+template <int N, int MM>
+__global__ void __launch_bounds__(256) k_part_reduce(float* __restrict__ y, AccArgs g, int32_t nblk) {
+  constexpr int NOUT = ipow(MM, N), TB = 64, KB = 64;
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;   // (block, tile, kernel)
+  const int k_l = int(i % KB), tl = int((i / KB) % TB);
+  const int blk = int(i / (KB * TB));
+  if (blk >= nblk) return;
+  const int tb = blk / g.nkb, kb = blk % g.nkb;
+  const int t = tb * TB + tl, kg = kb * KB + k_l;
+  if (t >= g.T || kg >= g.K) return;
+  int ti[3] = {0, 0, 0};
+  const int n = split_tile<N>(t, g.tiles, ti);
+  const float b = g.bias != nullptr ? g.bias[kg] : 0.0f;
+  const float* pp = g.part + int64_t(blk) * g.nparts * NOUT * (TB * KB) + tl * KB + k_l;
+  float* yk = y + (int64_t(n) * g.K + kg) * g.ystride_k;
+#pragma unroll
+  for (int o = 0; o < NOUT; ++o) {
+    int64_t off = 0;
+    bool in = true;
+#pragma unroll
+    for (int ax = 0; ax < N; ++ax) {
+      const int oa = (o / ipow(MM, N - 1 - ax)) % MM;
+      const int yc = ti[ax] * MM + oa;
+      in = in && yc < g.Y[ax];
+      off = off * g.Y[ax] + yc;
+    }
+    if (!in) continue;
+    float v = 0.0f;
+    for (int q = 0; q < g.nparts; ++q) v += pp[(int64_t(q) * NOUT + o) * (TB * KB)];
+    if (g.bias != nullptr) v += b;
+    if (g.relu) v = v > 0.0f ? v : 0.0f;
+    yk[off] = v;
   }
 }
 

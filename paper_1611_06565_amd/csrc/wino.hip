@@ -23,6 +23,9 @@ struct wino_plan_s {
   int32_t pad[3];
   int64_t T, T_pad;
   int blk, kblk, cg, cgu;
+  int nparts;             // k_gemm_acc pass-split parts (1: none)
+  int64_t v_floats;       // V in the workspace (rounded up to 256 bytes)
+  int64_t part_floats;    // partial outputs after V when nparts > 1
   uint32_t flags;
   bool const_mats;
   double AT[kMaxAlpha][kMaxAlpha], BT[kMaxAlpha][kMaxAlpha], G[kMaxAlpha][kMaxAlpha];
@@ -166,17 +169,19 @@ struct Launch {
   // round is half as long.  Not with a fused ReLU, which needs the whole sum.
   // Returns the grid size; zeroes the outputs of split blocks first.
   template <int TB, int KB>
-  static int64_t acc_setup(const wino_plan_s& p, AccArgs& a, const float* bias, float* y, hipStream_t s) {
+  static int64_t acc_setup(const wino_plan_s& p, AccArgs& a, const float* bias, float* y, hipStream_t s,
+                           int parts = 1) {
     a.vblock = int64_t(p.nxi) * p.C_pad * TB;
     a.uplane = int64_t(p.C_pad) * p.K_pad;
     a.ystride_k = 1;
     for (int i = 0; i < N; ++i) a.ystride_k *= p.Y[i];
     a.T = int32_t(p.T); a.C_pad = p.C_pad; a.K = p.K; a.K_pad = p.K_pad;
     a.nkb = p.K_pad / KB;
-    const int64_t nb = (p.T_pad / TB) * int64_t(a.nkb);
+    const int64_t nb = (p.T_pad / TB) * int64_t(a.nkb) * parts;   // work units
     for (int i = 0; i < 3; ++i) { a.tiles[i] = int32_t(p.tiles[i]); a.Y[i] = int32_t(p.Y[i]); }
     a.relu = (p.flags & WINO_RELU) ? 1 : 0;
     a.bias = bias;
+    a.nparts = parts;
     constexpr int NX = 8;
     const int64_t slots = 2 * int64_t(cu_count() / NX);
     int64_t maxu = 0, nsplit = 0;
@@ -184,7 +189,7 @@ struct Launch {
       const int64_t n = nb / NX + (x < nb % NX ? 1 : 0);
       const int64_t b0 = x * (nb / NX) + (x < nb % NX ? x : nb % NX);
       int64_t sx = 0;
-      if (!a.relu && slots > 0) sx = n < slots ? n : n % slots;
+      if (!a.relu && parts == 1 && slots > 0) sx = n < slots ? n : n % slots;
       a.xb0[x] = int32_t(b0); a.xn[x] = int32_t(n); a.xs[x] = int32_t(sx);
       maxu = maxu > n + sx ? maxu : n + sx;
       nsplit += sx;
@@ -196,15 +201,24 @@ struct Launch {
     return NX * maxu;
   }
 
-  static wino_status gemm(const wino_plan_s& p, const float* V, const float* U, const float* bias, float* y,
-                          hipStream_t s) {
+  static wino_status gemm(const wino_plan_s& p, const float* V, float* part, const float* U, const float* bias,
+                          float* y, hipStream_t s) {
     constexpr int KIND = Blocking<N, MM, R>::KIND;
     if constexpr (KIND == 0) {
       using G = AccGeom<N, MM, R>;
       AccArgs a{};
-      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, bias, y, s);
+      // small grids: each block's passes split over p.nparts units, whose
+      // partial outputs (after V in the workspace) are summed in order
+      a.part = part;
+      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, bias, y, s, p.nparts);
       hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST>), dim3(unsigned(grid)), dim3(G::NT), 0, s, V, U, y, a,
                          p.fm);
+      if (p.nparts > 1) {
+        const int64_t nblk = (p.T_pad / G::TB) * (p.K_pad / G::KB);
+        const int64_t items = nblk * G::TB * G::KB;
+        hipLaunchKernelGGL((k_part_reduce<N, MM>), dim3(unsigned((items + 255) / 256)), dim3(256), 0, s, y, a,
+                           int32_t(nblk));
+      }
       return launch_status();
     } else if constexpr (KIND == 1) {
       using G = Acc4Geom<N, MM, R>;
@@ -280,7 +294,7 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   if (!supported(N, m, r)) return WINO_EUNSUPPORTED;
   wino_opts o{};
   if (opts) o = *opts;
-  if (o.flags & ~WINO_RELU) return WINO_EINVAL;
+  if (o.flags & ~(WINO_RELU | WINO_NO_SPLIT)) return WINO_EINVAL;
   const int alpha = m + r - 1;
 
   wino_plan_s p{};
@@ -318,6 +332,25 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   p.nxi = 1;
   for (int i = 0; i < N; ++i) p.nxi *= alpha;
   if ((p.T_pad / p.blk) * (p.K_pad / p.blk) > kMaxI32) return WINO_EINVAL;   // GEMM grid
+  // workspace: V, then (k_gemm_acc with fewer blocks than a quarter of the
+  // resident work-group slots of the current device) the pass-split partials
+  p.v_floats = round_up(int64_t(p.nxi) * p.C_pad * p.T_pad, 64);
+  p.nparts = 1;
+  p.part_floats = 0;
+  if (m == 2 && !(o.flags & WINO_NO_SPLIT)) {
+    const int64_t nb = (p.T_pad / 64) * (p.K_pad / 64);
+    const int64_t slots = 2 * int64_t(cu_count());
+    const int npass = p.nxi / 2;
+    int np = 1;
+    if (slots > 0 && nb * 4 <= slots)
+      while (np * 2 <= npass && nb * np * 2 <= slots) np *= 2;
+    if (np > 1) {
+      int nout = 1;
+      for (int i = 0; i < N; ++i) nout *= m;
+      p.nparts = np;
+      p.part_floats = nb * np * nout * 64 * 64;
+    }
+  }
   if ((p.T_pad / p.blk) * (p.C_pad / p.cg) > kMaxI32) return WINO_EINVAL;     // input grid
 
   // Transform synthesis (a1): exact rationals, one rounding per entry.
@@ -371,6 +404,7 @@ wino_status wino_plan_describe(const wino_plan_t* p, wino_plan_desc* d) {
   d->block_kernels = p->K_pad > 0 ? p->kblk : 0;
   d->channel_group = p->cg;
   d->filter_channel_group = p->cgu;
+  d->gemm_parts = p->nparts;
   d->default_points = p->const_mats ? 1 : 0;
   return WINO_OK;
 }
@@ -380,7 +414,7 @@ size_t wino_filter_bytes(const wino_plan_t* p) {
 }
 
 size_t wino_workspace_bytes(const wino_plan_t* p) {
-  return p ? size_t(p->nxi) * size_t(p->C_pad) * size_t(p->T_pad) * sizeof(float) : 0;
+  return p ? size_t(p->v_floats + p->part_floats) * sizeof(float) : 0;
 }
 
 size_t wino_forward_workspace_bytes(const wino_plan_t* p) { return wino_workspace_bytes(p); }
@@ -419,7 +453,7 @@ wino_status wino_transform_input(const wino_plan_t* p, const float* x, void* ws,
   return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::input(*p, x, V, s); });
 }
 
-wino_status wino_gemm_inverse_ex(const wino_plan_t* p, const void* ws, size_t ws_bytes, const float* U,
+wino_status wino_gemm_inverse_ex(const wino_plan_t* p, void* ws, size_t ws_bytes, const float* U,
                                  const float* bias, float* y, void* stream) {
   if (p == nullptr || ws == nullptr || U == nullptr || y == nullptr) return WINO_EINVAL;
   if (!aligned16(ws) || !aligned16(U) || !aligned16(y)) return WINO_EINVAL;
@@ -427,10 +461,11 @@ wino_status wino_gemm_inverse_ex(const wino_plan_t* p, const void* ws, size_t ws
   if (ws_bytes < wino_workspace_bytes(p)) return WINO_EWORKSPACE;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const float* V = static_cast<const float*>(ws);
-  return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::gemm(*p, V, U, bias, y, s); });
+  float* part = p->nparts > 1 ? static_cast<float*>(ws) + p->v_floats : nullptr;
+  return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::gemm(*p, V, part, U, bias, y, s); });
 }
 
-wino_status wino_gemm_inverse(const wino_plan_t* p, const void* ws, size_t ws_bytes, const float* U,
+wino_status wino_gemm_inverse(const wino_plan_t* p, void* ws, size_t ws_bytes, const float* U,
                               float* y, void* stream) {
   return wino_gemm_inverse_ex(p, ws, ws_bytes, U, nullptr, y, stream);
 }

@@ -18,6 +18,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 HEADER = os.path.join(os.path.dirname(HERE), "include", "wino.h")
 
 WINO_RELU = 1
+WINO_NO_SPLIT = 2
 _STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported (N, m, r)",
            -3: "workspace too small", -4: "device launch failed"}
 
@@ -43,7 +44,7 @@ class _Desc(ctypes.Structure):
                 ("T", ctypes.c_int64), ("T_pad", ctypes.c_int64),
                 ("block_tiles", ctypes.c_int32), ("block_kernels", ctypes.c_int32),
                 ("default_points", ctypes.c_int32), ("channel_group", ctypes.c_int32),
-                ("filter_channel_group", ctypes.c_int32)]
+                ("filter_channel_group", ctypes.c_int32), ("gemm_parts", ctypes.c_int32)]
 
 
 _LIB = None
@@ -129,9 +130,12 @@ def _point(p):
 
 
 class Plan:
-    """One planned layer: Plan(N, m, r, C, K, dims=[batch, X_1..X_N], pad, points, relu)."""
+    """One planned layer: Plan(N, m, r, C, K, dims=[batch, X_1..X_N], pad, points, relu, split).
 
-    def __init__(self, N, m, r, C, K, dims, pad=0, points=None, relu=False):
+    split=False sets WINO_NO_SPLIT: no product block is split over several
+    work-groups, whatever the grid size."""
+
+    def __init__(self, N, m, r, C, K, dims, pad=0, points=None, relu=False, split=True):
         L = lib()
         dims = [int(d) for d in dims]
         if len(dims) != N + 1:
@@ -145,7 +149,7 @@ class Plan:
             self._pts = (ctypes.c_double * len(points))(*[_point(p) for p in points])
             opts.points = ctypes.cast(self._pts, ctypes.POINTER(ctypes.c_double))
             opts.n_points = len(points)
-        opts.flags = WINO_RELU if relu else 0
+        opts.flags = (WINO_RELU if relu else 0) | (0 if split else WINO_NO_SPLIT)
         arr = (ctypes.c_int64 * len(dims))(*dims)
         h = ctypes.c_void_p()
         _check(L.wino_plan(N, m, r, C, K, arr, ctypes.byref(opts), ctypes.byref(h)), "wino_plan")

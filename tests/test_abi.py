@@ -72,7 +72,8 @@ def test_plan_validation(L):
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1]) == -1      # count
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1, math.nan]) == -1
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1, math.pi]) == -1
-    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=2) == -1
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=4) == -1
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=3) == 0
     h = ctypes.c_void_p()
     assert L.wino_plan(3, 2, 3, 4, 4, None, None, ctypes.byref(h)) == -1
 
@@ -84,6 +85,7 @@ def test_sizes_and_dims():
     assert d["n_xi"] == 64 and d["alpha"] == 4
     assert p.filter_bytes == 4 * 64 * d["C_pad"] * d["K_pad"]
     assert p.workspace_bytes == 4 * 64 * d["C_pad"] * d["T_pad"]
+    assert d["gemm_parts"] == 1          # 3136 product blocks: no pass split
     assert p.output_shape == (8, 128, 16, 56, 56)
     q = wino.Plan(2, 4, 3, 3, 5, [2, 9, 10], pad=0)
     assert q.output_shape == (2, 5, 7, 8)

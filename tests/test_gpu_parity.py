@@ -117,25 +117,75 @@ def test_f54_layers_full_output(spec):
     check_full(spec, y, x, w)
 
 
+# F(2^N, 3^N) layers with few product blocks and many channels and kernels
+# (the late layers of a 3-D stack): each block's element passes are split over
+# up to 32 work-groups whose partial outputs are summed in order afterwards
+PARTS = [
+    LayerSpec("f2x3_3d_parts_c512", N=3, m=2, r=3, batch=2, C=512, K=192, X=(2, 7, 7), pad=1,
+              x_dist="relu_normal", w_dist="he", relu=True),
+    LayerSpec("f2x3_3d_parts_ragged", N=3, m=2, r=3, batch=4, C=250, K=150, X=(4, 14, 13), pad=1,
+              x_dist="normal", w_dist="he"),
+    LayerSpec("f2x3_2d_parts", N=2, m=2, r=3, batch=1, C=300, K=130, X=(15, 14), pad=1,
+              x_dist="uniform", w_dist="he"),
+]
+
+
+@pytest.mark.parametrize("spec", PARTS, ids=lambda s: s.name)
+def test_pass_split_layers_full_output(spec):
+    x, w = draw_layer(spec, seed=23)
+    b = (np.random.default_rng(6).standard_normal(spec.K) * 0.3).astype(np.float32)
+    y, plan = run_layer(spec, x, w, bias=b, guard=1024)
+    assert plan.desc["gemm_parts"] > 1, plan.desc
+    check_full(spec, y, x, w, bias=b)
+    # the same layer with every block in one work-group
+    y1, plan1 = run_layer(spec, x, w, bias=b, guard=1024, split=False)
+    assert plan1.desc["gemm_parts"] == 1
+    check_full(spec, y1, x, w, bias=b)
+
+
+def test_pass_split_determinism_bitwise():
+    spec = PARTS[1]
+    x, w = draw_layer(spec, seed=3)
+    b = np.linspace(-1, 1, spec.K).astype(np.float32)
+    y1, _ = run_layer(spec, x, w, bias=b)
+    y2, _ = run_layer(spec, x, w, bias=b)
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+
+
+# the small F(2^N, 3^N) layers above take the pass split; here every block is
+# one work-group again: whole blocks, and halves of the last blocks (no ReLU)
+M2_WHOLE = [s for s in SMALL + OVERLAP + EDGE if s.m == 2]
+
+
+@pytest.mark.parametrize("spec", M2_WHOLE, ids=lambda s: s.name)
+def test_small_m2_layers_no_split(spec):
+    x, w = draw_layer(spec, seed=11)
+    y, plan = run_layer(spec, x, w, guard=1024, split=False)
+    assert plan.desc["gemm_parts"] == 1
+    check_full(spec, y, x, w)
+
+
 # eq. (2)'s bias: every GEMM kernel, split-tail blocks (small layers split every
 # block into halves; the bias joins one half) and whole blocks (ReLU layers)
 BIAS = [SMALL[1], SMALL[5], SMALL[2], SMALL[7], SMALL[3], SMALL[6], F54[0]]
 
 
+@pytest.mark.parametrize("split", [True, False], ids=["split", "nosplit"])
 @pytest.mark.parametrize("spec", BIAS, ids=lambda s: s.name)
-def test_bias(spec):
+def test_bias(spec, split):
     x, w = draw_layer(spec, seed=13)
     b = (np.random.default_rng(4).standard_normal(spec.K) * 0.5).astype(np.float32)
-    y, _ = run_layer(spec, x, w, bias=b, guard=256)
+    y, _ = run_layer(spec, x, w, bias=b, guard=256, split=split)
     check_full(spec, y, x, w, bias=b)
 
 
 def test_bias_determinism_bitwise():
+    # halves of split-tail blocks added onto zeroed outputs
     spec = SMALL[1]
     x, w = draw_layer(spec, seed=2)
     b = np.linspace(-1, 1, spec.K).astype(np.float32)
-    y1, _ = run_layer(spec, x, w, bias=b)
-    y2, _ = run_layer(spec, x, w, bias=b)
+    y1, _ = run_layer(spec, x, w, bias=b, split=False)
+    y2, _ = run_layer(spec, x, w, bias=b, split=False)
     assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
 
 
