@@ -93,7 +93,8 @@ typedef struct {
   int32_t default_points;/* 1 when the transform constants are compiled in        */
   int32_t channel_group; /* CG: channels interleaved innermost in V                 */
   int32_t filter_channel_group; /* CGU: channels interleaved innermost in U        */
-  int32_t gemm_parts;    /* work-groups each product block's passes are split over */
+  int32_t gemm_parts;    /* parts each tail block of the product is split into   */
+  int64_t gemm_tail_blocks; /* product blocks split into gemm_parts parts         */
 } wino_plan_desc;
 
 /* Build a plan for one layer.  §3.1-§3.3 and §4.1.
@@ -127,13 +128,13 @@ size_t wino_filter_bytes(const wino_plan_t* plan);
  * input V (float32), laid out tile-block major as
  * V[T_pad/B][C_pad/CG][alpha^N][B][CG] with B = block_tiles: element
  * (xi, c, t) sits at (((t/B)*C_pad/CG + c/CG)*alpha^N + xi)*B*CG + (t%B)*CG
- * + c%CG.  For F(2^N, 3^N) layers whose product has at most half as many
- * 64 x 64 blocks as the device current at wino_plan has compute units, the
- * product's element passes are split over up to 32 work-groups per block,
- * and a scratch area for their partial outputs follows V (at V's size rounded
- * up to 256 bytes); wino_gemm_inverse overwrites it.  The split is fixed when
- * the plan is made and the partials are summed in a fixed order, so a plan's
- * results are bitwise reproducible. */
+ * + c%CG.  For F(2^N, 3^N) the product's 64 x 64 blocks that would run in a
+ * last, partly filled round of resident work-groups on the device current at
+ * wino_plan (gemm_tail_blocks) are split by element passes into gemm_parts
+ * work-groups each, and a scratch area for their partial outputs follows V
+ * (at V's size rounded up to 256 bytes); wino_gemm_inverse overwrites it.
+ * The split is fixed when the plan is made and the partials are summed in a
+ * fixed order, so a plan's results are bitwise reproducible. */
 size_t wino_workspace_bytes(const wino_plan_t* plan);
 
 /* Bytes of workspace wino_forward needs (today equal to wino_workspace_bytes). */

@@ -39,17 +39,20 @@ struct AccArgs {
   int32_t T, C_pad, K, K_pad;
   int32_t nkb;        // K_pad / 64
   // Work per XCD (work-group b runs on XCD b % 8 as its unit b / 8): XCD x
-  // owns blocks xb0[x] .. xb0[x] + xn[x] - 1; its last xs[x] blocks are done
-  // as two halves each (by passes), so its last round is half as long.
-  int32_t xb0[8], xn[8], xs[8];
+  // owns blocks xb0[x] .. xb0[x] + xn[x] - 1, whole blocks first.  Its last
+  // xs[x] blocks (those past its last full round of resident work-groups, or
+  // all of them when it has fewer than a round) are tail blocks, split by
+  // passes so the last round is shorter:
+  //  - k_gemm_acc4: two halves each, added onto zeroed outputs (no ReLU);
+  //  - k_gemm_acc: nparts parts each, 1/nparts of the passes apiece, whose
+  //    partial outputs go to part[(xt0[x] + s) * nparts + q][o][t][k] (tail
+  //    block s of XCD x, part q; 64 x 64 per output index o); k_part_reduce
+  //    sums them in part order and applies bias and ReLU.
+  int32_t xb0[8], xn[8], xs[8], xt0[8];
   int32_t tiles[3], Y[3];
   int32_t relu;
   const float* bias;  // [K] or null: b_k of eq. (2), added before the ReLU (by the
-                      // first half of a split block only, so it is added once)
-  // Pass-split mode for grids much smaller than the resident slots (nparts >
-  // 1): unit u of the per-XCD ranges is part u % nparts of block u / nparts,
-  // a contiguous 1/nparts of the passes, and its partial outputs go to
-  // part[u][o][t][k] (64 x 64 per output index); k_part_reduce sums them.
+                      // first half of a split k_gemm_acc4 block only)
   float* part;
   int32_t nparts;
 };
@@ -193,21 +196,20 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
 
   // Work unit -> (block, passes).  Each XCD runs its own contiguous range of
   // blocks (consecutive blocks share V rows in its L2), whole blocks first,
-  // then the two halves of its last few blocks, which would otherwise run
-  // alone after the XCD's last full round of resident work-groups.  Halves
-  // add their partial outputs into zeroed y.  Surplus units exit at once.
+  // then the nparts parts of each of its tail blocks, which would otherwise
+  // run alone after the XCD's last full round of resident work-groups (or
+  // leave most of the slots idle when there is less than a round).  Surplus
+  // units exit at once.
   const int xcd = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3;
-  const int xn = g.xn[xcd], xs = g.xs[xcd];
-  if (j >= xn + xs) return;
+  const int xn = g.xn[xcd], xs = g.xs[xcd], np = g.nparts;
   const int nwhole = xn - xs;
-  const bool split = j >= nwhole;
-  const bool parts = g.nparts > 1;                // pass-split mode (then xs = 0)
-  const int unit = g.xb0[xcd] + (split ? nwhole + (j - nwhole) / 2 : j);
-  const int blk = parts ? unit / g.nparts : unit;
-  const int prt = parts ? unit % g.nparts : 0;
-  const int p0 = parts ? prt * (G::NPASS / g.nparts) : split ? ((j - nwhole) & 1) * (G::NPASS / 2) : 0;
-  const int npass = parts ? G::NPASS / g.nparts : split ? G::NPASS / 2 : G::NPASS;
-  static_assert(G::NPASS % 2 == 0, "halves of whole passes");
+  if (j >= nwhole + xs * np) return;
+  const bool tail = j >= nwhole;
+  const int tj = tail ? j - nwhole : 0;           // unit among the XCD's tail units
+  const int blk = g.xb0[xcd] + (tail ? nwhole + tj / np : j);
+  const int p0 = tail ? (tj % np) * (G::NPASS / np) : 0;
+  const int npass = tail ? G::NPASS / np : G::NPASS;
+  const int64_t pslot = tail ? int64_t(g.xt0[xcd]) * np + tj : 0;   // partial-output slot
   const int tb = blk / g.nkb, kb = blk % g.nkb;
   const int nstage = g.C_pad / G::SC;             // channel stages per pass
   const int nsteps = npass * nstage;
@@ -406,10 +408,10 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
     if (finish()) break;
   }
 
-  if (parts) {
-    // partial outputs of this unit: part[unit][o][t][k], lanes over k
+  if (tail) {
+    // partial outputs of this unit: part[pslot][o][t][k], lanes over k
     __builtin_amdgcn_s_waitcnt(0x0f70);           // vmcnt(0): no copy still writes LDS
-    float* pp = g.part + int64_t(unit) * NOUT * (TB * KB);
+    float* pp = g.part + pslot * NOUT * (TB * KB);
 #pragma unroll
     for (int o = 0; o < NOUT; ++o)
 #pragma unroll
@@ -469,59 +471,53 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
           const int kg = kb * KB + kl;
           if (kg >= g.K) break;
           float v = pl[kl * TB + (tl ^ (kl & 31))];
-          if (split) {
-            // two partials onto zero: 0 + a + b rounds the same in either
-            // order; the bias joins the first half's partial
-            if (g.bias != nullptr && p0 == 0) v += g.bias[kg];
-            unsafeAtomicAdd(yo + int64_t(kg) * g.ystride_k, v);
-          } else {
-            if (g.bias != nullptr) v += g.bias[kg];
-            if (g.relu) v = v > 0.0f ? v : 0.0f;
-            __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
-          }
+          if (g.bias != nullptr) v += g.bias[kg];
+          if (g.relu) v = v > 0.0f ? v : 0.0f;
+          __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
         }
       }
     }
   }
 }
 
-// Pass-split mode: y = ReLU(sum over the parts, in part order + bias) for
-// every output of every block.  One thread per (block, tile, kernel); lanes
-// over kernels read the partials contiguously.  The fixed order keeps the
-// results bitwise reproducible.
+// Tail blocks of k_gemm_acc: y = ReLU(sum over the parts, in part order, +
+// bias) for every output of every tail block.  One thread per (tail block,
+// output index, tile, kernel); lanes over kernels read the partials
+// contiguously, and the part loads are independent (issued together), the
+// adds in fixed order, so the results are bitwise reproducible.
 template <int N, int MM>
-__global__ void __launch_bounds__(256) k_part_reduce(float* __restrict__ y, AccArgs g, int32_t nblk) {
+__global__ void __launch_bounds__(256) k_part_reduce(float* __restrict__ y, AccArgs g, int32_t ntail) {
   constexpr int NOUT = ipow(MM, N), TB = 64, KB = 64;
-  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;   // (block, tile, kernel)
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;   // ((tail block, o), tile, kernel)
   const int k_l = int(i % KB), tl = int((i / KB) % TB);
-  const int blk = int(i / (KB * TB));
-  if (blk >= nblk) return;
+  const int64_t bo = i / (KB * TB);
+  const int o = int(bo % NOUT), tix = int(bo / NOUT);
+  if (tix >= ntail) return;
+  int blk = -1;                                   // tail block tix -> its block
+#pragma unroll
+  for (int x = 0; x < 8; ++x)
+    if (tix >= g.xt0[x] && tix < g.xt0[x] + g.xs[x]) blk = g.xb0[x] + g.xn[x] - g.xs[x] + (tix - g.xt0[x]);
+  if (blk < 0) return;
   const int tb = blk / g.nkb, kb = blk % g.nkb;
   const int t = tb * TB + tl, kg = kb * KB + k_l;
   if (t >= g.T || kg >= g.K) return;
   int ti[3] = {0, 0, 0};
   const int n = split_tile<N>(t, g.tiles, ti);
-  const float b = g.bias != nullptr ? g.bias[kg] : 0.0f;
-  const float* pp = g.part + int64_t(blk) * g.nparts * NOUT * (TB * KB) + tl * KB + k_l;
-  float* yk = y + (int64_t(n) * g.K + kg) * g.ystride_k;
+  int64_t off = 0;
 #pragma unroll
-  for (int o = 0; o < NOUT; ++o) {
-    int64_t off = 0;
-    bool in = true;
-#pragma unroll
-    for (int ax = 0; ax < N; ++ax) {
-      const int oa = (o / ipow(MM, N - 1 - ax)) % MM;
-      const int yc = ti[ax] * MM + oa;
-      in = in && yc < g.Y[ax];
-      off = off * g.Y[ax] + yc;
-    }
-    if (!in) continue;
-    float v = 0.0f;
-    for (int q = 0; q < g.nparts; ++q) v += pp[(int64_t(q) * NOUT + o) * (TB * KB)];
-    if (g.bias != nullptr) v += b;
-    if (g.relu) v = v > 0.0f ? v : 0.0f;
-    yk[off] = v;
+  for (int ax = 0; ax < N; ++ax) {
+    const int oa = (o / ipow(MM, N - 1 - ax)) % MM;
+    const int yc = ti[ax] * MM + oa;
+    if (yc >= g.Y[ax]) return;                  // cropped output of a partial tile
+    off = off * g.Y[ax] + yc;
   }
+  const float* pp = g.part + (int64_t(tix) * g.nparts * NOUT + o) * (TB * KB) + tl * KB + k_l;
+  float v = 0.0f;
+#pragma unroll 8
+  for (int q = 0; q < g.nparts; ++q) v += __builtin_nontemporal_load(pp + int64_t(q) * NOUT * (TB * KB));
+  if (g.bias != nullptr) v += g.bias[kg];
+  if (g.relu) v = v > 0.0f ? v : 0.0f;
+  y[(int64_t(n) * g.K + kg) * g.ystride_k + off] = v;
 }
 
 // Zero the outputs of the blocks done in two halves (the last xs[x] blocks of

@@ -23,7 +23,11 @@ struct wino_plan_s {
   int32_t pad[3];
   int64_t T, T_pad;
   int blk, kblk, cg, cgu;
-  int nparts;             // k_gemm_acc pass-split parts (1: none)
+  // k_gemm_acc tail split, fixed at plan time from the device's compute
+  // units: the last xtail[x] blocks of XCD x are done in nparts parts each
+  int nparts;             // 1: no split
+  int32_t xtail[8];
+  int64_t ntail;          // sum of xtail
   int64_t v_floats;       // V in the workspace (rounded up to 256 bytes)
   int64_t part_floats;    // partial outputs after V when nparts > 1
   uint32_t flags;
@@ -164,35 +168,43 @@ struct Launch {
 
   // Per-XCD work ranges of a pass-accumulating GEMM (k_gemm_acc, k_gemm_acc4):
   // work-groups go to the 8 XCDs round-robin; each XCD takes a contiguous
-  // range of blocks.  On an XCD, the blocks past its last full round of
-  // resident work-groups (two per CU) are done as two halves each, so the last
-  // round is half as long.  Not with a fused ReLU, which needs the whole sum.
-  // Returns the grid size; zeroes the outputs of split blocks first.
-  template <int TB, int KB>
-  static int64_t acc_setup(const wino_plan_s& p, AccArgs& a, const float* bias, float* y, hipStream_t s,
-                           int parts = 1) {
+  // range of blocks.  With PARTS (k_gemm_acc) the plan's tail blocks of each
+  // XCD are split into p.nparts parts.  Otherwise (k_gemm_acc4) the blocks
+  // past an XCD's last full round of resident work-groups (two per CU) are
+  // done as two halves each, so the last round is half as long; not with a
+  // fused ReLU, which needs the whole sum.  Returns the grid size; zeroes the
+  // outputs of half-split blocks first.
+  template <int TB, int KB, bool PARTS>
+  static int64_t acc_setup(const wino_plan_s& p, AccArgs& a, const float* bias, float* y, hipStream_t s) {
     a.vblock = int64_t(p.nxi) * p.C_pad * TB;
     a.uplane = int64_t(p.C_pad) * p.K_pad;
     a.ystride_k = 1;
     for (int i = 0; i < N; ++i) a.ystride_k *= p.Y[i];
     a.T = int32_t(p.T); a.C_pad = p.C_pad; a.K = p.K; a.K_pad = p.K_pad;
     a.nkb = p.K_pad / KB;
-    const int64_t nb = (p.T_pad / TB) * int64_t(a.nkb) * parts;   // work units
+    const int64_t nb = (p.T_pad / TB) * int64_t(a.nkb);
     for (int i = 0; i < 3; ++i) { a.tiles[i] = int32_t(p.tiles[i]); a.Y[i] = int32_t(p.Y[i]); }
     a.relu = (p.flags & WINO_RELU) ? 1 : 0;
     a.bias = bias;
-    a.nparts = parts;
+    a.nparts = PARTS ? p.nparts : 1;
     constexpr int NX = 8;
     const int64_t slots = 2 * int64_t(cu_count() / NX);
-    int64_t maxu = 0, nsplit = 0;
+    int64_t maxu = 0, nsplit = 0, t0 = 0;
     for (int x = 0; x < NX; ++x) {
       const int64_t n = nb / NX + (x < nb % NX ? 1 : 0);
       const int64_t b0 = x * (nb / NX) + (x < nb % NX ? x : nb % NX);
-      int64_t sx = 0;
-      if (!a.relu && parts == 1 && slots > 0) sx = n < slots ? n : n % slots;
-      a.xb0[x] = int32_t(b0); a.xn[x] = int32_t(n); a.xs[x] = int32_t(sx);
-      maxu = maxu > n + sx ? maxu : n + sx;
-      nsplit += sx;
+      int64_t sx = 0, units = n;
+      if (PARTS) {
+        sx = p.nparts > 1 ? p.xtail[x] : 0;
+        units = n - sx + sx * p.nparts;
+      } else if (!a.relu && slots > 0) {
+        sx = n < slots ? n : n % slots;
+        units = n + sx;
+        nsplit += sx;
+      }
+      a.xb0[x] = int32_t(b0); a.xn[x] = int32_t(n); a.xs[x] = int32_t(sx); a.xt0[x] = int32_t(t0);
+      t0 += PARTS ? sx : 0;
+      maxu = maxu > units ? maxu : units;
     }
     if (nsplit > 0) {
       const int64_t items = nsplit * TB * ipow(MM, N);
@@ -210,20 +222,19 @@ struct Launch {
       // small grids: each block's passes split over p.nparts units, whose
       // partial outputs (after V in the workspace) are summed in order
       a.part = part;
-      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, bias, y, s, p.nparts);
+      const int64_t grid = acc_setup<G::TB, G::KB, true>(p, a, bias, y, s);
       hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST>), dim3(unsigned(grid)), dim3(G::NT), 0, s, V, U, y, a,
                          p.fm);
       if (p.nparts > 1) {
-        const int64_t nblk = (p.T_pad / G::TB) * (p.K_pad / G::KB);
-        const int64_t items = nblk * G::TB * G::KB;
+        const int64_t items = p.ntail * ipow(MM, N) * G::TB * G::KB;
         hipLaunchKernelGGL((k_part_reduce<N, MM>), dim3(unsigned((items + 255) / 256)), dim3(256), 0, s, y, a,
-                           int32_t(nblk));
+                           int32_t(p.ntail));
       }
       return launch_status();
     } else if constexpr (KIND == 1) {
       using G = Acc4Geom<N, MM, R>;
       AccArgs a{};
-      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, bias, y, s);
+      const int64_t grid = acc_setup<G::TB, G::KB, false>(p, a, bias, y, s);
       hipLaunchKernelGGL((k_gemm_acc4<N, MM, R, CONST>), dim3(unsigned(grid)), dim3(G::NT), 0, s, V, U, y, a,
                          p.fm);
       return launch_status();
@@ -332,23 +343,47 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   p.nxi = 1;
   for (int i = 0; i < N; ++i) p.nxi *= alpha;
   if ((p.T_pad / p.blk) * (p.K_pad / p.blk) > kMaxI32) return WINO_EINVAL;   // GEMM grid
-  // workspace: V, then (k_gemm_acc with fewer blocks than a quarter of the
-  // resident work-group slots of the current device) the pass-split partials
+  // workspace: V, then the partial outputs of k_gemm_acc's tail blocks.  The
+  // GEMM's 64 x 64 blocks go to the 8 XCDs in contiguous ranges, two
+  // resident work-groups per CU; an XCD's blocks past its last full round
+  // (all of them when it has less than a round) are its tail.  Each tail
+  // block is split into nparts parts by passes (a power of two; at most 8
+  // when full rounds precede, since every part writes a whole partial output)
+  // so that the tail units still have a CU each: one work-group alone on a CU
+  // already runs the MFMA pipes nearly full, so filling the second slot of a
+  // CU gains little against the partial outputs' traffic.
   p.v_floats = round_up(int64_t(p.nxi) * p.C_pad * p.T_pad, 64);
   p.nparts = 1;
+  p.ntail = 0;
   p.part_floats = 0;
-  if (m == 2 && !(o.flags & WINO_NO_SPLIT)) {
+  for (int x = 0; x < 8; ++x) p.xtail[x] = 0;
+  const int cus = cu_count();
+  if (m == 2 && !(o.flags & WINO_NO_SPLIT) && cus >= 8) {
     const int64_t nb = (p.T_pad / 64) * (p.K_pad / 64);
-    const int64_t slots = 2 * int64_t(cu_count());
+    const int64_t sx = 2 * int64_t(cus / 8);        // resident work-groups per XCD
+    const int64_t cx = cus / 8;                     // CUs per XCD
     const int npass = p.nxi / 2;
+    int64_t rmax = 0;
+    bool rounds = false;
+    for (int x = 0; x < 8; ++x) {
+      const int64_t n = nb / 8 + (x < nb % 8 ? 1 : 0);
+      rmax = n % sx > rmax ? n % sx : rmax;
+      rounds = rounds || n >= sx;
+    }
+    const int cap = rounds ? 8 : 32;
     int np = 1;
-    if (slots > 0 && nb * 4 <= slots)
-      while (np * 2 <= npass && nb * np * 2 <= slots) np *= 2;
+    if (rmax > 0)
+      while (np * 2 <= npass && np * 2 <= cap && rmax * np * 2 <= cx) np *= 2;
     if (np > 1) {
       int nout = 1;
       for (int i = 0; i < N; ++i) nout *= m;
+      for (int x = 0; x < 8; ++x) {
+        const int64_t n = nb / 8 + (x < nb % 8 ? 1 : 0);
+        p.xtail[x] = int32_t(n % sx);
+        p.ntail += n % sx;
+      }
       p.nparts = np;
-      p.part_floats = nb * np * nout * 64 * 64;
+      p.part_floats = p.ntail * np * nout * 64 * 64;
     }
   }
   if ((p.T_pad / p.blk) * (p.C_pad / p.cg) > kMaxI32) return WINO_EINVAL;     // input grid
@@ -405,6 +440,7 @@ wino_status wino_plan_describe(const wino_plan_t* p, wino_plan_desc* d) {
   d->channel_group = p->cg;
   d->filter_channel_group = p->cgu;
   d->gemm_parts = p->nparts;
+  d->gemm_tail_blocks = p->ntail;
   d->default_points = p->const_mats ? 1 : 0;
   return WINO_OK;
 }

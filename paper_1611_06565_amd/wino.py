@@ -44,7 +44,8 @@ class _Desc(ctypes.Structure):
                 ("T", ctypes.c_int64), ("T_pad", ctypes.c_int64),
                 ("block_tiles", ctypes.c_int32), ("block_kernels", ctypes.c_int32),
                 ("default_points", ctypes.c_int32), ("channel_group", ctypes.c_int32),
-                ("filter_channel_group", ctypes.c_int32), ("gemm_parts", ctypes.c_int32)]
+                ("filter_channel_group", ctypes.c_int32), ("gemm_parts", ctypes.c_int32),
+                ("gemm_tail_blocks", ctypes.c_int64)]
 
 
 _LIB = None

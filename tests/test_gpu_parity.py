@@ -119,7 +119,9 @@ def test_f54_layers_full_output(spec):
 
 # F(2^N, 3^N) layers with few product blocks and many channels and kernels
 # (the late layers of a 3-D stack): each block's element passes are split over
-# up to 32 work-groups whose partial outputs are summed in order afterwards
+# up to 32 work-groups whose partial outputs are summed in order afterwards;
+# and layers with full rounds of blocks and a few left over (the tail blocks,
+# split into 8 parts), with and without ReLU
 PARTS = [
     LayerSpec("f2x3_3d_parts_c512", N=3, m=2, r=3, batch=2, C=512, K=192, X=(2, 7, 7), pad=1,
               x_dist="relu_normal", w_dist="he", relu=True),
@@ -127,6 +129,10 @@ PARTS = [
               x_dist="normal", w_dist="he"),
     LayerSpec("f2x3_2d_parts", N=2, m=2, r=3, batch=1, C=300, K=130, X=(15, 14), pad=1,
               x_dist="uniform", w_dist="he"),
+    LayerSpec("f2x3_2d_tail_relu", N=2, m=2, r=3, batch=3, C=8, K=64, X=(212, 212), pad=1,
+              x_dist="normal", w_dist="he", relu=True),
+    LayerSpec("f2x3_3d_tail", N=3, m=2, r=3, batch=1, C=8, K=70, X=(16, 96, 92), pad=1,
+              x_dist="relu_normal", w_dist="he"),
 ]
 
 
@@ -135,7 +141,7 @@ def test_pass_split_layers_full_output(spec):
     x, w = draw_layer(spec, seed=23)
     b = (np.random.default_rng(6).standard_normal(spec.K) * 0.3).astype(np.float32)
     y, plan = run_layer(spec, x, w, bias=b, guard=1024)
-    assert plan.desc["gemm_parts"] > 1, plan.desc
+    assert plan.desc["gemm_parts"] > 1 and plan.desc["gemm_tail_blocks"] > 0, plan.desc
     check_full(spec, y, x, w, bias=b)
     # the same layer with every block in one work-group
     y1, plan1 = run_layer(spec, x, w, bias=b, guard=1024, split=False)
@@ -153,7 +159,7 @@ def test_pass_split_determinism_bitwise():
 
 
 # the small F(2^N, 3^N) layers above take the pass split; here every block is
-# one work-group again: whole blocks, and halves of the last blocks (no ReLU)
+# one work-group again
 M2_WHOLE = [s for s in SMALL + OVERLAP + EDGE if s.m == 2]
 
 
@@ -180,8 +186,8 @@ def test_bias(spec, split):
 
 
 def test_bias_determinism_bitwise():
-    # halves of split-tail blocks added onto zeroed outputs
-    spec = SMALL[1]
+    # F(4^2): halves of the last blocks added onto zeroed outputs
+    spec = SMALL[2]
     x, w = draw_layer(spec, seed=2)
     b = np.linspace(-1, 1, spec.K).astype(np.float32)
     y1, _ = run_layer(spec, x, w, bias=b, split=False)
