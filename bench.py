@@ -390,7 +390,11 @@ def main():
             "tiles": d["T"], "direct_gflop_per_step": flops / 1e9,
         },
         "roofline": {
-            "kernel": ("k_gemm_acc (batched fp32-MFMA GEMM, inverse transform accumulated per pass)"
+            "kernel": ("k_gemm_acc + k_part_reduce (batched fp32-MFMA GEMM, inverse transform accumulated "
+                       "per pass; the %d tail blocks in %d parts each, their partial outputs summed in order)"
+                       % (d["gemm_tail_blocks"], d["gemm_parts"])
+                       if spec.m == 2 and d["gemm_parts"] > 1 else
+                       "k_gemm_acc (batched fp32-MFMA GEMM, inverse transform accumulated per pass)"
                        if spec.m == 2 else
                        "k_gemm_acc4 (batched fp32-MFMA GEMM, inverse transform accumulated per pass)"
                        if (spec.N, spec.m, spec.r) == (2, 4, 3) else
