@@ -258,6 +258,8 @@ def main():
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5],
                     help="layer family (default 2, the F(2^3,3^3) C=64 K=128 video layer; "
                          "5 = the C3D-style stack)")
+    ap.add_argument("--adjoint", action="store_true",
+                    help="time the layer's data gradient dx = adjoint(dy) instead of its forward")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
@@ -294,6 +296,13 @@ def main():
     x, w = draw_layer(spec, seed=seed)
     plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X),
                 pad=spec.pad, relu=spec.relu)
+    transform_filter = plan.transform_filter
+    if args.adjoint:
+        # the data gradient: dy of the layer's output shape through the
+        # adjoint plan, kernels flipped and transposed by its filter transform
+        plan = plan.adjoint()
+        transform_filter = plan.transform_filter_adjoint
+        x = np.random.default_rng(seed + 100).standard_normal(plan.input_shape, dtype=np.float32)
     d = plan.desc
     xd = torch.from_numpy(x).cuda()
     wd = torch.from_numpy(w).cuda()
@@ -307,7 +316,7 @@ def main():
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        plan.transform_filter(wd, U)
+        transform_filter(wd, U)
         if ev is not None:
             ev[1].record()
         plan.transform_input(xd, ws)
@@ -336,19 +345,20 @@ def main():
 
     flops = direct_flops(spec)
     nxi = d["n_xi"]
-    gemm_flops = 2.0 * nxi * d["T"] * spec.C * spec.K
-    in_bytes = 4.0 * (spec.batch * spec.C * float(np.prod(spec.X)) + nxi * d["T"] * spec.C)
+    C, K = plan.C, plan.K                    # swapped for the data gradient
+    gemm_flops = 2.0 * nxi * d["T"] * C * K
+    in_bytes = 4.0 * (float(np.prod(plan.input_shape)) + nxi * d["T"] * C)
     # The GEMM's algorithmic bytes: V read once, U read once, y written once.
     # Below the ridge point (peak FLOP/s over peak bytes/s) it is bound by HBM.
-    gemm_bytes = 4.0 * (nxi * d["T"] * spec.C + nxi * spec.C * spec.K
-                        + spec.batch * spec.K * float(np.prod(spec.out_spatial)))
+    gemm_bytes = 4.0 * (nxi * d["T"] * C + nxi * C * K + float(np.prod(plan.output_shape)))
     hbm_bound = gemm_flops / gemm_bytes < PEAK_FP32_MFMA * 1e12 / (PEAK_HBM * 1e9)
     if hbm_bound:
         achieved = gemm_bytes / (gemm_ms * 1e-3) / 1e9
     else:
         achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
-    counters = read_counters(kernel_hash(), args.config)
-    traffic = read_traffic(kernel_hash(), args.config)
+    prof_key = f"{args.config}-adjoint" if args.adjoint else args.config
+    counters = read_counters(kernel_hash(), prof_key)
+    traffic = read_traffic(kernel_hash(), prof_key)
     try:
         mfma_counted = float(counters["mfma_flops_per_launch"])
     except (KeyError, ValueError):
@@ -361,14 +371,20 @@ def main():
         rng = np.random.default_rng(0)
         yh = y.cpu().numpy()
         coords = np.stack([rng.integers(0, s, size=2000) for s in yh.shape], axis=1)
-        ys, dens = direct_sampled(x, w, spec.pad, coords)
+        if args.adjoint:
+            from oracle.adjoint import direct_adjoint_sampled
+            ys, dens = direct_adjoint_sampled(x, w, spec.pad, coords)
+        else:
+            ys, dens = direct_sampled(x, w, spec.pad, coords)
         check = normalised_error(yh[tuple(coords.T)], ys, dens)["max"]
 
     extra = {"input_transform_hbm": {"achieved_GBps": in_bytes / (inp_ms * 1e-3) / 1e9,
                                      "peak_GBps": PEAK_HBM,
                                      "frac": in_bytes / (inp_ms * 1e-3) / 1e9 / PEAK_HBM}}
     out = {
-        "metric": "effective TFLOP/s per 3D conv layer (direct FLOPs); % fp32 MFMA / HBM peak",
+        "metric": ("effective TFLOP/s of a conv layer's data gradient (direct FLOPs); % fp32 MFMA / HBM peak"
+                   if args.adjoint else
+                   "effective TFLOP/s per 3D conv layer (direct FLOPs); % fp32 MFMA / HBM peak"),
         "value": flops / (ms_step * 1e-3) / 1e12,
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -381,7 +397,8 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": "F(%d^%d,3^%d) %d-D conv layer: batch %d, C=%d, K=%d, %s, %s, pad %d" % (
+            "workload": ("data gradient (adjoint plan: C and K swapped, pads r-1-pad) of " if args.adjoint
+                         else "") + "F(%d^%d,3^%d) %d-D conv layer: batch %d, C=%d, K=%d, %s, %s, pad %d" % (
                 spec.m, spec.N, spec.N, spec.N, spec.batch, spec.C, spec.K,
                 "x".join(str(v) for v in spec.X), "x".join(["3"] * spec.N), spec.pad),
             "N": spec.N, "m": spec.m, "r": spec.r, "batch": spec.batch, "C": spec.C, "K": spec.K,
@@ -421,7 +438,7 @@ def main():
         "kernel_sources_sha256_16": kernel_hash(),
     }
     out.update(extra)
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.adjoint:
         out["cpu_baseline"] = cpu_baseline(spec, x, w)
     print(json.dumps(out), flush=True)
 

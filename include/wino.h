@@ -154,6 +154,33 @@ wino_status wino_get_matrices(const wino_plan_t* plan, double* AT, double* BT, d
  *   U  device, wino_filter_bytes(plan) bytes, fully overwritten */
 wino_status wino_transform_filter(const wino_plan_t* plan, const float* w, float* U, void* stream);
 
+/* Data gradient (the adjoint of eq. 2's correlation; the backward pass of a
+ * layer, which the paper leaves out).  For a forward plan with C channels, K
+ * kernels, input extents X and padding pad <= r - 1 on every axis,
+ *
+ *     dx[n][c][q] = sum_k sum_{p in [0,r)^N} w[k][c][p] * dy~[n][k][q - p + pad]
+ *
+ * (dy~ = dy zero-extended outside [0, Y)) is itself a correlation: of dy with
+ * the kernel w'[c][k][p] = w[k][c][r-1-p] (every axis reversed) and padding
+ * r - 1 - pad, with output extent X.  So it runs on the forward path:
+ *
+ *   wino_plan_adjoint(fwd, &adj)              adjoint plan: C and K swapped,
+ *                                             dims [batch, Y_1..Y_N], pads
+ *                                             r - 1 - pad, the same points and
+ *                                             WINO_NO_SPLIT, no ReLU
+ *   wino_transform_filter_adjoint(adj, w, U)  U of w' from the forward kernels
+ *                                             w [K][C][r^N] (the plan's
+ *                                             [C_adj][K_adj][r^N])
+ *   wino_forward(adj, dy, U, dx, ...)         dy [batch][K][Y..] -> dx
+ *                                             [batch][C][X..]
+ *
+ * A ReLU of the forward layer is not part of the adjoint: mask dy first.
+ * wino_plan_adjoint returns WINO_EINVAL when a pad exceeds r - 1 and the
+ * errors of wino_plan otherwise; wino_transform_filter_adjoint behaves as
+ * wino_transform_filter (U fully overwritten). */
+wino_status wino_plan_adjoint(const wino_plan_t* forward_plan, wino_plan_t** out);
+wino_status wino_transform_filter_adjoint(const wino_plan_t* plan, const float* w, float* U, void* stream);
+
 /* Data transform V = d x_1 B^T ... x_N B^T of every tile and channel (eq. 4),
  * written straight into the GEMM operand layout above (§4.1's reshuffle).
  *   x          device, [batch][C][X_1..X_N] float32

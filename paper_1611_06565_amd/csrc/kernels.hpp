@@ -70,6 +70,7 @@ struct Blocking {
 struct FilterArgs {
   int64_t uplane;  // C_pad * K_pad
   int32_t C, K, C_pad, K_pad;
+  int32_t adjoint;  // w is [C][K][r^N]; use w[c][k] with every axis reversed
 };
 
 struct InputArgs {
@@ -132,9 +133,16 @@ __global__ void __launch_bounds__(64) k_filter(const float* __restrict__ w, floa
   float u[NXI];
   if (c < a.C && k < a.K) {
     float g[RN];
-    const float* src = w + (int64_t(k) * a.C + c) * RN;
+    if (a.adjoint) {
+      // reversing every axis of a C-order r^N array reverses its flat index
+      const float* src = w + (int64_t(c) * a.K + k) * RN;
 #pragma unroll
-    for (int i = 0; i < RN; ++i) g[i] = src[i];
+      for (int i = 0; i < RN; ++i) g[i] = src[RN - 1 - i];
+    } else {
+      const float* src = w + (int64_t(k) * a.C + c) * RN;
+#pragma unroll
+      for (int i = 0; i < RN; ++i) g[i] = src[i];
+    }
     transform_nd<N, R, A>(g, u, MatRef<Which::G, CONST, MM, R>{&fm});
   } else {
 #pragma unroll

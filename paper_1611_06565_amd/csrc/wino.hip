@@ -23,6 +23,8 @@ struct wino_plan_s {
   int32_t pad[3];
   int64_t T, T_pad;
   int blk, kblk, cg, cgu;
+  int32_t n_user_pts;     // the caller's points (0: default set), kept for wino_plan_adjoint
+  double user_pts[kMaxAlpha];
   // k_gemm_acc tail split, fixed at plan time from the device's compute
   // units: the last xtail[x] blocks of XCD x are done in nparts parts each
   int nparts;             // 1: no split
@@ -118,10 +120,11 @@ struct Launch {
   static constexpr int VEC = Blocking<N, MM, R>::VEC;
   static constexpr int DEPTH = 1;
 
-  static wino_status filter(const wino_plan_s& p, const float* w, float* U, hipStream_t s) {
+  static wino_status filter(const wino_plan_s& p, const float* w, float* U, bool adjoint, hipStream_t s) {
     FilterArgs a{};
     a.uplane = int64_t(p.C_pad) * p.K_pad;
     a.C = p.C; a.K = p.K; a.C_pad = p.C_pad; a.K_pad = p.K_pad;
+    a.adjoint = adjoint ? 1 : 0;
     const int64_t n = int64_t(p.C_pad) * p.K_pad;   // C_pad is a multiple of CGU
     // one thread per (channel, kernel): small work-groups spread the few
     // threads of a layer (8192 for C = 64, K = 128) over more CUs
@@ -403,6 +406,8 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
     if (o.n_points != np) return WINO_EINVAL;
     for (int i = 0; i < np; ++i)
       if (!rationalize(o.points[i], &pts[i])) return WINO_EINVAL;
+    p.n_user_pts = np;
+    for (int i = 0; i < np; ++i) p.user_pts[i] = o.points[i];
     int cnt = 0;
     const Rat* d = default_points(m, r, &cnt);
     defaults = d != nullptr && cnt == np;
@@ -476,7 +481,34 @@ wino_status wino_transform_filter(const wino_plan_t* p, const float* w, float* U
   if (p == nullptr || w == nullptr || U == nullptr) return WINO_EINVAL;
   if (!aligned16(w) || !aligned16(U)) return WINO_EINVAL;
   const hipStream_t s = static_cast<hipStream_t>(stream);
-  return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::filter(*p, w, U, s); });
+  return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::filter(*p, w, U, false, s); });
+}
+
+wino_status wino_transform_filter_adjoint(const wino_plan_t* p, const float* w, float* U, void* stream) {
+  if (p == nullptr || w == nullptr || U == nullptr) return WINO_EINVAL;
+  if (!aligned16(w) || !aligned16(U)) return WINO_EINVAL;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::filter(*p, w, U, true, s); });
+}
+
+// The adjoint of a layer's correlation (the data gradient, §3.1's eq. (2)
+// read backwards): dx[n][c][q] = sum_k sum_p w[k][c][p] dy~[n][k][q - p + pad],
+// with dy~ zero outside [0, Y).  Substituting p' = r - 1 - p makes it the
+// correlation of dy with the kernel w'[c][k][p'] = w[k][c][r - 1 - p'] and
+// padding r - 1 - pad, whose output extent is X again.
+wino_status wino_plan_adjoint(const wino_plan_t* f, wino_plan_t** out) {
+  if (f == nullptr || out == nullptr) return WINO_EINVAL;
+  wino_opts o{};
+  for (int i = 0; i < f->N; ++i) {
+    if (f->pad[i] > f->r - 1) return WINO_EINVAL;
+    o.pad[i] = f->r - 1 - f->pad[i];
+  }
+  o.points = f->n_user_pts > 0 ? f->user_pts : nullptr;
+  o.n_points = f->n_user_pts;
+  o.flags = f->flags & WINO_NO_SPLIT;
+  int64_t dims[4] = {f->batch, 1, 1, 1};
+  for (int i = 0; i < f->N; ++i) dims[1 + i] = f->Y[i];
+  return wino_plan(f->N, f->m, f->r, f->K, f->C, dims, &o, out);
 }
 
 wino_status wino_transform_input(const wino_plan_t* p, const float* x, void* ws, size_t ws_bytes,

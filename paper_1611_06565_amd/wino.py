@@ -86,6 +86,8 @@ def lib():
         "wino_status_string": (ctypes.c_char_p, [i32]),
         "wino_points_error_growth": (i32, [i32, i32, i32, P_dbl, i32, P_dbl]),
         "wino_search_points": (i32, [i32, i32, i32, P_dbl, P_dbl]),
+        "wino_plan_adjoint": (i32, [vp, ctypes.POINTER(vp)]),
+        "wino_transform_filter_adjoint": (i32, [vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -154,19 +156,48 @@ class Plan:
         arr = (ctypes.c_int64 * len(dims))(*dims)
         h = ctypes.c_void_p()
         _check(L.wino_plan(N, m, r, C, K, arr, ctypes.byref(opts), ctypes.byref(h)), "wino_plan")
+        self._adopt(L, h, relu)
+
+    def _adopt(self, L, h, relu):
         self._h = h
         self._L = L
         d = _Desc()
         _check(L.wino_plan_describe(h, ctypes.byref(d)), "wino_plan_describe")
         self.desc = {f: (list(getattr(d, f)) if f in ("X", "Y", "tiles") else getattr(d, f))
                      for f, _ in _Desc._fields_}
-        self.N, self.m, self.r, self.C, self.K = N, m, r, C, K
+        N, C, K, r = d.N, d.C, d.K, d.r
+        self.N, self.m, self.r, self.C, self.K = N, d.m, r, C, K
         self.relu = relu
         out = (ctypes.c_int64 * (N + 2))()
         _check(L.wino_output_dims(h, out), "wino_output_dims")
         self.output_shape = tuple(int(v) for v in out)
-        self.input_shape = (dims[0], C) + tuple(dims[1:])
+        self.input_shape = (int(d.batch), C) + tuple(int(v) for v in list(d.X)[:N])
         self.weight_shape = (K, C) + (r,) * N
+
+    def adjoint(self):
+        """The plan of this layer's data gradient dx from dy (wino_plan_adjoint):
+        C and K swapped, input extents Y, pads r - 1 - pad; run it with
+        transform_filter_adjoint(w) of this layer's kernels and forward(dy, U)."""
+        h = ctypes.c_void_p()
+        _check(self._L.wino_plan_adjoint(self._h, ctypes.byref(h)), "wino_plan_adjoint")
+        p = Plan.__new__(Plan)
+        p._pts = None
+        p._adopt(self._L, h, False)
+        return p
+
+    def transform_filter_adjoint(self, w, U=None):
+        """U of the flipped, transposed kernels from the forward layer's w [C][K][r^N]
+        (this plan's C and K are the forward layer's K and C)."""
+        import torch
+        self._check_shape(w, (self.C, self.K) + (self.r,) * self.N, "w")
+        if U is None:
+            U = self.new_filter()
+        if U.numel() * 4 < self.filter_bytes:
+            raise ValueError("U is too small")
+        _check(self._L.wino_transform_filter_adjoint(self._h, _dev_ptr(w, "w", torch.float32),
+                                                     _dev_ptr(U, "U", torch.float32), _stream()),
+               "wino_transform_filter_adjoint")
+        return U
 
     def __del__(self):
         h = getattr(self, "_h", None)

@@ -207,3 +207,28 @@ def test_points_error_growth_rejects(L):
     assert L.wino_points_error_growth(2, 6, 4, None, 0, ctypes.byref(g)) == -1  # alpha 9
     out = (ctypes.c_double * 5)()
     assert L.wino_search_points(3, 4, 3, out, None) == -1
+
+
+def test_adjoint_plan():
+    # the data gradient's plan: C and K swapped, extents Y -> X, pads r - 1 - pad,
+    # the forward plan's points and WINO_NO_SPLIT, no ReLU
+    f = wino.Plan(3, 2, 3, 16, 24, [2, 9, 10, 11], pad=[1, 0, 2], points=[0, 0.5, -0.5], relu=True,
+                  split=False)
+    a = f.adjoint()
+    assert (a.C, a.K, a.N, a.m, a.r) == (24, 16, 3, 2, 3)
+    assert a.input_shape == f.output_shape and a.output_shape == f.input_shape
+    assert a.weight_shape == (16, 24, 3, 3, 3)
+    assert a.desc["gemm_parts"] == 1
+    for u, v in zip(f.matrices(), a.matrices()):
+        assert np.array_equal(u, v)
+    assert not a.relu
+    q = wino.Plan(2, 4, 3, 3, 5, [1, 9, 10], pad=0).adjoint()
+    assert q.input_shape == (1, 5, 7, 8) and q.output_shape == (1, 3, 9, 10)
+    assert q.desc["default_points"] == 1
+    L = wino.lib()
+    with pytest.raises(wino.WinoError):
+        wino.Plan(2, 2, 3, 3, 5, [1, 9, 10], pad=3).adjoint()       # pad > r - 1
+    h = ctypes.c_void_p()
+    assert L.wino_plan_adjoint(None, ctypes.byref(h)) == -1
+    assert L.wino_plan_adjoint(f.handle, None) == -1
+    assert L.wino_transform_filter_adjoint(None, None, None, None) == -1

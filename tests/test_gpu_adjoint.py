@@ -1,0 +1,89 @@
+"""GPU parity of the data gradient (the adjoint of eq. (2)'s correlation) run on
+the forward path: wino_plan_adjoint + wino_transform_filter_adjoint +
+wino_forward, against the fp64 adjoint oracle on the same seeded inputs, to the
+forward path's bars (normalised max error 1e-5 for m = 2, 1e-4 otherwise)."""
+import math
+
+import numpy as np
+import pytest
+
+from gpu_util import TOL, log, require_gpu
+from oracle.adjoint import direct_adjoint, direct_adjoint_sampled
+from oracle.metric import normalised_error
+from workloads import CONFIGS
+
+pytestmark = pytest.mark.gpu
+
+# (name, N, m, r, batch, C, K, X, pad): the adjoint plan's padding is r - 1 - pad
+ADJ = [
+    ("f2x3_3d", 3, 2, 3, 2, 24, 40, (6, 13, 15), 1),
+    ("f2x3_2d_pad0", 2, 2, 3, 2, 10, 33, (19, 14), 0),
+    ("f2x3_3d_parts", 3, 2, 3, 2, 192, 300, (2, 7, 7), 1),
+    ("f4x3_2d", 2, 4, 3, 3, 36, 70, (17, 23), 1),
+    ("f4x3_3d", 3, 4, 3, 1, 20, 24, (13, 11, 17), 1),
+    ("f4x3_3d_pad2", 3, 4, 3, 1, 6, 9, (7, 8, 9), 2),
+    ("f5x4_2d", 2, 5, 4, 2, 9, 20, (23, 31), 1),
+    ("f3x2_2d", 2, 3, 2, 3, 17, 40, (20, 23), 0),
+    ("f4x5_2d", 2, 4, 5, 2, 12, 19, (21, 26), 2),
+    ("f3x6_2d", 2, 3, 6, 1, 20, 33, (25, 19), 0),
+]
+
+
+def run_adjoint(N, m, r, batch, C, K, X, pad, dy_fn, w_fn, name):
+    torch = require_gpu()
+    from paper_1611_06565_amd.wino import Plan
+    log(f"[gpu] adjoint {name} N={N} m={m} r={r} C={C} K={K} X={X} batch={batch} pad={pad}")
+    f = Plan(N, m, r, C, K, [batch] + list(X), pad=pad)
+    a = f.adjoint()
+    w = w_fn((K, C) + (r,) * N)
+    dy = dy_fn(f.output_shape)
+    U = a.transform_filter_adjoint(torch.from_numpy(w).cuda())
+    dx = a.forward(torch.from_numpy(dy).cuda(), U)
+    torch.cuda.synchronize()
+    assert tuple(dx.shape) == f.input_shape
+    return dx.cpu().numpy(), dy, w
+
+
+@pytest.mark.parametrize("case", ADJ, ids=lambda c: c[0])
+def test_adjoint_full_output(case):
+    name, N, m, r, batch, C, K, X, pad = case
+    rng = np.random.default_rng(31)
+    std = math.sqrt(2.0 / (C * r ** N))
+    dx, dy, w = run_adjoint(N, m, r, batch, C, K, X, pad,
+                            lambda s: rng.standard_normal(s).astype(np.float32),
+                            lambda s: (rng.standard_normal(s) * std).astype(np.float32), name)
+    ref, den = direct_adjoint(dy, w, pad)
+    err = normalised_error(dx, ref, den)
+    log(f"  max err {err['max']:.3e} p99.99 {err['p9999']:.3e}")
+    assert err["nonfinite"] == 0
+    assert err["max"] <= TOL[m], err
+
+
+def test_adjoint_integer_inputs_bitwise_exact():
+    # F(2^3): every intermediate of small-integer data is an exact fp32 value
+    rng = np.random.default_rng(5)
+    dx, dy, w = run_adjoint(3, 2, 3, 2, 12, 20, (5, 9, 7), 1,
+                            lambda s: rng.integers(-3, 4, size=s).astype(np.float32),
+                            lambda s: rng.integers(-2, 3, size=s).astype(np.float32), "int")
+    ref, _ = direct_adjoint(dy, w, 1, with_den=False)
+    assert np.array_equal(dx, ref.astype(np.float32))
+
+
+def test_adjoint_full_size_sampled():
+    # the data gradient of the F(2^3) C = 64, K = 128, 16 x 56 x 56 layer at
+    # batch 8, in the launch configuration of its forward
+    spec = CONFIGS[2]
+    rng = np.random.default_rng(8)
+    std = math.sqrt(2.0 / (spec.C * 27))
+    dx, dy, w = run_adjoint(spec.N, spec.m, spec.r, spec.batch, spec.C, spec.K, spec.X, spec.pad,
+                            lambda s: rng.standard_normal(s, dtype=np.float32),
+                            lambda s: (rng.standard_normal(s) * std).astype(np.float32), spec.name)
+    coords = np.stack([rng.integers(0, s, size=3000) for s in dx.shape], axis=1)
+    corners = [[b, c] + [v if (i >> a) & 1 else 0 for a, v in enumerate(np.array(dx.shape[2:]) - 1)]
+               for b in (0, dx.shape[0] - 1) for c in (0, dx.shape[1] - 1) for i in range(8)]
+    coords = np.concatenate([coords, np.array(corners)])
+    ref, den = direct_adjoint_sampled(dy, w, spec.pad, coords)
+    got = dx[tuple(coords.T)]
+    err = np.max(np.abs(got - ref) / np.maximum(den, 1e-30))
+    log(f"  sampled max err {err:.3e}")
+    assert np.all(np.isfinite(got)) and err <= TOL[spec.m]
