@@ -181,6 +181,33 @@ wino_status wino_transform_filter(const wino_plan_t* plan, const float* w, float
 wino_status wino_plan_adjoint(const wino_plan_t* forward_plan, wino_plan_t** out);
 wino_status wino_transform_filter_adjoint(const wino_plan_t* plan, const float* w, float* U, void* stream);
 
+/* Weight gradient (the backward pass on the kernel side, which the paper also
+ * leaves out) of the layer of a forward plan:
+ *
+ *     dw[k][c][p] = sum_n sum_o dy[n][k][o] * x~[n][c][o + p - pad]
+ *
+ * Per axis the r taps' gradient over one output tile is the minimal filtering
+ * algorithm F(r, m) (§2.2) with the tile's m output gradients as its kernel
+ * and the tile's alpha-value input window as its data; its data transform is
+ * the forward's B^T (same points), so the forward's V is reused, the
+ * output gradients are transformed with F(r, m)'s G, one product per element
+ * xi sums over every tile of the batch (M_xi[K x C] = sum_t D_xi V_xi^T,
+ * eq. 5 read the other way) and F(r, m)'s A^T maps M back to r^N taps.
+ * Supported for F(2^N, 3^N) and F(4^2, 3^2) plans (V in 64-tile blocks);
+ * otherwise WINO_EUNSUPPORTED and a workspace size of 0.  Bias, ReLU and the
+ * plan's flags play no part (mask dy for a ReLU layer first).
+ *   x          device, [batch][C][X_1..X_N] float32 (the layer's input)
+ *   dy         device, [batch][K][Y_1..Y_N] float32 (the output gradient)
+ *   dw         device, [K][C][r^N] float32, fully overwritten
+ *   workspace  device, wino_weight_gradient_workspace_bytes(plan) bytes: V,
+ *              then the transformed dy and the partial products of the
+ *              tile ranges (all overwritten)
+ * The partial products are summed in a fixed order: results are bitwise
+ * reproducible for a plan. */
+size_t wino_weight_gradient_workspace_bytes(const wino_plan_t* plan);
+wino_status wino_weight_gradient(const wino_plan_t* plan, const float* x, const float* dy, float* dw,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
 /* Data transform V = d x_1 B^T ... x_N B^T of every tile and channel (eq. 4),
  * written straight into the GEMM operand layout above (§4.1's reshuffle).
  *   x          device, [batch][C][X_1..X_N] float32

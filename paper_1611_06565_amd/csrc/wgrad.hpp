@@ -1,0 +1,185 @@
+// Weight gradient of an F(2^N, 3^N) layer (the backward pass on the kernel
+// side; the paper measures forward passes only).
+//
+// Per axis, the gradient of the r kernel taps over one output tile is a
+// correlation of the tile's m output gradients with the alpha-value input
+// window: dw_t[p] = sum_{o<m} dy_t[o] d_t[o + p], p < r.  That is the
+// minimal filtering algorithm F(r, m) of §2.2 with the roles of kernel and
+// output swapped, and over N axes (eq. 3-4)
+//
+//   dw_t = A'^T [ (dy_t x_n G') (.) (d_t x_n B'^T) ]
+//
+// with (A'^T, G', B'^T) the triple of F(r, m) on the forward's points.  B'^T
+// equals the forward's B^T (both come from the same points; the plan checks
+// it exactly), so d_t x_n B'^T is the forward's V.  Summed over the tiles of
+// the whole batch, the inverse transform comes out of the sum, and the sum
+// per element is a product (eq. 5 read the other way):
+//
+//   M_xi [K x C] = sum_t D_xi[k][t] V_xi[c][t],   dw = M x_n A'^T.
+//
+//   k_dy          D[xi][k][t] = (dy_t[k] x_n G')[xi], layout of V
+//   k_wgrad_gemm  partial M_xi over a range of tile blocks, fp32 MFMA
+//   k_wgrad_finish  sum of the partials (fixed order), then A'^T
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "kernels.hpp"
+#include "synth.hpp"
+#include "transforms.hpp"
+
+namespace wino {
+
+struct WgArgs {
+  int64_t ystride_k;    // prod Y_i (dy per kernel)
+  int32_t T, T_pad, ntb; // tiles, padded to 64, tile blocks
+  int32_t K, K_pad4;    // kernels, rounded up to 4 (D's channel groups)
+  int32_t C, C_pad;     // channels (V's C_pad, a multiple of 4)
+  int32_t nkb, ncb;     // 64-blocks of kernels and channels in M
+  int32_t nsplit;       // tile-block ranges summed separately
+  int32_t nblocks;      // work-groups of k_wgrad_gemm
+  int32_t tiles[3], Y[3];
+};
+
+// One thread per (tile, kernel): lane = 4 * tile + kernel % 4 within a (tile
+// block, kernel group), so every element's 64 x 4 values are stored as one
+// contiguous 1 KB run.  Outputs past Y (partial tiles) and padding tiles and
+// kernels read as zero.
+template <int N, int MM, int R>
+__global__ void __launch_bounds__(256) k_dy(const float* __restrict__ dy, float* __restrict__ D, WgArgs a,
+                                            FMats fw) {
+  constexpr int A = MM + R - 1, NXI = ipow(A, N), NIN = ipow(MM, N);
+  const int tb = int(blockIdx.x) / (a.K_pad4 / 4), kg = int(blockIdx.x) % (a.K_pad4 / 4);
+  const int tl = int(threadIdx.x) >> 2, kl = int(threadIdx.x) & 3;
+  const int t = tb * 64 + tl, k = kg * 4 + kl;
+  float g[NIN];
+  if (t < a.T && k < a.K) {
+    int ti[3] = {0, 0, 0};
+    const int n = split_tile<N>(t, a.tiles, ti);
+    const float* src = dy + (int64_t(n) * a.K + k) * a.ystride_k;
+#pragma unroll
+    for (int i = 0; i < NIN; ++i) {
+      int64_t off = 0;
+      bool in = true;
+      int rem = i;
+#pragma unroll
+      for (int ax = N - 1; ax >= 0; --ax) {
+        const int yc = ti[ax] * MM + rem % MM;
+        rem /= MM;
+        in = in && yc < a.Y[ax];
+      }
+      rem = i;
+      int64_t mul = 1;
+#pragma unroll
+      for (int ax = N - 1; ax >= 0; --ax) {
+        const int yc = ti[ax] * MM + rem % MM;
+        rem /= MM;
+        off += int64_t(yc) * mul;
+        mul *= a.Y[ax];
+      }
+      g[i] = in ? src[off] : 0.0f;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < NIN; ++i) g[i] = 0.0f;
+  }
+  float u[NXI];
+  // G' of F(r, m): alpha x m, from the kernel argument
+  transform_nd<N, MM, A>(g, u, MatRef<Which::G, false, R, MM>{&fw});
+  float* dst = D + (int64_t(tb) * (a.K_pad4 / 4) + kg) * NXI * 256 + threadIdx.x;
+#pragma unroll
+  for (int xi = 0; xi < NXI; ++xi) __builtin_nontemporal_store(u[xi], dst + xi * 256);
+}
+
+// Partial M_xi over tile blocks [tb0, tb1) for one 64-kernel x 64-channel
+// block: work-group = four waves, each a 32 x 32 quadrant on
+// v_mfma_f32_32x32x2f32 with the tiles as the contraction.  A step stages
+// the 16 D chunks and 16 V chunks (1 KB each: 64 tiles x 4 kernels or
+// channels) of one tile block through LDS; chunks are padded by 4 floats so
+// that the 32 lanes of an operand read hit 32 banks.  The next step's chunks
+// are loaded into registers while this step multiplies.
+__global__ void __launch_bounds__(256) k_wgrad_gemm(const float* __restrict__ V, const float* __restrict__ D,
+                                                    float* __restrict__ part, WgArgs a, int32_t nxi) {
+  using S = MfmaShape<32>;
+  constexpr int CP = 260;                          // padded chunk stride (floats)
+  __shared__ __attribute__((aligned(16))) float Ds[16 * CP];
+  __shared__ __attribute__((aligned(16))) float Vs[16 * CP];
+  const int lane = int(threadIdx.x) & 63, wave = int(threadIdx.x) >> 6;
+  const int L = xcd_remap(int(blockIdx.x), a.nblocks);
+  const int cb = L % a.ncb, kb = (L / a.ncb) % a.nkb;
+  const int xi = (L / (a.ncb * a.nkb)) % nxi, sp = L / (a.ncb * a.nkb * nxi);
+  const int tb0 = int(int64_t(sp) * a.ntb / a.nsplit), tb1 = int(int64_t(sp + 1) * a.ntb / a.nsplit);
+  const int kgroups = a.K_pad4 / 4, cgroups = a.C_pad / 4;
+
+  // loads of one step: chunk j * 4 + wave (j < 4: D kernel groups, else V
+  // channel groups), lane l takes floats 4l .. 4l + 3
+  f32x4 reg[8];
+  auto load = [&](int tb) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int ch = (j & 3) * 4 + wave;
+      const bool isd = j < 4;
+      const int g = (isd ? kb : cb) * 16 + ch;
+      const bool ok = g < (isd ? kgroups : cgroups);
+      const float* src = isd ? D + ((int64_t(tb) * kgroups + g) * nxi + xi) * 256
+                             : V + ((int64_t(tb) * cgroups + g) * nxi + xi) * 256;
+      reg[j] = ok ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src) + lane) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+  };
+  const int kq = wave >> 1, cq = wave & 1;
+  const int i = lane & 31, kk = lane >> 5;
+  // operand reads: D row k = 32 kq + i, V column c = 32 cq + i, tile 2 s + kk
+  const float* da = Ds + (kq * 8 + i / 4) * CP + kk * 4 + (i & 3);
+  const float* vb = Vs + (cq * 8 + i / 4) * CP + kk * 4 + (i & 3);
+  S::acc_t acc = S::acc_t{};
+  if (tb0 < tb1) load(tb0);
+  for (int tb = tb0; tb < tb1; ++tb) {
+    __syncthreads();                               // the previous step's reads are done
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      float* dst = (j < 4 ? Ds : Vs) + ((j & 3) * 4 + wave) * CP + lane * 4;
+      *reinterpret_cast<f32x4*>(dst) = reg[j];
+    }
+    __syncthreads();
+    if (tb + 1 < tb1) load(tb + 1);
+#pragma unroll
+    for (int s = 0; s < 32; ++s) acc = S::mma(da[s * 8], vb[s * 8], acc);
+  }
+  // part[sp][xi][k][c] over the 64-padded kernel and channel ranges
+  const int64_t kp = int64_t(a.nkb) * 64, cpn = int64_t(a.ncb) * 64;
+  float* pp = part + (int64_t(sp) * nxi + xi) * kp * cpn;
+#pragma unroll
+  for (int r = 0; r < S::NACC; ++r) {
+    const int k = kb * 64 + kq * 32 + S::acc_row(lane, r), c = cb * 64 + cq * 32 + i;
+    pp[int64_t(k) * cpn + c] = acc[r];
+  }
+}
+
+// dw[k][c] = (sum over the splits, in split order, of M[:, k, c]) x_n A'^T.
+template <int N, int MM, int R>
+__global__ void __launch_bounds__(256) k_wgrad_finish(const float* __restrict__ part, float* __restrict__ dw,
+                                                      WgArgs a, FMats fw) {
+  constexpr int A = MM + R - 1, NXI = ipow(A, N), NOUT = ipow(R, N);
+  const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  const int c = int(idx % a.C), k = int(idx / a.C);
+  if (k >= a.K) return;
+  const int64_t kp = int64_t(a.nkb) * 64, cpn = int64_t(a.ncb) * 64;
+  const float* pp = part + int64_t(k) * cpn + c;
+  float m[NXI];
+#pragma unroll
+  for (int xi = 0; xi < NXI; ++xi) {
+    float v = 0.0f;
+    for (int sp = 0; sp < a.nsplit; ++sp) v += pp[(int64_t(sp) * NXI + xi) * kp * cpn];
+    m[xi] = v;
+  }
+  float o[NOUT];
+  // A'^T of F(r, m): r x alpha, from the kernel argument
+  transform_nd<N, A, R>(m, o, MatRef<Which::AT, false, R, MM>{&fw});
+  float* dst = dw + (int64_t(k) * a.C + c) * NOUT;
+#pragma unroll
+  for (int p = 0; p < NOUT; ++p) dst[p] = o[p];
+}
+
+}  // namespace wino

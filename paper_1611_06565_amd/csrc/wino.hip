@@ -11,6 +11,7 @@
 #include "gemm_acc4.hpp"
 #include "kernels.hpp"
 #include "synth.hpp"
+#include "wgrad.hpp"
 #include "wino.h"
 
 using namespace wino;
@@ -25,6 +26,11 @@ struct wino_plan_s {
   int blk, kblk, cg, cgu;
   int32_t n_user_pts;     // the caller's points (0: default set), kept for wino_plan_adjoint
   double user_pts[kMaxAlpha];
+  // weight gradient: F(r, m) on the same points (its B^T is the forward's)
+  bool wgrad_ok;
+  FMats fmw;
+  int32_t wg_nsplit, wg_kpad4;
+  int64_t wg_d_floats, wg_part_floats;
   // k_gemm_acc tail split, fixed at plan time from the device's compute
   // units: the last xtail[x] blocks of XCD x are done in nparts parts each
   int nparts;             // 1: no split
@@ -177,6 +183,38 @@ struct Launch {
   // done as two halves each, so the last round is half as long; not with a
   // fused ReLU, which needs the whole sum.  Returns the grid size; zeroes the
   // outputs of half-split blocks first.
+  // Weight gradient (wgrad.hpp): V by the forward's input transform, D by
+  // k_dy, partial products over tile-block ranges, then their sum and A'^T.
+  static wino_status wgrad(const wino_plan_s& p, const float* x, const float* dy, float* dw, float* ws,
+                           hipStream_t s) {
+    if constexpr (BLK != 64 || CG != 4) {
+      return WINO_EUNSUPPORTED;
+    } else {
+      float* V = ws;
+      float* D = ws + p.v_floats;
+      float* part = D + p.wg_d_floats;
+      wino_status st = input(p, x, V, s);
+      if (st != WINO_OK) return st;
+      WgArgs a{};
+      a.ystride_k = 1;
+      for (int i = 0; i < N; ++i) a.ystride_k *= p.Y[i];
+      a.T = int32_t(p.T); a.T_pad = int32_t(p.T_pad); a.ntb = int32_t(p.T_pad / 64);
+      a.K = p.K; a.K_pad4 = p.wg_kpad4; a.C = p.C; a.C_pad = p.C_pad;
+      a.nkb = (p.wg_kpad4 + 63) / 64; a.ncb = (p.C_pad + 63) / 64;
+      a.nsplit = p.wg_nsplit;
+      for (int i = 0; i < 3; ++i) { a.tiles[i] = int32_t(p.tiles[i]); a.Y[i] = int32_t(p.Y[i]); }
+      const int64_t nb = int64_t(a.nsplit) * NXI * a.nkb * a.ncb;
+      a.nblocks = int32_t(nb);
+      hipLaunchKernelGGL((k_dy<N, MM, R>), dim3(unsigned(int64_t(a.ntb) * (a.K_pad4 / 4))), dim3(256), 0, s, dy,
+                         D, a, p.fmw);
+      hipLaunchKernelGGL(k_wgrad_gemm, dim3(unsigned(nb)), dim3(256), 0, s, V, D, part, a, int32_t(NXI));
+      const int64_t nkc = int64_t(p.K) * p.C;
+      hipLaunchKernelGGL((k_wgrad_finish<N, MM, R>), dim3(unsigned((nkc + 255) / 256)), dim3(256), 0, s, part,
+                         dw, a, p.fmw);
+      return launch_status();
+    }
+  }
+
   template <int TB, int KB, bool PARTS>
   static int64_t acc_setup(const wino_plan_s& p, AccArgs& a, const float* bias, float* y, hipStream_t s) {
     a.vblock = int64_t(p.nxi) * p.C_pad * TB;
@@ -423,6 +461,32 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
     }
   p.fm = to_fmats(R);
   p.const_mats = defaults;
+  // weight gradient: F(r, m) on the same points, for the sizes whose V is
+  // stored in 64-tile blocks of 4-channel groups (F(2^N, 3^N), F(4^2, 3^2))
+  {
+    p.wgrad_ok = false;
+    int cg_, cgu_, cpad_, kblk_;
+    channel_groups(N, m, r, &cg_, &cgu_, &cpad_, &kblk_);
+    if (p.blk == 64 && cg_ == 4) {
+      const RatMats Rw = synthesize(r, m, pts);
+      bool same = Rw.ok;
+      for (int i = 0; same && i < alpha; ++i)
+        for (int j = 0; same && j < alpha; ++j) same = eq(Rw.BT[i][j], R.BT[i][j]);
+      if (same) {
+        p.wgrad_ok = true;
+        p.fmw = to_fmats(Rw);
+        p.wg_kpad4 = int(round_up(K, 4));
+        const int64_t nkb = (p.wg_kpad4 + 63) / 64, ncb = (p.C_pad + 63) / 64, ntb = p.T_pad / 64;
+        const int64_t units = int64_t(p.nxi) * nkb * ncb;
+        int64_t ns = (2048 + units - 1) / units;
+        ns = ns < ntb ? ns : ntb;
+        p.wg_nsplit = int32_t(ns < 1 ? 1 : ns);
+        p.wg_d_floats = round_up(int64_t(p.nxi) * p.wg_kpad4 * p.T_pad, 64);
+        p.wg_part_floats = int64_t(p.wg_nsplit) * p.nxi * nkb * 64 * ncb * 64;
+        if (units * p.wg_nsplit > kMaxI32) p.wgrad_ok = false;
+      }
+    }
+  }
 
   wino_plan_s* h = new (std::nothrow) wino_plan_s(p);
   if (h == nullptr) return WINO_EINVAL;
@@ -482,6 +546,22 @@ wino_status wino_transform_filter(const wino_plan_t* p, const float* w, float* U
   if (!aligned16(w) || !aligned16(U)) return WINO_EINVAL;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::filter(*p, w, U, false, s); });
+}
+
+size_t wino_weight_gradient_workspace_bytes(const wino_plan_t* p) {
+  if (p == nullptr || !p->wgrad_ok) return 0;
+  return size_t(p->v_floats + p->wg_d_floats + p->wg_part_floats) * sizeof(float);
+}
+
+wino_status wino_weight_gradient(const wino_plan_t* p, const float* x, const float* dy, float* dw, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  if (p == nullptr || x == nullptr || dy == nullptr || dw == nullptr || ws == nullptr) return WINO_EINVAL;
+  if (!aligned16(x) || !aligned16(dy) || !aligned16(dw) || !aligned16(ws)) return WINO_EINVAL;
+  if (!p->wgrad_ok) return WINO_EUNSUPPORTED;
+  if (ws_bytes < wino_weight_gradient_workspace_bytes(p)) return WINO_EWORKSPACE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  float* w = static_cast<float*>(ws);
+  return dispatch<Launch>(*p, [&](auto L) { return decltype(L)::wgrad(*p, x, dy, dw, w, s); });
 }
 
 wino_status wino_transform_filter_adjoint(const wino_plan_t* p, const float* w, float* U, void* stream) {

@@ -87,6 +87,8 @@ def lib():
         "wino_points_error_growth": (i32, [i32, i32, i32, P_dbl, i32, P_dbl]),
         "wino_search_points": (i32, [i32, i32, i32, P_dbl, P_dbl]),
         "wino_plan_adjoint": (i32, [vp, ctypes.POINTER(vp)]),
+        "wino_weight_gradient_workspace_bytes": (sz, [vp]),
+        "wino_weight_gradient": (i32, [vp, vp, vp, vp, vp, sz, vp]),
         "wino_transform_filter_adjoint": (i32, [vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
@@ -184,6 +186,28 @@ class Plan:
         p._pts = None
         p._adopt(self._L, h, False)
         return p
+
+    @property
+    def weight_gradient_workspace_bytes(self):
+        return int(self._L.wino_weight_gradient_workspace_bytes(self._h))
+
+    def weight_gradient(self, x, dy, dw=None, workspace=None):
+        """dw [K][C][r^N] of this layer from its input x and output gradient dy."""
+        import torch
+        self._check_shape(x, self.input_shape, "x")
+        self._check_shape(dy, self.output_shape, "dy")
+        if dw is None:
+            dw = torch.empty(self.weight_shape, dtype=torch.float32, device="cuda")
+        self._check_shape(dw, self.weight_shape, "dw")
+        need = self.weight_gradient_workspace_bytes
+        if workspace is None:
+            workspace = torch.empty(max(need, 4) // 4, dtype=torch.float32, device="cuda")
+        _check(self._L.wino_weight_gradient(self._h, _dev_ptr(x, "x", torch.float32),
+                                            _dev_ptr(dy, "dy", torch.float32), _dev_ptr(dw, "dw", torch.float32),
+                                            _dev_ptr(workspace, "workspace"),
+                                            workspace.numel() * workspace.element_size(), _stream()),
+               "wino_weight_gradient")
+        return dw
 
     def transform_filter_adjoint(self, w, U=None):
         """U of the flipped, transposed kernels from the forward layer's w [C][K][r^N]
