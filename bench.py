@@ -249,6 +249,61 @@ def bench_stack(args):
     print(json.dumps(out), flush=True)
 
 
+def bench_wgrad(args):
+    """The weight gradient of one layer (wino_weight_gradient: input
+    transform, output-gradient transform, the product over the tiles and
+    A'^T): effective TFLOP/s over the direct FLOPs of the same layer."""
+    import numpy as np
+    import torch
+
+    from paper_1611_06565_amd.wino import Plan
+    from workloads import CONFIGS, direct_flops, draw_layer
+
+    spec = CONFIGS[args.config]
+    seed = args.config if args.seed is None else args.seed
+    x, _ = draw_layer(spec, seed=seed)
+    plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X), pad=spec.pad)
+    d = plan.desc
+    dy = np.random.default_rng(seed + 200).standard_normal(plan.output_shape, dtype=np.float32)
+    xd, dyd = torch.from_numpy(x).cuda(), torch.from_numpy(dy).cuda()
+    ws = torch.empty(plan.weight_gradient_workspace_bytes // 4, dtype=torch.float32, device="cuda")
+    dw = torch.empty(plan.weight_shape, dtype=torch.float32, device="cuda")
+    for _ in range(args.warmup):
+        plan.weight_gradient(xd, dyd, dw, ws)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    ev[0].record()
+    for i in range(args.steps):
+        plan.weight_gradient(xd, dyd, dw, ws)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    ev_ms = float(np.mean([ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]))
+    flops = direct_flops(spec)
+    gemm_flops = 2.0 * d["n_xi"] * d["T"] * spec.C * spec.K
+    check = None
+    if not args.no_check:
+        from oracle.metric import normalised_error
+        from oracle.wgrad import direct_wgrad
+        ref, den = direct_wgrad(x, dy, spec.r, spec.pad)
+        check = normalised_error(dw.cpu().numpy(), ref, den)["max"]
+    out = {
+        "metric": "effective TFLOP/s of a conv layer's weight gradient (direct FLOPs)",
+        "value": flops / (ms_step * 1e-3) / 1e12, "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "weight gradient of F(%d^%d,3^%d) %d-D conv layer: batch %d, C=%d, K=%d, %s, pad %d"
+                               % (spec.m, spec.N, spec.N, spec.N, spec.batch, spec.C, spec.K,
+                                  "x".join(str(v) for v in spec.X), spec.pad)},
+        "call_ms_events": ev_ms,
+        # the product over the tiles, 2 * alpha^N * T * C * K FLOP, over the whole call
+        "gemm_tflops_over_call": gemm_flops / (ev_ms * 1e-3) / 1e12,
+        "max_normalised_error": check,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -258,6 +313,8 @@ def main():
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5],
                     help="layer family (default 2, the F(2^3,3^3) C=64 K=128 video layer; "
                          "5 = the C3D-style stack)")
+    ap.add_argument("--wgrad", action="store_true",
+                    help="time the layer's weight gradient dw from x and dy instead of its forward")
     ap.add_argument("--adjoint", action="store_true",
                     help="time the layer's data gradient dx = adjoint(dy) instead of its forward")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -286,6 +343,9 @@ def main():
         return
     if args.config == 5:
         bench_stack(args)
+        return
+    if args.wgrad:
+        bench_wgrad(args)
         return
 
     from paper_1611_06565_amd.wino import Plan

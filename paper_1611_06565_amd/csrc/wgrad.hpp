@@ -19,7 +19,8 @@
 //
 //   k_dy          D[xi][k][t] = (dy_t[k] x_n G')[xi], layout of V
 //   k_wgrad_gemm  partial M_xi over a range of tile blocks, fp32 MFMA
-//   k_wgrad_finish  sum of the partials (fixed order), then A'^T
+//   k_wgrad_sum     sum of the partials (fixed order)
+//   k_wgrad_finish  A'^T
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -157,7 +158,25 @@ __global__ void __launch_bounds__(256) k_wgrad_gemm(const float* __restrict__ V,
   }
 }
 
-// dw[k][c] = (sum over the splits, in split order, of M[:, k, c]) x_n A'^T.
+// M[xi][k][c] = sum over the splits, in split order; written over split 0's
+// partial (each entry is read and written by its own thread only).  One
+// thread per (xi, k, c), channels fastest, so the partial reads coalesce and
+// the split loads of a thread are independent.
+__global__ void __launch_bounds__(256) k_wgrad_sum(float* __restrict__ part, WgArgs a, int32_t nxi) {
+  const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  const int c = int(idx % a.C);
+  const int64_t r = idx / a.C;
+  const int k = int(r % a.K), xi = int(r / a.K);
+  if (xi >= nxi) return;
+  const int64_t kp = int64_t(a.nkb) * 64, cpn = int64_t(a.ncb) * 64, plane = int64_t(nxi) * kp * cpn;
+  float* pp = part + (int64_t(xi) * kp + k) * cpn + c;
+  float v = 0.0f;
+#pragma unroll 8
+  for (int sp = 0; sp < a.nsplit; ++sp) v += pp[sp * plane];
+  pp[0] = v;
+}
+
+// dw[k][c] = M[:, k, c] x_n A'^T, M summed over the splits by k_wgrad_sum.
 template <int N, int MM, int R>
 __global__ void __launch_bounds__(256) k_wgrad_finish(const float* __restrict__ part, float* __restrict__ dw,
                                                       WgArgs a, FMats fw) {
@@ -169,11 +188,7 @@ __global__ void __launch_bounds__(256) k_wgrad_finish(const float* __restrict__ 
   const float* pp = part + int64_t(k) * cpn + c;
   float m[NXI];
 #pragma unroll
-  for (int xi = 0; xi < NXI; ++xi) {
-    float v = 0.0f;
-    for (int sp = 0; sp < a.nsplit; ++sp) v += pp[(int64_t(sp) * NXI + xi) * kp * cpn];
-    m[xi] = v;
-  }
+  for (int xi = 0; xi < NXI; ++xi) m[xi] = pp[int64_t(xi) * kp * cpn];
   float o[NOUT];
   // A'^T of F(r, m): r x alpha, from the kernel argument
   transform_nd<N, A, R>(m, o, MatRef<Which::AT, false, R, MM>{&fw});

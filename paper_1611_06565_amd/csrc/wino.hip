@@ -209,6 +209,8 @@ struct Launch {
                          D, a, p.fmw);
       hipLaunchKernelGGL(k_wgrad_gemm, dim3(unsigned(nb)), dim3(256), 0, s, V, D, part, a, int32_t(NXI));
       const int64_t nkc = int64_t(p.K) * p.C;
+      hipLaunchKernelGGL(k_wgrad_sum, dim3(unsigned((nkc * NXI + 255) / 256)), dim3(256), 0, s, part, a,
+                         int32_t(NXI));
       hipLaunchKernelGGL((k_wgrad_finish<N, MM, R>), dim3(unsigned((nkc + 255) / 256)), dim3(256), 0, s, part,
                          dw, a, p.fmw);
       return launch_status();
@@ -483,7 +485,8 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
         p.wg_nsplit = int32_t(ns < 1 ? 1 : ns);
         p.wg_d_floats = round_up(int64_t(p.nxi) * p.wg_kpad4 * p.T_pad, 64);
         p.wg_part_floats = int64_t(p.wg_nsplit) * p.nxi * nkb * 64 * ncb * 64;
-        if (units * p.wg_nsplit > kMaxI32) p.wgrad_ok = false;
+        if (units * p.wg_nsplit > kMaxI32) p.wgrad_ok = false;                      // product grid
+        if (int64_t(K) * C * p.nxi > kMaxI32 * int64_t(256)) p.wgrad_ok = false;   // sum grid
       }
     }
   }
