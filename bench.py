@@ -32,7 +32,8 @@ PEAK_HBM = 8000.0           # GB/s, MI355X HBM3E
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["paper_1611_06565_amd/csrc/kernels.hpp", "paper_1611_06565_amd/csrc/gemm_acc.hpp",
                   "paper_1611_06565_amd/csrc/gemm_acc4.hpp", "paper_1611_06565_amd/csrc/transforms.hpp",
-                  "paper_1611_06565_amd/csrc/synth.hpp", "paper_1611_06565_amd/csrc/wino.hip"]
+                  "paper_1611_06565_amd/csrc/synth.hpp", "paper_1611_06565_amd/csrc/wgrad.hpp",
+                  "paper_1611_06565_amd/csrc/wino.hip"]
 
 
 def kernel_hash():

@@ -44,16 +44,21 @@ struct WgArgs {
   int32_t tiles[3], Y[3];
 };
 
-// One thread per (tile, kernel): lane = 4 * tile + kernel % 4 within a (tile
-// block, kernel group), so every element's 64 x 4 values are stored as one
-// contiguous 1 KB run.  Outputs past Y (partial tiles) and padding tiles and
-// kernels read as zero.
+// One thread per (tile, kernel) of a (tile block, kernel group): lane = tile,
+// wave = kernel % 4, so a wave reads one kernel's output gradients at 64
+// consecutive tiles (neighbouring lanes, neighbouring outputs).  The values
+// then cross an LDS stage (tiles padded to 5 floats, conflict-free writes) so
+// that every element's 64 x 4 values are stored as one contiguous 1 KB run.
+// Outputs past Y (partial tiles) and padding tiles and kernels read as zero.
 template <int N, int MM, int R>
 __global__ void __launch_bounds__(256) k_dy(const float* __restrict__ dy, float* __restrict__ D, WgArgs a,
                                             FMats fw) {
   constexpr int A = MM + R - 1, NXI = ipow(A, N), NIN = ipow(MM, N);
+  constexpr int XR = NXI < 16 ? NXI : 16;          // elements per LDS round
+  constexpr int TP = 5;                            // padded tile stride in the stage
+  __shared__ float stage[XR][64 * TP];
   const int tb = int(blockIdx.x) / (a.K_pad4 / 4), kg = int(blockIdx.x) % (a.K_pad4 / 4);
-  const int tl = int(threadIdx.x) >> 2, kl = int(threadIdx.x) & 3;
+  const int tl = int(threadIdx.x) & 63, kl = int(threadIdx.x) >> 6;
   const int t = tb * 64 + tl, k = kg * 4 + kl;
   float g[NIN];
   if (t < a.T && k < a.K) {
@@ -65,18 +70,12 @@ __global__ void __launch_bounds__(256) k_dy(const float* __restrict__ dy, float*
       int64_t off = 0;
       bool in = true;
       int rem = i;
-#pragma unroll
-      for (int ax = N - 1; ax >= 0; --ax) {
-        const int yc = ti[ax] * MM + rem % MM;
-        rem /= MM;
-        in = in && yc < a.Y[ax];
-      }
-      rem = i;
       int64_t mul = 1;
 #pragma unroll
       for (int ax = N - 1; ax >= 0; --ax) {
         const int yc = ti[ax] * MM + rem % MM;
         rem /= MM;
+        in = in && yc < a.Y[ax];
         off += int64_t(yc) * mul;
         mul *= a.Y[ax];
       }
@@ -90,8 +89,18 @@ __global__ void __launch_bounds__(256) k_dy(const float* __restrict__ dy, float*
   // G' of F(r, m): alpha x m, from the kernel argument
   transform_nd<N, MM, A>(g, u, MatRef<Which::G, false, R, MM>{&fw});
   float* dst = D + (int64_t(tb) * (a.K_pad4 / 4) + kg) * NXI * 256 + threadIdx.x;
+  const int rd = (int(threadIdx.x) >> 2) * TP + (int(threadIdx.x) & 3);   // (tile, kernel) of the store
 #pragma unroll
-  for (int xi = 0; xi < NXI; ++xi) __builtin_nontemporal_store(u[xi], dst + xi * 256);
+  for (int x0 = 0; x0 < NXI; x0 += XR) {
+    if (x0 > 0) __syncthreads();                   // the previous round has been read
+#pragma unroll
+    for (int j = 0; j < XR; ++j)
+      if (x0 + j < NXI) stage[j][tl * TP + kl] = u[x0 + j];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < XR; ++j)
+      if (x0 + j < NXI) __builtin_nontemporal_store(stage[j][rd], dst + (x0 + j) * 256);
+  }
 }
 
 // Partial M_xi over tile blocks [tb0, tb1) for one 64-kernel x 64-channel
