@@ -858,4 +858,30 @@ __global__ void __launch_bounds__(256) k_maxpool3d(const float* __restrict__ x, 
   y[i] = best;
 }
 
+// The same for a last-axis window of 2 on rows of a multiple of 4 values:
+// one thread per pair of neighbouring outputs reads each window row as one
+// aligned 16-byte load and writes the pair as 8 bytes.
+__global__ void __launch_bounds__(256) k_maxpool3d_pair(const float* __restrict__ x, float* __restrict__ y,
+                                                        PoolArgs a) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;   // output pair
+  if (i >= a.total / 2) return;
+  int64_t r = i;
+  const int h = int(r % (a.Y[2] / 2)); r /= a.Y[2] / 2;
+  const int y1 = int(r % a.Y[1]); r /= a.Y[1];
+  const int y0 = int(r % a.Y[0]); r /= a.Y[0];
+  const float* src = x + r * (int64_t(a.X[0]) * a.X[1] * a.X[2]) + 4 * h;
+  float b0 = -__builtin_inff(), b1 = -__builtin_inff();
+  for (int i0 = 0; i0 < a.p[0]; ++i0)
+    for (int i1 = 0; i1 < a.p[1]; ++i1) {
+      const float4 v = *reinterpret_cast<const float4*>(
+          src + (int64_t(y0 * a.p[0] + i0) * a.X[1] + (y1 * a.p[1] + i1)) * a.X[2]);
+      // the one-output kernel's comparisons, in its order
+      b0 = v.x > b0 ? v.x : b0;
+      b0 = v.y > b0 ? v.y : b0;
+      b1 = v.z > b1 ? v.z : b1;
+      b1 = v.w > b1 ? v.w : b1;
+    }
+  *reinterpret_cast<float2*>(y + 2 * i) = make_float2(b0, b1);
+}
+
 }  // namespace wino

@@ -657,7 +657,12 @@ wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const flo
   }
   a.total = total;
   const hipStream_t s = static_cast<hipStream_t>(stream);
-  hipLaunchKernelGGL(k_maxpool3d, dim3(unsigned((total + 255) / 256)), dim3(256), 0, s, x, y, a);
+  if (a.p[2] == 2 && a.X[2] % 4 == 0) {
+    // Y_3 = X_3 / 2 is even: whole output pairs, 16-byte aligned input rows
+    hipLaunchKernelGGL(k_maxpool3d_pair, dim3(unsigned((total / 2 + 255) / 256)), dim3(256), 0, s, x, y, a);
+  } else {
+    hipLaunchKernelGGL(k_maxpool3d, dim3(unsigned((total + 255) / 256)), dim3(256), 0, s, x, y, a);
+  }
   return launch_status();
 }
 

@@ -271,11 +271,17 @@ def test_maxpool_matches_oracle():
     torch = require_gpu()
     from paper_1611_06565_amd.wino import maxpool3d
     rng = np.random.default_rng(1)
-    x = rng.standard_normal((2, 3, 5, 9, 7)).astype(np.float32)
-    for win in [(1, 2, 2), (2, 2, 2), (2, 3, 1)]:
-        y = maxpool3d(torch.from_numpy(x).cuda(), win)
-        torch.cuda.synchronize()
-        assert np.array_equal(y.cpu().numpy(), maxpool(x, win))
+    # odd rows: the one-output-per-thread kernel; rows of a multiple of 4 with
+    # a last-axis window of 2: the output-pair kernel (odd leading extents,
+    # floors on every axis)
+    for shape in [(2, 3, 5, 9, 7), (2, 3, 5, 9, 12), (1, 2, 3, 7, 8), (3, 1, 4, 6, 4)]:
+        x = rng.standard_normal(shape).astype(np.float32)
+        for win in [(1, 2, 2), (2, 2, 2), (2, 3, 1), (1, 1, 2), (3, 3, 2)]:
+            if any(s // w < 1 for s, w in zip(shape[2:], win)):
+                continue
+            y = maxpool3d(torch.from_numpy(x).cuda(), win)
+            torch.cuda.synchronize()
+            assert np.array_equal(y.cpu().numpy(), maxpool(x, win)), (shape, win)
 
 
 def test_small_c3d_stack_per_layer():
