@@ -227,6 +227,35 @@ def bench_stack(args):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.graph:
+        # the whole step (26 launches) captured once as a HIP graph and replayed
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            step()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+        flops = [direct_flops(spec) for spec, *_ in layers]
+        print(json.dumps({
+            "metric": "effective TFLOP/s of the C3D-style 3-D stack forward (direct FLOPs; kernels transformed once)",
+            "value": sum(flops) / (ms_step * 1e-3) / 1e12, "unit": "TFLOP/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+            "config": {"workload": "C3D-style stack: batch 4, 3x16x112x112, eight 3x3x3 pad-1 layers "
+                                   "(64, 128, 256, 256, 512 x4), ReLU, max-pools; F(2^3,3^3); one HIP graph "
+                                   "per step"}}), flush=True)
+        return
     nev = len(layers) + 1
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
     t0 = time.perf_counter()
@@ -314,6 +343,8 @@ def main():
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5],
                     help="layer family (default 2, the F(2^3,3^3) C=64 K=128 video layer; "
                          "5 = the C3D-style stack)")
+    ap.add_argument("--graph", action="store_true",
+                    help="with --config 5: replay each step as one captured HIP graph")
     ap.add_argument("--wgrad", action="store_true",
                     help="time the layer's weight gradient dw from x and dy instead of its forward")
     ap.add_argument("--adjoint", action="store_true",
