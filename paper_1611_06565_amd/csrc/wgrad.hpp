@@ -20,7 +20,7 @@
 //   k_dy          D[xi][k][t] = (dy_t[k] x_n G')[xi], layout of V
 //   k_wgrad_gemm  partial M_xi over a range of tile blocks, fp32 MFMA
 //   k_wgrad_sum     sum of the partials (fixed order)
-//   k_wgrad_finish  A'^T
+//   k_wgrad_finish  A'^T, one output tap per thread
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -185,25 +185,40 @@ __global__ void __launch_bounds__(256) k_wgrad_sum(float* __restrict__ part, WgA
   pp[0] = v;
 }
 
-// dw[k][c] = M[:, k, c] x_n A'^T, M summed over the splits by k_wgrad_sum.
+// dw[k][c][p] = sum_xi (prod over the axes of A'^T[p_ax][xi_ax]) M[xi][k][c],
+// M summed over the splits by k_wgrad_sum: the N-mode product with A'^T
+// written as one sum per output tap.  One thread per (k, p, c), channels
+// fastest, so the M reads of a wave coalesce.
 template <int N, int MM, int R>
 __global__ void __launch_bounds__(256) k_wgrad_finish(const float* __restrict__ part, float* __restrict__ dw,
                                                       WgArgs a, FMats fw) {
   constexpr int A = MM + R - 1, NXI = ipow(A, N), NOUT = ipow(R, N);
   const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  const int c = int(idx % a.C), k = int(idx / a.C);
+  const int c = int(idx % a.C);
+  const int64_t rest = idx / a.C;
+  const int p = int(rest % NOUT), k = int(rest / NOUT);
   if (k >= a.K) return;
+  int pa[3] = {0, 0, 0};                           // the tap's index per axis
+  {
+    int q = p;
+#pragma unroll
+    for (int ax = N - 1; ax >= 0; --ax) { pa[ax] = q % R; q /= R; }
+  }
   const int64_t kp = int64_t(a.nkb) * 64, cpn = int64_t(a.ncb) * 64;
   const float* pp = part + int64_t(k) * cpn + c;
-  float m[NXI];
+  float acc = 0.0f;
 #pragma unroll
-  for (int xi = 0; xi < NXI; ++xi) m[xi] = pp[int64_t(xi) * kp * cpn];
-  float o[NOUT];
-  // A'^T of F(r, m): r x alpha, from the kernel argument
-  transform_nd<N, A, R>(m, o, MatRef<Which::AT, false, R, MM>{&fw});
-  float* dst = dw + (int64_t(k) * a.C + c) * NOUT;
+  for (int xi = 0; xi < NXI; ++xi) {
+    float coef = 1.0f;
+    int q = xi;
 #pragma unroll
-  for (int p = 0; p < NOUT; ++p) dst[p] = o[p];
+    for (int ax = N - 1; ax >= 0; --ax) {
+      coef *= fw.AT[pa[ax]][q % A];
+      q /= A;
+    }
+    if (coef != 0.0f) acc = __builtin_fmaf(coef, pp[int64_t(xi) * kp * cpn], acc);
+  }
+  dw[(int64_t(k) * a.C + c) * NOUT + p] = acc;
 }
 
 }  // namespace wino

@@ -211,7 +211,8 @@ struct Launch {
       const int64_t nkc = int64_t(p.K) * p.C;
       hipLaunchKernelGGL(k_wgrad_sum, dim3(unsigned((nkc * NXI + 255) / 256)), dim3(256), 0, s, part, a,
                          int32_t(NXI));
-      hipLaunchKernelGGL((k_wgrad_finish<N, MM, R>), dim3(unsigned((nkc + 255) / 256)), dim3(256), 0, s, part,
+      const int64_t ntap = nkc * ipow(R, N);
+      hipLaunchKernelGGL((k_wgrad_finish<N, MM, R>), dim3(unsigned((ntap + 255) / 256)), dim3(256), 0, s, part,
                          dw, a, p.fmw);
       return launch_status();
     }
@@ -486,7 +487,8 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
         p.wg_d_floats = round_up(int64_t(p.nxi) * p.wg_kpad4 * p.T_pad, 64);
         p.wg_part_floats = int64_t(p.wg_nsplit) * p.nxi * nkb * 64 * ncb * 64;
         if (units * p.wg_nsplit > kMaxI32) p.wgrad_ok = false;                      // product grid
-        if (int64_t(K) * C * p.nxi > kMaxI32 * int64_t(256)) p.wgrad_ok = false;   // sum grid
+        if (int64_t(K) * C * (p.nxi > r * r * r ? p.nxi : r * r * r) > kMaxI32 * int64_t(256))
+          p.wgrad_ok = false;                                                        // sum and tap grids
       }
     }
   }
