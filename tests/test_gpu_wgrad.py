@@ -32,6 +32,12 @@ WG = [
     ("f2x3_3d_one_tile", 3, 2, 3, 1, 3, 2, (3, 3, 3), 0),
     ("f4x3_2d", 2, 4, 3, 3, 36, 70, (17, 23), 1),
     ("f4x3_2d_c130", 2, 4, 3, 2, 130, 20, (12, 9), 1),
+    # edges: one channel and one kernel, a pad wider than r - 1 (windows
+    # entirely in the padding), odd extents (partial tiles on every axis)
+    ("f2x3_3d_c1k1", 3, 2, 3, 1, 1, 1, (5, 4, 6), 1),
+    ("f2x3_2d_pad3", 2, 2, 3, 2, 3, 5, (6, 7), 3),
+    ("f2x3_3d_odd", 3, 2, 3, 3, 5, 66, (7, 5, 9), 0),
+    ("f4x3_2d_c1", 2, 4, 3, 1, 1, 9, (10, 13), 2),
 ]
 
 
