@@ -128,10 +128,10 @@ size_t wino_filter_bytes(const wino_plan_t* plan);
  * input V (float32), laid out tile-block major as
  * V[T_pad/B][C_pad/CG][alpha^N][B][CG] with B = block_tiles: element
  * (xi, c, t) sits at (((t/B)*C_pad/CG + c/CG)*alpha^N + xi)*B*CG + (t%B)*CG
- * + c%CG.  For F(2^N, 3^N) the product's 64 x 64 blocks that would run in a
- * last, partly filled round of resident work-groups on the device current at
- * wino_plan (gemm_tail_blocks) are split by element passes into gemm_parts
- * work-groups each, and a scratch area for their partial outputs follows V
+ * + c%CG.  For F(2^N, 3^N) and F(4^2, 3^2) the product's blocks (64 tiles x 64
+ * or 32 kernels) that would run in a last, partly filled round of resident
+ * work-groups on the device current at wino_plan (gemm_tail_blocks) are split
+ * by element passes into gemm_parts work-groups each, and a scratch area for their partial outputs follows V
  * (at V's size rounded up to 256 bytes); wino_gemm_inverse overwrites it.
  * The split is fixed when the plan is made and the partials are summed in a
  * fixed order, so a plan's results are bitwise reproducible. */

@@ -41,18 +41,15 @@ struct AccArgs {
   // Work per XCD (work-group b runs on XCD b % 8 as its unit b / 8): XCD x
   // owns blocks xb0[x] .. xb0[x] + xn[x] - 1, whole blocks first.  Its last
   // xs[x] blocks (those past its last full round of resident work-groups, or
-  // all of them when it has fewer than a round) are tail blocks, split by
-  // passes so the last round is shorter:
-  //  - k_gemm_acc4: two halves each, added onto zeroed outputs (no ReLU);
-  //  - k_gemm_acc: nparts parts each, 1/nparts of the passes apiece, whose
-  //    partial outputs go to part[(xt0[x] + s) * nparts + q][o][t][k] (tail
-  //    block s of XCD x, part q; 64 x 64 per output index o); k_part_reduce
-  //    sums them in part order and applies bias and ReLU.
+  // all of them when it has fewer than a round) are tail blocks, split into
+  // nparts parts of contiguous passes so the last round is shorter; the
+  // parts' partial outputs go to part[(xt0[x] + s) * nparts + q][o][t][k]
+  // (tail block s of XCD x, part q; TB x KB per output index o), and
+  // k_part_reduce sums them in part order and applies bias and ReLU.
   int32_t xb0[8], xn[8], xs[8], xt0[8];
   int32_t tiles[3], Y[3];
   int32_t relu;
-  const float* bias;  // [K] or null: b_k of eq. (2), added before the ReLU (by the
-                      // first half of a split k_gemm_acc4 block only)
+  const float* bias;  // [K] or null: b_k of eq. (2), added before the ReLU
   float* part;
   int32_t nparts;
 };
@@ -480,14 +477,15 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
   }
 }
 
-// Tail blocks of k_gemm_acc: y = ReLU(sum over the parts, in part order, +
-// bias) for every output of every tail block.  One thread per (tail block,
+// Tail blocks of k_gemm_acc (TB x KB = 64 x 64) and k_gemm_acc4 (64 x 32):
+// y = ReLU(sum over the parts, in part order, + bias) for every output of
+// every tail block.  One thread per (tail block,
 // output index, tile, kernel); lanes over kernels read the partials
 // contiguously, and the part loads are independent (issued together), the
 // adds in fixed order, so the results are bitwise reproducible.
-template <int N, int MM>
+template <int N, int MM, int TB, int KB>
 __global__ void __launch_bounds__(256) k_part_reduce(float* __restrict__ y, AccArgs g, int32_t ntail) {
-  constexpr int NOUT = ipow(MM, N), TB = 64, KB = 64;
+  constexpr int NOUT = ipow(MM, N);
   const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;   // ((tail block, o), tile, kernel)
   const int k_l = int(i % KB), tl = int((i / KB) % TB);
   const int64_t bo = i / (KB * TB);
@@ -518,43 +516,6 @@ __global__ void __launch_bounds__(256) k_part_reduce(float* __restrict__ y, AccA
   if (g.bias != nullptr) v += g.bias[kg];
   if (g.relu) v = v > 0.0f ? v : 0.0f;
   y[(int64_t(n) * g.K + kg) * g.ystride_k + off] = v;
-}
-
-// Zero the outputs of the blocks done in two halves (the last xs[x] blocks of
-// each XCD's range): a block covers the TB tiles of tile block tb and the KB
-// kernels of kernel block kb, every output of a tile (m^N) inside the output
-// extent.
-template <int N, int MM, int TB, int KB>
-__global__ void __launch_bounds__(256) k_zero_split(float* __restrict__ y, AccArgs g) {
-  constexpr int NOUT = ipow(MM, N);
-  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;   // (split block j, tile, output)
-  const int o = int(i % NOUT), tl = int((i / NOUT) % TB);
-  int j = int(i / (NOUT * TB)), blk = -1;
-#pragma unroll
-  for (int x = 0; x < 8; ++x) {
-    if (blk < 0 && j < g.xs[x]) blk = g.xb0[x] + g.xn[x] - g.xs[x] + j;
-    else if (blk < 0) j -= g.xs[x];
-  }
-  if (blk < 0) return;
-  const int tb = blk / g.nkb, kb = blk % g.nkb;
-  const int t = tb * TB + tl;
-  if (t >= g.T) return;
-  int ti[3] = {0, 0, 0};
-  const int n = split_tile<N>(t, g.tiles, ti);
-  int64_t off = 0;
-#pragma unroll
-  for (int ax = 0; ax < N; ++ax) {
-    const int oa = (o / ipow(MM, N - 1 - ax)) % MM;
-    const int yc = ti[ax] * MM + oa;
-    if (yc >= g.Y[ax]) return;
-    off = off * g.Y[ax] + yc;
-  }
-  float* yo = y + int64_t(n) * g.K * g.ystride_k + off;
-  for (int kl = 0; kl < KB; ++kl) {
-    const int kg = kb * KB + kl;
-    if (kg >= g.K) break;
-    yo[int64_t(kg) * g.ystride_k] = 0.0f;
-  }
 }
 
 }  // namespace wino

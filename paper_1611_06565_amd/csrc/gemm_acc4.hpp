@@ -106,16 +106,19 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
   const int tq = wave >> 1, kq = wave & 1;        // 32-tile half and 16-kernel half of the block
   const int row = lane & 15, kr = lane >> 4;      // MFMA operand row / column and lane group
 
-  // Work unit -> (block, passes), as in k_gemm_acc.
+  // Work unit -> (block, passes), as in k_gemm_acc; the 18 passes of a tail
+  // block are split into nparts contiguous runs of 2 or 3.
   const int xcd = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3;
-  const int xn = g.xn[xcd], xs = g.xs[xcd];
-  if (j >= xn + xs) return;
+  const int xn = g.xn[xcd], xs = g.xs[xcd], np = g.nparts;
   const int nwhole = xn - xs;
-  const bool split = j >= nwhole;
-  const int blk = g.xb0[xcd] + (split ? nwhole + (j - nwhole) / 2 : j);
-  const int p0 = split ? ((j - nwhole) & 1) * (G::NPASS / 2) : 0;
-  const int npass = split ? G::NPASS / 2 : G::NPASS;
-  static_assert(G::NPASS % 2 == 0, "halves of whole passes");
+  if (j >= nwhole + xs * np) return;
+  const bool tail = j >= nwhole;
+  const int tj = tail ? j - nwhole : 0;           // unit among the XCD's tail units
+  const int blk = g.xb0[xcd] + (tail ? nwhole + tj / np : j);
+  const int prt = tj % np;
+  const int p0 = tail ? prt * G::NPASS / np : 0;
+  const int npass = tail ? (prt + 1) * G::NPASS / np - p0 : G::NPASS;
+  const int64_t pslot = tail ? int64_t(g.xt0[xcd]) * np + tj : 0;   // partial-output slot
   const int tb = blk / g.nkb, kb = blk % g.nkb;
   const int nstage = g.C_pad / G::SC;             // channel stages per pass
   const int nsteps = npass * nstage;
@@ -315,6 +318,20 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
   // axis) per round; thread (ol, tl) stores its tile's output ol of the last
   // axis for every kernel, so neighbouring lanes store neighbouring outputs.
   __builtin_amdgcn_s_waitcnt(0x0f70);             // vmcnt(0): no copy still writes LDS
+  if (tail) {
+    // partial outputs of this unit: part[pslot][o][t][k], lanes over k
+    float* pp = g.part + pslot * G::NOUT * (TB * KB);
+#pragma unroll
+    for (int o = 0; o < G::NOUT; ++o)
+#pragma unroll
+      for (int h = 0; h < NH; ++h)
+#pragma unroll
+        for (int r = 0; r < NACC; ++r) {
+          const int tt = tq * 32 + h * 16 + S::acc_row(lane, r), k = kq * 16 + row;
+          pp[(o * TB + tt) * KB + k] = yacc[o][h][r];
+        }
+    return;
+  }
   // the block's bias values go through LDS: a global load inside the store
   // loop would make its stores wait for each other (vmcnt counts both)
   __shared__ float bsm[KB];
@@ -357,16 +374,9 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
           const int kg = kb * KB + kl;
           if (kg >= g.K) break;
           float v = pl[kl * TB + (tl ^ (kl & 31))];
-          if (split) {
-            // two partials onto zero: 0 + a + b rounds the same in either
-            // order; the bias joins the first half's partial
-            if (g.bias != nullptr && p0 == 0) v += bsm[kl];
-            unsafeAtomicAdd(yo + int64_t(kg) * g.ystride_k, v);
-          } else {
-            if (g.bias != nullptr) v += bsm[kl];
-            if (g.relu) v = v > 0.0f ? v : 0.0f;
-            __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
-          }
+          if (g.bias != nullptr) v += bsm[kl];
+          if (g.relu) v = v > 0.0f ? v : 0.0f;
+          __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
         }
       }
     }

@@ -175,14 +175,6 @@ struct Launch {
     return launch_status();
   }
 
-  // Per-XCD work ranges of a pass-accumulating GEMM (k_gemm_acc, k_gemm_acc4):
-  // work-groups go to the 8 XCDs round-robin; each XCD takes a contiguous
-  // range of blocks.  With PARTS (k_gemm_acc) the plan's tail blocks of each
-  // XCD are split into p.nparts parts.  Otherwise (k_gemm_acc4) the blocks
-  // past an XCD's last full round of resident work-groups (two per CU) are
-  // done as two halves each, so the last round is half as long; not with a
-  // fused ReLU, which needs the whole sum.  Returns the grid size; zeroes the
-  // outputs of half-split blocks first.
   // Weight gradient (wgrad.hpp): V by the forward's input transform, D by
   // k_dy, partial products over tile-block ranges, then their sum and A'^T.
   static wino_status wgrad(const wino_plan_s& p, const float* x, const float* dy, float* dw, float* ws,
@@ -218,8 +210,12 @@ struct Launch {
     }
   }
 
-  template <int TB, int KB, bool PARTS>
-  static int64_t acc_setup(const wino_plan_s& p, AccArgs& a, const float* bias, float* y, hipStream_t s) {
+  // Per-XCD work ranges of a pass-accumulating GEMM (k_gemm_acc, k_gemm_acc4):
+  // work-groups go to the 8 XCDs round-robin; each XCD takes a contiguous
+  // range of blocks, and the plan's tail blocks of each XCD are split into
+  // p.nparts parts.  Returns the grid size.
+  template <int TB, int KB>
+  static int64_t acc_setup(const wino_plan_s& p, AccArgs& a, const float* bias) {
     a.vblock = int64_t(p.nxi) * p.C_pad * TB;
     a.uplane = int64_t(p.C_pad) * p.K_pad;
     a.ystride_k = 1;
@@ -230,29 +226,17 @@ struct Launch {
     for (int i = 0; i < 3; ++i) { a.tiles[i] = int32_t(p.tiles[i]); a.Y[i] = int32_t(p.Y[i]); }
     a.relu = (p.flags & WINO_RELU) ? 1 : 0;
     a.bias = bias;
-    a.nparts = PARTS ? p.nparts : 1;
+    a.nparts = p.nparts;
     constexpr int NX = 8;
-    const int64_t slots = 2 * int64_t(cu_count() / NX);
-    int64_t maxu = 0, nsplit = 0, t0 = 0;
+    int64_t maxu = 0, t0 = 0;
     for (int x = 0; x < NX; ++x) {
       const int64_t n = nb / NX + (x < nb % NX ? 1 : 0);
       const int64_t b0 = x * (nb / NX) + (x < nb % NX ? x : nb % NX);
-      int64_t sx = 0, units = n;
-      if (PARTS) {
-        sx = p.nparts > 1 ? p.xtail[x] : 0;
-        units = n - sx + sx * p.nparts;
-      } else if (!a.relu && slots > 0) {
-        sx = n < slots ? n : n % slots;
-        units = n + sx;
-        nsplit += sx;
-      }
+      const int64_t sx = p.nparts > 1 ? p.xtail[x] : 0;
+      const int64_t units = n - sx + sx * p.nparts;
       a.xb0[x] = int32_t(b0); a.xn[x] = int32_t(n); a.xs[x] = int32_t(sx); a.xt0[x] = int32_t(t0);
-      t0 += PARTS ? sx : 0;
+      t0 += sx;
       maxu = maxu > units ? maxu : units;
-    }
-    if (nsplit > 0) {
-      const int64_t items = nsplit * TB * ipow(MM, N);
-      hipLaunchKernelGGL((k_zero_split<N, MM, TB, KB>), dim3(unsigned((items + 255) / 256)), dim3(256), 0, s, y, a);
     }
     return NX * maxu;
   }
@@ -263,24 +247,30 @@ struct Launch {
     if constexpr (KIND == 0) {
       using G = AccGeom<N, MM, R>;
       AccArgs a{};
-      // small grids: each block's passes split over p.nparts units, whose
-      // partial outputs (after V in the workspace) are summed in order
+      // tail blocks: passes split over p.nparts units, whose partial outputs
+      // (after V in the workspace) are summed in order
       a.part = part;
-      const int64_t grid = acc_setup<G::TB, G::KB, true>(p, a, bias, y, s);
+      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, bias);
       hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST>), dim3(unsigned(grid)), dim3(G::NT), 0, s, V, U, y, a,
                          p.fm);
       if (p.nparts > 1) {
         const int64_t items = p.ntail * ipow(MM, N) * G::TB * G::KB;
-        hipLaunchKernelGGL((k_part_reduce<N, MM>), dim3(unsigned((items + 255) / 256)), dim3(256), 0, s, y, a,
-                           int32_t(p.ntail));
+        hipLaunchKernelGGL((k_part_reduce<N, MM, G::TB, G::KB>), dim3(unsigned((items + 255) / 256)), dim3(256),
+                           0, s, y, a, int32_t(p.ntail));
       }
       return launch_status();
     } else if constexpr (KIND == 1) {
       using G = Acc4Geom<N, MM, R>;
       AccArgs a{};
-      const int64_t grid = acc_setup<G::TB, G::KB, false>(p, a, bias, y, s);
+      a.part = part;
+      const int64_t grid = acc_setup<G::TB, G::KB>(p, a, bias);
       hipLaunchKernelGGL((k_gemm_acc4<N, MM, R, CONST>), dim3(unsigned(grid)), dim3(G::NT), 0, s, V, U, y, a,
                          p.fm);
+      if (p.nparts > 1) {
+        const int64_t items = p.ntail * ipow(MM, N) * G::TB * G::KB;
+        hipLaunchKernelGGL((k_part_reduce<N, MM, G::TB, G::KB>), dim3(unsigned((items + 255) / 256)), dim3(256),
+                           0, s, y, a, int32_t(p.ntail));
+      }
       return launch_status();
     } else {
       using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
@@ -402,8 +392,10 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   p.part_floats = 0;
   for (int x = 0; x < 8; ++x) p.xtail[x] = 0;
   const int cus = cu_count();
-  if (m == 2 && !(o.flags & WINO_NO_SPLIT) && cus >= 8) {
-    const int64_t nb = (p.T_pad / 64) * (p.K_pad / 64);
+  const bool acc4 = N == 2 && m == 4 && r == 3;   // k_gemm_acc4: 64 x 32 blocks
+  if ((m == 2 || acc4) && !(o.flags & WINO_NO_SPLIT) && cus >= 8) {
+    const int kbw = acc4 ? 32 : 64;                 // kernels per block
+    const int64_t nb = (p.T_pad / 64) * (p.K_pad / kbw);
     const int64_t sx = 2 * int64_t(cus / 8);        // resident work-groups per XCD
     const int64_t cx = cus / 8;                     // CUs per XCD
     const int npass = p.nxi / 2;
@@ -427,7 +419,7 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
         p.ntail += n % sx;
       }
       p.nparts = np;
-      p.part_floats = p.ntail * np * nout * 64 * 64;
+      p.part_floats = p.ntail * np * nout * 64 * kbw;
     }
   }
   if ((p.T_pad / p.blk) * (p.C_pad / p.cg) > kMaxI32) return WINO_EINVAL;     // input grid

@@ -1,8 +1,8 @@
 """The library's calls under HIP graph capture: every forward launches kernels
-only (no allocation, no memset; outputs that are summed into are zeroed by a
-kernel), so a captured forward, data gradient or weight gradient replays to
-the bits of the eager call.  Each graph is replayed several times with eager
-work and synchronisations between the replays, and every replay is checked."""
+only (no allocation, no memset), so a captured forward, data gradient or
+weight gradient replays to the bits of the eager call.  Each graph is replayed
+several times with eager work and synchronisations between the replays, and
+every replay is checked."""
 import numpy as np
 import pytest
 
@@ -17,7 +17,7 @@ CASES = [
                x_dist="normal", w_dist="he"), True),
     (LayerSpec("g_f2x3_nosplit", N=3, m=2, r=3, batch=2, C=24, K=40, X=(6, 13, 15), pad=1,
                x_dist="normal", w_dist="he", relu=True), False),
-    # F(4^2): halves of the last blocks summed onto zeroed outputs
+    # F(4^2): tail blocks split into parts of 1 or 2 of its 18 passes
     (LayerSpec("g_f4x3_2d", N=2, m=4, r=3, batch=3, C=36, K=70, X=(17, 23), pad=1,
                x_dist="normal", w_dist="he"), True),
     # F(4^3): k_gemm_inv

@@ -133,6 +133,9 @@ PARTS = [
               x_dist="normal", w_dist="he", relu=True),
     LayerSpec("f2x3_3d_tail", N=3, m=2, r=3, batch=1, C=8, K=70, X=(16, 96, 92), pad=1,
               x_dist="relu_normal", w_dist="he"),
+    # F(4^2): 18 passes per block, so the parts hold 1 or 2 passes
+    LayerSpec("f4x3_2d_parts", N=2, m=4, r=3, batch=2, C=200, K=100, X=(30, 26), pad=1,
+              x_dist="normal", w_dist="he", relu=True),
 ]
 
 
@@ -171,8 +174,8 @@ def test_small_m2_layers_no_split(spec):
     check_full(spec, y, x, w)
 
 
-# eq. (2)'s bias: every GEMM kernel, split-tail blocks (small layers split every
-# block into halves; the bias joins one half) and whole blocks (ReLU layers)
+# eq. (2)'s bias: every GEMM kernel, with the tail blocks split into parts (the
+# bias joins their sum) and with every block whole
 BIAS = [SMALL[1], SMALL[5], SMALL[2], SMALL[7], SMALL[3], SMALL[6], F54[0]]
 
 
@@ -186,7 +189,7 @@ def test_bias(spec, split):
 
 
 def test_bias_determinism_bitwise():
-    # F(4^2): halves of the last blocks added onto zeroed outputs
+    # F(4^2): tail blocks split into parts, summed in order
     spec = SMALL[2]
     x, w = draw_layer(spec, seed=2)
     b = np.linspace(-1, 1, spec.K).astype(np.float32)
