@@ -505,6 +505,10 @@ def main():
                        if spec.m == 2 and d["gemm_parts"] > 1 else
                        "k_gemm_acc (batched fp32-MFMA GEMM, inverse transform accumulated per pass)"
                        if spec.m == 2 else
+                       "k_gemm_acc4 + k_part_reduce (batched fp32-MFMA GEMM, inverse transform accumulated "
+                       "per pass; the %d tail blocks in %d parts each, their partial outputs summed in order)"
+                       % (d["gemm_tail_blocks"], d["gemm_parts"])
+                       if (spec.N, spec.m, spec.r) == (2, 4, 3) and d["gemm_parts"] > 1 else
                        "k_gemm_acc4 (batched fp32-MFMA GEMM, inverse transform accumulated per pass)"
                        if (spec.N, spec.m, spec.r) == (2, 4, 3) else
                        "k_gemm_inv (batched fp32-MFMA GEMM + fused inverse transform)"),
