@@ -360,7 +360,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: this build runs the layer on a single MI355X "
-              "(batch or slab sharding across GPUs is described in DESIGN.md but not built); "
+              "(sharding the batch or slabs of the volume across GPUs is designed but not built); "
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
