@@ -29,11 +29,11 @@ ADJ = [
 ]
 
 
-def run_adjoint(N, m, r, batch, C, K, X, pad, dy_fn, w_fn, name):
+def run_adjoint(N, m, r, batch, C, K, X, pad, dy_fn, w_fn, name, points=None):
     torch = require_gpu()
     from paper_1611_06565_amd.wino import Plan
-    log(f"[gpu] adjoint {name} N={N} m={m} r={r} C={C} K={K} X={X} batch={batch} pad={pad}")
-    f = Plan(N, m, r, C, K, [batch] + list(X), pad=pad)
+    log(f"[gpu] adjoint {name} N={N} m={m} r={r} C={C} K={K} X={X} batch={batch} pad={pad} points={points}")
+    f = Plan(N, m, r, C, K, [batch] + list(X), pad=pad, points=points)
     a = f.adjoint()
     w = w_fn((K, C) + (r,) * N)
     dy = dy_fn(f.output_shape)
@@ -56,6 +56,21 @@ def test_adjoint_full_output(case):
     err = normalised_error(dx, ref, den)
     log(f"  max err {err['max']:.3e} p99.99 {err['p9999']:.3e}")
     assert err["nonfinite"] == 0
+    assert err["max"] <= TOL[m], err
+
+
+@pytest.mark.parametrize("N,m,points", [(3, 4, (0, 1, -1, 1.0 / 3.0, -1.0 / 3.0)), (2, 2, (0, 0.5, -0.5))],
+                         ids=["f43_3d_paper_pts", "f23_2d_half_pts"])
+def test_adjoint_caller_points(N, m, points):
+    # the adjoint plan keeps the forward plan's points
+    rng = np.random.default_rng(33)
+    X = (9, 8, 10) if N == 3 else (15, 13)
+    dx, dy, w = run_adjoint(N, m, 3, 1, 10, 14, X, 1,
+                            lambda s: rng.standard_normal(s).astype(np.float32),
+                            lambda s: (rng.standard_normal(s) * 0.2).astype(np.float32), "points", points)
+    ref, den = direct_adjoint(dy, w, 1)
+    err = normalised_error(dx, ref, den)
+    log(f"  max err {err['max']:.3e}")
     assert err["max"] <= TOL[m], err
 
 

@@ -41,11 +41,11 @@ WG = [
 ]
 
 
-def run_wgrad(N, m, r, batch, C, K, X, pad, x_fn, dy_fn, name):
+def run_wgrad(N, m, r, batch, C, K, X, pad, x_fn, dy_fn, name, points=None):
     torch = require_gpu()
     from paper_1611_06565_amd.wino import Plan
-    log(f"[gpu] wgrad {name} N={N} m={m} r={r} C={C} K={K} X={X} batch={batch} pad={pad}")
-    plan = Plan(N, m, r, C, K, [batch] + list(X), pad=pad)
+    log(f"[gpu] wgrad {name} N={N} m={m} r={r} C={C} K={K} X={X} batch={batch} pad={pad} points={points}")
+    plan = Plan(N, m, r, C, K, [batch] + list(X), pad=pad, points=points)
     assert plan.weight_gradient_workspace_bytes > 0
     x = x_fn(plan.input_shape)
     dy = dy_fn(plan.output_shape)
@@ -70,6 +70,20 @@ def test_wgrad_full_output(case):
                           lambda s: rng.standard_normal(s).astype(np.float32),
                           lambda s: rng.standard_normal(s).astype(np.float32), name)
     _check(dw, x, dy, r, pad)
+
+
+@pytest.mark.parametrize("N,m,points", [(3, 2, (0, 0.5, -0.5)), (2, 4, (0, 1, -1, 1.0 / 3.0, -1.0 / 3.0)),
+                                         (2, 4, (0, 2, -2, 0.5, -0.5))],
+                         ids=["f23_half_pts", "f43_paper_pts", "f43_searched_pts"])
+def test_wgrad_caller_points(N, m, points):
+    # F(r, m) is built on the caller's points as well (its B^T is again the
+    # forward's, checked exactly by the plan)
+    rng = np.random.default_rng(43)
+    X = (6, 9, 11) if N == 3 else (17, 14)
+    dw, x, dy = run_wgrad(N, m, 3, 2, 12, 20, X, 1,
+                          lambda s: rng.standard_normal(s).astype(np.float32),
+                          lambda s: rng.standard_normal(s).astype(np.float32), "points", points)
+    _check(dw, x, dy, 3, 1)
 
 
 def test_wgrad_integer_inputs_bitwise_exact():
