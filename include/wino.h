@@ -193,9 +193,10 @@ wino_status wino_transform_filter_adjoint(const wino_plan_t* plan, const float* 
  * output gradients are transformed with F(r, m)'s G, one product per element
  * xi sums over every tile of the batch (M_xi[K x C] = sum_t D_xi V_xi^T,
  * eq. 5 read the other way) and F(r, m)'s A^T maps M back to r^N taps.
- * Supported for F(2^N, 3^N) and F(4^2, 3^2) plans (V in 64-tile blocks);
- * otherwise WINO_EUNSUPPORTED and a workspace size of 0.  Bias, ReLU and the
- * plan's flags play no part (mask dy for a ReLU layer first).
+ * Supported for every size (WINO_EUNSUPPORTED and a workspace size of 0 only
+ * if F(r, m)'s data transform differed from the forward's, or for grids past
+ * 32-bit counts).  Bias, ReLU and the plan's flags play no part (mask dy for
+ * a ReLU layer first).
  *   x          device, [batch][C][X_1..X_N] float32 (the layer's input)
  *   dy         device, [batch][K][Y_1..Y_N] float32 (the output gradient)
  *   dw         device, [K][C][r^N] float32, fully overwritten

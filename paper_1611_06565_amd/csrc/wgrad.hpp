@@ -1,5 +1,5 @@
-// Weight gradient of an F(2^N, 3^N) layer (the backward pass on the kernel
-// side; the paper measures forward passes only).
+// Weight gradient of a layer (the backward pass on the kernel side; the paper
+// measures forward passes only).
 //
 // Per axis, the gradient of the r kernel taps over one output tile is a
 // correlation of the tile's m output gradients with the alpha-value input
@@ -35,7 +35,8 @@ namespace wino {
 
 struct WgArgs {
   int64_t ystride_k;    // prod Y_i (dy per kernel)
-  int32_t T, T_pad, ntb; // tiles, padded to 64, tile blocks
+  int32_t T, ntb;       // tiles; 64-tile steps (D is stored in 64-tile blocks)
+  int32_t nvb;          // V's tile blocks (of VB tiles)
   int32_t K, K_pad4;    // kernels, rounded up to 4 (D's channel groups)
   int32_t C, C_pad;     // channels (V's C_pad, a multiple of 4)
   int32_t nkb, ncb;     // 64-blocks of kernels and channels in M
@@ -50,56 +51,96 @@ struct WgArgs {
 // then cross an LDS stage (tiles padded to 5 floats, conflict-free writes) so
 // that every element's 64 x 4 values are stored as one contiguous 1 KB run.
 // Outputs past Y (partial tiles) and padding tiles and kernels read as zero.
-template <int N, int MM, int R>
+// For alpha^N > 64 (F(4^3)) a work-group produces one plane i0 of the first
+// axis only (blockIdx = block * alpha + i0): its threads take the tile's m^N
+// values one first-axis plane o0 at a time, transform each along the other
+// axes and accumulate G'[i0][o0] times it, so no thread holds alpha^N values.
+// CONST: the forward's points are the default set, which is also F(r, m)'s
+// default (the same first alpha - 1 points), so G' is compiled in.
+template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(256) k_dy(const float* __restrict__ dy, float* __restrict__ D, WgArgs a,
                                             FMats fw) {
   constexpr int A = MM + R - 1, NXI = ipow(A, N), NIN = ipow(MM, N);
-  constexpr int XR = NXI < 16 ? NXI : 16;          // elements per LDS round
+  constexpr bool PLANES = NXI > 64;
+  constexpr int NV = PLANES ? NXI / A : NXI;       // values of this thread
+  constexpr int XR = NV < 16 ? NV : 16;            // values per LDS round
   constexpr int TP = 5;                            // padded tile stride in the stage
   __shared__ float stage[XR][64 * TP];
-  const int tb = int(blockIdx.x) / (a.K_pad4 / 4), kg = int(blockIdx.x) % (a.K_pad4 / 4);
+  // the A planes of a block are neighbours in the grid, so they run together
+  // and read the block's output gradients from L2 rather than from HBM A times
+  const int i0 = PLANES ? int(blockIdx.x) % A : 0;
+  const int bid = PLANES ? int(blockIdx.x) / A : int(blockIdx.x);
+  const int tb = bid / (a.K_pad4 / 4), kg = bid % (a.K_pad4 / 4);
   const int tl = int(threadIdx.x) & 63, kl = int(threadIdx.x) >> 6;
   const int t = tb * 64 + tl, k = kg * 4 + kl;
-  float g[NIN];
-  if (t < a.T && k < a.K) {
-    int ti[3] = {0, 0, 0};
-    const int n = split_tile<N>(t, a.tiles, ti);
-    const float* src = dy + (int64_t(n) * a.K + k) * a.ystride_k;
+  const bool live = t < a.T && k < a.K;
+  int ti[3] = {0, 0, 0};
+  const int n = split_tile<N>(live ? t : 0, a.tiles, ti);
+  const float* src = dy + (int64_t(n) * a.K + (live ? k : 0)) * a.ystride_k;
+  // output gradient i of the tile (last axis fastest), zero past Y
+  auto load = [&](int i) {
+    int64_t off = 0, mul = 1;
+    bool in = live;
+    int rem = i;
 #pragma unroll
-    for (int i = 0; i < NIN; ++i) {
-      int64_t off = 0;
-      bool in = true;
-      int rem = i;
-      int64_t mul = 1;
+    for (int ax = N - 1; ax >= 0; --ax) {
+      const int yc = ti[ax] * MM + rem % MM;
+      rem /= MM;
+      in = in && yc < a.Y[ax];
+      off += int64_t(yc) * mul;
+      mul *= a.Y[ax];
+    }
+    return in ? src[off] : 0.0f;
+  };
+  const MatRef<Which::G, CONST, R, MM> Gp{&fw};    // G' of F(r, m): alpha x m
+  float u[NV];
+  if constexpr (PLANES) {
+    constexpr int NP = NIN / MM;                   // values of one first-axis plane
 #pragma unroll
-      for (int ax = N - 1; ax >= 0; --ax) {
-        const int yc = ti[ax] * MM + rem % MM;
-        rem /= MM;
-        in = in && yc < a.Y[ax];
-        off += int64_t(yc) * mul;
-        mul *= a.Y[ax];
+    for (int j = 0; j < NV; ++j) u[j] = 0.0f;
+#pragma unroll
+    for (int o0 = 0; o0 < MM; ++o0) {
+      const float c = Gp(i0, o0);
+      if (c == 0.0f) continue;
+      float g[NP], q[NV];
+      if (N == 3 && MM == 4 && a.Y[2] % 4 == 0) {
+        // whole tiles on the last axis: each row of the plane is one aligned
+        // 16-byte load (4 * ti[2] and the row starts are multiples of 4)
+        const int y0 = ti[0] * MM + o0;
+#pragma unroll
+        for (int rr = 0; rr < MM; ++rr) {
+          const int y1 = ti[1] * MM + rr;
+          const bool in = live && y0 < a.Y[0] && y1 < a.Y[1];
+          const int64_t off = (int64_t(in ? y0 : 0) * a.Y[1] + (in ? y1 : 0)) * a.Y[2] + ti[2] * MM;
+          const float4 v = in ? *reinterpret_cast<const float4*>(src + off) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+          g[rr * 4 + 0] = v.x; g[rr * 4 + 1] = v.y; g[rr * 4 + 2] = v.z; g[rr * 4 + 3] = v.w;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < NP; ++i) g[i] = load(o0 * NP + i);
       }
-      g[i] = in ? src[off] : 0.0f;
+      transform_nd<N - 1, MM, A>(g, q, Gp);
+#pragma unroll
+      for (int j = 0; j < NV; ++j) u[j] = __builtin_fmaf(c, q[j], u[j]);
     }
   } else {
+    float g[NIN];
 #pragma unroll
-    for (int i = 0; i < NIN; ++i) g[i] = 0.0f;
+    for (int i = 0; i < NIN; ++i) g[i] = load(i);
+    transform_nd<N, MM, A>(g, u, Gp);
   }
-  float u[NXI];
-  // G' of F(r, m): alpha x m, from the kernel argument
-  transform_nd<N, MM, A>(g, u, MatRef<Which::G, false, R, MM>{&fw});
-  float* dst = D + (int64_t(tb) * (a.K_pad4 / 4) + kg) * NXI * 256 + threadIdx.x;
+  float* dst = D + (int64_t(tb) * (a.K_pad4 / 4) + kg) * NXI * 256 + int64_t(i0) * NV * 256 + threadIdx.x;
   const int rd = (int(threadIdx.x) >> 2) * TP + (int(threadIdx.x) & 3);   // (tile, kernel) of the store
 #pragma unroll
-  for (int x0 = 0; x0 < NXI; x0 += XR) {
+  for (int x0 = 0; x0 < NV; x0 += XR) {
     if (x0 > 0) __syncthreads();                   // the previous round has been read
 #pragma unroll
     for (int j = 0; j < XR; ++j)
-      if (x0 + j < NXI) stage[j][tl * TP + kl] = u[x0 + j];
+      if (x0 + j < NV) stage[j][tl * TP + kl] = u[x0 + j];
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < XR; ++j)
-      if (x0 + j < NXI) __builtin_nontemporal_store(stage[j][rd], dst + (x0 + j) * 256);
+      if (x0 + j < NV) __builtin_nontemporal_store(stage[j][rd], dst + (x0 + j) * 256);
   }
 }
 
@@ -109,9 +150,13 @@ __global__ void __launch_bounds__(256) k_dy(const float* __restrict__ dy, float*
 // the 16 D chunks and 16 V chunks (1 KB each: 64 tiles x 4 kernels or
 // channels) of one tile block through LDS; chunks are padded by 4 floats so
 // that the 32 lanes of an operand read hit 32 banks.  The next step's chunks
-// are loaded into registers while this step multiplies.
+// are loaded into registers while this step multiplies.  VB is V's tile block:
+// 64 (one chunk per step) or 16 (a V chunk of the step is four 256-byte runs
+// of consecutive 16-tile blocks; blocks past V's end read as zero).
+template <int VB>
 __global__ void __launch_bounds__(256) k_wgrad_gemm(const float* __restrict__ V, const float* __restrict__ D,
                                                     float* __restrict__ part, WgArgs a, int32_t nxi) {
+  static_assert(VB == 64 || VB == 16, "V tile blocks of 64 or 16");
   using S = MfmaShape<32>;
   constexpr int CP = 260;                          // padded chunk stride (floats)
   __shared__ __attribute__((aligned(16))) float Ds[16 * CP];
@@ -132,10 +177,17 @@ __global__ void __launch_bounds__(256) k_wgrad_gemm(const float* __restrict__ V,
       const int ch = (j & 3) * 4 + wave;
       const bool isd = j < 4;
       const int g = (isd ? kb : cb) * 16 + ch;
-      const bool ok = g < (isd ? kgroups : cgroups);
-      const float* src = isd ? D + ((int64_t(tb) * kgroups + g) * nxi + xi) * 256
-                             : V + ((int64_t(tb) * cgroups + g) * nxi + xi) * 256;
-      reg[j] = ok ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src) + lane) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      bool ok = g < (isd ? kgroups : cgroups);
+      const float* src;
+      if (isd || VB == 64) {
+        src = (isd ? D + ((int64_t(tb) * kgroups + g) * nxi + xi) * 256
+                   : V + ((int64_t(tb) * cgroups + g) * nxi + xi) * 256) + 4 * lane;
+      } else {
+        const int vb = tb * 4 + lane / 16;               // lane's 16-tile block of V
+        ok = ok && vb < a.nvb;
+        src = V + ((int64_t(vb) * cgroups + g) * nxi + xi) * 64 + 4 * (lane % 16);
+      }
+      reg[j] = ok ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src)) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     }
   };
   const int kq = wave >> 1, cq = wave & 1;
@@ -189,9 +241,10 @@ __global__ void __launch_bounds__(256) k_wgrad_sum(float* __restrict__ part, WgA
 // M summed over the splits by k_wgrad_sum: the N-mode product with A'^T
 // written as one sum per output tap.  One thread per (k, p, c), channels
 // fastest, so the M reads of a wave coalesce.
-template <int N, int MM, int R>
+template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(256) k_wgrad_finish(const float* __restrict__ part, float* __restrict__ dw,
                                                       WgArgs a, FMats fw) {
+  const MatRef<Which::AT, CONST, R, MM> ATp{&fw};  // A'^T of F(r, m): r x alpha
   constexpr int A = MM + R - 1, NXI = ipow(A, N), NOUT = ipow(R, N);
   const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
   const int c = int(idx % a.C);
@@ -213,7 +266,7 @@ __global__ void __launch_bounds__(256) k_wgrad_finish(const float* __restrict__ 
     int q = xi;
 #pragma unroll
     for (int ax = N - 1; ax >= 0; --ax) {
-      coef *= fw.AT[pa[ax]][q % A];
+      coef *= ATp(pa[ax], q % A);
       q /= A;
     }
     if (coef != 0.0f) acc = __builtin_fmaf(coef, pp[int64_t(xi) * kp * cpn], acc);

@@ -179,7 +179,7 @@ struct Launch {
   // k_dy, partial products over tile-block ranges, then their sum and A'^T.
   static wino_status wgrad(const wino_plan_s& p, const float* x, const float* dy, float* dw, float* ws,
                            hipStream_t s) {
-    if constexpr (BLK != 64 || CG != 4) {
+    if constexpr ((BLK != 64 && BLK != 16) || CG != 4) {
       return WINO_EUNSUPPORTED;
     } else {
       float* V = ws;
@@ -190,21 +190,21 @@ struct Launch {
       WgArgs a{};
       a.ystride_k = 1;
       for (int i = 0; i < N; ++i) a.ystride_k *= p.Y[i];
-      a.T = int32_t(p.T); a.T_pad = int32_t(p.T_pad); a.ntb = int32_t(p.T_pad / 64);
+      a.T = int32_t(p.T); a.ntb = int32_t((p.T_pad + 63) / 64); a.nvb = int32_t(p.T_pad / BLK);
       a.K = p.K; a.K_pad4 = p.wg_kpad4; a.C = p.C; a.C_pad = p.C_pad;
       a.nkb = (p.wg_kpad4 + 63) / 64; a.ncb = (p.C_pad + 63) / 64;
       a.nsplit = p.wg_nsplit;
       for (int i = 0; i < 3; ++i) { a.tiles[i] = int32_t(p.tiles[i]); a.Y[i] = int32_t(p.Y[i]); }
       const int64_t nb = int64_t(a.nsplit) * NXI * a.nkb * a.ncb;
       a.nblocks = int32_t(nb);
-      hipLaunchKernelGGL((k_dy<N, MM, R>), dim3(unsigned(int64_t(a.ntb) * (a.K_pad4 / 4))), dim3(256), 0, s, dy,
-                         D, a, p.fmw);
-      hipLaunchKernelGGL(k_wgrad_gemm, dim3(unsigned(nb)), dim3(256), 0, s, V, D, part, a, int32_t(NXI));
+      const int64_t dy_grid = int64_t(a.ntb) * (a.K_pad4 / 4) * (NXI > 64 ? A : 1);   // k_dy: planes for alpha^N > 64
+      hipLaunchKernelGGL((k_dy<N, MM, R, CONST>), dim3(unsigned(dy_grid)), dim3(256), 0, s, dy, D, a, p.fmw);
+      hipLaunchKernelGGL((k_wgrad_gemm<BLK>), dim3(unsigned(nb)), dim3(256), 0, s, V, D, part, a, int32_t(NXI));
       const int64_t nkc = int64_t(p.K) * p.C;
       hipLaunchKernelGGL(k_wgrad_sum, dim3(unsigned((nkc * NXI + 255) / 256)), dim3(256), 0, s, part, a,
                          int32_t(NXI));
       const int64_t ntap = nkc * ipow(R, N);
-      hipLaunchKernelGGL((k_wgrad_finish<N, MM, R>), dim3(unsigned((ntap + 255) / 256)), dim3(256), 0, s, part,
+      hipLaunchKernelGGL((k_wgrad_finish<N, MM, R, CONST>), dim3(unsigned((ntap + 255) / 256)), dim3(256), 0, s, part,
                          dw, a, p.fmw);
       return launch_status();
     }
@@ -456,13 +456,13 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
     }
   p.fm = to_fmats(R);
   p.const_mats = defaults;
-  // weight gradient: F(r, m) on the same points, for the sizes whose V is
-  // stored in 64-tile blocks of 4-channel groups (F(2^N, 3^N), F(4^2, 3^2))
+  // weight gradient: F(r, m) on the same points (V in 64- or 16-tile blocks
+  // of 4-channel groups: every size)
   {
     p.wgrad_ok = false;
     int cg_, cgu_, cpad_, kblk_;
     channel_groups(N, m, r, &cg_, &cgu_, &cpad_, &kblk_);
-    if (p.blk == 64 && cg_ == 4) {
+    if ((p.blk == 64 || p.blk == 16) && cg_ == 4) {
       const RatMats Rw = synthesize(r, m, pts);
       bool same = Rw.ok;
       for (int i = 0; same && i < alpha; ++i)
@@ -471,12 +471,12 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
         p.wgrad_ok = true;
         p.fmw = to_fmats(Rw);
         p.wg_kpad4 = int(round_up(K, 4));
-        const int64_t nkb = (p.wg_kpad4 + 63) / 64, ncb = (p.C_pad + 63) / 64, ntb = p.T_pad / 64;
+        const int64_t nkb = (p.wg_kpad4 + 63) / 64, ncb = (p.C_pad + 63) / 64, ntb = (p.T_pad + 63) / 64;
         const int64_t units = int64_t(p.nxi) * nkb * ncb;
         int64_t ns = (2048 + units - 1) / units;
         ns = ns < ntb ? ns : ntb;
         p.wg_nsplit = int32_t(ns < 1 ? 1 : ns);
-        p.wg_d_floats = round_up(int64_t(p.nxi) * p.wg_kpad4 * p.T_pad, 64);
+        p.wg_d_floats = round_up(int64_t(p.nxi) * p.wg_kpad4 * ntb * 64, 64);
         p.wg_part_floats = int64_t(p.wg_nsplit) * p.nxi * nkb * 64 * ncb * 64;
         if (units * p.wg_nsplit > kMaxI32) p.wgrad_ok = false;                      // product grid
         if (int64_t(K) * C * (p.nxi > r * r * r ? p.nxi : r * r * r) > kMaxI32 * int64_t(256))

@@ -235,8 +235,7 @@ def test_adjoint_plan():
 
 
 def test_weight_gradient_host_side():
-    # supported where V has 64-tile blocks (F(2^N, 3^N), F(4^2)): V, then D, then
-    # the tile-range partials; elsewhere no workspace and WINO_EUNSUPPORTED
+    # every size: V, then D, then the tile-range partials
     p = wino.Plan(3, 2, 3, 64, 128, [8, 16, 56, 56], pad=1)
     d = p.desc
     v = 4 * 64 * d["C_pad"] * d["T_pad"]
@@ -246,7 +245,7 @@ def test_weight_gradient_host_side():
     assert wino.Plan(2, 2, 3, 3, 5, [2, 9, 10], pad=4).weight_gradient_workspace_bytes > 0
     for args in [(3, 4, 3), (2, 5, 4), (2, 3, 2), (2, 4, 5), (2, 3, 6)]:
         q = wino.Plan(*args, 3, 5, [1] + [12] * args[0], pad=1)
-        assert q.weight_gradient_workspace_bytes == 0, args
+        assert q.weight_gradient_workspace_bytes > 0, args
     L = wino.lib()
     assert L.wino_weight_gradient_workspace_bytes(None) == 0
     assert L.wino_weight_gradient(None, None, None, None, None, 0, None) == -1

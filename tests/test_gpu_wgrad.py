@@ -38,6 +38,16 @@ WG = [
     ("f2x3_2d_pad3", 2, 2, 3, 2, 3, 5, (6, 7), 3),
     ("f2x3_3d_odd", 3, 2, 3, 3, 5, 66, (7, 5, 9), 0),
     ("f4x3_2d_c1", 2, 4, 3, 1, 1, 9, (10, 13), 2),
+    # V in 16-tile blocks: F(4^3) and the alpha = 8 sizes of Table 1, F(3,2)
+    ("f4x3_3d", 3, 4, 3, 1, 20, 24, (13, 11, 17), 1),
+    ("f4x3_3d_c40k70", 3, 4, 3, 2, 40, 70, (9, 8, 12), 2),
+    # F(4^3) with whole tiles on the last axis (16-byte row loads of dy) and
+    # partial tiles on the other two
+    ("f4x3_3d_rows", 3, 4, 3, 2, 6, 10, (7, 9, 16), 1),
+    ("f5x4_2d", 2, 5, 4, 2, 9, 20, (23, 31), 1),
+    ("f4x5_2d", 2, 4, 5, 2, 12, 19, (21, 26), 2),
+    ("f3x6_2d", 2, 3, 6, 1, 20, 33, (25, 19), 0),
+    ("f3x2_2d", 2, 3, 2, 3, 17, 40, (20, 23), 0),
 ]
 
 
@@ -118,11 +128,12 @@ def test_wgrad_full_size():
     _check(dw, x, dy, spec.r, spec.pad)
 
 
-def test_wgrad_unsupported_sizes():
-    require_gpu()
-    from paper_1611_06565_amd.wino import Plan, WinoError
-    p = Plan(3, 4, 3, 4, 4, [1, 8, 8, 8], pad=1)
-    assert p.weight_gradient_workspace_bytes == 0
-    import torch
-    with pytest.raises(WinoError):
-        p.weight_gradient(torch.zeros(p.input_shape, device="cuda"), torch.zeros(p.output_shape, device="cuda"))
+def test_wgrad_f4x3_3d_full_size():
+    # the F(4^3) C = K = 32, 128^3 layer (V in 16-tile blocks), every output
+    spec = CONFIGS[4]
+    rng = np.random.default_rng(10)
+    dw, x, dy = run_wgrad(spec.N, spec.m, spec.r, spec.batch, spec.C, spec.K, spec.X, spec.pad,
+                          lambda s: rng.random(s, dtype=np.float32),
+                          lambda s: rng.standard_normal(s, dtype=np.float32) * math.sqrt(1.0 / spec.K),
+                          spec.name)
+    _check(dw, x, dy, spec.r, spec.pad)
