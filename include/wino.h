@@ -1,6 +1,7 @@
 /*
  * wino.h -- C ABI of libwino, an N-dimensional Winograd correlation forward
- * F(m^N, r^N) for 2-D and 3-D ConvNet layers on AMD MI355X (gfx950).
+ * F(m^N, r^N) for 2-D and 3-D ConvNet layers on AMD MI355X (gfx950), with
+ * the layer's data and weight gradients on the same transforms.
  *
  * Method: Budden et al., "Deep Tensor Convolution on Multicores" (arXiv
  * 1611.06565).  The layer is eq. (2) of §3.1: for every sample n, kernel k and
@@ -109,7 +110,9 @@ typedef struct {
  *   opts   may be NULL (no padding, default points, no ReLU)
  *   out    receives the plan; unchanged on error
  * Generates A^T (m x alpha), B^T (alpha x alpha) and G (alpha x r) in exact
- * rational arithmetic and rounds each entry once to float32.  No device work. */
+ * rational arithmetic and rounds each entry once to float32.  No device work;
+ * the compute-unit count of the current device is read to size the product's
+ * tail split (see wino_workspace_bytes). */
 wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims,
                       const wino_opts* opts, wino_plan_t** out);
 
@@ -131,8 +134,9 @@ size_t wino_filter_bytes(const wino_plan_t* plan);
  * + c%CG.  For F(2^N, 3^N) and F(4^2, 3^2) the product's blocks (64 tiles x 64
  * or 32 kernels) that would run in a last, partly filled round of resident
  * work-groups on the device current at wino_plan (gemm_tail_blocks) are split
- * by element passes into gemm_parts work-groups each, and a scratch area for their partial outputs follows V
- * (at V's size rounded up to 256 bytes); wino_gemm_inverse overwrites it.
+ * by element passes into gemm_parts work-groups each, and a scratch area for
+ * their partial outputs follows V (at V's size rounded up to 256 bytes);
+ * wino_gemm_inverse overwrites it.
  * The split is fixed when the plan is made and the partials are summed in a
  * fixed order, so a plan's results are bitwise reproducible. */
 size_t wino_workspace_bytes(const wino_plan_t* plan);
