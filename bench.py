@@ -33,7 +33,10 @@ PROFILE_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["paper_1611_06565_amd/csrc/kernels.hpp", "paper_1611_06565_amd/csrc/gemm_acc.hpp",
                   "paper_1611_06565_amd/csrc/gemm_acc4.hpp", "paper_1611_06565_amd/csrc/transforms.hpp",
                   "paper_1611_06565_amd/csrc/synth.hpp", "paper_1611_06565_amd/csrc/wgrad.hpp",
-                  "paper_1611_06565_amd/csrc/wino.hip"]
+                  "paper_1611_06565_amd/csrc/layout.hpp", "paper_1611_06565_amd/csrc/launch.hpp",
+                  "paper_1611_06565_amd/csrc/plan.cpp", "paper_1611_06565_amd/csrc/wino.hip"]
+# normalised max-error bars per output-tile extent m (the same as the GPU tests')
+TOL = {2: 1e-5, 3: 1e-4, 4: 1e-4, 5: 1e-4}
 
 
 def kernel_hash():
@@ -69,16 +72,38 @@ def read_traffic(expected_hash, config):
         return None
 
 
-def cpu_baseline(spec, x, w, budget_s=10.0):
-    """Time the fp64 direct-correlation oracle on whole samples of the batch
-    until about budget_s seconds have elapsed."""
-    from oracle.direct import direct_blas
-    from workloads import direct_flops
+def host_record():
+    """The host the CPU baseline runs on: logical CPUs, CPU model, BLAS threads."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
     try:
         import threadpoolctl
-        threads = max(int(i.get("num_threads", 1)) for i in threadpoolctl.threadpool_info()) or 1
+        blas = max(int(i.get("num_threads", 1)) for i in threadpoolctl.threadpool_info()) or None
     except Exception:  # noqa: BLE001
-        threads = os.cpu_count() or 1
+        blas = None
+    return {"os_cpu_count": os.cpu_count(), "cpu_model": model, "blas_threads": blas}
+
+
+def cpu_baseline(spec, x, w, budget_s=10.0, winograd_budget_s=8.0):
+    """Time the fp64 oracles on the host: the direct correlation (per-offset
+    BLAS form) on whole samples of the batch until about budget_s seconds have
+    elapsed, and the reference Winograd path (eq. 3-5 step by step) on one
+    sample, cut along the first spatial axis to about winograd_budget_s."""
+    import numpy as np
+
+    from oracle.direct import direct_blas
+    from oracle.winograd import winograd_forward
+    from workloads import direct_flops
+    host = host_record()
+    threads = host["blas_threads"] or host["os_cpu_count"] or 1
     per_sample = direct_flops(spec) / spec.batch
     done, t_total = 0, 0.0
     while done < spec.batch and (done == 0 or t_total < budget_s):
@@ -86,6 +111,22 @@ def cpu_baseline(spec, x, w, budget_s=10.0):
         direct_blas(x[done:done + 1], w, spec.pad)
         t_total += time.perf_counter() - t0
         done += 1
+    # reference Winograd: one sample, first axis cut to rows whose outputs
+    # take about the budget (a slab of whole output rows, valid extent only)
+    X0 = spec.X[0]
+    rows, t_w, rows_done = max(1, 2 * spec.r), 0.0, 0
+    while True:
+        take = min(rows, X0)
+        xs = x[:1, :, :take]
+        t0 = time.perf_counter()
+        winograd_forward(xs, w, spec.m, spec.r, pad=spec.pad)
+        dt = time.perf_counter() - t0
+        rows_done, t_w = take, dt
+        if take == X0 or dt > winograd_budget_s / 4:
+            break
+        rows *= 2
+    ys = [v + 2 * spec.pad - spec.r + 1 for v in (rows_done,) + tuple(spec.X[1:])]
+    wino_flops = 2.0 * spec.K * spec.C * spec.r ** spec.N * float(np.prod(ys))
     return {
         "value": per_sample * done / t_total / 1e12,
         "unit": "TFLOP/s",
@@ -94,6 +135,11 @@ def cpu_baseline(spec, x, w, budget_s=10.0):
         "sample": (f"fp64 direct correlation (per-offset BLAS form, with the |w||x| "
                    f"denominator) on {done} of {spec.batch} samples of the same layer, "
                    f"{t_total:.1f} s"),
+        **host,
+        "reference_winograd": {
+            "value": wino_flops / t_w / 1e12, "unit": "TFLOP/s (direct FLOPs)",
+            "sample": f"fp64 reference Winograd (tile, transforms, one product per element, inverse, "
+                      f"stitch) on 1 sample cut to {rows_done} of {X0} rows of the first axis, {t_w:.1f} s"},
     }
 
 
@@ -332,6 +378,9 @@ def bench_wgrad(args):
         "max_normalised_error": check,
     }
     print(json.dumps(out), flush=True)
+    if check is not None and not check <= 1e-4:
+        print(f"bench.py: weight gradient misses the oracle by {check:.3e}", file=sys.stderr)
+        sys.exit(3)
 
 
 def main():
@@ -351,6 +400,7 @@ def main():
                     help="time the layer's data gradient dx = adjoint(dy) instead of its forward")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache repetitions")
     ap.add_argument("--calib-copy", action="store_true",
                     help="only run a 1 GiB device copy (for HBM counter scaling)")
     ap.add_argument("--fig4", type=int, default=0, metavar="BATCH",
@@ -435,6 +485,27 @@ def main():
     filt_ms, inp_ms, gemm_ms = (float(v) for v in st.mean(axis=0))
     fwd_ms = inp_ms + gemm_ms
 
+    # Cold-cache variant (outside the timed region above): a 1 GiB read
+    # between repetitions evicts the L2s and the 256 MB memory-side cache, so
+    # the stages read x, V and U from HBM.  A read, not a write: written
+    # lines would still be dirty in the caches and their write-back would
+    # compete with the next stage's traffic.
+    cold = None
+    if not args.no_cold:
+        flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        sink = torch.empty((), dtype=torch.float32, device="cuda")
+        torch.sum(flush, out=sink)
+        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+        for i in range(args.steps):
+            torch.sum(flush, out=sink)
+            step(cev[i])
+        torch.cuda.synchronize()
+        cst = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
+                        for e in cev]).mean(axis=0)
+        cold = {"filter_transform": float(cst[0]), "input_transform": float(cst[1]),
+                "gemm_inverse": float(cst[2])}
+        del flush, sink
+
     flops = direct_flops(spec)
     nxi = d["n_xi"]
     C, K = plan.C, plan.K                    # swapped for the data gradient
@@ -473,6 +544,20 @@ def main():
     extra = {"input_transform_hbm": {"achieved_GBps": in_bytes / (inp_ms * 1e-3) / 1e9,
                                      "peak_GBps": PEAK_HBM,
                                      "frac": in_bytes / (inp_ms * 1e-3) / 1e9 / PEAK_HBM}}
+    if cold is not None:
+        c_in, c_g = cold["input_transform"], cold["gemm_inverse"]
+        extra["cold_cache"] = {
+            "stages_ms": cold,
+            "forward_tflops": flops / ((c_in + c_g) * 1e-3) / 1e12,
+            "input_transform_hbm_frac": in_bytes / (c_in * 1e-3) / 1e9 / PEAK_HBM,
+            "gemm_frac": ((gemm_bytes / (c_g * 1e-3) / 1e9 / PEAK_HBM) if hbm_bound
+                          else (gemm_flops / (c_g * 1e-3) / 1e12 / PEAK_FP32_MFMA)),
+            "gemm_bound": "hbm" if hbm_bound else "mfma",
+            "flush": "1 GiB device read between repetitions",
+        }
+    if check is not None:
+        extra["parity"] = {"max_normalised_error_sampled": check, "tolerance": TOL[spec.m],
+                           "ok": bool(check <= TOL[spec.m])}
     out = {
         "metric": ("effective TFLOP/s of a conv layer's data gradient (direct FLOPs); % fp32 MFMA / HBM peak"
                    if args.adjoint else
@@ -537,6 +622,10 @@ def main():
     if not args.no_cpu_baseline and not args.adjoint:
         out["cpu_baseline"] = cpu_baseline(spec, x, w)
     print(json.dumps(out), flush=True)
+    if check is not None and not check <= TOL[spec.m]:
+        print(f"bench.py: the sampled outputs miss the oracle by {check:.3e} "
+              f"(bar {TOL[spec.m]:.0e}): the throughput above is of a wrong result", file=sys.stderr)
+        sys.exit(3)
 
 
 if __name__ == "__main__":

@@ -9,7 +9,7 @@
  *
  *     y[n][k][o] = f( b[k] + sum_c sum_{p in [0,r)^N} w[k][c][p] * x~[n][c][o + p - pad] )
  *
- * a cross-correlation (no kernel flip) with f = identity or ReLU, b = 0 unless
+ * a cross-correlation (no kernel flip) with f = identity, ReLU or leaky ReLU, b = 0 unless
  * given (wino_forward_ex) and x~ equal to x zero-extended outside [0, X).
  * Sizes (N, m, r): F(2,3) and F(4,3) in 2-D and 3-D; F(3,2), F(5,4), F(4,5)
  * and F(3,6) (Table 1) in 2-D.  It is computed by eq. (4),
@@ -57,9 +57,14 @@ typedef enum {
 
 typedef struct wino_plan_s wino_plan_t; /* opaque, immutable after creation */
 
-/* Apply max(0, .) to every output in the output-transform epilogue
- * (the activation f of eq. 2). */
+/* The activation f of eq. (2) (§3.1: a ReLU or another non-linear
+ * activation), applied to every output in the output-transform epilogue,
+ * after the bias.  At most one of the two may be set.
+ *   WINO_RELU        f(v) = max(0, v)
+ *   WINO_LEAKY_RELU  f(v) = v for v > 0, slope * v otherwise
+ *                    (slope = wino_opts.slope, finite) */
 #define WINO_RELU 1u
+#define WINO_LEAKY_RELU 4u
 /* Never split the channel-element passes of a product block over several
  * work-groups (no partials scratch in the workspace; see
  * wino_workspace_bytes). */
@@ -76,7 +81,8 @@ typedef struct {
    * from these points is the only input of transform synthesis. */
   const double* points;
   int32_t n_points;
-  uint32_t flags; /* WINO_RELU | WINO_NO_SPLIT, or 0 */
+  uint32_t flags; /* WINO_RELU or WINO_LEAKY_RELU, | WINO_NO_SPLIT; or 0 */
+  float slope;    /* WINO_LEAKY_RELU: the slope below zero; ignored otherwise */
 } wino_opts;
 
 /* Plan summary (host-side numbers only). */
@@ -104,11 +110,16 @@ typedef struct {
  *          (2, 3) and (4, 3) for N = 2 and 3 (alpha = 4 or 6), and (3, 2),
  *          (5, 4), (4, 5), (3, 6) for N = 2 (alpha = 4 or 8); others give
  *          WINO_EUNSUPPORTED
- *   C, K   input channels and kernels, each >= 1
- *   dims   [batch, X_1 .. X_N], each >= 1; the output extent per axis
- *          Y_i = X_i + 2 pad_i - r + 1 must be >= 1
- *   opts   may be NULL (no padding, default points, no ReLU)
+ *   C, K   input channels and kernels, each in [1, 2^20]
+ *   dims   [batch, X_1 .. X_N], each in [1, 2^31 - 1]; the output extent per
+ *          axis Y_i = X_i + 2 pad_i - r + 1 must be >= 1
+ *   opts   may be NULL (no padding, default points, no activation); pads in
+ *          [0, 2^20]
  *   out    receives the plan; unchanged on error
+ * Returns WINO_EINVAL for bad arguments and for layers whose tile count
+ * (batch x tiles over every axis), padded sizes, byte counts or launch grids
+ * do not fit the library's integer ranges (all computed in 64 bits with
+ * overflow checks before any narrowing).
  * Generates A^T (m x alpha), B^T (alpha x alpha) and G (alpha x r) in exact
  * rational arithmetic and rounds each entry once to float32.  No device work;
  * the compute-unit count of the current device is read to size the product's
@@ -116,19 +127,26 @@ typedef struct {
 wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims,
                       const wino_opts* opts, wino_plan_t** out);
 
+/* Free a plan's host memory (NULL is a no-op).  The plan must not be in use
+ * by a call in progress; device buffers stay the caller's. */
 void wino_destroy(wino_plan_t* plan);
 
-/* Fill *desc from the plan.  Returns WINO_EINVAL for NULL arguments. */
+/* Fill *desc from the plan (the numbers of §3.3's tiling and §4.1's products).
+ * Returns WINO_EINVAL for NULL arguments. */
 wino_status wino_plan_describe(const wino_plan_t* plan, wino_plan_desc* desc);
 
-/* Bytes of the transformed-filter buffer U (float32), laid out as
+/* Bytes of the transformed-filter buffer U (float32): the alpha^N transformed
+ * elements of every (kernel, channel) pair, the kernel side of eq. (4)
+ * (§3.3 caches it across forwards), laid out as
  * U[alpha^N][C_pad/CGU][K_pad][CGU] with CGU = filter_channel_group: element
  * (xi, c, k) sits at ((xi*C_pad/CGU + c/CGU)*K_pad + k)*CGU + c%CGU.
  * Padding channels and kernels are zero. */
 size_t wino_filter_bytes(const wino_plan_t* plan);
 
 /* Bytes of workspace wino_forward needs.  It starts with the transformed
- * input V (float32), laid out tile-block major as
+ * input V (float32): the data side of eq. (4), one alpha^N tile per (tile,
+ * channel) with tiles of alpha values stepping by m along each axis (§3.3),
+ * stored as the [T x C] operands of eq. (5) (§4.1), tile-block major as
  * V[T_pad/B][C_pad/CG][alpha^N][B][CG] with B = block_tiles: element
  * (xi, c, t) sits at (((t/B)*C_pad/CG + c/CG)*alpha^N + xi)*B*CG + (t%B)*CG
  * + c%CG.  For F(2^N, 3^N) and F(4^2, 3^2) the product's blocks (64 tiles x 64
@@ -141,15 +159,15 @@ size_t wino_filter_bytes(const wino_plan_t* plan);
  * fixed order, so a plan's results are bitwise reproducible. */
 size_t wino_workspace_bytes(const wino_plan_t* plan);
 
-/* Bytes of workspace wino_forward needs (today equal to wino_workspace_bytes). */
-size_t wino_forward_workspace_bytes(const wino_plan_t* plan);
-
-/* out[0..N+1] = [batch, K, Y_1 .. Y_N]. */
+/* out[0..N+1] = [batch, K, Y_1 .. Y_N]: the output extent of the valid
+ * correlation S = D - G + 1 per axis (§2.2), on the zero-padded input,
+ * Y_i = X_i + 2 pad_i - r + 1.  WINO_EINVAL for NULL arguments. */
 wino_status wino_output_dims(const wino_plan_t* plan, int64_t* out);
 
-/* Test hook: copy the transform matrices, each entry the exact rational
- * rounded once to the nearest double, row-major: AT [m][alpha],
- * BT [alpha][alpha], G [alpha][r].  Any pointer may be NULL. */
+/* Test hook: copy the transform matrices of Theorem 1 / Algorithm 1 (§2.1-§2.2;
+ * the paper's A, B and C of eq. (1)), each entry the exact rational rounded
+ * once to the nearest double, row-major: AT [m][alpha], BT [alpha][alpha],
+ * G [alpha][r].  Any pointer may be NULL; WINO_EINVAL for a NULL plan. */
 wino_status wino_get_matrices(const wino_plan_t* plan, double* AT, double* BT, double* G);
 
 /* Kernel transform U = g x_1 G ... x_N G for every (k, c) (eq. 4; §3.3 caches
@@ -229,13 +247,13 @@ wino_status wino_gemm_inverse(const wino_plan_t* plan, void* workspace, size_t w
                               const float* U, float* y, void* stream);
 
 /* The whole forward (eq. 4 with eq. 5) on one stream: wino_transform_input
- * followed by wino_gemm_inverse, with wino_forward_workspace_bytes(plan)
- * bytes of workspace. */
+ * followed by wino_gemm_inverse, with wino_workspace_bytes(plan) bytes of
+ * workspace. */
 wino_status wino_forward(const wino_plan_t* plan, const float* x, const float* U, float* y,
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /* wino_gemm_inverse and wino_forward with the per-kernel bias b of eq. (2)
- * (§3.1): y[n][k][...] = sum + bias[k], then the optional ReLU.
+ * (§3.1): y[n][k][...] = f(sum + bias[k]), f the plan's activation.
  *   bias  device, [K] float32, 4-byte aligned, read only; NULL = no bias
  *         (then identical to the calls above).
  * Errors as for the calls above; a misaligned bias is WINO_EINVAL. */
@@ -270,6 +288,8 @@ wino_status wino_points_error_growth(int N, int m, int r, const double* points, 
                                      double* growth);
 wino_status wino_search_points(int N, int m, int r, double* points, double* growth);
 
+/* A static, NUL-terminated description of a status code ("unknown status"
+ * for values outside wino_status); never NULL. */
 const char* wino_status_string(wino_status s);
 
 #ifdef __cplusplus

@@ -8,6 +8,10 @@ channel sum: the input is channel m of the previous layer.  Outputs cover the
 valid extent Y = X + 2 pad - r + 1 (§2.2 gives S = D - G + 1 unpadded), with
 x zero-extended outside [0, X).
 
+The activation f of eq. (2) is the identity, ReLU (relu=True) or a leaky
+ReLU (leaky=s: v for v > 0, s * v otherwise); the section allows a ReLU or
+another non-linear activation for f.
+
 Each function returns (y, den) where den = sum |w| |x| over the same
 receptive field (plus |b_k| with a bias), the denominator of the normalised
 error metric.  All
@@ -29,7 +33,18 @@ def out_extent(X, pad, r):
     return tuple(int(x) + 2 * int(pad) - int(r) + 1 for x in X)
 
 
-def direct_naive(x, w, pad=0, relu=False, bias=None):
+def activate(y, relu=False, leaky=None):
+    """f of eq. (2) on an fp64 array (or scalar)."""
+    if relu and leaky is not None:
+        raise ValueError("one activation at most")
+    if relu:
+        return np.maximum(y, 0.0)
+    if leaky is not None:
+        return np.where(y > 0.0, y, float(leaky) * y)
+    return y
+
+
+def direct_naive(x, w, pad=0, relu=False, bias=None, leaky=None):
     """O1: the literal 2N+3 nested loops of eq. (2); tiny inputs only.
 
     x: [n][C][X_1..X_N], w: [K][C][r..r] -> (y [n][K][Y..], den)."""
@@ -55,7 +70,11 @@ def direct_naive(x, w, pad=0, relu=False, bias=None):
                             v = x[(b, c) + src]
                             acc += w[(k, c) + p] * v
                             mag += abs(w[(k, c) + p]) * abs(v)
-                y[(b, k) + o] = max(acc, 0.0) if relu else acc
+                if relu:
+                    acc = max(acc, 0.0)
+                elif leaky is not None and not acc > 0.0:
+                    acc = float(leaky) * acc
+                y[(b, k) + o] = acc
                 den[(b, k) + o] = mag
     return y, den
 
@@ -65,7 +84,7 @@ def _padded(x, pad):
     return np.pad(x, [(0, 0), (0, 0)] + [(pad, pad)] * N)
 
 
-def direct_blas(x, w, pad=0, relu=False, bias=None, with_den=True):
+def direct_blas(x, w, pad=0, relu=False, bias=None, with_den=True, leaky=None):
     """O2: one fp64 BLAS contraction per kernel offset p in [0, r)^N.
 
     y[n,k,o] = sum_p sum_c w[k,c,p] x~[n,c,o+p-pad]."""
@@ -96,12 +115,10 @@ def direct_blas(x, w, pad=0, relu=False, bias=None, with_den=True):
         y = y + b
         if with_den:
             den = den + np.abs(b)
-    if relu:
-        y = np.maximum(y, 0.0)
-    return y, den
+    return activate(y, relu, leaky), den
 
 
-def direct_sampled(x, w, pad, coords, relu=False, chunk=2048, bias=None):
+def direct_sampled(x, w, pad, coords, relu=False, chunk=2048, bias=None, leaky=None):
     """O3: outputs at selected positions only, one receptive field at a time.
 
     coords: int array [S][2+N] of (n, k, o_1..o_N).  Returns (y [S], den [S])."""
@@ -128,6 +145,6 @@ def direct_sampled(x, w, pad, coords, relu=False, chunk=2048, bias=None):
             bv = np.asarray(bias, dtype=np.float64)[cc[:, 1]]
             yv = yv + bv
             dv = dv + np.abs(bv)
-        ys.append(np.maximum(yv, 0.0) if relu else yv)
+        ys.append(activate(yv, relu, leaky))
         dens.append(dv)
     return np.concatenate(ys), np.concatenate(dens)

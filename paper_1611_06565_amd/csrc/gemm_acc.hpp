@@ -48,8 +48,9 @@ struct AccArgs {
   // k_part_reduce sums them in part order and applies bias and ReLU.
   int32_t xb0[8], xn[8], xs[8], xt0[8];
   int32_t tiles[3], Y[3];
-  int32_t relu;
-  const float* bias;  // [K] or null: b_k of eq. (2), added before the ReLU
+  int32_t act;        // activation f of eq. (2): 0 none, 1 ReLU, 2 leaky ReLU
+  float slope;        // leaky ReLU: f(v) = slope * v for v <= 0
+  const float* bias;  // [K] or null: b_k of eq. (2), added before the activation
   float* part;
   int32_t nparts;
 };
@@ -469,7 +470,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
           if (kg >= g.K) break;
           float v = pl[kl * TB + (tl ^ (kl & 31))];
           if (g.bias != nullptr) v += g.bias[kg];
-          if (g.relu) v = v > 0.0f ? v : 0.0f;
+          v = activate(v, g.act, g.slope);
           __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
         }
       }
@@ -514,7 +515,7 @@ __global__ void __launch_bounds__(256) k_part_reduce(float* __restrict__ y, AccA
 #pragma unroll 8
   for (int q = 0; q < g.nparts; ++q) v += __builtin_nontemporal_load(pp + int64_t(q) * NOUT * (TB * KB));
   if (g.bias != nullptr) v += g.bias[kg];
-  if (g.relu) v = v > 0.0f ? v : 0.0f;
+  v = activate(v, g.act, g.slope);
   y[(int64_t(n) * g.K + kg) * g.ystride_k + off] = v;
 }
 

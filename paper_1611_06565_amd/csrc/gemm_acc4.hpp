@@ -375,7 +375,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
           if (kg >= g.K) break;
           float v = pl[kl * TB + (tl ^ (kl & 31))];
           if (g.bias != nullptr) v += bsm[kl];
-          if (g.relu) v = v > 0.0f ? v : 0.0f;
+          v = activate(v, g.act, g.slope);
           __builtin_nontemporal_store(v, yo + int64_t(kg) * g.ystride_k);
         }
       }

@@ -29,6 +29,7 @@
 #include <cstdint>
 #include <type_traits>
 
+#include "layout.hpp"
 #include "synth.hpp"
 #include "transforms.hpp"
 
@@ -36,35 +37,6 @@ namespace wino {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-// GEMM kind, block (tiles and kernels per work-group), operand load width
-// and channel group per (N, m, r).
-//   KIND 0 (m = 2) and 1 (F(4^2)): pass-accumulating GEMMs (gemm_acc.hpp,
-//     gemm_acc4.hpp) on 64-tile blocks of V with channel groups of 4.
-//   KIND 2 (F(4^3) and the other 2-D sizes): k_gemm_inv, all alpha^N
-//     elements resident, 16-tile blocks.  A GEMM
-//     "stage" covers KSTEP * VEC channels: lane group kr of an MFMA operand
-//     loads channels VEC*kr .. VEC*kr+VEC-1 of the stage, and k-step j uses
-//     the j-th of them; the stage is KSTEP groups of VEC channels (CG = VEC),
-//     so that one input-transform work-group (16 tiles x one group) writes
-//     256 contiguous bytes per element.
-template <int N, int MM, int R>
-struct Blocking {
-  static constexpr int A = MM + R - 1;
-  static constexpr int NXI = ipow(A, N);
-  static constexpr int KIND = MM == 2 ? 0 : ((N == 2 && MM == 4 && R == 3) ? 1 : 2);
-  static constexpr bool ACC = KIND == 0;                         // k_gemm_acc
-  static constexpr bool PASS = KIND != 2;                        // k_gemm_acc or k_gemm_acc4
-  static constexpr int BLK = PASS ? 64 : 16;                     // tiles per V block
-  static constexpr int KBLK = KIND == 0 ? 64 : (KIND == 1 ? 32 : 16);   // kernels padded to this
-  static constexpr int KSTEP = 4;                                // channels per MFMA (k_gemm_inv)
-  static constexpr int VEC = 4;                                  // floats per operand load (k_gemm_inv)
-  static constexpr int STAGE = KSTEP * VEC;                      // channels per GEMM stage (k_gemm_inv)
-  static constexpr int CG = 4;                                   // channels per V group
-  static constexpr int CGU = CG;                                 // channels per U group
-  // channels are padded to whole operand stages of the GEMM (16 channels)
-  static constexpr int CPAD = 16;
-};
 
 // ---------------------------------------------------------------- arguments
 struct FilterArgs {
@@ -89,8 +61,9 @@ struct GemmArgs {
   int32_t nkb;        // K_pad / BLK
   int32_t nblocks;    // work-groups in the grid
   int32_t tiles[3], Y[3];
-  int32_t relu;
-  const float* bias;  // [K] or null: b_k of eq. (2), added before the ReLU
+  int32_t act;        // activation f of eq. (2): 0 none, 1 ReLU, 2 leaky ReLU
+  float slope;        // leaky ReLU: f(v) = slope * v for v <= 0
+  const float* bias;  // [K] or null: b_k of eq. (2), added before the activation
 };
 
 // Tile t (linear over batch and the tile grid, last axis fastest) -> sample
@@ -113,6 +86,15 @@ __device__ __forceinline__ int xcd_remap(int b, int nb) {
   const int xcd = b % NX, j = b / NX;
   const int per = nb / NX, rem = nb % NX;
   return xcd < rem ? xcd * (per + 1) + j : rem * (per + 1) + (xcd - rem) * per + j;
+}
+
+// The activation f of eq. (2) applied in the output epilogues after the bias:
+// kind 0 identity, 1 ReLU max(0, v), 2 leaky ReLU (v for v > 0, slope * v
+// otherwise).  kind is uniform over a launch.
+__device__ __forceinline__ float activate(float v, int32_t kind, float slope) {
+  if (kind == 1) return v > 0.0f ? v : 0.0f;
+  if (kind == 2) return v > 0.0f ? v : v * slope;
+  return v;
 }
 
 // ------------------------------------------------------------ filter (a2)
@@ -608,7 +590,8 @@ struct EpiArgs {
   int32_t K;
   int64_t ystride_k;  // prod Y_i
   int32_t Y[3];
-  int32_t relu;
+  int32_t act;
+  float slope;
   const float* bias;  // [K] or null
 };
 
@@ -725,7 +708,7 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
 #pragma unroll
       for (int ax = 1; ax < N; ++ax) off = off * g.Y[ax] + yc[ax];
       float val = out[q];
-      if (g.relu) val = val > 0.0f ? val : 0.0f;
+      val = activate(val, g.act, g.slope);
       yk[off] = val;
     }
   }
@@ -821,7 +804,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
     }
   }
 
-  EpiArgs e{y, g.K, g.ystride_k, {g.Y[0], g.Y[1], g.Y[2]}, g.relu, g.bias};
+  EpiArgs e{y, g.K, g.ystride_k, {g.Y[0], g.Y[1], g.Y[2]}, g.act, g.slope, g.bias};
   auto tile_of = [&](int tl, int* ti) -> int {
     const int t = tb * BLK + tl;
     if (t >= g.T) return -1;
@@ -838,7 +821,7 @@ struct PoolArgs {
   int64_t total;  // lead * prod Y
 };
 
-__global__ void __launch_bounds__(256) k_maxpool3d(const float* __restrict__ x, float* __restrict__ y,
+static __global__ void __launch_bounds__(256) k_maxpool3d(const float* __restrict__ x, float* __restrict__ y,
                                                    PoolArgs a) {
   const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
   if (i >= a.total) return;
@@ -861,7 +844,7 @@ __global__ void __launch_bounds__(256) k_maxpool3d(const float* __restrict__ x, 
 // The same for a last-axis window of 2 on rows of a multiple of 4 values:
 // one thread per pair of neighbouring outputs reads each window row as one
 // aligned 16-byte load and writes the pair as 8 bytes.
-__global__ void __launch_bounds__(256) k_maxpool3d_pair(const float* __restrict__ x, float* __restrict__ y,
+static __global__ void __launch_bounds__(256) k_maxpool3d_pair(const float* __restrict__ x, float* __restrict__ y,
                                                         PoolArgs a) {
   const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;   // output pair
   if (i >= a.total / 2) return;

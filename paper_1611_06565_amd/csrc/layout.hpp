@@ -1,0 +1,56 @@
+// Operand layouts and work-group blocking of every compiled size, as
+// compile-time constants shared by the kernels and the host-side planner
+// (plain C++: the planner builds without the HIP compiler).
+#pragma once
+
+#include "synth.hpp"
+
+namespace wino {
+
+// GEMM kind, block (tiles and kernels per work-group), operand load width
+// and channel group per (N, m, r).
+//   KIND 0 (m = 2) and 1 (F(4^2)): pass-accumulating GEMMs (gemm_acc.hpp,
+//     gemm_acc4.hpp) on 64-tile blocks of V with channel groups of 4.
+//   KIND 2 (F(4^3) and the other 2-D sizes): k_gemm_inv, all alpha^N
+//     elements resident, 16-tile blocks.  A GEMM
+//     "stage" covers KSTEP * VEC channels: lane group kr of an MFMA operand
+//     loads channels VEC*kr .. VEC*kr+VEC-1 of the stage, and k-step j uses
+//     the j-th of them; the stage is KSTEP groups of VEC channels (CG = VEC),
+//     so that one input-transform work-group (16 tiles x one group) writes
+//     256 contiguous bytes per element.
+template <int N, int MM, int R>
+struct Blocking {
+  static constexpr int A = MM + R - 1;
+  static constexpr int NXI = ipow(A, N);
+  static constexpr int KIND = MM == 2 ? 0 : ((N == 2 && MM == 4 && R == 3) ? 1 : 2);
+  static constexpr bool ACC = KIND == 0;                         // k_gemm_acc
+  static constexpr bool PASS = KIND != 2;                        // k_gemm_acc or k_gemm_acc4
+  static constexpr int BLK = PASS ? 64 : 16;                     // tiles per V block
+  static constexpr int KBLK = KIND == 0 ? 64 : (KIND == 1 ? 32 : 16);   // kernels padded to this
+  static constexpr int KSTEP = 4;                                // channels per MFMA (k_gemm_inv)
+  static constexpr int VEC = 4;                                  // floats per operand load (k_gemm_inv)
+  static constexpr int STAGE = KSTEP * VEC;                      // channels per GEMM stage (k_gemm_inv)
+  static constexpr int CG = 4;                                   // channels per V group
+  static constexpr int CGU = CG;                                 // channels per U group
+  // channels are padded to whole operand stages of the GEMM (16 channels)
+  static constexpr int CPAD = 16;
+};
+
+// The same constants as run-time values, for the planner.
+struct SizeTraits {
+  int A, NXI, KIND, BLK, KBLK, CG, CGU, CPAD;
+  int TB, KB;   // tiles and kernels per product work-group
+};
+
+template <int N, int MM, int R>
+constexpr SizeTraits size_traits() {
+  using B = Blocking<N, MM, R>;
+  SizeTraits t{};
+  t.A = B::A; t.NXI = B::NXI; t.KIND = B::KIND; t.BLK = B::BLK; t.KBLK = B::KBLK;
+  t.CG = B::CG; t.CGU = B::CGU; t.CPAD = B::CPAD;
+  t.TB = B::PASS ? 64 : B::BLK;
+  t.KB = B::KBLK;
+  return t;
+}
+
+}  // namespace wino

@@ -1,0 +1,8 @@
+// Kernel instances of the 2-D size F(3,2) of Table 1 (k_input, k_gemm_inv).
+#include "launch.hpp"
+
+namespace wino {
+
+WINO_DEFINE_OPS(2, 3, 2)
+
+}  // namespace wino

@@ -1,0 +1,8 @@
+// Kernel instances of the 2-D size F(4,5) of Table 1 (k_input, k_gemm_inv).
+#include "launch.hpp"
+
+namespace wino {
+
+WINO_DEFINE_OPS(2, 4, 5)
+
+}  // namespace wino

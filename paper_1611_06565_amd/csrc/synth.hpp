@@ -30,6 +30,14 @@ namespace wino {
 
 constexpr int kMaxAlpha = 8;
 
+// b^e for small non-negative e; iterative (not recursive) so that device
+// code can always inline it (constexpr functions serve host and device).
+constexpr int ipow(int b, int e) {
+  int r = 1;
+  for (int i = 0; i < e; ++i) r *= b;
+  return r;
+}
+
 struct Rat {
   int64_t n = 0, d = 1;  // d > 0, gcd(|n|, d) == 1
 };

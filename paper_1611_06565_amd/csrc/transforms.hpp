@@ -20,13 +20,6 @@
 
 namespace wino {
 
-// Iterative (not recursive) so that device code can always inline it.
-__host__ __device__ constexpr int ipow(int b, int e) {
-  int r = 1;
-  for (int i = 0; i < e; ++i) r *= b;
-  return r;
-}
-
 // Which matrix of the triple a transform reads.
 enum class Which { AT, BT, G };
 

@@ -223,7 +223,7 @@ __global__ void __launch_bounds__(256) k_wgrad_gemm(const float* __restrict__ V,
 // partial (each entry is read and written by its own thread only).  One
 // thread per (xi, k, c), channels fastest, so the partial reads coalesce and
 // the split loads of a thread are independent.
-__global__ void __launch_bounds__(256) k_wgrad_sum(float* __restrict__ part, WgArgs a, int32_t nxi) {
+static __global__ void __launch_bounds__(256) k_wgrad_sum(float* __restrict__ part, WgArgs a, int32_t nxi) {
   const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
   const int c = int(idx % a.C);
   const int64_t r = idx / a.C;

@@ -19,6 +19,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "wino.h")
 
 WINO_RELU = 1
 WINO_NO_SPLIT = 2
+WINO_LEAKY_RELU = 4
 _STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported (N, m, r)",
            -3: "workspace too small", -4: "device launch failed"}
 
@@ -31,7 +32,7 @@ class WinoError(RuntimeError):
 
 class _Opts(ctypes.Structure):
     _fields_ = [("pad", ctypes.c_int32 * 3), ("points", ctypes.POINTER(ctypes.c_double)),
-                ("n_points", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+                ("n_points", ctypes.c_int32), ("flags", ctypes.c_uint32), ("slope", ctypes.c_float)]
 
 
 class _Desc(ctypes.Structure):
@@ -73,7 +74,6 @@ def lib():
         "wino_plan_describe": (i32, [vp, ctypes.POINTER(_Desc)]),
         "wino_filter_bytes": (sz, [vp]),
         "wino_workspace_bytes": (sz, [vp]),
-        "wino_forward_workspace_bytes": (sz, [vp]),
         "wino_output_dims": (i32, [vp, P_i64]),
         "wino_get_matrices": (i32, [vp, P_dbl, P_dbl, P_dbl]),
         "wino_transform_filter": (i32, [vp, vp, vp, vp]),
@@ -135,12 +135,13 @@ def _point(p):
 
 
 class Plan:
-    """One planned layer: Plan(N, m, r, C, K, dims=[batch, X_1..X_N], pad, points, relu, split).
+    """One planned layer: Plan(N, m, r, C, K, dims=[batch, X_1..X_N], pad, points, relu, split, leaky).
 
-    split=False sets WINO_NO_SPLIT: no product block is split over several
-    work-groups, whatever the grid size."""
+    relu=True sets WINO_RELU; leaky=s (a float) sets WINO_LEAKY_RELU with
+    slope s (the activation f of eq. 2).  split=False sets WINO_NO_SPLIT: no
+    product block is split over several work-groups, whatever the grid size."""
 
-    def __init__(self, N, m, r, C, K, dims, pad=0, points=None, relu=False, split=True):
+    def __init__(self, N, m, r, C, K, dims, pad=0, points=None, relu=False, split=True, leaky=None):
         L = lib()
         dims = [int(d) for d in dims]
         if len(dims) != N + 1:
@@ -155,10 +156,14 @@ class Plan:
             opts.points = ctypes.cast(self._pts, ctypes.POINTER(ctypes.c_double))
             opts.n_points = len(points)
         opts.flags = (WINO_RELU if relu else 0) | (0 if split else WINO_NO_SPLIT)
+        if leaky is not None:
+            opts.flags |= WINO_LEAKY_RELU
+            opts.slope = float(leaky)
         arr = (ctypes.c_int64 * len(dims))(*dims)
         h = ctypes.c_void_p()
         _check(L.wino_plan(N, m, r, C, K, arr, ctypes.byref(opts), ctypes.byref(h)), "wino_plan")
         self._adopt(L, h, relu)
+        self.leaky = leaky
 
     def _adopt(self, L, h, relu):
         self._h = h
@@ -170,6 +175,7 @@ class Plan:
         N, C, K, r = d.N, d.C, d.K, d.r
         self.N, self.m, self.r, self.C, self.K = N, d.m, r, C, K
         self.relu = relu
+        self.leaky = None
         out = (ctypes.c_int64 * (N + 2))()
         _check(L.wino_output_dims(h, out), "wino_output_dims")
         self.output_shape = tuple(int(v) for v in out)
@@ -239,13 +245,8 @@ class Plan:
 
     @property
     def workspace_bytes(self):
-        """Workspace of the two-stage API (transform_input + gemm_inverse)."""
+        """Workspace of forward() and of the two-stage API (transform_input + gemm_inverse)."""
         return int(self._L.wino_workspace_bytes(self._h))
-
-    @property
-    def forward_workspace_bytes(self):
-        """Workspace forward() needs."""
-        return int(self._L.wino_forward_workspace_bytes(self._h))
 
     def matrices(self):
         a, m, r = self.desc["alpha"], self.m, self.r
@@ -321,7 +322,7 @@ class Plan:
         return _dev_ptr(bias, "bias", torch.float32)
 
     def gemm_inverse(self, ws, U, y=None, bias=None):
-        """bias: optional device [K] float32, b of eq. (2), added before the ReLU."""
+        """bias: optional device [K] float32, b of eq. (2), added before the activation."""
         import torch
         if y is None:
             y = self.new_output()
@@ -334,13 +335,13 @@ class Plan:
         return y
 
     def forward(self, x, U, y=None, workspace=None, bias=None):
-        """bias: optional device [K] float32, b of eq. (2), added before the ReLU."""
+        """bias: optional device [K] float32, b of eq. (2), added before the activation."""
         import torch
         self._check_shape(x, self.input_shape, "x")
         if y is None:
             y = self.new_output()
         self._check_shape(y, self.output_shape, "y")
-        need = self.forward_workspace_bytes
+        need = self.workspace_bytes
         if workspace is None and need:
             workspace = torch.empty(need // 4, dtype=torch.float32, device="cuda")
         ws_ptr = _dev_ptr(workspace, "workspace") if workspace is not None else ctypes.c_void_p()

@@ -34,9 +34,9 @@ def run_layer(spec, x, w, points=None, guard=0, bias=None, split=True):
     torch = require_gpu()
     from paper_1611_06565_amd.wino import Plan
     log(f"[gpu] {spec.name} N={spec.N} m={spec.m} C={spec.C} K={spec.K} X={spec.X} "
-        f"batch={spec.batch} pad={spec.pad} points={points} split={split}")
+        f"batch={spec.batch} pad={spec.pad} points={points} split={split} relu={spec.relu} leaky={spec.leaky}")
     plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X),
-                pad=spec.pad, points=points, relu=spec.relu, split=split)
+                pad=spec.pad, points=points, relu=spec.relu, split=split, leaky=spec.leaky)
     xd = torch.from_numpy(np.ascontiguousarray(x)).cuda()
     wd = torch.from_numpy(np.ascontiguousarray(w)).cuda()
     U = plan.transform_filter(wd)
@@ -57,7 +57,7 @@ def run_layer(spec, x, w, points=None, guard=0, bias=None, split=True):
 
 
 def check_full(spec, y, x, w, bias=None):
-    y_ref, den = direct_blas(x, w, spec.pad, relu=spec.relu, bias=bias)
+    y_ref, den = direct_blas(x, w, spec.pad, relu=spec.relu, bias=bias, leaky=spec.leaky)
     err = normalised_error(y, y_ref, den)
     log(f"  max err {err['max']:.3e} p99.99 {err['p9999']:.3e} at {err['argmax']} "
         f"clamped {err['clamped']}")
@@ -85,7 +85,7 @@ def sample_coords(shape, n, rng, edges=True):
 def check_sampled(spec, y, x, w, n=4000, seed=0, bias=None):
     rng = np.random.default_rng(seed)
     coords = sample_coords(y.shape, n, rng)
-    ys, dens = direct_sampled(x, w, spec.pad, coords, relu=spec.relu, bias=bias)
+    ys, dens = direct_sampled(x, w, spec.pad, coords, relu=spec.relu, bias=bias, leaky=spec.leaky)
     got = y[tuple(coords.T)]
     err = normalised_error(got, ys, dens)
     log(f"  sampled {len(coords)}: max err {err['max']:.3e} p99.99 {err['p9999']:.3e}")

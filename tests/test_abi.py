@@ -37,7 +37,7 @@ def test_status_strings(L):
     assert L.wino_status_string(-3) == b"workspace too small"
 
 
-def _plan_status(L, N, m, r, C, K, dims, pad=None, points=None, flags=0):
+def _plan_status(L, N, m, r, C, K, dims, pad=None, points=None, flags=0, slope=0.0):
     opts = wino._Opts()
     if pad is not None:
         for i, p in enumerate(pad):
@@ -48,6 +48,7 @@ def _plan_status(L, N, m, r, C, K, dims, pad=None, points=None, flags=0):
         opts.points = ctypes.cast(keep, ctypes.POINTER(ctypes.c_double))
         opts.n_points = len(points)
     opts.flags = flags
+    opts.slope = slope
     arr = (ctypes.c_int64 * len(dims))(*dims)
     h = ctypes.c_void_p()
     st = L.wino_plan(N, m, r, C, K, arr, ctypes.byref(opts), ctypes.byref(h))
@@ -72,8 +73,13 @@ def test_plan_validation(L):
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1]) == -1      # count
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1, math.nan]) == -1
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1, math.pi]) == -1
-    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=4) == -1
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=8) == -1       # unknown flag
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=3) == 0
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=4) == 0        # leaky ReLU, slope 0
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=5) == -1       # two activations
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=4, slope=math.nan) == -1
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=4, slope=math.inf) == -1
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=6, slope=0.1) == 0
     h = ctypes.c_void_p()
     assert L.wino_plan(3, 2, 3, 4, 4, None, None, ctypes.byref(h)) == -1
 
@@ -141,7 +147,6 @@ def test_device_calls_reject_bad_arguments(L):
     # NULL or misaligned pointers, or short workspaces, are passed.
     p = wino.Plan(2, 4, 3, 4, 4, [1, 8, 8])
     need = p.workspace_bytes
-    assert p.forward_workspace_bytes == need
     vp = ctypes.c_void_p
     assert L.wino_transform_filter(p.handle, None, vp(4096), None) == -1
     assert L.wino_transform_filter(p.handle, vp(4096 + 4), vp(4096), None) == -1
@@ -150,7 +155,7 @@ def test_device_calls_reject_bad_arguments(L):
     assert L.wino_forward(p.handle, vp(4096), vp(8192), vp(16384), vp(32768), 0, None) == -3
     assert L.wino_forward(p.handle, vp(4096), vp(8192), vp(16384), None, need, None) == -1
     f = wino.Plan(3, 2, 3, 4, 4, [1, 8, 8, 8])
-    assert f.forward_workspace_bytes == f.workspace_bytes > 0
+    assert f.workspace_bytes > 0
     assert L.wino_forward(f.handle, None, vp(8192), vp(16384), vp(32768), 1 << 30, None) == -1
     assert L.wino_forward(f.handle, vp(4096 + 4), vp(8192), vp(16384), vp(32768), 1 << 30, None) == -1
     assert L.wino_forward(f.handle, vp(4096), vp(8192), vp(16384 + 8), vp(32768), 1 << 30, None) == -1
@@ -250,3 +255,23 @@ def test_weight_gradient_host_side():
     assert L.wino_weight_gradient_workspace_bytes(None) == 0
     assert L.wino_weight_gradient(None, None, None, None, None, 0, None) == -1
     assert L.wino_weight_gradient(p.handle, None, None, None, None, 0, None) == -1
+
+
+def test_plan_rejects_overflowing_sizes(L):
+    """Sizes whose padded counts, byte counts or grids overflow are refused
+    before any number is narrowed (the planner computes them in 64 bits)."""
+    big = 2 ** 31 - 1
+    d = [1, 8, 8, 8]
+    assert _plan_status(L, 3, 2, 3, big, 16, d, pad=[1, 1, 1]) == -1
+    assert _plan_status(L, 3, 2, 3, 16, big, d, pad=[1, 1, 1]) == -1
+    assert _plan_status(L, 3, 4, 3, 16, big - 39, d, pad=[1, 1, 1]) == -1
+    assert _plan_status(L, 2, 4, 3, 2 ** 20 + 1, 4, [1, 8, 8]) == -1
+    assert _plan_status(L, 2, 4, 3, 2 ** 20, 4, [1, 8, 8]) == 0
+    assert _plan_status(L, 3, 2, 3, 4, 4, [big] * 4) == -1
+    assert _plan_status(L, 3, 2, 3, 4, 4, [big, 1, 1, 4], pad=[1, 1, 1]) == -1
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 4, 4, 4], pad=[2 ** 20] * 3) == -1
+    vp = ctypes.c_void_p
+    win = (ctypes.c_int32 * 3)(2, 2, 2)
+    for dims in [(1 << 62, 2, 2, 2), (1 << 40, big, big, big), (1 << 34, 2, 2, 2), (-1, 2, 2, 2)]:
+        arr = (ctypes.c_int64 * 4)(*dims)
+        assert L.wino_maxpool3d(arr, win, vp(4096), vp(8192), None) == -1, dims

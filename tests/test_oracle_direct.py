@@ -133,3 +133,37 @@ def test_maxpool_hand_example():
     x = np.array([[1, 5, 2], [3, 4, 9]], dtype=np.float32).reshape(1, 1, 1, 2, 3)
     # floor rounding drops the last column: windows {1,5,3,4} -> 5
     assert maxpool(x, (1, 2, 2)).reshape(-1).tolist() == [5.0]
+
+
+@pytest.mark.parametrize("N,n,C,K,X,r,pad", SHAPES[1::2])
+@pytest.mark.parametrize("slope", [0.1, -0.5, 0.0, 2.0])
+def test_leaky_relu_all_forms_and_torch(N, n, C, K, X, r, pad, slope):
+    """A leaky ReLU as eq. (2)'s activation f, after the bias: the three forms
+    agree with torch's CPU fp64 convNd followed by its leaky_relu; the
+    denominator is the activation-free one (slope 0 equals the ReLU)."""
+    rng = np.random.default_rng(N * 31 + C)
+    x = _rand(rng, (n, C) + X)
+    w = _rand(rng, (K, C) + (r,) * N)
+    b = rng.standard_normal(K).astype(np.float32)
+    conv = {1: torch.nn.functional.conv1d, 2: torch.nn.functional.conv2d,
+            3: torch.nn.functional.conv3d}[N]
+    ref = torch.nn.functional.leaky_relu(
+        conv(torch.from_numpy(x).double(), torch.from_numpy(w).double(), bias=torch.from_numpy(b).double(),
+             padding=pad), negative_slope=slope).numpy()
+    tol = 1e-12 * np.abs(ref).max()
+    y1, d1 = direct_naive(x, w, pad, bias=b, leaky=slope)
+    y2, d2 = direct_blas(x, w, pad, bias=b, leaky=slope)
+    np.testing.assert_allclose(y1, ref, rtol=1e-12, atol=tol)
+    np.testing.assert_allclose(y2, ref, rtol=1e-12, atol=tol)
+    _, d0 = direct_blas(x, w, pad, bias=b)
+    np.testing.assert_array_equal(d2, d0)
+    coords = np.stack(np.meshgrid(*[np.arange(v) for v in y2.shape], indexing="ij"), -1).reshape(-1, 2 + N)
+    ys, _ = direct_sampled(x, w, pad, coords, bias=b, leaky=slope, chunk=11)
+    np.testing.assert_allclose(ys, y2[tuple(coords.T)], rtol=1e-13, atol=1e-13)
+    if slope == 0.0:
+        yr, _ = direct_blas(x, w, pad, bias=b, relu=True)
+        np.testing.assert_array_equal(np.abs(y2), yr)   # -0.0 from 0 * v compares equal
+    pre, _ = direct_blas(x, w, pad, bias=b)
+    assert np.any(pre < 0) and np.any(pre > 0)      # both sides of f are exercised
+    with pytest.raises(ValueError):
+        direct_blas(x, w, pad, relu=True, leaky=slope)

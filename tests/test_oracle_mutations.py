@@ -82,7 +82,10 @@ def test_wrong_tile_stride_caught(monkeypatch):
         Y, T = orig(X, pad, m, r)
         return Y, tuple(max(1, t - 1) for t in T)
     monkeypatch.setattr(ow, "tile_counts", fake)
-    with pytest.raises(Exception):
-        y_bad = ow.winograd_forward(x, w, 2, 3, pad=1, exact=True)
-        assert y_bad.shape == y_ref.shape
-        assert all(Fraction(float(a)) == b for a, b in zip(y_ref.reshape(-1), y_bad.reshape(-1)))
+    y_bad = ow.winograd_forward(x, w, 2, 3, pad=1, exact=True)
+    # one tile fewer per axis covers fewer outputs: the result cannot match
+    # the direct correlation (a crop too short, or missing values)
+    same = y_bad.shape == y_ref.shape and all(
+        Fraction(float(a)) == b for a, b in zip(y_ref.reshape(-1), y_bad.reshape(-1)))
+    assert not same
+    assert y_bad.shape != y_ref.shape

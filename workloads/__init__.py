@@ -49,6 +49,7 @@ class LayerSpec:
     w_dist: str = "normal"
     relu: bool = False
     points: Tuple = None       # interpolation points; None = library default
+    leaky: float = None        # leaky ReLU slope (activation v or slope * v); None = off
 
     def with_(self, **kw) -> "LayerSpec":
         return replace(self, **kw)
