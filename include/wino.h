@@ -262,6 +262,22 @@ wino_status wino_gemm_inverse_ex(const wino_plan_t* plan, void* workspace, size_
 wino_status wino_forward_ex(const wino_plan_t* plan, const float* x, const float* U, const float* bias,
                             float* y, void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * wino_forward_ex without a workspace argument.  The workspace is a static
+ * device array of WINO_NOALLOC_SCRATCH_BYTES inside the library, one per GPU
+ * the library runs on, held until the process ends; its device address is
+ * looked up once per device on the first call with that device current.
+ * The call allocates nothing.  Plans whose wino_workspace_bytes exceeds
+ * WINO_NOALLOC_SCRATCH_BYTES get WINO_EWORKSPACE.  Every call on a GPU
+ * shares that GPU's array: calls that overlap in time on one GPU (different
+ * streams, or host threads without ordering) race and give wrong results;
+ * calls on one stream are ordered and safe.  Other arguments and errors as
+ * wino_forward_ex. */
+#define WINO_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+wino_status wino_forward_noalloc(const wino_plan_t* plan, const float* x, const float* U, const float* bias,
+                                 float* y, void* stream);
+
 /* Max-pool with window = stride and floor rounding over the trailing 3 axes
  * of x [lead][X_1][X_2][X_3] -> y [lead][X_1/p_1][X_2/p_2][X_3/p_3]
  * (the C3D stack's pooling layers; not part of the Winograd method).

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 
 #include "kernels.hpp"
 #include "launch.hpp"
@@ -31,9 +32,34 @@ int device_cu_count() {
 
 }  // namespace wino
 
+// Scratch of wino_forward_noalloc: the forward's workspace (V, then the
+// product's partial outputs) for callers that cannot allocate device memory.
+// One copy per device, held until the process ends.  In host code `scratch`
+// names a host-side stand-in, so only its device address (from
+// hipGetSymbolAddress, kept per device below) is ever passed to kernels.
+static __device__ __align__(256) float scratch[WINO_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
 namespace {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+std::mutex scratch_mu;
+void* scratch_dev[64] = {};
+
+wino_status scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return WINO_EDEVICE;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (scratch_dev[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return WINO_EDEVICE;
+    scratch_dev[dev] = ptr;
+  }
+  *out = scratch_dev[dev];
+  return WINO_OK;
+}
 
 // The launch table of a plan's size (the planner only makes plans of
 // compiled sizes).
@@ -122,6 +148,20 @@ wino_status wino_forward_ex(const wino_plan_t* p, const float* x, const float* U
 wino_status wino_forward(const wino_plan_t* p, const float* x, const float* U, float* y, void* ws,
                          size_t ws_bytes, void* stream) {
   return wino_forward_ex(p, x, U, nullptr, y, ws, ws_bytes, stream);
+}
+
+wino_status wino_forward_noalloc(const wino_plan_t* p, const float* x, const float* U, const float* bias,
+                                 float* y, void* stream) {
+  if (p == nullptr || x == nullptr || U == nullptr || y == nullptr) return WINO_EINVAL;
+  if (!aligned16(x) || !aligned16(U) || !aligned16(y)) return WINO_EINVAL;
+  if (bias != nullptr && (reinterpret_cast<uintptr_t>(bias) & 3u) != 0) return WINO_EINVAL;
+  if (wino_workspace_bytes(p) > WINO_NOALLOC_SCRATCH_BYTES) return WINO_EWORKSPACE;
+  void* ws = nullptr;
+  const wino_status st = scratch_address(&ws);
+  if (st != WINO_OK) return st;
+  // every word of V and of the partial outputs that the product reads is
+  // written first by this call's own kernels: nothing needs clearing
+  return wino_forward_ex(p, x, U, bias, y, ws, WINO_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const float* x, float* y,

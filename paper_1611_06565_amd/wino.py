@@ -82,6 +82,7 @@ def lib():
         "wino_forward": (i32, [vp, vp, vp, vp, vp, sz, vp]),
         "wino_gemm_inverse_ex": (i32, [vp, vp, sz, vp, vp, vp, vp]),
         "wino_forward_ex": (i32, [vp, vp, vp, vp, vp, vp, sz, vp]),
+        "wino_forward_noalloc": (i32, [vp, vp, vp, vp, vp, vp]),
         "wino_maxpool3d": (i32, [P_i64, ctypes.POINTER(i32), vp, vp, vp]),
         "wino_status_string": (ctypes.c_char_p, [i32]),
         "wino_points_error_growth": (i32, [i32, i32, i32, P_dbl, i32, P_dbl]),
@@ -351,6 +352,24 @@ class Plan:
                                        _dev_ptr(y, "y", torch.float32), ws_ptr, ws_len, _stream()),
                "wino_forward_ex")
         return y
+
+    def forward_noalloc(self, x, U, y=None, bias=None):
+        """wino_forward_noalloc: the forward with the library's static device
+        scratch as its workspace (the call allocates nothing; y is allocated
+        here only when not given)."""
+        import torch
+        self._check_shape(x, self.input_shape, "x")
+        if y is None:
+            y = self.new_output()
+        self._check_shape(y, self.output_shape, "y")
+        _check(self._L.wino_forward_noalloc(self._h, _dev_ptr(x, "x", torch.float32),
+                                            _dev_ptr(U, "U", torch.float32), self._bias_ptr(bias),
+                                            _dev_ptr(y, "y", torch.float32), _stream()),
+               "wino_forward_noalloc")
+        return y
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20   # WINO_NOALLOC_SCRATCH_BYTES of include/wino.h
 
 
 def points_error_growth(N, m, r, points=None):
