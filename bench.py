@@ -401,6 +401,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-check", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache repetitions")
+    ap.add_argument("--no-fuse", action="store_true",
+                    help="keep an F(4^3) forward in two stages (input transform to V, then the product)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="only run a 1 GiB device copy (for HBM counter scaling)")
     ap.add_argument("--fig4", type=int, default=0, metavar="BATCH",
@@ -437,7 +439,7 @@ def main():
     seed = args.config if args.seed is None else args.seed
     x, w = draw_layer(spec, seed=seed)
     plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X),
-                pad=spec.pad, relu=spec.relu)
+                pad=spec.pad, relu=spec.relu, fuse=not args.no_fuse)
     transform_filter = plan.transform_filter
     if args.adjoint:
         # the data gradient: dy of the layer's output shape through the
@@ -453,18 +455,26 @@ def main():
     y = plan.new_output()
     torch.cuda.synchronize()
 
+    fused = bool(d["fused"])
+
     # One step: kernel transform, input transform, then the batched GEMM with
     # the inverse transform (the two calls wino_forward makes), each timed.
+    # A fused plan (F(4^3), few kernels) runs the last two in one kernel: its
+    # stage is recorded as the GEMM stage and the input stage is empty.
     def step(ev=None):
         if ev is not None:
             ev[0].record()
         transform_filter(wd, U)
         if ev is not None:
             ev[1].record()
-        plan.transform_input(xd, ws)
+        if not fused:
+            plan.transform_input(xd, ws)
         if ev is not None:
             ev[2].record()
-        plan.gemm_inverse(ws, U, y)
+        if fused:
+            plan.forward(xd, U, y=y)
+        else:
+            plan.gemm_inverse(ws, U, y)
         if ev is not None:
             ev[3].record()
 
@@ -493,11 +503,10 @@ def main():
     cold = None
     if not args.no_cold:
         flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
-        sink = torch.empty((), dtype=torch.float32, device="cuda")
-        torch.sum(flush, out=sink)
+        sink = flush.sum()
         cev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
         for i in range(args.steps):
-            torch.sum(flush, out=sink)
+            sink += flush.sum()
             step(cev[i])
         torch.cuda.synchronize()
         cst = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
@@ -514,6 +523,9 @@ def main():
     # The GEMM's algorithmic bytes: V read once, U read once, y written once.
     # Below the ridge point (peak FLOP/s over peak bytes/s) it is bound by HBM.
     gemm_bytes = 4.0 * (nxi * d["T"] * C + nxi * C * K + float(np.prod(plan.output_shape)))
+    if fused:
+        # the fused kernel reads x (not V), U, and writes y
+        gemm_bytes = 4.0 * (float(np.prod(plan.input_shape)) + nxi * C * K + float(np.prod(plan.output_shape)))
     hbm_bound = gemm_flops / gemm_bytes < PEAK_FP32_MFMA * 1e12 / (PEAK_HBM * 1e9)
     if hbm_bound:
         achieved = gemm_bytes / (gemm_ms * 1e-3) / 1e9
@@ -541,15 +553,21 @@ def main():
             ys, dens = direct_sampled(x, w, spec.pad, coords)
         check = normalised_error(yh[tuple(coords.T)], ys, dens)["max"]
 
-    extra = {"input_transform_hbm": {"achieved_GBps": in_bytes / (inp_ms * 1e-3) / 1e9,
-                                     "peak_GBps": PEAK_HBM,
-                                     "frac": in_bytes / (inp_ms * 1e-3) / 1e9 / PEAK_HBM}}
+    extra = {}
+    if fused:
+        extra["fused_forward_hbm"] = {
+            "algorithmic_bytes": gemm_bytes, "achieved_GBps": gemm_bytes / (gemm_ms * 1e-3) / 1e9,
+            "peak_GBps": PEAK_HBM, "frac": gemm_bytes / (gemm_ms * 1e-3) / 1e9 / PEAK_HBM}
+    else:
+        extra["input_transform_hbm"] = {"achieved_GBps": in_bytes / (inp_ms * 1e-3) / 1e9,
+                                        "peak_GBps": PEAK_HBM,
+                                        "frac": in_bytes / (inp_ms * 1e-3) / 1e9 / PEAK_HBM}
     if cold is not None:
         c_in, c_g = cold["input_transform"], cold["gemm_inverse"]
         extra["cold_cache"] = {
             "stages_ms": cold,
             "forward_tflops": flops / ((c_in + c_g) * 1e-3) / 1e12,
-            "input_transform_hbm_frac": in_bytes / (c_in * 1e-3) / 1e9 / PEAK_HBM,
+            "input_transform_hbm_frac": (in_bytes / (c_in * 1e-3) / 1e9 / PEAK_HBM) if not fused else None,
             "gemm_frac": ((gemm_bytes / (c_g * 1e-3) / 1e9 / PEAK_HBM) if hbm_bound
                           else (gemm_flops / (c_g * 1e-3) / 1e12 / PEAK_FP32_MFMA)),
             "gemm_bound": "hbm" if hbm_bound else "mfma",
@@ -584,7 +602,9 @@ def main():
             "tiles": d["T"], "direct_gflop_per_step": flops / 1e9,
         },
         "roofline": {
-            "kernel": ("k_gemm_acc + k_part_reduce (batched fp32-MFMA GEMM, inverse transform accumulated "
+            "kernel": ("k_fused43 (input transform in LDS, batched fp32-MFMA GEMM, fused inverse transform; "
+                       "V never in memory)" if fused else
+                       "k_gemm_acc + k_part_reduce (batched fp32-MFMA GEMM, inverse transform accumulated "
                        "per pass; the %d tail blocks in %d parts each, their partial outputs summed in order)"
                        % (d["gemm_tail_blocks"], d["gemm_parts"])
                        if spec.m == 2 and d["gemm_parts"] > 1 else
@@ -612,8 +632,8 @@ def main():
             "mfma_frac_counted": (mfma_counted / (gemm_ms * 1e-3) / 1e12 / PEAK_FP32_MFMA
                                   if mfma_counted is not None else None),
         },
-        "stages_ms": {"filter_transform": filt_ms, "input_transform": inp_ms,
-                      "gemm_inverse": gemm_ms},
+        "stages_ms": ({"filter_transform": filt_ms, "fused_forward": gemm_ms} if fused else
+                      {"filter_transform": filt_ms, "input_transform": inp_ms, "gemm_inverse": gemm_ms}),
         "forward_U_cached_tflops": flops / (fwd_ms * 1e-3) / 1e12,
         "max_normalised_error_sampled": check,
         "kernel_sources_sha256_16": kernel_hash(),

@@ -69,6 +69,10 @@ typedef struct wino_plan_s wino_plan_t; /* opaque, immutable after creation */
  * work-groups (no partials scratch in the workspace; see
  * wino_workspace_bytes). */
 #define WINO_NO_SPLIT 2u
+/* Keep the forward of an F(4^3, 3^3) layer with at most 64 kernels in two
+ * stages (input transform to the workspace, then the product) instead of
+ * fusing the input transform into the product (see wino_forward). */
+#define WINO_NO_FUSE 8u
 
 typedef struct {
   /* Symmetric zero padding per spatial axis, outer to inner.  0 is the
@@ -81,7 +85,7 @@ typedef struct {
    * from these points is the only input of transform synthesis. */
   const double* points;
   int32_t n_points;
-  uint32_t flags; /* WINO_RELU or WINO_LEAKY_RELU, | WINO_NO_SPLIT; or 0 */
+  uint32_t flags; /* WINO_RELU or WINO_LEAKY_RELU, | WINO_NO_SPLIT | WINO_NO_FUSE; or 0 */
   float slope;    /* WINO_LEAKY_RELU: the slope below zero; ignored otherwise */
 } wino_opts;
 
@@ -102,6 +106,7 @@ typedef struct {
   int32_t filter_channel_group; /* CGU: channels interleaved innermost in U        */
   int32_t gemm_parts;    /* parts each tail block of the product is split into   */
   int64_t gemm_tail_blocks; /* product blocks split into gemm_parts parts         */
+  int32_t fused;         /* 1: wino_forward fuses the input transform into the product */
 } wino_plan_desc;
 
 /* Build a plan for one layer.  §3.1-§3.3 and §4.1.
@@ -158,6 +163,13 @@ size_t wino_filter_bytes(const wino_plan_t* plan);
  * The split is fixed when the plan is made and the partials are summed in a
  * fixed order, so a plan's results are bitwise reproducible. */
 size_t wino_workspace_bytes(const wino_plan_t* plan);
+
+/* Bytes of workspace wino_forward (and wino_forward_ex) needs: 0 when the
+ * plan fuses the input transform into the product (desc.fused: F(4^3, 3^3)
+ * with at most 64 kernels, unless WINO_NO_FUSE), wino_workspace_bytes
+ * otherwise.  The two-stage calls (wino_transform_input, wino_gemm_inverse)
+ * always need wino_workspace_bytes. */
+size_t wino_forward_workspace_bytes(const wino_plan_t* plan);
 
 /* out[0..N+1] = [batch, K, Y_1 .. Y_N]: the output extent of the valid
  * correlation S = D - G + 1 per axis (§2.2), on the zero-padded input,
@@ -246,9 +258,13 @@ wino_status wino_transform_input(const wino_plan_t* plan, const float* x, void* 
 wino_status wino_gemm_inverse(const wino_plan_t* plan, void* workspace, size_t workspace_bytes,
                               const float* U, float* y, void* stream);
 
-/* The whole forward (eq. 4 with eq. 5) on one stream: wino_transform_input
- * followed by wino_gemm_inverse, with wino_workspace_bytes(plan) bytes of
- * workspace. */
+/* The whole forward (eq. 4 with eq. 5) on one stream, with
+ * wino_forward_workspace_bytes(plan) bytes of workspace (workspace may be
+ * NULL when that is 0).  Two-stage plans run wino_transform_input and then
+ * wino_gemm_inverse; fused plans (F(4^3, 3^3), at most 64 kernels) form
+ * each tile block's transformed input in LDS inside the product, 8 channels
+ * at a time, so V never reaches memory (§4.1's reshuffle and §4.3's
+ * cache-sized tile blocks, on the GPU). */
 wino_status wino_forward(const wino_plan_t* plan, const float* x, const float* U, float* y,
                          void* workspace, size_t workspace_bytes, void* stream);
 
@@ -268,8 +284,8 @@ wino_status wino_forward_ex(const wino_plan_t* plan, const float* x, const float
  * device array of WINO_NOALLOC_SCRATCH_BYTES inside the library, one per GPU
  * the library runs on, held until the process ends; its device address is
  * looked up once per device on the first call with that device current.
- * The call allocates nothing.  Plans whose wino_workspace_bytes exceeds
- * WINO_NOALLOC_SCRATCH_BYTES get WINO_EWORKSPACE.  Every call on a GPU
+ * The call allocates nothing.  Plans whose wino_forward_workspace_bytes
+ * exceeds WINO_NOALLOC_SCRATCH_BYTES get WINO_EWORKSPACE.  Every call on a GPU
  * shares that GPU's array: calls that overlap in time on one GPU (different
  * streams, or host threads without ordering) race and give wrong results;
  * calls on one stream are ordered and safe.  Other arguments and errors as

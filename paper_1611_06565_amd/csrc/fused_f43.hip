@@ -1,0 +1,34 @@
+// Kernel instances and launch of k_fused43: F(4^3, 3^3) with the input
+// transform inside the product.
+#include "fused43.hpp"
+#include "launch.hpp"
+
+namespace wino {
+
+wino_status launch_fused43(const wino_plan_s& p, bool const_mats, const float* x, const float* U,
+                           const float* bias, float* y, hipStream_t s) {
+  FusedArgs a{};
+  a.xstride_c = p.X[0] * p.X[1] * p.X[2];
+  a.uplane = int64_t(p.C_pad) * p.K_pad;
+  a.ystride_k = p.Y[0] * p.Y[1] * p.Y[2];
+  a.C = p.C; a.C_pad = p.C_pad; a.K = p.K; a.K_pad = p.K_pad;
+  a.T = int32_t(p.T);
+  a.nkb = p.K_pad / Fused43Geom::BLK;
+  a.nblocks = int32_t(p.grid_fused);
+  for (int i = 0; i < 3; ++i) {
+    a.X[i] = int32_t(p.X[i]); a.tiles[i] = int32_t(p.tiles[i]); a.pad[i] = p.pad[i]; a.Y[i] = int32_t(p.Y[i]);
+  }
+  // whole 16-tile blocks along input rows of a multiple of 4 values (x is
+  // 16-byte aligned: the entry points check it)
+  a.rowfast = (p.tiles[2] % Fused43Geom::BLK == 0 && p.X[2] % 4 == 0 && p.pad[2] <= 2) ? 1 : 0;
+  a.act = act_kind(p);
+  a.slope = p.slope;
+  a.bias = bias;
+  if (const_mats)
+    hipLaunchKernelGGL((k_fused43<true>), dim3(p.grid_fused), dim3(Fused43Geom::NT), 0, s, x, U, y, a, p.fm);
+  else
+    hipLaunchKernelGGL((k_fused43<false>), dim3(p.grid_fused), dim3(Fused43Geom::NT), 0, s, x, U, y, a, p.fm);
+  return launch_status();
+}
+
+}  // namespace wino

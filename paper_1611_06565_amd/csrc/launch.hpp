@@ -26,6 +26,11 @@ inline int32_t act_kind(const wino_plan_s& p) {
   return (p.flags & WINO_RELU) ? 1 : ((p.flags & WINO_LEAKY_RELU) ? 2 : 0);
 }
 
+// k_fused43 (F(4^3) with the input transform inside the product), defined in
+// fused_f43.hip.
+wino_status launch_fused43(const wino_plan_s& p, bool const_mats, const float* x, const float* U,
+                           const float* bias, float* y, hipStream_t s);
+
 // The launches of one size, as plain function pointers.
 struct SizeOps {
   wino_status (*filter)(const wino_plan_s&, const float* w, float* U, bool adjoint, hipStream_t);
@@ -33,6 +38,9 @@ struct SizeOps {
   wino_status (*gemm)(const wino_plan_s&, const float* V, float* part, const float* U, const float* bias,
                       float* y, hipStream_t);
   wino_status (*wgrad)(const wino_plan_s&, const float* x, const float* dy, float* dw, float* ws, hipStream_t);
+  // the forward with the input transform inside the product (null for sizes without one)
+  wino_status (*fused)(const wino_plan_s&, const float* x, const float* U, const float* bias, float* y,
+                       hipStream_t);
 };
 
 template <int N, int MM, int R, bool CONST>
@@ -143,6 +151,14 @@ struct Launch {
     }
   }
 
+  // F(4^3): the input transform inside the product (fused43.hpp, launched
+  // from its own unit); no workspace.
+  static wino_status fused(const wino_plan_s& p, const float* x, const float* U, const float* bias, float* y,
+                           hipStream_t s) {
+    if constexpr (N == 3 && MM == 4 && R == 3) return launch_fused43(p, CONST, x, U, bias, y, s);
+    else return WINO_EUNSUPPORTED;
+  }
+
   static wino_status gemm(const wino_plan_s& p, const float* V, float* part, const float* U, const float* bias,
                           float* y, hipStream_t s) {
     constexpr int KIND = Blocking<N, MM, R>::KIND;
@@ -192,7 +208,10 @@ struct Launch {
 template <int N, int MM, int R, bool CONST>
 constexpr SizeOps make_ops() {
   using L = Launch<N, MM, R, CONST>;
-  return SizeOps{&L::filter, &L::input, &L::gemm, &L::wgrad};
+  if constexpr (N == 3 && MM == 4 && R == 3)
+    return SizeOps{&L::filter, &L::input, &L::gemm, &L::wgrad, &L::fused};
+  else
+    return SizeOps{&L::filter, &L::input, &L::gemm, &L::wgrad, nullptr};
 }
 
 // The tables, one per compiled size (defined in the sizes_*.hip units);

@@ -254,7 +254,7 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   if (!traits_of(N, m, r, &t)) return WINO_EUNSUPPORTED;
   wino_opts o{};
   if (opts) o = *opts;
-  if (o.flags & ~(WINO_RELU | WINO_NO_SPLIT | WINO_LEAKY_RELU)) return WINO_EINVAL;
+  if (o.flags & ~(WINO_RELU | WINO_NO_SPLIT | WINO_LEAKY_RELU | WINO_NO_FUSE)) return WINO_EINVAL;
   if ((o.flags & WINO_RELU) && (o.flags & WINO_LEAKY_RELU)) return WINO_EINVAL;
   if ((o.flags & WINO_LEAKY_RELU) && !std::isfinite(o.slope)) return WINO_EINVAL;
   const int alpha = m + r - 1;
@@ -325,6 +325,11 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
     if (!mul_ok(tpad / p.blk, kpad / t.KB, &gg) || !grid_ok(gg, 768, &p.grid_gemm)) return WINO_EINVAL;
   }
   if (p.v_floats + p.part_floats > kMaxFloats) return WINO_EINVAL;
+  // F(4^3) with few kernels: the input transform runs inside the product
+  // (recomputed for each block of 16 kernels, so only while there are at
+  // most 4 such blocks); same grid as k_gemm_inv
+  p.fused = N == 3 && m == 4 && r == 3 && p.K_pad <= 64 && !(o.flags & WINO_NO_FUSE);
+  if (p.fused && !grid_ok(int64_t(p.T_pad / p.blk) * (p.K_pad / 16), 768, &p.grid_fused)) return WINO_EINVAL;
 
   // Transform synthesis (a1): exact rationals, one rounding per entry.
   Rat pts[kMaxAlpha];
@@ -383,6 +388,7 @@ wino_status wino_plan_describe(const wino_plan_t* p, wino_plan_desc* d) {
   d->gemm_parts = p->nparts;
   d->gemm_tail_blocks = p->ntail;
   d->default_points = p->const_mats ? 1 : 0;
+  d->fused = p->fused ? 1 : 0;
   return WINO_OK;
 }
 
@@ -392,6 +398,11 @@ size_t wino_filter_bytes(const wino_plan_t* p) {
 
 size_t wino_workspace_bytes(const wino_plan_t* p) {
   return p ? size_t(p->v_floats + p->part_floats) * sizeof(float) : 0;
+}
+
+size_t wino_forward_workspace_bytes(const wino_plan_t* p) {
+  if (p == nullptr) return 0;
+  return p->fused ? 0 : wino_workspace_bytes(p);
 }
 
 size_t wino_weight_gradient_workspace_bytes(const wino_plan_t* p) {

@@ -49,6 +49,10 @@ struct wino_plan_s {
   int32_t acc_xb0[8], acc_xn[8], acc_xs[8], acc_xt0[8];
   int32_t gemm_nkb;       // kernel blocks of the product
   uint32_t grid_dy, grid_wgemm, grid_wsum, grid_wfin;   // weight gradient
+  // F(4^3): the forward runs the input transform inside the product
+  // (k_fused43, one work-group per 16 tiles x 16 kernels) and needs no workspace
+  bool fused;
+  uint32_t grid_fused;
 };
 
 namespace wino {

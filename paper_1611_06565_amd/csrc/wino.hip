@@ -137,6 +137,12 @@ wino_status wino_forward_ex(const wino_plan_t* p, const float* x, const float* U
   if (p == nullptr || x == nullptr || U == nullptr || y == nullptr) return WINO_EINVAL;
   if (!aligned16(x) || !aligned16(U) || !aligned16(y)) return WINO_EINVAL;
   if (bias != nullptr && (reinterpret_cast<uintptr_t>(bias) & 3u) != 0) return WINO_EINVAL;
+  if (p->fused) {
+    // the input transform runs inside the product: no workspace
+    const SizeOps* ops = ops_of(*p);
+    if (ops == nullptr || ops->fused == nullptr) return WINO_EUNSUPPORTED;
+    return ops->fused(*p, x, U, bias, y, static_cast<hipStream_t>(stream));
+  }
   if (ws == nullptr) return WINO_EINVAL;
   if (!aligned16(ws)) return WINO_EINVAL;
   if (ws_bytes < wino_workspace_bytes(p)) return WINO_EWORKSPACE;
@@ -155,7 +161,7 @@ wino_status wino_forward_noalloc(const wino_plan_t* p, const float* x, const flo
   if (p == nullptr || x == nullptr || U == nullptr || y == nullptr) return WINO_EINVAL;
   if (!aligned16(x) || !aligned16(U) || !aligned16(y)) return WINO_EINVAL;
   if (bias != nullptr && (reinterpret_cast<uintptr_t>(bias) & 3u) != 0) return WINO_EINVAL;
-  if (wino_workspace_bytes(p) > WINO_NOALLOC_SCRATCH_BYTES) return WINO_EWORKSPACE;
+  if (wino_forward_workspace_bytes(p) > WINO_NOALLOC_SCRATCH_BYTES) return WINO_EWORKSPACE;
   void* ws = nullptr;
   const wino_status st = scratch_address(&ws);
   if (st != WINO_OK) return st;

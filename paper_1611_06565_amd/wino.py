@@ -20,6 +20,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "wino.h")
 WINO_RELU = 1
 WINO_NO_SPLIT = 2
 WINO_LEAKY_RELU = 4
+WINO_NO_FUSE = 8
 _STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported (N, m, r)",
            -3: "workspace too small", -4: "device launch failed"}
 
@@ -46,7 +47,7 @@ class _Desc(ctypes.Structure):
                 ("block_tiles", ctypes.c_int32), ("block_kernels", ctypes.c_int32),
                 ("default_points", ctypes.c_int32), ("channel_group", ctypes.c_int32),
                 ("filter_channel_group", ctypes.c_int32), ("gemm_parts", ctypes.c_int32),
-                ("gemm_tail_blocks", ctypes.c_int64)]
+                ("gemm_tail_blocks", ctypes.c_int64), ("fused", ctypes.c_int32)]
 
 
 _LIB = None
@@ -74,6 +75,7 @@ def lib():
         "wino_plan_describe": (i32, [vp, ctypes.POINTER(_Desc)]),
         "wino_filter_bytes": (sz, [vp]),
         "wino_workspace_bytes": (sz, [vp]),
+        "wino_forward_workspace_bytes": (sz, [vp]),
         "wino_output_dims": (i32, [vp, P_i64]),
         "wino_get_matrices": (i32, [vp, P_dbl, P_dbl, P_dbl]),
         "wino_transform_filter": (i32, [vp, vp, vp, vp]),
@@ -140,9 +142,11 @@ class Plan:
 
     relu=True sets WINO_RELU; leaky=s (a float) sets WINO_LEAKY_RELU with
     slope s (the activation f of eq. 2).  split=False sets WINO_NO_SPLIT: no
-    product block is split over several work-groups, whatever the grid size."""
+    product block is split over several work-groups, whatever the grid size.
+    fuse=False sets WINO_NO_FUSE: an F(4^3) forward stays in two stages."""
 
-    def __init__(self, N, m, r, C, K, dims, pad=0, points=None, relu=False, split=True, leaky=None):
+    def __init__(self, N, m, r, C, K, dims, pad=0, points=None, relu=False, split=True, leaky=None,
+                 fuse=True):
         L = lib()
         dims = [int(d) for d in dims]
         if len(dims) != N + 1:
@@ -156,7 +160,7 @@ class Plan:
             self._pts = (ctypes.c_double * len(points))(*[_point(p) for p in points])
             opts.points = ctypes.cast(self._pts, ctypes.POINTER(ctypes.c_double))
             opts.n_points = len(points)
-        opts.flags = (WINO_RELU if relu else 0) | (0 if split else WINO_NO_SPLIT)
+        opts.flags = (WINO_RELU if relu else 0) | (0 if split else WINO_NO_SPLIT) | (0 if fuse else WINO_NO_FUSE)
         if leaky is not None:
             opts.flags |= WINO_LEAKY_RELU
             opts.slope = float(leaky)
@@ -246,8 +250,14 @@ class Plan:
 
     @property
     def workspace_bytes(self):
-        """Workspace of forward() and of the two-stage API (transform_input + gemm_inverse)."""
+        """Workspace of the two-stage API (transform_input + gemm_inverse)."""
         return int(self._L.wino_workspace_bytes(self._h))
+
+    @property
+    def forward_workspace_bytes(self):
+        """Workspace forward() needs: 0 when the plan fuses the input transform
+        into the product, workspace_bytes otherwise."""
+        return int(self._L.wino_forward_workspace_bytes(self._h))
 
     def matrices(self):
         a, m, r = self.desc["alpha"], self.m, self.r
@@ -342,7 +352,7 @@ class Plan:
         if y is None:
             y = self.new_output()
         self._check_shape(y, self.output_shape, "y")
-        need = self.workspace_bytes
+        need = self.forward_workspace_bytes
         if workspace is None and need:
             workspace = torch.empty(need // 4, dtype=torch.float32, device="cuda")
         ws_ptr = _dev_ptr(workspace, "workspace") if workspace is not None else ctypes.c_void_p()

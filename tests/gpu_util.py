@@ -26,7 +26,7 @@ def require_gpu():
     return torch
 
 
-def run_layer(spec, x, w, points=None, guard=0, bias=None, split=True):
+def run_layer(spec, x, w, points=None, guard=0, bias=None, split=True, fuse=True):
     """Plan, transform the filter and run the forward.  Returns (y numpy, plan).
 
     With guard > 0 the output is a view inside a larger buffer whose guard
@@ -34,9 +34,10 @@ def run_layer(spec, x, w, points=None, guard=0, bias=None, split=True):
     torch = require_gpu()
     from paper_1611_06565_amd.wino import Plan
     log(f"[gpu] {spec.name} N={spec.N} m={spec.m} C={spec.C} K={spec.K} X={spec.X} "
-        f"batch={spec.batch} pad={spec.pad} points={points} split={split} relu={spec.relu} leaky={spec.leaky}")
+        f"batch={spec.batch} pad={spec.pad} points={points} split={split} fuse={fuse} relu={spec.relu} "
+        f"leaky={spec.leaky}")
     plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X),
-                pad=spec.pad, points=points, relu=spec.relu, split=split, leaky=spec.leaky)
+                pad=spec.pad, points=points, relu=spec.relu, split=split, leaky=spec.leaky, fuse=fuse)
     xd = torch.from_numpy(np.ascontiguousarray(x)).cuda()
     wd = torch.from_numpy(np.ascontiguousarray(w)).cuda()
     U = plan.transform_filter(wd)

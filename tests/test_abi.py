@@ -73,7 +73,8 @@ def test_plan_validation(L):
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1]) == -1      # count
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1, math.nan]) == -1
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], points=[0, 1, math.pi]) == -1
-    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=8) == -1       # unknown flag
+    assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=16) == -1      # unknown flag
+    assert _plan_status(L, 3, 4, 3, 4, 4, [1, 8, 8, 8], flags=8) == 0        # WINO_NO_FUSE
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=3) == 0
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=4) == 0        # leaky ReLU, slope 0
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 8, 8, 8], flags=5) == -1       # two activations

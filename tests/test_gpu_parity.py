@@ -90,6 +90,55 @@ def test_small_layers_full_output(spec):
     check_full(spec, y, x, w)
 
 
+# F(4^3) forward in both forms: the input transform fused into the product
+# (k_fused43, planned for at most 64 kernels) and the two stages through V
+# (k_input_split + k_gemm_inv); row-aligned and gathered loads, padding
+# channels in the last 8-channel chunk, 1 to 4 kernel blocks, pads 0 to 2
+F43_BOTH = [s for s in SMALL + EDGE + ROWFAST if s.N == 3 and s.m == 4] + [
+    LayerSpec("f4x3_k64_c40", N=3, m=4, r=3, batch=2, C=40, K=64, X=(9, 10, 12), pad=1,
+              x_dist="normal", w_dist="he"),
+    LayerSpec("f4x3_k80_two_stage", N=3, m=4, r=3, batch=1, C=24, K=80, X=(8, 11, 9), pad=1,
+              x_dist="relu_normal", w_dist="he"),
+    LayerSpec("f4x3_row_c33_k48", N=3, m=4, r=3, batch=1, C=33, K=48, X=(6, 5, 64), pad=1,
+              x_dist="uniform", w_dist="he"),
+]
+
+
+@pytest.mark.parametrize("spec", F43_BOTH, ids=lambda s: s.name)
+def test_f43_fused_and_two_stage(spec):
+    x, w = draw_layer(spec, seed=19)
+    b = (0.2 * np.random.default_rng(3).standard_normal(spec.K)).astype(np.float32)
+    y_f, plan_f = run_layer(spec, x, w, guard=512, bias=b)
+    assert plan_f.desc["fused"] == (1 if spec.K <= 64 else 0)
+    assert plan_f.forward_workspace_bytes == (0 if spec.K <= 64 else plan_f.workspace_bytes)
+    check_full(spec, y_f, x, w, bias=b)
+    y_s, plan_s = run_layer(spec, x, w, guard=512, bias=b, fuse=False)
+    assert plan_s.desc["fused"] == 0
+    check_full(spec, y_s, x, w, bias=b)
+
+
+def test_f43_fused_determinism_bitwise():
+    spec = ROWFAST[0]
+    x, w = draw_layer(spec, seed=4)
+    y1, p1 = run_layer(spec, x, w)
+    y2, _ = run_layer(spec, x, w)
+    assert p1.desc["fused"] == 1
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+
+
+def test_f43_fused_integer_inputs():
+    """Integer data through the fused F(4^3) kernel: F(4,3)'s matrices hold
+    non-dyadic entries, so the bar is the m = 4 tolerance (no bit-exactness),
+    but the result must also match the two-stage path within it."""
+    spec = LayerSpec("f4x3_int", N=3, m=4, r=3, batch=1, C=16, K=32, X=(8, 9, 64), pad=1,
+                     x_dist="int2", w_dist="int2")
+    x, w = draw_layer(spec, seed=8)
+    y_f, _ = run_layer(spec, x, w)
+    y_s, _ = run_layer(spec, x, w, fuse=False)
+    check_full(spec, y_f, x, w)
+    check_full(spec, y_s, x, w)
+
+
 # F(5^2, 4^2): alpha = 8, 4 x 4 kernels (the kernel size of the paper's 2-D
 # benchmark, §4.4); k_gemm_inv with 64 elements and 25 outputs per (tile, kernel)
 F54 = [
@@ -361,9 +410,19 @@ def _run_stack(stack, seed, full):
 def test_full_size_configs_full_output(cfg):
     spec = CONFIGS[cfg]
     x, w = draw_layer(spec, seed=cfg)
-    y, _ = run_layer(spec, x, w)
+    y, plan = run_layer(spec, x, w)
     assert y.shape == (spec.batch, spec.K) + spec.out_spatial
     assert np.all(np.isfinite(y))
+    assert plan.desc["fused"] == (1 if cfg == 4 else 0)
+    check_full(spec, y, x, w)
+
+
+def test_full_size_config4_two_stage_full_output():
+    """The F(4^3) volume layer through V in memory (WINO_NO_FUSE)."""
+    spec = CONFIGS[4]
+    x, w = draw_layer(spec, seed=4)
+    y, plan = run_layer(spec, x, w, fuse=False)
+    assert plan.desc["fused"] == 0
     check_full(spec, y, x, w)
 
 
