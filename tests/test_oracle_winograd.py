@@ -194,3 +194,92 @@ def test_one_hot_kernel_selects_input(p):
     Y = y.shape[2:]
     want = x[0, 0, p[0]:p[0] + Y[0], p[1]:p[1] + Y[1], p[2]:p[2] + Y[2]]
     assert np.array_equal(y[0, 0], want)
+
+
+# ---- per-axis transforms (eq. 4 with its own C_n, B_n, A_n on each axis)
+ANISO_EXACT = [
+    # N, m per axis, r, n, C, K, X, pad
+    (3, (2, 4, 4), 3, 1, 2, 2, (5, 9, 7), 1),
+    (3, (4, 2, 2), 3, 1, 2, 3, (7, 4, 5), 1),
+    (3, (2, 4, 4), 3, 2, 2, 2, (3, 6, 6), 0),
+    (3, (4, 2, 2), 3, 1, 3, 2, (6, 5, 3), 0),
+    (3, (2, 4, 2), 3, 1, 2, 2, (4, 7, 5), 1),
+    (2, (2, 4), 3, 1, 2, 2, (7, 9), 1),
+    (2, (4, 2), 3, 2, 2, 3, (6, 5), 0),
+    (2, (3, 5), 4, 1, 2, 2, (9, 11), 1),
+]
+
+
+@pytest.mark.parametrize("N,ms,r,n,C,K,X,pad", ANISO_EXACT)
+def test_anisotropic_exact_equals_direct(N, ms, r, n, C, K, X, pad):
+    """Mixed per-axis tiles reach the direct correlation exactly (rationals):
+    ragged tiles on every axis, pad 0 and 1."""
+    rng = np.random.default_rng(abs(hash((N, ms, X))) % 2**32)
+    x = rng.integers(-3, 4, size=(n, C) + X)
+    w = rng.integers(-3, 4, size=(K, C) + (r,) * N)
+    y_ref, _ = direct_naive(x, w, pad)
+    y = winograd_forward(x, w, ms, r, pad=pad, exact=True)
+    assert y.shape == y_ref.shape
+    assert all(Fraction(float(a)) == b for a, b in zip(y_ref.reshape(-1), y.reshape(-1)))
+
+
+def test_anisotropic_separability():
+    """The N-D data and kernel transforms with per-axis matrices equal the
+    Kronecker product of the per-axis 1-D transforms applied to the
+    vectorised tile, in any axis order (exact)."""
+    ms, r = (2, 4, 4), 3
+    mats = [matrices(mi, r, exact=True) for mi in ms]
+    alphas = tuple(mi + r - 1 for mi in ms)
+    rng = random.Random(17)
+    d = np.array([Fraction(rng.randint(-4, 4)) for _ in range(int(np.prod(alphas)))],
+                 dtype=object).reshape(alphas)
+    kB = np.kron(np.kron(mats[0][1], mats[1][1]), mats[2][1])
+    ref = kB.dot(d.reshape(-1)).reshape(alphas)
+    for order in itertools.permutations(range(3)):
+        got = mode_products(d, [mats[a][1] for a in order], list(order))
+        assert (got == ref).all()
+    g = np.array([Fraction(rng.randint(-4, 4)) for _ in range(r ** 3)], dtype=object).reshape((r,) * 3)
+    kG = np.kron(np.kron(mats[0][2], mats[1][2]), mats[2][2])
+    refg = kG.dot(g.reshape(-1)).reshape(alphas)
+    assert (mode_products(g, [mats[a][2] for a in range(3)], [0, 1, 2]) == refg).all()
+
+
+def test_anisotropic_axis_mistakes_caught():
+    """Planted mistakes in the per-axis matrices: the first axis's B^T applied
+    along the second (sizes 4 and 6 clash), and a dropped CRT factor in one
+    axis's G only (the result is no longer the correlation)."""
+    import oracle.winograd as ow
+    orig = ow._axis_matrices
+    x = np.random.default_rng(3).integers(-3, 4, size=(1, 2, 5, 7, 6))
+    w = np.random.default_rng(4).integers(-3, 4, size=(2, 2, 3, 3, 3))
+
+    def swapped(m, r, N, points, exact):
+        mats = orig(m, r, N, points, exact)
+        (A0, B0, G0), (A1, B1, G1) = mats[0], mats[1]
+        return [(A0, B1, G0), (A1, B0, G1)] + mats[2:]
+    ow._axis_matrices = swapped
+    try:
+        with pytest.raises(ValueError):
+            ow.winograd_forward(x, w, (2, 4, 4), 3, pad=1, exact=True)
+    finally:
+        ow._axis_matrices = orig
+
+    def scaled(m, r, N, points, exact):
+        mats = orig(m, r, N, points, exact)
+        A0, B0, G0 = mats[0]
+        return [(A0, B0, G0 * 2)] + mats[1:]
+    y_ref, _ = direct_naive(x, w, 1)
+    good = ow.winograd_forward(x, w, (2, 4, 4), 3, pad=1, exact=True)
+    assert all(Fraction(float(a)) == b for a, b in zip(y_ref.reshape(-1), good.reshape(-1)))
+    ow._axis_matrices = scaled
+    try:
+        bad = ow.winograd_forward(x, w, (2, 4, 4), 3, pad=1, exact=True)
+    finally:
+        ow._axis_matrices = orig
+    assert not all(Fraction(float(a)) == b for a, b in zip(y_ref.reshape(-1), bad.reshape(-1)))
+
+
+def test_anisotropic_points_rejected():
+    with pytest.raises(ValueError):
+        winograd_forward(np.zeros((1, 1, 5, 5, 5)), np.zeros((1, 1, 3, 3, 3)), (2, 4, 4), 3,
+                         points=(0, 1, -1))
