@@ -87,12 +87,20 @@ typedef struct {
   int32_t n_points;
   uint32_t flags; /* WINO_RELU or WINO_LEAKY_RELU, | WINO_NO_SPLIT | WINO_NO_FUSE; or 0 */
   float slope;    /* WINO_LEAKY_RELU: the slope below zero; ignored otherwise */
+  /* Per-axis output tiles: eq. (4) lets every axis n carry its own transform
+   * triple (C_n, B_n, A_n).  tile[i] = 0 keeps m; a non-zero entry sets axis
+   * i's tile extent m_i, with F(m_i, r)'s matrices on that axis.  Compiled
+   * mixed tiles: N = 3, r = 3, m_0 != m_1 = m_2 with {m_0, m_1} = {2, 4}
+   * (e.g. {2, 4, 4}: 2 on a short first axis, 4 on the others); each axis
+   * uses its F(m, r)'s default points (points must be NULL).  Entries past N
+   * must be 0. */
+  int32_t tile[3];
 } wino_opts;
 
 /* Plan summary (host-side numbers only). */
 typedef struct {
-  int32_t N, m, r, alpha;
-  int32_t n_xi;          /* alpha^N transformed elements                         */
+  int32_t N, m, r, alpha; /* alpha = m + r - 1; 0 when the axes' tiles differ    */
+  int32_t n_xi;          /* transformed elements per tile: prod of alpha_axis     */
   int32_t C, K;
   int32_t C_pad, K_pad;  /* C and K rounded up to the GEMM step / block           */
   int64_t batch;
@@ -107,6 +115,8 @@ typedef struct {
   int32_t gemm_parts;    /* parts each tail block of the product is split into   */
   int64_t gemm_tail_blocks; /* product blocks split into gemm_parts parts         */
   int32_t fused;         /* 1: wino_forward fuses the input transform into the product */
+  int32_t tile[3];       /* output-tile extent per axis (1 past N)                */
+  int32_t alpha_axis[3]; /* input-tile extent per axis, tile + r - 1 (1 past N)   */
 } wino_plan_desc;
 
 /* Build a plan for one layer.  §3.1-§3.3 and §4.1.
@@ -179,7 +189,8 @@ wino_status wino_output_dims(const wino_plan_t* plan, int64_t* out);
 /* Test hook: copy the transform matrices of Theorem 1 / Algorithm 1 (§2.1-§2.2;
  * the paper's A, B and C of eq. (1)), each entry the exact rational rounded
  * once to the nearest double, row-major: AT [m][alpha], BT [alpha][alpha],
- * G [alpha][r].  Any pointer may be NULL; WINO_EINVAL for a NULL plan. */
+ * G [alpha][r].  Any pointer may be NULL; WINO_EINVAL for a NULL plan,
+ * WINO_EUNSUPPORTED for a plan with per-axis tiles (one triple per axis). */
 wino_status wino_get_matrices(const wino_plan_t* plan, double* AT, double* BT, double* G);
 
 /* Kernel transform U = g x_1 G ... x_N G for every (k, c) (eq. 4; §3.3 caches

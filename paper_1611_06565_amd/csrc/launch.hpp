@@ -214,6 +214,10 @@ constexpr SizeOps make_ops() {
     return SizeOps{&L::filter, &L::input, &L::gemm, &L::wgrad, nullptr};
 }
 
+// Per-axis tiles (aniso.hpp): F(M0, R) on axis 0, F(M1, R) on axes 1 and 2;
+// instances in sizes_ax.hip.
+const SizeOps* size_ops_ax(int m0, int m1);
+
 // The tables, one per compiled size (defined in the sizes_*.hip units);
 // const_mats selects the instances with the default points compiled in.
 #define WINO_SIZES(X) \

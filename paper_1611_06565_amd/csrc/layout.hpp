@@ -53,4 +53,18 @@ constexpr SizeTraits size_traits() {
   return t;
 }
 
+// Anisotropic 3-D tiles (F(M0, R) on axis 0, F(M1, R) on axes 1 and 2):
+// k_input_ax and k_gemm_ax on the F(4^3) layouts (16-tile V blocks of
+// 4-channel groups, 16-kernel blocks).
+template <int M0, int M1, int R>
+constexpr SizeTraits size_traits_ax() {
+  SizeTraits t{};
+  t.A = 0;
+  t.NXI = (M0 + R - 1) * (M1 + R - 1) * (M1 + R - 1);
+  t.KIND = 3;
+  t.BLK = 16; t.KBLK = 16; t.CG = 4; t.CGU = 4; t.CPAD = 16;
+  t.TB = 16; t.KB = 16;
+  return t;
+}
+
 }  // namespace wino

@@ -250,17 +250,40 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   if (N < 1 || N > 3 || m < 1 || r < 1 || C < 1 || K < 1) return WINO_EINVAL;
   if (C > kMaxChannels || K > kMaxChannels) return WINO_EINVAL;
   if (m + r - 1 > kMaxAlpha) return WINO_EUNSUPPORTED;
-  SizeTraits t{};
-  if (!traits_of(N, m, r, &t)) return WINO_EUNSUPPORTED;
   wino_opts o{};
   if (opts) o = *opts;
   if (o.flags & ~(WINO_RELU | WINO_NO_SPLIT | WINO_LEAKY_RELU | WINO_NO_FUSE)) return WINO_EINVAL;
   if ((o.flags & WINO_RELU) && (o.flags & WINO_LEAKY_RELU)) return WINO_EINVAL;
   if ((o.flags & WINO_LEAKY_RELU) && !std::isfinite(o.slope)) return WINO_EINVAL;
-  const int alpha = m + r - 1;
+  // per-axis output tiles (eq. 4): tile[i] = 0 keeps m
+  int ms[3] = {1, 1, 1};
+  bool aniso = false;
+  for (int i = 0; i < 3; ++i) {
+    if (o.tile[i] < 0 || o.tile[i] > kMaxAlpha || (i >= N && o.tile[i] != 0)) return WINO_EINVAL;
+    if (i < N) ms[i] = o.tile[i] != 0 ? o.tile[i] : m;
+    aniso = aniso || (i < N && ms[i] != m);
+  }
+  SizeTraits t{};
+  if (aniso) {
+    // compiled: 3-D, r = 3, F(m0, 3) on axis 0 and F(m1, 3) on axes 1 and 2,
+    // {m0, m1} = {2, 4}; each axis takes its F(m, r)'s default points
+    if (N != 3 || r != 3 || ms[1] != ms[2] || ms[0] == ms[1]) return WINO_EUNSUPPORTED;
+    if (ms[0] == 2 && ms[1] == 4) t = size_traits_ax<2, 4, 3>();
+    else if (ms[0] == 4 && ms[1] == 2) t = size_traits_ax<4, 2, 3>();
+    else return WINO_EUNSUPPORTED;
+    if (o.points != nullptr || o.n_points != 0) return WINO_EINVAL;
+  } else if (!traits_of(N, m, r, &t)) {
+    return WINO_EUNSUPPORTED;
+  }
+  const int alpha = aniso ? 0 : m + r - 1;
 
   wino_plan_s p{};
   p.N = N; p.m = m; p.r = r; p.alpha = alpha; p.C = C; p.K = K;
+  p.aniso = aniso;
+  for (int i = 0; i < 3; ++i) {
+    p.mv[i] = ms[i];
+    p.av[i] = i < N ? ms[i] + r - 1 : 1;
+  }
   p.flags = o.flags;
   p.slope = (o.flags & WINO_LEAKY_RELU) ? o.slope : 0.0f;
   p.kind = t.KIND;
@@ -276,7 +299,7 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
     const int64_t Y = X + 2 * int64_t(pad) - r + 1;
     if (Y < 1 || Y > kMaxI32) return WINO_EINVAL;
     p.X[i] = X; p.pad[i] = pad; p.Y[i] = Y;
-    p.tiles[i] = (Y + m - 1) / m;
+    p.tiles[i] = (Y + ms[i] - 1) / ms[i];
     T *= p.tiles[i];                          // < 2^31 * 2^31: no overflow before the check
     if (T > kMaxI32) return WINO_EINVAL;
     if (!mul_ok(xin, X, &xin) || !mul_ok(yout, Y, &yout)) return WINO_EINVAL;
@@ -306,7 +329,10 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   if (!grid_ok(cdiv(cpad * kpad, 64), 64, &p.grid_filter)) return WINO_EINVAL;
   const int64_t groups = cpad / p.cg;
   int64_t ig = 0;
-  if (p.nxi > 64) {
+  if (aniso) {
+    // k_input_ax: one V block per work-group, alpha0 waves
+    if (!mul_ok(tpad / p.blk, groups, &ig) || !grid_ok(ig, p.av[0] * 64, &p.grid_input)) return WINO_EINVAL;
+  } else if (p.nxi > 64) {
     // k_input_split: one V block (BLK tiles x one channel group) per work-group
     if (!mul_ok(tpad / p.blk, groups, &ig) || !grid_ok(ig, alpha * 64, &p.grid_input)) return WINO_EINVAL;
   } else {
@@ -318,7 +344,7 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   if (t.KIND == 0 || t.KIND == 1) {
     if (!acc_geometry(p, t, !(o.flags & WINO_NO_SPLIT), device_cu_count())) return WINO_EINVAL;
   } else {
-    // k_gemm_inv: one (tile block, kernel block) per work-group, up to 12 waves
+    // k_gemm_inv, k_gemm_ax: one (tile block, kernel block) per work-group, up to 12 waves
     p.nparts = 1;
     p.grid_reduce = 0;
     int64_t gg = 0;
@@ -328,8 +354,18 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   // F(4^3) with few kernels: the input transform runs inside the product
   // (recomputed for each block of 16 kernels, so only while there are at
   // most 4 such blocks); same grid as k_gemm_inv
-  p.fused = N == 3 && m == 4 && r == 3 && p.K_pad <= 64 && !(o.flags & WINO_NO_FUSE);
+  p.fused = !aniso && N == 3 && m == 4 && r == 3 && p.K_pad <= 64 && !(o.flags & WINO_NO_FUSE);
   if (p.fused && !grid_ok(int64_t(p.T_pad / p.blk) * (p.K_pad / 16), 768, &p.grid_fused)) return WINO_EINVAL;
+
+  if (aniso) {
+    // every axis uses its F(m, r)'s default points, compiled into the kernels
+    p.const_mats = true;
+    p.wgrad_ok = false;
+    wino_plan_s* h = new (std::nothrow) wino_plan_s(p);
+    if (h == nullptr) return WINO_EINVAL;
+    *out = h;
+    return WINO_OK;
+  }
 
   // Transform synthesis (a1): exact rationals, one rounding per entry.
   Rat pts[kMaxAlpha];
@@ -389,6 +425,7 @@ wino_status wino_plan_describe(const wino_plan_t* p, wino_plan_desc* d) {
   d->gemm_tail_blocks = p->ntail;
   d->default_points = p->const_mats ? 1 : 0;
   d->fused = p->fused ? 1 : 0;
+  for (int i = 0; i < 3; ++i) { d->tile[i] = p->mv[i]; d->alpha_axis[i] = p->av[i]; }
   return WINO_OK;
 }
 
@@ -420,6 +457,7 @@ wino_status wino_output_dims(const wino_plan_t* p, int64_t* out) {
 
 wino_status wino_get_matrices(const wino_plan_t* p, double* AT, double* BT, double* G) {
   if (p == nullptr) return WINO_EINVAL;
+  if (p->aniso) return WINO_EUNSUPPORTED;   // one triple per axis
   const int a = p->alpha;
   if (AT) for (int i = 0; i < p->m; ++i) for (int j = 0; j < a; ++j) AT[i * a + j] = p->AT[i][j];
   if (BT) for (int i = 0; i < a; ++i) for (int j = 0; j < a; ++j) BT[i * a + j] = p->BT[i][j];
@@ -442,6 +480,8 @@ wino_status wino_plan_adjoint(const wino_plan_t* f, wino_plan_t** out) {
   o.points = f->n_user_pts > 0 ? f->user_pts : nullptr;
   o.n_points = f->n_user_pts;
   o.flags = f->flags & WINO_NO_SPLIT;
+  if (f->aniso)
+    for (int i = 0; i < f->N; ++i) o.tile[i] = f->mv[i];
   int64_t dims[4] = {f->batch, 1, 1, 1};
   for (int i = 0; i < f->N; ++i) dims[1 + i] = f->Y[i];
   return wino_plan(f->N, f->m, f->r, f->K, f->C, dims, &o, out);

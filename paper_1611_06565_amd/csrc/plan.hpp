@@ -17,6 +17,11 @@ struct wino_plan_s {
   int32_t pad[3];
   int64_t T, T_pad;
   int blk, kblk, cg, cgu, kind;
+  // per-axis output tiles (eq. 4's own transform triple per axis): mv[i] is
+  // the tile extent of axis i (1 on unused axes); aniso when they differ
+  // (then axis 0 uses F(mv[0], r) and axes 1, 2 F(mv[1], r), default points)
+  int mv[3], av[3];
+  bool aniso;
   int32_t n_user_pts;     // the caller's points (0: default set), kept for wino_plan_adjoint
   double user_pts[wino::kMaxAlpha];
   // weight gradient: F(r, m) on the same points (its B^T is the forward's)

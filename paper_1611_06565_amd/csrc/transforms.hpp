@@ -315,4 +315,16 @@ __device__ __forceinline__ void transform_nd(const float* src, float* dst, const
   }
 }
 
+// 3-D transform with its own matrix per axis (eq. 4's C_n, B_n, A_n):
+// [I0][I1][I2] -> [O0][O1][O2], axis 0 first.
+template <int I0, int O0, int I1, int O1, int I2, int O2, class M0, class M1, class M2>
+__device__ __forceinline__ void transform3_axes(const float* src, float* dst, const M0& a, const M1& b,
+                                                const M2& c) {
+  float t1[O0 * I1 * I2];
+  float t2[O0 * O1 * I2];
+  apply_axis<1, I0, O0, I1 * I2>(src, t1, a);
+  apply_axis<O0, I1, O1, I2>(t1, t2, b);
+  apply_axis<O0 * O1, I2, O2, 1>(t2, dst, c);
+}
+
 }  // namespace wino

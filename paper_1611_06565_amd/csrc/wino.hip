@@ -64,6 +64,7 @@ wino_status scratch_address(void** out) {
 // The launch table of a plan's size (the planner only makes plans of
 // compiled sizes).
 const SizeOps* ops_of(const wino_plan_s& p) {
+  if (p.aniso) return size_ops_ax(p.mv[0], p.mv[1]);
 #define WINO_PICK(N_, M_, R_) \
   if (p.N == N_ && p.m == M_ && p.r == R_) return size_ops_##N_##_##M_##_##R_(p.const_mats);
   WINO_SIZES(WINO_PICK)

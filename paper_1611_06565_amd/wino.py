@@ -33,7 +33,8 @@ class WinoError(RuntimeError):
 
 class _Opts(ctypes.Structure):
     _fields_ = [("pad", ctypes.c_int32 * 3), ("points", ctypes.POINTER(ctypes.c_double)),
-                ("n_points", ctypes.c_int32), ("flags", ctypes.c_uint32), ("slope", ctypes.c_float)]
+                ("n_points", ctypes.c_int32), ("flags", ctypes.c_uint32), ("slope", ctypes.c_float),
+                ("tile", ctypes.c_int32 * 3)]
 
 
 class _Desc(ctypes.Structure):
@@ -47,7 +48,8 @@ class _Desc(ctypes.Structure):
                 ("block_tiles", ctypes.c_int32), ("block_kernels", ctypes.c_int32),
                 ("default_points", ctypes.c_int32), ("channel_group", ctypes.c_int32),
                 ("filter_channel_group", ctypes.c_int32), ("gemm_parts", ctypes.c_int32),
-                ("gemm_tail_blocks", ctypes.c_int64), ("fused", ctypes.c_int32)]
+                ("gemm_tail_blocks", ctypes.c_int64), ("fused", ctypes.c_int32),
+                ("tile", ctypes.c_int32 * 3), ("alpha_axis", ctypes.c_int32 * 3)]
 
 
 _LIB = None
@@ -143,10 +145,11 @@ class Plan:
     relu=True sets WINO_RELU; leaky=s (a float) sets WINO_LEAKY_RELU with
     slope s (the activation f of eq. 2).  split=False sets WINO_NO_SPLIT: no
     product block is split over several work-groups, whatever the grid size.
-    fuse=False sets WINO_NO_FUSE: an F(4^3) forward stays in two stages."""
+    fuse=False sets WINO_NO_FUSE: an F(4^3) forward stays in two stages.
+    tile=(m_0, .., m_{N-1}) sets per-axis output tiles (wino_opts.tile)."""
 
     def __init__(self, N, m, r, C, K, dims, pad=0, points=None, relu=False, split=True, leaky=None,
-                 fuse=True):
+                 fuse=True, tile=None):
         L = lib()
         dims = [int(d) for d in dims]
         if len(dims) != N + 1:
@@ -164,6 +167,11 @@ class Plan:
         if leaky is not None:
             opts.flags |= WINO_LEAKY_RELU
             opts.slope = float(leaky)
+        if tile is not None:
+            if len(tile) != N:
+                raise ValueError("one tile extent per axis")
+            for i, t in enumerate(tile):
+                opts.tile[i] = int(t)
         arr = (ctypes.c_int64 * len(dims))(*dims)
         h = ctypes.c_void_p()
         _check(L.wino_plan(N, m, r, C, K, arr, ctypes.byref(opts), ctypes.byref(h)), "wino_plan")
@@ -175,7 +183,7 @@ class Plan:
         self._L = L
         d = _Desc()
         _check(L.wino_plan_describe(h, ctypes.byref(d)), "wino_plan_describe")
-        self.desc = {f: (list(getattr(d, f)) if f in ("X", "Y", "tiles") else getattr(d, f))
+        self.desc = {f: (list(getattr(d, f)) if f in ("X", "Y", "tiles", "tile", "alpha_axis") else getattr(d, f))
                      for f, _ in _Desc._fields_}
         N, C, K, r = d.N, d.C, d.K, d.r
         self.N, self.m, self.r, self.C, self.K = N, d.m, r, C, K

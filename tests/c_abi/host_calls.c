@@ -18,7 +18,7 @@
 
 int main(void) {
   const int64_t dims[4] = {8, 16, 56, 56};
-  wino_opts o = {{1, 1, 1}, NULL, 0, WINO_RELU, 0.0f};
+  wino_opts o = {{1, 1, 1}, NULL, 0, WINO_RELU, 0.0f, {0, 0, 0}};
   wino_plan_t* p = NULL;
   CHECK(wino_plan(3, 2, 3, 64, 128, dims, &o, &p) == WINO_OK && p != NULL, "plan F(2^3,3^3)");
 
@@ -29,6 +29,17 @@ int main(void) {
   CHECK(wino_filter_bytes(p) == (size_t)4 * 64 * d.C_pad * d.K_pad, "filter bytes");
   CHECK(wino_workspace_bytes(p) >= (size_t)4 * 64 * d.C_pad * d.T_pad, "workspace holds V");
   CHECK(wino_weight_gradient_workspace_bytes(p) > wino_workspace_bytes(p), "weight-gradient workspace");
+  CHECK(wino_forward_workspace_bytes(p) == wino_workspace_bytes(p), "two-stage forward workspace");
+
+  /* per-axis tiles: 2 on the first axis, 4 on the others (eq. 4) */
+  wino_opts ot = {{1, 1, 1}, NULL, 0, 0u, 0.0f, {2, 4, 4}};
+  wino_plan_t* pa = NULL;
+  const int64_t dims_a[4] = {2, 7, 13, 11};
+  CHECK(wino_plan(3, 4, 3, 20, 24, dims_a, &ot, &pa) == WINO_OK && pa != NULL, "plan with per-axis tiles");
+  wino_plan_desc dd;
+  CHECK(wino_plan_describe(pa, &dd) == WINO_OK && dd.n_xi == 4 * 6 * 6 && dd.tile[0] == 2 && dd.alpha_axis[1] == 6,
+        "per-axis tiles described");
+  wino_destroy(pa);
 
   int64_t out[5];
   CHECK(wino_output_dims(p, out) == WINO_OK && out[0] == 8 && out[1] == 128 && out[4] == 56, "output dims");

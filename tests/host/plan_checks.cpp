@@ -132,6 +132,33 @@ int main() {
     CHECK(wino_plan(3, 7, 3, 4, 4, dims, nullptr, &p) == WINO_EUNSUPPORTED, "alpha 9");
     wino_destroy(nullptr);
   }
+  // per-axis tiles (eq. 4 with one transform triple per axis)
+  {
+    const int64_t dims[4] = {4, 8, 28, 28};
+    wino_opts o{};
+    o.pad[0] = o.pad[1] = o.pad[2] = 1;
+    o.tile[0] = 2;
+    wino_plan_t* p = nullptr;
+    CHECK(wino_plan(3, 4, 3, 256, 256, dims, &o, &p) == WINO_OK, "tiles (2, 4, 4)");
+    wino_plan_desc d{};
+    CHECK(wino_plan_describe(p, &d) == WINO_OK && d.n_xi == 144 && d.T == 4 * 4 * 7 * 7 && d.fused == 0,
+          "tiles (2, 4, 4) described");
+    CHECK(wino_weight_gradient_workspace_bytes(p) == 0, "no weight gradient for per-axis tiles");
+    wino_plan_t* a = nullptr;
+    CHECK(wino_plan_adjoint(p, &a) == WINO_OK, "adjoint of per-axis tiles");
+    wino_destroy(a);
+    wino_destroy(p);
+    o.tile[0] = 4; o.tile[1] = 2; o.tile[2] = 2;
+    CHECK(wino_plan(3, 2, 3, 3, 64, dims, &o, &p) == WINO_OK, "tiles (4, 2, 2)");
+    wino_destroy(p);
+    o.tile[2] = 4;
+    CHECK(wino_plan(3, 2, 3, 3, 64, dims, &o, &p) == WINO_EUNSUPPORTED, "tiles (4, 2, 4)");
+    o.tile[0] = 0; o.tile[1] = 0; o.tile[2] = int32_t(1) << 30;
+    CHECK(wino_plan(3, 2, 3, 3, 64, dims, &o, &p) == WINO_EINVAL, "tile 2^30");
+    const int64_t big[4] = {0x7fffffff, 3, 3, 0x7fffffff};
+    o.tile[0] = 2; o.tile[1] = 4; o.tile[2] = 4;
+    CHECK(wino_plan(3, 4, 3, 4, 4, big, &o, &p) == WINO_EINVAL, "per-axis tiles, tiles past 2^31");
+  }
   // max-pool geometry
   {
     using wino::PoolGeom;

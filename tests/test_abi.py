@@ -276,3 +276,48 @@ def test_plan_rejects_overflowing_sizes(L):
     for dims in [(1 << 62, 2, 2, 2), (1 << 40, big, big, big), (1 << 34, 2, 2, 2), (-1, 2, 2, 2)]:
         arr = (ctypes.c_int64 * 4)(*dims)
         assert L.wino_maxpool3d(arr, win, vp(4096), vp(8192), None) == -1, dims
+
+
+def test_per_axis_tiles_host_side(L):
+    """wino_opts.tile: mixed tiles (2, 4, 4) and (4, 2, 2) in 3-D plan; other
+    mixes are unsupported, caller points and entries past N are refused."""
+    def st(N, m, tile, points=None, dims=None):
+        opts = wino._Opts()
+        for i, t in enumerate(tile):
+            opts.tile[i] = t
+        keep = None
+        if points is not None:
+            keep = (ctypes.c_double * len(points))(*points)
+            opts.points = ctypes.cast(keep, ctypes.POINTER(ctypes.c_double))
+            opts.n_points = len(points)
+        dims = dims or [1] + [9] * N
+        arr = (ctypes.c_int64 * len(dims))(*dims)
+        h = ctypes.c_void_p()
+        s = L.wino_plan(N, m, 3, 4, 4, arr, ctypes.byref(opts), ctypes.byref(h))
+        if s == 0:
+            L.wino_destroy(h)
+        return s
+    assert st(3, 4, (2, 0, 0)) == 0
+    assert st(3, 2, (4, 2, 2)) == 0
+    assert st(3, 2, (0, 4, 4)) == 0          # (2, 4, 4) from m = 2
+    assert st(3, 4, (4, 4, 4)) == 0          # isotropic
+    assert st(3, 4, (2, 4, 2)) == -2
+    assert st(3, 4, (2, 2, 4)) == -2
+    assert st(2, 4, (2, 4, 0)) == -2
+    assert st(3, 4, (2, 0, 0), points=(0, 1, -1, 2, -2)) == -1
+    assert st(2, 4, (0, 0, 2)) == -1         # entry past N
+    assert st(3, 4, (-1, 0, 0)) == -1
+    p = wino.Plan(3, 4, 3, 20, 24, [2, 7, 13, 11], pad=1, tile=(2, 4, 4))
+    d = p.desc
+    assert d["tile"] == [2, 4, 4] and d["alpha_axis"] == [4, 6, 6] and d["alpha"] == 0
+    assert d["n_xi"] == 144 and d["tiles"] == [4, 4, 3] and d["T"] == 2 * 4 * 4 * 3
+    assert d["fused"] == 0 and p.forward_workspace_bytes == p.workspace_bytes > 0
+    assert p.filter_bytes == 4 * 144 * d["C_pad"] * d["K_pad"]
+    assert p.weight_gradient_workspace_bytes == 0
+    a = p.adjoint()
+    assert a.desc["tile"] == [2, 4, 4] and a.input_shape == p.output_shape
+    AT = np.zeros(64)
+    P = ctypes.POINTER(ctypes.c_double)
+    assert L.wino_get_matrices(p.handle, AT.ctypes.data_as(P), None, None) == -2
+    q = wino.Plan(3, 2, 3, 3, 5, [1, 9, 6, 7], tile=(4, 2, 2))
+    assert q.desc["tile"] == [4, 2, 2] and q.desc["n_xi"] == 96 and q.output_shape == (1, 5, 7, 4, 5)

@@ -50,6 +50,7 @@ class LayerSpec:
     relu: bool = False
     points: Tuple = None       # interpolation points; None = library default
     leaky: float = None        # leaky ReLU slope (activation v or slope * v); None = off
+    tile: Tuple = None         # per-axis output tiles (eq. 4, one triple per axis); None = m on every axis
 
     def with_(self, **kw) -> "LayerSpec":
         return replace(self, **kw)
