@@ -89,7 +89,8 @@ typedef struct {
   float slope;    /* WINO_LEAKY_RELU: the slope below zero; ignored otherwise */
   /* Per-axis output tiles: eq. (4) lets every axis n carry its own transform
    * triple (C_n, B_n, A_n).  tile[i] = 0 keeps m; a non-zero entry sets axis
-   * i's tile extent m_i, with F(m_i, r)'s matrices on that axis.  Compiled
+   * i's tile extent m_i, with F(m_i, r)'s matrices on that axis (equal
+   * extents on every axis make an ordinary plan of that m).  Compiled
    * mixed tiles: N = 3, r = 3, m_0 != m_1 = m_2 with {m_0, m_1} = {2, 4}
    * (e.g. {2, 4, 4}: 2 on a short first axis, 4 on the others); each axis
    * uses its F(m, r)'s default points (points must be NULL).  Entries past N

@@ -262,7 +262,9 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
     }
   };
 
-  const int nchunks = a.C_pad / CH;
+  // chunks past the last real channel hold only zero padding (x and U are
+  // zero there): they are skipped
+  const int nchunks = (a.C + CH - 1) / CH;
   for (int chunk = 0; chunk < nchunks; ++chunk) {
     if (chunk > 0) __syncthreads();             // the previous chunk's planes are read
     produce(chunk);

@@ -261,8 +261,10 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   for (int i = 0; i < 3; ++i) {
     if (o.tile[i] < 0 || o.tile[i] > kMaxAlpha || (i >= N && o.tile[i] != 0)) return WINO_EINVAL;
     if (i < N) ms[i] = o.tile[i] != 0 ? o.tile[i] : m;
-    aniso = aniso || (i < N && ms[i] != m);
+    aniso = aniso || (i < N && ms[i] != ms[0]);
   }
+  if (!aniso) m = ms[0];   // the same tile on every axis: an isotropic plan of that m
+  if (m + r - 1 > kMaxAlpha) return WINO_EUNSUPPORTED;
   SizeTraits t{};
   if (aniso) {
     // compiled: 3-D, r = 3, F(m0, 3) on axis 0 and F(m1, 3) on axes 1 and 2,

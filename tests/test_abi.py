@@ -301,6 +301,8 @@ def test_per_axis_tiles_host_side(L):
     assert st(3, 2, (4, 2, 2)) == 0
     assert st(3, 2, (0, 4, 4)) == 0          # (2, 4, 4) from m = 2
     assert st(3, 4, (4, 4, 4)) == 0          # isotropic
+    assert st(3, 2, (4, 4, 4)) == 0          # isotropic, m = 4 from the tiles
+    assert wino.Plan(3, 2, 3, 4, 4, [1, 9, 9, 9], tile=(4, 4, 4)).desc["m"] == 4
     assert st(3, 4, (2, 4, 2)) == -2
     assert st(3, 4, (2, 2, 4)) == -2
     assert st(2, 4, (2, 4, 0)) == -2

@@ -380,13 +380,17 @@ def test_small_c3d_stack_per_layer():
     _run_stack(stack, seed=4, full=True)
 
 
-def _run_stack(stack, seed, full):
+def _run_stack(stack, seed, full, ms=None):
+    """Run the stack layer by layer (ms: the output tile of each layer), each
+    layer's output checked against the oracle fed with the GPU's input."""
     torch = require_gpu()
     from paper_1611_06565_amd.wino import Plan, maxpool3d
     x, ws = draw_stack(stack, seed)
     cur = torch.from_numpy(x).cuda()
-    for (spec, pool), w in zip(stack.layers(), ws):
-        log(f"[gpu] {spec.name} C={spec.C} K={spec.K} X={spec.X}")
+    for i, ((spec, pool), w) in enumerate(zip(stack.layers(), ws)):
+        if ms is not None:
+            spec = spec.with_(m=ms[i])
+        log(f"[gpu] {spec.name} C={spec.C} K={spec.K} X={spec.X} m={spec.m}")
         plan = Plan(3, spec.m, 3, spec.C, spec.K, [spec.batch] + list(spec.X), pad=1, relu=True)
         U = plan.transform_filter(torch.from_numpy(w).cuda())
         y = plan.forward(cur, U)
@@ -458,6 +462,16 @@ def test_full_size_fig4_layer_full_output():
     assert y.shape == (20, 32, 221, 221)
     assert np.all(np.isfinite(y))
     check_full(spec, y, x, w)
+
+
+def test_full_size_c3d_stack_mixed_tiles_full_output():
+    """The stack with F(4^3) on conv1-conv4 (conv1, 64 kernels, through the
+    fused kernel with its 3 channels in one 8-channel chunk; conv2-conv4 in
+    two stages) and F(2^3) on conv5-conv8, the per-layer choice that
+    bench.py --stack-tiles times; every layer on every output, at its own
+    tile's bar."""
+    out = _run_stack(C3D_STACK, seed=6, full=True, ms=(4, 4, 4, 4, 2, 2, 2, 2))
+    assert tuple(out.shape) == (4, 512, 1, 3, 3)
 
 
 def test_full_size_c3d_stack_full_output():
