@@ -30,20 +30,50 @@ sys.path.insert(0, ROOT)
 PEAK_FP32_MFMA = 157.3      # TFLOP/s, MI355X dense fp32 matrix
 PEAK_HBM = 8000.0           # GB/s, MI355X HBM3E
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = ["paper_1611_06565_amd/csrc/kernels.hpp", "paper_1611_06565_amd/csrc/gemm_acc.hpp",
-                  "paper_1611_06565_amd/csrc/gemm_acc4.hpp", "paper_1611_06565_amd/csrc/transforms.hpp",
-                  "paper_1611_06565_amd/csrc/synth.hpp", "paper_1611_06565_amd/csrc/wgrad.hpp",
-                  "paper_1611_06565_amd/csrc/layout.hpp", "paper_1611_06565_amd/csrc/launch.hpp",
-                  "paper_1611_06565_amd/csrc/plan.cpp", "paper_1611_06565_amd/csrc/wino.hip"]
+CSRC = "paper_1611_06565_amd/csrc/"
+_COMMON = ["kernels.hpp", "transforms.hpp", "synth.hpp", "layout.hpp", "launch.hpp", "plan.hpp"]
+# the sources that define each kernel family's code (a profile stays valid
+# while they and the plan's launch geometry are unchanged)
+FAMILY_SOURCES = {
+    "m2": _COMMON + ["gemm_acc.hpp", "sizes_m2.hip"],
+    "f42": _COMMON + ["gemm_acc.hpp", "gemm_acc4.hpp", "sizes_f42.hip"],
+    "f43": _COMMON + ["sizes_f43.hip"],
+    "f43fused": _COMMON + ["fused43.hpp", "fused_f43.hip"],
+    "ax": _COMMON + ["aniso.hpp", "sizes_ax.hip"],
+    "a8": _COMMON + ["sizes_f54.hip", "sizes_f45.hip", "sizes_f36.hip", "sizes_f32.hip"],
+}
 # normalised max-error bars per output-tile extent m (the same as the GPU tests')
 TOL = {2: 1e-5, 3: 1e-4, 4: 1e-4, 5: 1e-4}
 
 
-def kernel_hash():
+def family_of(desc):
+    if desc.get("fused"):
+        return "f43fused"
+    tile = desc.get("tile", [])
+    if desc["N"] == 3 and len(set(tile[:3])) > 1:
+        return "ax"
+    if desc["m"] == 2:
+        return "m2"
+    if (desc["N"], desc["m"], desc["r"]) == (2, 4, 3):
+        return "f42"
+    if (desc["N"], desc["m"], desc["r"]) == (3, 4, 3):
+        return "f43"
+    return "a8"
+
+
+def kernel_hash(desc=None):
+    """sha256[:16] of a kernel family's sources and the plan's launch geometry
+    (block sizes, padded sizes, tail split), or of every source without a plan."""
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
+    files = FAMILY_SOURCES[family_of(desc)] if desc is not None else sorted(
+        {f for v in FAMILY_SOURCES.values() for f in v})
+    for rel in files:
+        with open(os.path.join(ROOT, CSRC, rel), "rb") as f:
             h.update(f.read())
+    if desc is not None:
+        geo = {k: desc[k] for k in ("T_pad", "C_pad", "K_pad", "block_tiles", "block_kernels", "gemm_parts",
+                                    "gemm_tail_blocks", "fused", "tile")}
+        h.update(json.dumps(geo, sort_keys=True).encode())
     return h.hexdigest()[:16]
 
 
@@ -543,9 +573,11 @@ def main():
         achieved = gemm_bytes / (gemm_ms * 1e-3) / 1e9
     else:
         achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
-    prof_key = f"{args.config}-adjoint" if args.adjoint else args.config
-    counters = read_counters(kernel_hash(), prof_key)
-    traffic = read_traffic(kernel_hash(), prof_key)
+    prof_key = (f"{args.config}" + ("-adjoint" if args.adjoint else "") + ("-no-fuse" if args.no_fuse else "")
+                + (f"-tile{args.tile}" if args.tile else ""))
+    khash = kernel_hash(d)
+    counters = read_counters(khash, prof_key)
+    traffic = read_traffic(khash, prof_key)
     try:
         mfma_counted = float(counters["mfma_flops_per_launch"])
     except (KeyError, ValueError):
@@ -653,7 +685,7 @@ def main():
                       {"filter_transform": filt_ms, "input_transform": inp_ms, "gemm_inverse": gemm_ms}),
         "forward_U_cached_tflops": flops / (fwd_ms * 1e-3) / 1e12,
         "max_normalised_error_sampled": check,
-        "kernel_sources_sha256_16": kernel_hash(),
+        "kernel_sources_sha256_16": khash,
     }
     out.update(extra)
     if not args.no_cpu_baseline and not args.adjoint:

@@ -106,14 +106,19 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   const int n_t = split_tile<N>(tlive ? t : 0, a.tiles, ti_t);
 
   auto produce = [&](int chunk) {
-    const int c = chunk * CH + pch;
+    // an opaque zero, new every chunk: the window addresses below depend on
+    // it, so the compiler recomputes them per chunk instead of keeping them
+    // live across the loop (where they would spill)
+    int z;
+    asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+    const int c = chunk * CH + pch + z;
     const bool clive = c < a.C;
     const float* xc = x + int64_t(clive ? c : 0) * a.xstride_c;
     float d[PL];   // the plane's rows, each transformed along the last axis
     if (a.rowfast) {
       const float* xn = xc + int64_t(n_b) * a.C * a.xstride_c;
       const int tW = ti_b[2] + tl;
-      const int q0 = ti_b[0] * MM - a.pad[0] + i0;
+      const int q0 = ti_b[0] * MM - a.pad[0] + i0 + z;
       const bool valid0 = clive && (unsigned)q0 < (unsigned)a.X[0];
       const int wo = min(MM * tW, XL - 4);
       const bool own_in = MM * tW < XL;
@@ -122,24 +127,32 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
       const bool left = tl < BLK / 2;
       const int wh = left ? max(wl, 0) : min(wr, XL - 2);
       const bool h_in = left ? wl >= 0 : wr < XL;
+      // the twelve loads of the six rows are issued before any is used
+      float4 o[A];
+      float2 h[A];
+      bool rv[A];
+#pragma unroll
+      for (int i1 = 0; i1 < A; ++i1) {
+        const int q1 = ti_b[1] * MM - a.pad[1] + i1;
+        rv[i1] = valid0 && (unsigned)q1 < (unsigned)a.X[1];
+        // 32-bit offsets inside one channel's volume (the planner bounds it below 2^31)
+        const int roff = (min(max(q0, 0), a.X[0] - 1) * a.X[1] + min(max(q1, 0), a.X[1] - 1)) * XL;
+        o[i1] = *reinterpret_cast<const float4*>(xn + roff + wo);
+        h[i1] = *reinterpret_cast<const float2*>(xn + roff + wh);
+      }
       auto rows = [&](auto PP) {
         constexpr int P = decltype(PP)::value;
 #pragma unroll
         for (int i1 = 0; i1 < A; ++i1) {
-          const int q1 = ti_b[1] * MM - a.pad[1] + i1;
-          const bool valid = valid0 && (unsigned)q1 < (unsigned)a.X[1];
-          const float* xr = xn + (int64_t(min(max(q0, 0), a.X[0] - 1)) * a.X[1] + min(max(q1, 0), a.X[1] - 1)) * XL;
-          float4 o = *reinterpret_cast<const float4*>(xr + wo);
-          float2 h = *reinterpret_cast<const float2*>(xr + wh);
           // the 16 lanes of a DPP row share channel, plane and row, hence validity
-          if (!(own_in && valid)) o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-          if (!(h_in && valid)) h = make_float2(0.0f, 0.0f);
+          const float4 ov = (own_in && rv[i1]) ? o[i1] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+          const float2 hv = (h_in && rv[i1]) ? h[i1] : make_float2(0.0f, 0.0f);
           float e[8];   // offsets -2 .. 5 from 4 * tW
-          e[0] = dpp_from_prev(h.x, o.z);
-          e[1] = dpp_from_prev(h.y, o.w);
-          e[2] = o.x; e[3] = o.y; e[4] = o.z; e[5] = o.w;
-          e[6] = dpp_from_next(h.x, o.x);
-          e[7] = dpp_from_next(h.y, o.y);
+          e[0] = dpp_from_prev(hv.x, ov.z);
+          e[1] = dpp_from_prev(hv.y, ov.w);
+          e[2] = ov.x; e[3] = ov.y; e[4] = ov.z; e[5] = ov.w;
+          e[6] = dpp_from_next(hv.x, ov.x);
+          e[7] = dpp_from_next(hv.y, ov.y);
           float w6[A];
 #pragma unroll
           for (int i = 0; i < A; ++i) w6[i] = e[i + 2 - P];
@@ -156,19 +169,19 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
       const float* xn = xc + int64_t(n_t) * a.C * a.xstride_c;
       int o[3];
 #pragma unroll
-      for (int ax = 0; ax < N; ++ax) o[ax] = ti_t[ax] * MM - a.pad[ax];
+      for (int ax = 0; ax < N; ++ax) o[ax] = ti_t[ax] * MM - a.pad[ax] + z;
       const int oL = o[N - 1];
       const bool wide = XL >= A;
       const int sL = wide ? min(max(oL, 0), XL - A) : 0;
       const int delta = oL - sL;
       const int q0 = o[0] + i0;
       const bool valid0 = live && (unsigned)q0 < (unsigned)a.X[0];
-      const int64_t off0 = min(max(q0, 0), a.X[0] - 1);
+      const int off0 = min(max(q0, 0), a.X[0] - 1);
 #pragma unroll
       for (int i1 = 0; i1 < A; ++i1) {
         const int q1 = o[1] + i1;
         const bool valid = valid0 && (unsigned)q1 < (unsigned)a.X[1];
-        const float* xr = xn + (off0 * a.X[1] + min(max(q1, 0), a.X[1] - 1)) * XL;
+        const float* xr = xn + (off0 * a.X[1] + min(max(q1, 0), a.X[1] - 1)) * XL;   // 32-bit, as above
         float w6[A];
         if (wide) {
           float ld[A];
@@ -212,16 +225,18 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   for (int e = 0; e < XPW; ++e) acc[e] = typename S::acc_t{};
   const float2* P2 = reinterpret_cast<const float2*>(sm);
   // U[xi][c/4][k][c%4]: lane (kr, col) reads channels 2kr, 2kr + 1 of the chunk
-  const float* ubase = U + int64_t(wave) * XPW * a.uplane + (int64_t(kr >> 1) * a.K_pad + kb * BLK + col) * 4 +
+  // 32-bit offsets into U (the planner bounds U below 2^31 floats)
+  const int uplane = int(a.uplane);
+  const float* ubase = U + wave * XPW * uplane + ((kr >> 1) * a.K_pad + kb * BLK + col) * 4 +
                        2 * (kr & 1);
 
   // the chunk's 18 U operands, loaded together before the chunk's barrier
   // so that their latency overlaps the other waves' producing
   float2 ur[XPW];
   auto load_u = [&](int chunk) {
-    const float* uc = ubase + int64_t(chunk) * 2 * a.K_pad * 4;
+    const float* uc = ubase + chunk * 8 * a.K_pad;
 #pragma unroll
-    for (int e = 0; e < XPW; ++e) ur[e] = *reinterpret_cast<const float2*>(uc + int64_t(e) * a.uplane);
+    for (int e = 0; e < XPW; ++e) ur[e] = *reinterpret_cast<const float2*>(uc + e * uplane);
   };
   auto consume = [&](auto X0) {
     constexpr int xr = decltype(X0)::value;

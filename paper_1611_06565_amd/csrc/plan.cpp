@@ -356,7 +356,9 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   // F(4^3) with few kernels: the input transform runs inside the product
   // (recomputed for each block of 16 kernels, so only while there are at
   // most 4 such blocks); same grid as k_gemm_inv
-  p.fused = !aniso && N == 3 && m == 4 && r == 3 && p.K_pad <= 64 && !(o.flags & WINO_NO_FUSE);
+  // (its offsets inside one channel's input volume and into U are 32-bit)
+  p.fused = !aniso && N == 3 && m == 4 && r == 3 && p.K_pad <= 64 && !(o.flags & WINO_NO_FUSE) &&
+            p.X[0] * p.X[1] * p.X[2] <= kMaxI32 && uf <= kMaxI32;
   if (p.fused && !grid_ok(int64_t(p.T_pad / p.blk) * (p.K_pad / 16), 768, &p.grid_fused)) return WINO_EINVAL;
 
   if (aniso) {
