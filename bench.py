@@ -274,7 +274,10 @@ def bench_stack(args):
     x, ws = draw_stack(C3D_STACK, seed=5 if args.seed is None else args.seed)
     x0 = torch.from_numpy(x).cuda()
     # per-layer tiles: "2" F(2^3), "4" F(4^3), "244" per-axis (2, 4, 4), ...
-    codes = args.stack_tiles.split(",") if args.stack_tiles else ["2"] * len(C3D_STACK.widths)
+    # default: F(4^3) while the output rows are at least 28 wide (conv1-4),
+    # F(2^3) on the small late layers, where F(4^3)'s partial tiles waste work
+    codes = (args.stack_tiles.split(",") if args.stack_tiles else
+             ["4" if min(spec.out_spatial[1:]) >= 28 else "2" for spec, _ in C3D_STACK.layers()])
     if len(codes) != len(C3D_STACK.widths):
         raise SystemExit("--stack-tiles needs one code per layer")
     layers = []
@@ -335,8 +338,8 @@ def bench_stack(args):
             "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
             "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
             "config": {"workload": "C3D-style stack: batch 4, 3x16x112x112, eight 3x3x3 pad-1 layers "
-                                   "(64, 128, 256, 256, 512 x4), ReLU, max-pools; F(2^3,3^3); one HIP graph "
-                                   "per step"}}), flush=True)
+                                   "(64, 128, 256, 256, 512 x4), ReLU, max-pools; tiles per layer " + ",".join(codes)
+                                   + "; one HIP graph per step"}}), flush=True)
         return
     nev = len(layers) + 1
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
@@ -439,7 +442,8 @@ def main():
     ap.add_argument("--no-check", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache repetitions")
     ap.add_argument("--stack-tiles", default=None, metavar="CODES",
-                    help="with --config 5: per-layer tiles, e.g. 2,2,244,244,244,244,2,2 (default all 2)")
+                    help="with --config 5: per-layer tiles, e.g. 2,2,244,244,244,244,2,2 (default F(4^3) on layers "
+                         "with output rows of 28 or more, F(2^3) after them: 4,4,4,4,2,2,2,2)")
     ap.add_argument("--tile", default=None, metavar="M0,M1,M2",
                     help="per-axis output tiles of the chosen 3-D layer, e.g. 2,4,4")
     ap.add_argument("--no-fuse", action="store_true",

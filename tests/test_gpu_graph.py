@@ -14,15 +14,20 @@ pytestmark = pytest.mark.gpu
 CASES = [
     # F(2^3) with the tail split (partial outputs + k_part_reduce), and without
     (LayerSpec("g_f2x3_parts", N=3, m=2, r=3, batch=2, C=96, K=130, X=(4, 10, 9), pad=1,
-               x_dist="normal", w_dist="he"), True),
+               x_dist="normal", w_dist="he"), {"split": True}),
     (LayerSpec("g_f2x3_nosplit", N=3, m=2, r=3, batch=2, C=24, K=40, X=(6, 13, 15), pad=1,
-               x_dist="normal", w_dist="he", relu=True), False),
+               x_dist="normal", w_dist="he", relu=True), {"split": False}),
     # F(4^2): tail blocks split into parts of 1 or 2 of its 18 passes
     (LayerSpec("g_f4x3_2d", N=2, m=4, r=3, batch=3, C=36, K=70, X=(17, 23), pad=1,
-               x_dist="normal", w_dist="he"), True),
-    # F(4^3): k_gemm_inv
-    (LayerSpec("g_f4x3_3d", N=3, m=4, r=3, batch=1, C=20, K=24, X=(13, 11, 17), pad=1,
-               x_dist="normal", w_dist="he"), True),
+               x_dist="normal", w_dist="he"), {"split": True}),
+    # F(4^3): k_fused43, and k_input_split + k_gemm_inv
+    (LayerSpec("g_f4x3_3d_fused", N=3, m=4, r=3, batch=1, C=20, K=24, X=(13, 11, 17), pad=1,
+               x_dist="normal", w_dist="he"), {"split": True, "fuse": True}),
+    (LayerSpec("g_f4x3_3d_two_stage", N=3, m=4, r=3, batch=1, C=20, K=24, X=(13, 11, 17), pad=1,
+               x_dist="normal", w_dist="he"), {"split": True, "fuse": False}),
+    # per-axis tiles F(2,3) x F(4,3)^2
+    (LayerSpec("g_aniso_244", N=3, m=2, r=3, batch=2, C=12, K=20, X=(10, 15, 13), pad=1,
+               x_dist="normal", w_dist="he", tile=(2, 4, 4)), {"split": True}),
 ]
 
 
@@ -36,14 +41,16 @@ def _replay_check(torch, graph, out, eager, scratch):
         assert torch.equal(out, eager), f"replay {rep} differs"
 
 
-@pytest.mark.parametrize("spec,split", CASES, ids=lambda c: getattr(c, "name", str(c)))
-def test_forward_graph_replay(spec, split):
+@pytest.mark.parametrize("spec,kw", CASES, ids=[c[0].name for c in CASES])
+def test_forward_graph_replay(spec, kw):
     torch = require_gpu()
     from paper_1611_06565_amd.wino import Plan
-    log(f"[gpu] graph forward {spec.name} split={split}")
+    log(f"[gpu] graph forward {spec.name} {kw}")
     x, w = draw_layer(spec, seed=21)
     plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X), pad=spec.pad,
-                relu=spec.relu, split=split)
+                relu=spec.relu, tile=spec.tile, **kw)
+    if "fuse" in kw:
+        assert plan.desc["fused"] == (1 if kw["fuse"] else 0)
     xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
     U = plan.transform_filter(wd)
     ws = plan.new_workspace()
