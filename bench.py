@@ -557,8 +557,9 @@ def main():
         torch.cuda.synchronize()
         cst = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
                         for e in cev]).mean(axis=0)
-        cold = {"filter_transform": float(cst[0]), "input_transform": float(cst[1]),
-                "gemm_inverse": float(cst[2])}
+        cold = ({"filter_transform": float(cst[0]), "fused_forward": float(cst[2])} if fused else
+                {"filter_transform": float(cst[0]), "input_transform": float(cst[1]),
+                 "gemm_inverse": float(cst[2])})
         del flush, sink
 
     flops = direct_flops(spec)
@@ -612,7 +613,7 @@ def main():
                                         "peak_GBps": PEAK_HBM,
                                         "frac": in_bytes / (inp_ms * 1e-3) / 1e9 / PEAK_HBM}
     if cold is not None:
-        c_in, c_g = cold["input_transform"], cold["gemm_inverse"]
+        c_in, c_g = (0.0, cold["fused_forward"]) if fused else (cold["input_transform"], cold["gemm_inverse"])
         extra["cold_cache"] = {
             "stages_ms": cold,
             "forward_tflops": flops / ((c_in + c_g) * 1e-3) / 1e12,
