@@ -52,20 +52,23 @@ struct FusedArgs {
   int32_t T, nkb, nblocks;
   int32_t X[3], tiles[3], pad[3], Y[3];
   int32_t rowfast;     // every 16-tile block is 16 tiles of one input row (rows of a multiple of 4, pad <= 2)
+  int32_t vec_store;   // output rows a multiple of 4 long and y 16-byte aligned: rows of 4 stored as float4
   int32_t act;         // activation f of eq. (2): 0 none, 1 ReLU, 2 leaky ReLU
   float slope;
   const float* bias;   // [K] or null
 };
 
 struct Fused43Geom {
-  static constexpr int A = 6, NXI = 216, BLK = 16, NW = 12, NT = NW * 64, LOC = 1;
+  static constexpr int A = 6, MM = 4, NXI = 216, BLK = 16, NW = 12, NT = NW * 64;
   static constexpr int CH = 8;                       // channels per chunk
   static constexpr int PL = A * A;                   // values of a plane after two axes
-  static constexpr int XPW = NXI / NW;               // elements per wave (18: three alpha-rows)
+  static constexpr int XPW = NXI / NW;               // elements per wave (18)
+  static constexpr int NPOS = PL / NW;               // plane positions per wave (3, all six xi0 each)
   static constexpr int P_FLOATS = A * PL * CH * BLK; // 27648: the chunk's planes
-  using Epi = GemmGeom<3, 4, 3, BLK, NW, LOC>;
-  static constexpr int LDS_FLOATS = Epi::LDS_FLOATS > P_FLOATS ? Epi::LDS_FLOATS : P_FLOATS;
-  static_assert(XPW == 18 && NW * 4 == CH * A, "a wave is 4 (channel, plane) rows of 16 tiles");
+  static constexpr int EPL = BLK * BLK + 8;          // epilogue plane stride (bank spread)
+  static constexpr int E_FLOATS = PL * MM * EPL;     // 38016: (position, o0) planes
+  static constexpr int LDS_FLOATS = E_FLOATS > P_FLOATS ? E_FLOATS : P_FLOATS;
+  static_assert(XPW == NPOS * A && NW * 4 == CH * A, "a wave is 4 (channel, plane) rows of 16 tiles");
 };
 
 // P layout in LDS: P[i0][j][pair][tile][2] (j < 36 the plane value, pair =
@@ -216,66 +219,61 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
     }
   };
 
-  // ---- consumer role: MFMA lane (kr, col); wave owns elements wave * 18 ..
+  // ---- consumer role: MFMA lane (kr, col).  Wave w owns the plane
+  // positions j = 3w .. 3w + 2 (j = 6 xi1 + xi2) for all six first-axis
+  // indices xi0: it reads each P_i0[j] once and forms the six elements
+  // V_(xi0, j) = sum_i0 B^T[xi0][i0] P_i0[j] from them (eq. 4 along the
+  // first axis, the shared sub-expressions of B^T's rows computed once).
+  // acc[p * 6 + xi0] is the 16 x 16 product block of element (xi0, 3w + p).
+  const int jw = __builtin_amdgcn_readfirstlane(wave) * G::NPOS;   // wave-uniform
   const int col = lane & 15, kr = lane >> 4;
-  const int x0 = wave >> 1;                      // first-axis index of the wave's elements
-  const int j0 = (wave & 1) * XPW;               // first plane value of the wave: 18 * (wave % 2)
   typename S::acc_t acc[XPW];
 #pragma unroll
   for (int e = 0; e < XPW; ++e) acc[e] = typename S::acc_t{};
-  const float2* P2 = reinterpret_cast<const float2*>(sm);
-  // U[xi][c/4][k][c%4]: lane (kr, col) reads channels 2kr, 2kr + 1 of the chunk
-  // 32-bit offsets into U (the planner bounds U below 2^31 floats)
+  // U[xi][c/4][k][c%4]: lane (kr, col) reads channels 2kr, 2kr + 1 of the
+  // chunk; 32-bit offsets (the planner bounds U below 2^31 floats).  The
+  // chunk's 18 operands are loaded together after its producing.
   const int uplane = int(a.uplane);
-  const float* ubase = U + wave * XPW * uplane + ((kr >> 1) * a.K_pad + kb * BLK + col) * 4 +
-                       2 * (kr & 1);
-
-  // the chunk's 18 U operands, loaded together before the chunk's barrier
-  // so that their latency overlaps the other waves' producing
+  // per-lane base at element (0, jw); the element offsets are wave-uniform
+  const float* ubase = U + jw * uplane + ((kr >> 1) * a.K_pad + kb * BLK + col) * 4 + 2 * (kr & 1);
   float2 ur[XPW];
   auto load_u = [&](int chunk) {
     const float* uc = ubase + chunk * 8 * a.K_pad;
 #pragma unroll
-    for (int e = 0; e < XPW; ++e) ur[e] = *reinterpret_cast<const float2*>(uc + e * uplane);
+    for (int p = 0; p < G::NPOS; ++p)
+#pragma unroll
+      for (int x0 = 0; x0 < A; ++x0)
+        ur[p * A + x0] = *reinterpret_cast<const float2*>(uc + (x0 * PL + p) * uplane);
   };
-  auto consume = [&](auto X0) {
-    constexpr int xr = decltype(X0)::value;
-    // the P values an element needs: one 8-byte read per first-axis plane
-    // whose B^T coefficient is not zero (a compile-time test for the default
-    // points); element e + 1's reads are issued before element e's products
-    auto fetch = [&](float2* pv, int e) {
+  const float2* P2 = reinterpret_cast<const float2*>(sm);
+  auto fetch = [&](float2* pv, int p) {
 #pragma unroll
-      for (int i = 0; i < A; ++i)
-        if (BT(xr, i) != 0.0f) pv[i] = P2[((i * PL + j0 + e) * 4 + kr) * 16 + col];
-    };
-    auto product = [&](const float2* pv, int e) {
-      float2 v = make_float2(0.0f, 0.0f);
-      bool first = true;
+    for (int i = 0; i < A; ++i) pv[i] = P2[((i * PL + jw + p) * 4 + kr) * 16 + col];
+  };
+  auto product = [&](const float2* pv, int p) {
+    float vx[A], vy[A], ox[A], oy[A];
 #pragma unroll
-      for (int i = 0; i < A; ++i) {
-        const float cf = BT(xr, i);
-        if (cf == 0.0f) continue;
-        if (first) {
-          v.x = cf * pv[i].x; v.y = cf * pv[i].y;
-          first = false;
-        } else {
-          v.x = __builtin_fmaf(cf, pv[i].x, v.x);
-          v.y = __builtin_fmaf(cf, pv[i].y, v.y);
-        }
-      }
-      acc[e] = S::mma(v.x, ur[e].x, acc[e]);
-      acc[e] = S::mma(v.y, ur[e].y, acc[e]);
-    };
+    for (int i = 0; i < A; ++i) {
+      vx[i] = pv[i].x;
+      vy[i] = pv[i].y;
+    }
+    apply_vec<A, A>(BT, vx, 1, ox, 1);
+    apply_vec<A, A>(BT, vy, 1, oy, 1);
+#pragma unroll
+    for (int x0 = 0; x0 < A; ++x0) acc[p * A + x0] = S::mma(ox[x0], ur[p * A + x0].x, acc[p * A + x0]);
+#pragma unroll
+    for (int x0 = 0; x0 < A; ++x0) acc[p * A + x0] = S::mma(oy[x0], ur[p * A + x0].y, acc[p * A + x0]);
+  };
+  auto consume = [&]() {
     float2 pa[A], pb[A];
     fetch(pa, 0);
-#pragma unroll
-    for (int e = 0; e < XPW; e += 2) {
-      fetch(pb, e + 1);
-      product(pa, e);
-      if (e + 2 < XPW) fetch(pa, e + 2);
-      product(pb, e + 1);
-    }
+    fetch(pb, 1);
+    product(pa, 0);
+    fetch(pa, 2);
+    product(pb, 1);
+    product(pa, 2);
   };
+  static_assert(G::NPOS == 3, "three plane positions per wave");
 
   // chunks past the last real channel hold only zero padding (x and U are
   // zero there): they are skipped
@@ -285,25 +283,74 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
     produce(chunk);
     load_u(chunk);
     __syncthreads();
-    switch (x0) {
-      case 0: consume(std::integral_constant<int, 0>{}); break;
-      case 1: consume(std::integral_constant<int, 1>{}); break;
-      case 2: consume(std::integral_constant<int, 2>{}); break;
-      case 3: consume(std::integral_constant<int, 3>{}); break;
-      case 4: consume(std::integral_constant<int, 4>{}); break;
-      default: consume(std::integral_constant<int, 5>{}); break;
+    consume();
+  }
+
+  // ---- epilogue (eq. 4 inverted): A^T along the first axis in registers,
+  // then along the last two axes, bias, activation, crop and store.
+  // Part 1: wave w writes, for each of its positions j and output o0, the
+  // 16 x 16 (tile, kernel) block to LDS plane (j, o0) at [k][t ^ k].
+  const MatRef<Which::AT, CONST, MM, R> AT{&fm};
+  __shared__ float bsm[BLK];
+  if (a.bias != nullptr && int(threadIdx.x) < BLK) {
+    const int kg = kb * BLK + int(threadIdx.x);
+    bsm[threadIdx.x] = kg < a.K ? a.bias[kg] : 0.0f;
+  }
+  __syncthreads();                              // the planes' LDS is reused below
+#pragma unroll
+  for (int r = 0; r < S::NACC; ++r) {
+    const int tr = S::acc_row(lane, r);
+#pragma unroll
+    for (int p = 0; p < G::NPOS; ++p) {
+      float sv[A], o[MM];
+#pragma unroll
+      for (int x0 = 0; x0 < A; ++x0) sv[x0] = acc[p * A + x0][r];
+      apply_vec<A, MM>(AT, sv, 1, o, 1);
+      float* dst = sm + (jw + p) * MM * G::EPL + col * BLK + (tr ^ col);
+#pragma unroll
+      for (int o0 = 0; o0 < MM; ++o0) dst[o0 * G::EPL] = o[o0];
     }
   }
-  __syncthreads();                              // the planes' LDS is reused by the epilogue
+  __syncthreads();
 
-  EpiArgs e{y, a.K, a.ystride_k, {a.Y[0], a.Y[1], a.Y[2]}, a.act, a.slope, a.bias};
-  auto tile_of = [&](int tl2, int* ti) -> int {
+  // Part 2: item (o0, kernel, tile), tiles fastest, reads the 36 values of
+  // its plane, applies A^T along the last two axes and stores 4 x 4 outputs,
+  // each row of 4 as one 16-byte store when every row of the output is a
+  // whole number of aligned tiles (a.vec_store)
+  constexpr int ITEMS = MM * BLK * BLK;
+  for (int i = int(threadIdx.x); i < ITEMS; i += G::NT) {
+    const int tl2 = i % BLK, kl = (i / BLK) % BLK, o0 = i / (BLK * BLK);
     const int t2 = tb * BLK + tl2;
-    if (t2 >= a.T) return -1;
-    return split_tile<N>(t2, a.tiles, ti);
-  };
-  if (a.bias != nullptr) gemm_epilogue<N, MM, R, CONST, BLK, G::NW, G::LOC, true>(acc, sm, kb, e, fm, tile_of);
-  else gemm_epilogue<N, MM, R, CONST, BLK, G::NW, G::LOC, false>(acc, sm, kb, e, fm, tile_of);
+    const int kg = kb * BLK + kl;
+    if (t2 >= a.T || kg >= a.K) continue;
+    int ti[3] = {0, 0, 0};
+    const int n = split_tile<N>(t2, a.tiles, ti);
+    const int y0 = ti[0] * MM + o0;
+    if (y0 >= a.Y[0]) continue;
+    float v[PL], out[MM * MM];
+#pragma unroll
+    for (int j = 0; j < PL; ++j) v[j] = sm[(j * MM + o0) * G::EPL + kl * BLK + (tl2 ^ kl)];
+    transform_nd<2, A, MM>(v, out, AT);
+    const float bk = a.bias != nullptr ? bsm[kl] : 0.0f;
+#pragma unroll
+    for (int q2 = 0; q2 < MM * MM; ++q2) out[q2] = activate(out[q2] + bk, a.act, a.slope);
+    float* yk = y + (int64_t(n) * a.K + kg) * a.ystride_k + int64_t(y0) * a.Y[1] * a.Y[2];
+    const int y2 = ti[2] * MM;
+#pragma unroll
+    for (int o1 = 0; o1 < MM; ++o1) {
+      const int y1 = ti[1] * MM + o1;
+      if (y1 >= a.Y[1]) continue;
+      float* row = yk + int64_t(y1) * a.Y[2] + y2;
+      if (a.vec_store) {
+        const f32x4 v4 = {out[o1 * MM], out[o1 * MM + 1], out[o1 * MM + 2], out[o1 * MM + 3]};
+        __builtin_nontemporal_store(v4, reinterpret_cast<f32x4*>(row));
+      } else {
+#pragma unroll
+        for (int o2 = 0; o2 < MM; ++o2)
+          if (y2 + o2 < a.Y[2]) row[o2] = out[o1 * MM + o2];
+      }
+    }
+  }
 }
 
 }  // namespace wino

@@ -1,5 +1,7 @@
 // Kernel instances and launch of k_fused43: F(4^3, 3^3) with the input
 // transform inside the product.
+#include <cstdint>
+
 #include "fused43.hpp"
 #include "launch.hpp"
 
@@ -21,6 +23,9 @@ wino_status launch_fused43(const wino_plan_s& p, bool const_mats, const float* x
   // whole 16-tile blocks along input rows of a multiple of 4 values (x is
   // 16-byte aligned: the entry points check it)
   a.rowfast = (p.tiles[2] % Fused43Geom::BLK == 0 && p.X[2] % 4 == 0 && p.pad[2] <= 2) ? 1 : 0;
+  // every output row a whole number of 4-wide tiles, y 16-byte aligned:
+  // the epilogue stores rows of four as one 16-byte store
+  a.vec_store = (p.Y[2] % 4 == 0 && (reinterpret_cast<uintptr_t>(y) & 15) == 0) ? 1 : 0;
   a.act = act_kind(p);
   a.slope = p.slope;
   a.bias = bias;
