@@ -45,6 +45,11 @@ EXACT_CASES = [
     (2, 4, 5, None, 1, 2, 2, (11, 12), 0),
     (2, 3, 6, None, 1, 2, 1, (13, 10), 1),
     (2, 3, 2, None, 2, 2, 2, (7, 8), 1),
+    # Table 1's sizes in 3-D (alpha = 4 and 8): one or two ragged tiles per axis
+    (3, 3, 2, None, 1, 2, 2, (5, 4, 6), 1),
+    (3, 5, 4, None, 1, 1, 2, (8, 6, 9), 0),
+    (3, 4, 5, None, 1, 2, 1, (8, 9, 6), 1),
+    (3, 3, 6, None, 1, 1, 1, (9, 8, 7), 1),
 ]
 
 
