@@ -41,6 +41,7 @@ FAMILY_SOURCES = {
     "f43fused": _COMMON + ["fused43.hpp", "fused_f43.hip"],
     "ax": _COMMON + ["aniso.hpp", "sizes_ax.hip"],
     "a8": _COMMON + ["sizes_f54.hip", "sizes_f45.hip", "sizes_f36.hip", "sizes_f32.hip"],
+    "a8_3d": _COMMON + ["a8.hpp", "sizes_a8.hip"],
 }
 # normalised max-error bars per output-tile extent m (the same as the GPU tests')
 TOL = {2: 1e-5, 3: 1e-4, 4: 1e-4, 5: 1e-4}
@@ -58,6 +59,8 @@ def family_of(desc):
         return "f42"
     if (desc["N"], desc["m"], desc["r"]) == (3, 4, 3):
         return "f43"
+    if desc["N"] == 3 and desc["n_xi"] == 512:
+        return "a8_3d"
     return "a8"
 
 
@@ -446,6 +449,9 @@ def main():
                          "with output rows of 28 or more, F(2^3) after them: 4,4,4,4,2,2,2,2)")
     ap.add_argument("--tile", default=None, metavar="M0,M1,M2",
                     help="per-axis output tiles of the chosen 3-D layer, e.g. 2,4,4")
+    ap.add_argument("--size", default=None, metavar="M,R",
+                    help="another tile and kernel size on the chosen layer's shape, e.g. 5,4 for F(5^3,4^3) "
+                         "(pad (r - 1) // 2)")
     ap.add_argument("--no-fuse", action="store_true",
                     help="keep an F(4^3) forward in two stages (input transform to V, then the product)")
     ap.add_argument("--calib-copy", action="store_true",
@@ -481,6 +487,10 @@ def main():
     from workloads import CONFIGS, direct_flops, draw_layer
 
     spec = CONFIGS[args.config]
+    if args.size:
+        # another (m, r) on the same layer shape; pad (r - 1) // 2 per axis
+        m_, r_ = (int(v) for v in args.size.split(","))
+        spec = spec.with_(m=m_, r=r_, pad=(r_ - 1) // 2, name=f"{spec.name}_f{m_}x{r_}")
     seed = args.config if args.seed is None else args.seed
     x, w = draw_layer(spec, seed=seed)
     tile = tuple(int(v) for v in args.tile.split(",")) if args.tile else None
@@ -579,7 +589,7 @@ def main():
     else:
         achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
     prof_key = (f"{args.config}" + ("-adjoint" if args.adjoint else "") + ("-no-fuse" if args.no_fuse else "")
-                + (f"-tile{args.tile}" if args.tile else ""))
+                + (f"-tile{args.tile}" if args.tile else "") + (f"-size{args.size}" if args.size else ""))
     khash = kernel_hash(d)
     counters = read_counters(khash, prof_key)
     traffic = read_traffic(khash, prof_key)
@@ -644,13 +654,14 @@ def main():
         "config": {
             "workload": ("data gradient (adjoint plan: C and K swapped, pads r-1-pad) of " if args.adjoint
                          else "") + ("F(%s,3^%d) per-axis tiles " % ("x".join(str(v) for v in tile), spec.N)
-                                     if tile else "F(%d^%d,3^%d) " % (spec.m, spec.N, spec.N)) +
+                                     if tile else "F(%d^%d,%d^%d) " % (spec.m, spec.N, spec.r, spec.N)) +
                         "%d-D conv layer: batch %d, C=%d, K=%d, %s, %s, pad %d" % (
                 spec.N, spec.batch, spec.C, spec.K,
-                "x".join(str(v) for v in spec.X), "x".join(["3"] * spec.N), spec.pad),
+                "x".join(str(v) for v in spec.X), "x".join([str(spec.r)] * spec.N), spec.pad),
             "N": spec.N, "m": spec.m, "r": spec.r, "batch": spec.batch, "C": spec.C, "K": spec.K,
             "X": list(spec.X), "pad": spec.pad,
-            "points": "0,1,-1,inf" if spec.m == 2 else "0,1,-1,2,-2,inf", "seed": seed,
+            "points": ",".join(["0", "1", "-1", "2", "-2", "1/2", "-1/2"][:spec.m + spec.r - 2] + ["inf"]),
+            "seed": seed,
             "tile": list(tile) if tile else [spec.m] * spec.N,
             "tiles": d["T"], "direct_gflop_per_step": flops / 1e9,
         },
@@ -658,6 +669,8 @@ def main():
             "kernel": ("k_fused43 (input transform in LDS, batched fp32-MFMA GEMM, fused inverse transform; "
                        "V never in memory)" if fused else
                        "k_gemm_ax (batched fp32-MFMA GEMM, per-axis inverse transform)" if tile else
+                       "k_gemm_a8 (batched fp32-MFMA GEMM over each first-axis plane of the 512 elements, "
+                       "inverse transform accumulated plane by plane)" if spec.N == 3 and d["n_xi"] == 512 else
                        "k_gemm_acc + k_part_reduce (batched fp32-MFMA GEMM, inverse transform accumulated "
                        "per pass; the %d tail blocks in %d parts each, their partial outputs summed in order)"
                        % (d["gemm_tail_blocks"], d["gemm_parts"])

@@ -17,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libwino.so")
 SOURCES = ["plan.cpp", "wino.hip", "sizes_m2.hip", "sizes_f42.hip", "sizes_f43.hip", "fused_f43.hip", "sizes_f54.hip",
-           "sizes_f45.hip", "sizes_f36.hip", "sizes_f32.hip", "sizes_ax.hip"]
+           "sizes_f45.hip", "sizes_f36.hip", "sizes_f32.hip", "sizes_ax.hip", "sizes_a8.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CXX = os.environ.get("CXX", "g++")
 

@@ -51,10 +51,11 @@ struct Launch {
   static constexpr int CG = Blocking<N, MM, R>::CG;
   static constexpr int CGU = Blocking<N, MM, R>::CGU;
   // k_gemm_inv work-group shape: F(4^3): 12 waves x three alpha-rows (18
-  // elements); 2-D sizes: alpha waves x one alpha-row (alpha elements).  The last
+  // elements); F(3^3, 2^3): 8 waves x two alpha-rows (8 elements); 2-D sizes:
+  // alpha waves x one alpha-row (alpha elements).  The last
   // axis is reduced in registers, 16-byte operand loads, no register ring
   // (the other waves of the SIMD hide the load latency).
-  static constexpr int NW = (N == 3 && A == 6) ? 12 : ipow(A, N - 1);
+  static constexpr int NW = (N == 3 && A == 6) ? 12 : (N == 3 && A == 4) ? 8 : ipow(A, N - 1);
   static constexpr int LOC = 1;
   static constexpr int VEC = Blocking<N, MM, R>::VEC;
   static constexpr int DEPTH = 1;
@@ -218,10 +219,12 @@ constexpr SizeOps make_ops() {
 // instances in sizes_ax.hip.
 const SizeOps* size_ops_ax(int m0, int m1);
 
-// The tables, one per compiled size (defined in the sizes_*.hip units);
+// 3-D sizes with alpha = 8 (a8.hpp): F(5^3, 4^3), F(4^3, 5^3), F(3^3, 6^3);
+// instances in sizes_a8.hip.
+const SizeOps* size_ops_a8(int m, int r, bool const_mats);
+
+// The tables, one per size of WINO_SIZES (defined in the sizes_*.hip units);
 // const_mats selects the instances with the default points compiled in.
-#define WINO_SIZES(X) \
-  X(2, 2, 3) X(3, 2, 3) X(2, 4, 3) X(3, 4, 3) X(2, 5, 4) X(2, 4, 5) X(2, 3, 6) X(2, 3, 2)
 #define WINO_DECLARE_OPS(N_, M_, R_) const SizeOps* size_ops_##N_##_##M_##_##R_(bool const_mats);
 WINO_SIZES(WINO_DECLARE_OPS)
 #undef WINO_DECLARE_OPS

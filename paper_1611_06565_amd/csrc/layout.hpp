@@ -7,6 +7,13 @@
 
 namespace wino {
 
+// The (N, m, r) compiled on the layouts below (KIND 0-2): F(2,3) and F(4,3)
+// in 2-D and 3-D, F(3,2) in 2-D and 3-D, and in 2-D the alpha = 8 sizes of
+// Table 1, F(5,4), F(4,5), F(3,6).  The 3-D alpha = 8 sizes (KIND 4) and the
+// per-axis tiles (KIND 3) have their own traits below.
+#define WINO_SIZES(X) \
+  X(2, 2, 3) X(3, 2, 3) X(2, 4, 3) X(3, 4, 3) X(2, 5, 4) X(2, 4, 5) X(2, 3, 6) X(2, 3, 2) X(3, 3, 2)
+
 // GEMM kind, block (tiles and kernels per work-group), operand load width
 // and channel group per (N, m, r).
 //   KIND 0 (m = 2) and 1 (F(4^2)): pass-accumulating GEMMs (gemm_acc.hpp,
@@ -62,6 +69,20 @@ constexpr SizeTraits size_traits_ax() {
   t.A = 0;
   t.NXI = (M0 + R - 1) * (M1 + R - 1) * (M1 + R - 1);
   t.KIND = 3;
+  t.BLK = 16; t.KBLK = 16; t.CG = 4; t.CGU = 4; t.CPAD = 16;
+  t.TB = 16; t.KB = 16;
+  return t;
+}
+
+// 3-D sizes with alpha = 8 (F(5^3, 4^3), F(4^3, 5^3), F(3^3, 6^3)): k_input_a8
+// and k_gemm_a8 on the F(4^3) layouts (16-tile V blocks of 4-channel groups,
+// 16-kernel blocks, channels padded to 16).
+template <int MM, int R>
+constexpr SizeTraits size_traits_a8() {
+  SizeTraits t{};
+  t.A = MM + R - 1;
+  t.NXI = t.A * t.A * t.A;
+  t.KIND = 4;
   t.BLK = 16; t.KBLK = 16; t.CG = 4; t.CGU = 4; t.CPAD = 16;
   t.TB = 16; t.KB = 16;
   return t;

@@ -72,11 +72,6 @@ bool rationalize(double v, Rat* out) {
   return false;
 }
 
-// The (N, m, r) with compiled kernels: F(2,3) and F(4,3) in 2-D and 3-D;
-// in 2-D also the other sizes of Table 1, F(3,2) (alpha = 4) and F(5,4),
-// F(4,5), F(3,6) (alpha = 8).
-#define WINO_SIZES(X) \
-  X(2, 2, 3) X(3, 2, 3) X(2, 4, 3) X(3, 4, 3) X(2, 5, 4) X(2, 4, 5) X(2, 3, 6) X(2, 3, 2)
 
 bool traits_of(int N, int m, int r, SizeTraits* t) {
 #define WINO_TRAITS(N_, M_, R_)                    \
@@ -86,6 +81,9 @@ bool traits_of(int N, int m, int r, SizeTraits* t) {
   }
   WINO_SIZES(WINO_TRAITS)
 #undef WINO_TRAITS
+  if (N == 3 && m == 5 && r == 4) { *t = size_traits_a8<5, 4>(); return true; }
+  if (N == 3 && m == 4 && r == 5) { *t = size_traits_a8<4, 5>(); return true; }
+  if (N == 3 && m == 3 && r == 6) { *t = size_traits_a8<3, 6>(); return true; }
   return false;
 }
 
@@ -159,6 +157,7 @@ bool acc_geometry(wino_plan_s& p, const SizeTraits& t, bool split, int cus) {
 void wgrad_geometry(wino_plan_s& p, const SizeTraits& t, const Rat* pts, const RatMats& R) {
   p.wgrad_ok = false;
   if (!((t.BLK == 64 || t.BLK == 16) && t.CG == 4)) return;
+  if (t.KIND == 4) return;   // the 3-D alpha = 8 sizes have no weight gradient
   const RatMats Rw = synthesize(p.r, p.m, pts);
   bool same = Rw.ok;
   for (int i = 0; same && i < p.alpha; ++i)
@@ -327,8 +326,8 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   if (!mul3_ok(int64_t(p.nxi), cpad, tpad, &vf) || !round_up(vf, 64, &p.v_floats) || p.v_floats > kMaxFloats)
     return WINO_EINVAL;
 
-  // launch grids
-  if (!grid_ok(cdiv(cpad * kpad, 64), 64, &p.grid_filter)) return WINO_EINVAL;
+  // launch grids (k_filter_a8: one thread per (channel, kernel, first-axis plane))
+  if (!grid_ok(cdiv(cpad * kpad * (t.KIND == 4 ? t.A : 1), 64), 64, &p.grid_filter)) return WINO_EINVAL;
   const int64_t groups = cpad / p.cg;
   int64_t ig = 0;
   if (aniso) {
@@ -346,11 +345,13 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   if (t.KIND == 0 || t.KIND == 1) {
     if (!acc_geometry(p, t, !(o.flags & WINO_NO_SPLIT), device_cu_count())) return WINO_EINVAL;
   } else {
-    // k_gemm_inv, k_gemm_ax: one (tile block, kernel block) per work-group, up to 12 waves
+    // k_gemm_inv, k_gemm_ax, k_gemm_a8: one (tile block, kernel block) per
+    // work-group, up to 12 waves (16 for k_gemm_a8)
     p.nparts = 1;
     p.grid_reduce = 0;
     int64_t gg = 0;
-    if (!mul_ok(tpad / p.blk, kpad / t.KB, &gg) || !grid_ok(gg, 768, &p.grid_gemm)) return WINO_EINVAL;
+    if (!mul_ok(tpad / p.blk, kpad / t.KB, &gg) || !grid_ok(gg, t.KIND == 4 ? 1024 : 768, &p.grid_gemm))
+      return WINO_EINVAL;
   }
   if (p.v_floats + p.part_floats > kMaxFloats) return WINO_EINVAL;
   // F(4^3) with few kernels: the input transform runs inside the product

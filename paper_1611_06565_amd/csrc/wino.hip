@@ -69,6 +69,7 @@ const SizeOps* ops_of(const wino_plan_s& p) {
   if (p.N == N_ && p.m == M_ && p.r == R_) return size_ops_##N_##_##M_##_##R_(p.const_mats);
   WINO_SIZES(WINO_PICK)
 #undef WINO_PICK
+  if (p.kind == 4) return size_ops_a8(p.m, p.r, p.const_mats);
   return nullptr;
 }
 

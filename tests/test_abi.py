@@ -63,6 +63,10 @@ def test_plan_validation(L):
     assert _plan_status(L, 4, 2, 3, 4, 4, [1, 8, 8, 8, 8]) == -1      # N out of range
     assert _plan_status(L, 3, 3, 3, 4, 4, [1, 8, 8, 8]) == -2         # no kernel for m = 3
     assert _plan_status(L, 3, 2, 5, 4, 4, [1, 8, 8, 8]) == -2         # r = 5
+    # Table 1's sizes in 3-D
+    for m, r in ((3, 2), (5, 4), (4, 5), (3, 6)):
+        assert _plan_status(L, 3, m, r, 4, 4, [1, 9, 9, 9]) == 0, (m, r)
+    assert _plan_status(L, 3, 6, 3, 4, 4, [1, 9, 9, 9]) == -2         # alpha = 8, no kernel for m = 6
     assert _plan_status(L, 3, 2, 3, 0, 4, [1, 8, 8, 8]) == -1         # C = 0
     assert _plan_status(L, 3, 2, 3, 4, 0, [1, 8, 8, 8]) == -1         # K = 0
     assert _plan_status(L, 3, 2, 3, 4, 4, [0, 8, 8, 8]) == -1         # batch 0
@@ -249,9 +253,14 @@ def test_weight_gradient_host_side():
     assert p.weight_gradient_workspace_bytes > v + dbytes
     assert wino.Plan(2, 4, 3, 3, 5, [2, 9, 10], pad=1).weight_gradient_workspace_bytes > 0
     assert wino.Plan(2, 2, 3, 3, 5, [2, 9, 10], pad=4).weight_gradient_workspace_bytes > 0
-    for args in [(3, 4, 3), (2, 5, 4), (2, 3, 2), (2, 4, 5), (2, 3, 6)]:
+    for args in [(3, 4, 3), (2, 5, 4), (2, 3, 2), (2, 4, 5), (2, 3, 6), (3, 3, 2)]:
         q = wino.Plan(*args, 3, 5, [1] + [12] * args[0], pad=1)
         assert q.weight_gradient_workspace_bytes > 0, args
+    # the 3-D alpha = 8 sizes have no weight gradient
+    for args in [(3, 5, 4), (3, 4, 5), (3, 3, 6)]:
+        q = wino.Plan(*args, 3, 5, [1] + [12] * args[0], pad=1)
+        assert q.weight_gradient_workspace_bytes == 0, args
+        assert q.desc["n_xi"] == 512 and q.desc["block_tiles"] == 16 and q.desc["channel_group"] == 4
     L = wino.lib()
     assert L.wino_weight_gradient_workspace_bytes(None) == 0
     assert L.wino_weight_gradient(None, None, None, None, None, 0, None) == -1

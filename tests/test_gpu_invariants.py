@@ -45,6 +45,11 @@ PATHS = [
                x_dist="normal", w_dist="he", tile=(2, 4, 4)), {}),
     (LayerSpec("inv_f5x4_2d", N=2, m=5, r=4, batch=2, C=8, K=12, X=(27, 24), pad=0,
                x_dist="normal", w_dist="he"), {}),
+    # Table 1's sizes in 3-D: k_gemm_inv with 8 waves (F(3^3, 2^3)) and k_gemm_a8
+    (LayerSpec("inv_f3x2_3d", N=3, m=3, r=2, batch=2, C=10, K=20, X=(10, 9, 11), pad=0,
+               x_dist="normal", w_dist="he"), {}),
+    (LayerSpec("inv_f5x4_3d", N=3, m=5, r=4, batch=2, C=6, K=20, X=(14, 12, 13), pad=0,
+               x_dist="normal", w_dist="he"), {}),
 ]
 IDS = [p[0].name for p in PATHS]
 

@@ -1,0 +1,128 @@
+"""GPU parity of Table 1's sizes in 3-D (§4.2): F(3^3, 2^3) (alpha = 4, on
+k_input and k_gemm_inv) and the alpha = 8 sizes F(5^3, 4^3), F(4^3, 5^3) and
+F(3^3, 6^3) (k_filter_a8, k_input_a8, k_gemm_a8), against the fp64 direct
+correlation of eq. (2) on every output.  Bar: the m = 4 tolerance 1e-4 for
+every size with m >= 3, as for the 2-D sizes of Table 1.  These sizes have no
+weight gradient; the data gradient runs on the same kernels."""
+import numpy as np
+import pytest
+
+from gpu_util import check_full, log, require_gpu, run_layer
+from oracle.adjoint import direct_adjoint
+from oracle.metric import normalised_error
+from oracle.winograd import transform_filter as o_filter
+from oracle.winograd import transform_input as o_input
+from workloads import LayerSpec, draw_layer
+
+pytestmark = pytest.mark.gpu
+
+LAYERS = [
+    LayerSpec("f3x2_3d_ragged", N=3, m=3, r=2, batch=2, C=10, K=20, X=(7, 9, 8), pad=1,
+              x_dist="normal", w_dist="he"),
+    LayerSpec("f3x2_3d_valid", N=3, m=3, r=2, batch=1, C=17, K=33, X=(10, 6, 12), pad=0,
+              x_dist="relu_normal", w_dist="he"),
+    LayerSpec("f5x4_3d_ragged", N=3, m=5, r=4, batch=2, C=6, K=20, X=(9, 12, 11), pad=1,
+              x_dist="normal", w_dist="he"),
+    LayerSpec("f5x4_3d_c20", N=3, m=5, r=4, batch=1, C=20, K=17, X=(13, 8, 14), pad=0,
+              x_dist="uniform", w_dist="he"),
+    LayerSpec("f4x5_3d_ragged", N=3, m=4, r=5, batch=1, C=5, K=9, X=(10, 11, 12), pad=2,
+              x_dist="normal", w_dist="he"),
+    LayerSpec("f4x5_3d_c33", N=3, m=4, r=5, batch=2, C=33, K=16, X=(8, 9, 7), pad=1,
+              x_dist="relu_normal", w_dist="he"),
+    LayerSpec("f3x6_3d_ragged", N=3, m=3, r=6, batch=1, C=7, K=12, X=(11, 10, 13), pad=2,
+              x_dist="normal", w_dist="he"),
+    LayerSpec("f3x6_3d_one_tile", N=3, m=3, r=6, batch=1, C=3, K=2, X=(6, 6, 6), pad=0,
+              x_dist="normal", w_dist="normal"),
+]
+IDS = [s.name for s in LAYERS]
+
+
+@pytest.mark.parametrize("spec", LAYERS, ids=IDS)
+def test_table1_3d_full_output(spec):
+    x, w = draw_layer(spec, seed=31)
+    y, plan = run_layer(spec, x, w, guard=512)
+    assert plan.desc["n_xi"] == (spec.m + spec.r - 1) ** 3
+    assert y.shape == (spec.batch, spec.K) + spec.out_spatial
+    check_full(spec, y, x, w)
+
+
+@pytest.mark.parametrize("spec", [LAYERS[1], LAYERS[3], LAYERS[5], LAYERS[6]], ids=lambda s: s.name)
+def test_table1_3d_bias_and_activations(spec):
+    x, w = draw_layer(spec, seed=32)
+    b = (0.3 * np.random.default_rng(7).standard_normal(spec.K)).astype(np.float32)
+    for act in ({"relu": True}, {"leaky": 0.125}):
+        s2 = spec.with_(**act)
+        y, _ = run_layer(s2, x, w, bias=b)
+        check_full(s2, y, x, w, bias=b)
+
+
+@pytest.mark.parametrize("spec", [LAYERS[0], LAYERS[2], LAYERS[4], LAYERS[6]], ids=lambda s: s.name)
+def test_table1_3d_transform_stages(spec):
+    """U and V on their own against the oracle's steps 2 and 3."""
+    torch = require_gpu()
+    from paper_1611_06565_amd.wino import Plan
+    x, w = draw_layer(spec, seed=33)
+    plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X), pad=spec.pad)
+    d = plan.desc
+    U = plan.transform_filter(torch.from_numpy(w).cuda())
+    ws = plan.transform_input(torch.from_numpy(x).cuda())
+    torch.cuda.synchronize()
+    nxi = d["n_xi"]
+    Ug = plan.unpack_filter(U)
+    Vg = plan.unpack_workspace(ws)
+    Uo = o_filter(w, spec.m, spec.r).reshape(spec.K, spec.C, nxi).transpose(2, 1, 0)
+    Vo = o_input(x, spec.m, spec.r, spec.pad).reshape(d["T"], spec.C, nxi).transpose(2, 1, 0)
+    assert np.all(Ug[:, spec.C:, :] == 0) and np.all(Ug[:, :, spec.K:] == 0)
+    assert np.all(Vg[:, spec.C:, :] == 0) and np.all(Vg[:, :, d["T"]:] == 0)
+    log(f"  U max rel {np.abs(Ug[:, :spec.C, :spec.K] - Uo).max() / np.abs(Uo).max():.2e}, "
+        f"V max rel {np.abs(Vg[:, :spec.C, :d['T']] - Vo).max() / np.abs(Vo).max():.2e}")
+    assert np.abs(Ug[:, :spec.C, :spec.K] - Uo).max() <= 1e-6 * np.abs(Uo).max()
+    assert np.abs(Vg[:, :spec.C, :d["T"]] - Vo).max() <= 1e-6 * np.abs(Vo).max()
+
+
+@pytest.mark.parametrize("spec", [LAYERS[0], LAYERS[2], LAYERS[4], LAYERS[6]], ids=lambda s: s.name)
+def test_table1_3d_data_gradient(spec):
+    """dx = adjoint of the correlation, on the same kernels (pad r - 1 - pad)."""
+    torch = require_gpu()
+    from paper_1611_06565_amd.wino import Plan
+    x, w = draw_layer(spec, seed=34)
+    plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X), pad=spec.pad)
+    adj = plan.adjoint()
+    dy = np.random.default_rng(9).standard_normal(plan.output_shape).astype(np.float32)
+    wd = torch.from_numpy(w).cuda()
+    dx = adj.forward(torch.from_numpy(dy).cuda(), adj.transform_filter_adjoint(wd))
+    torch.cuda.synchronize()
+    ref, den = direct_adjoint(dy, w, spec.pad)
+    err = normalised_error(dx.cpu().numpy(), ref, den)
+    log(f"  data gradient max err {err['max']:.3e}")
+    assert err["nonfinite"] == 0 and err["max"] <= 1e-4
+
+
+def test_table1_3d_caller_points():
+    """F(5^3, 4^3) on another set of seven points: the kernels take the
+    matrices from their argument."""
+    spec = LAYERS[2]
+    pts = (0.0, 1.0, -1.0, 0.5, -0.5, 2.0, -2.0)
+    x, w = draw_layer(spec, seed=35)
+    y, plan = run_layer(spec, x, w, points=pts)
+    assert plan.desc["default_points"] == 0
+    check_full(spec, y, x, w)
+
+
+def test_table1_3d_determinism_bitwise():
+    spec = LAYERS[3]
+    x, w = draw_layer(spec, seed=36)
+    y1, _ = run_layer(spec, x, w)
+    y2, _ = run_layer(spec, x, w)
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+
+
+def test_table1_3d_no_weight_gradient():
+    torch = require_gpu()
+    from paper_1611_06565_amd.wino import Plan, WinoError
+    plan = Plan(3, 5, 4, 4, 4, [1, 9, 9, 9], pad=1)
+    assert plan.weight_gradient_workspace_bytes == 0
+    x = torch.zeros(plan.input_shape, device="cuda")
+    dy = torch.zeros(plan.output_shape, device="cuda")
+    with pytest.raises(WinoError):
+        plan.weight_gradient(x, dy)

@@ -48,6 +48,7 @@ WG = [
     ("f4x5_2d", 2, 4, 5, 2, 12, 19, (21, 26), 2),
     ("f3x6_2d", 2, 3, 6, 1, 20, 33, (25, 19), 0),
     ("f3x2_2d", 2, 3, 2, 3, 17, 40, (20, 23), 0),
+    ("f3x2_3d", 3, 3, 2, 2, 10, 20, (7, 9, 8), 1),
 ]
 
 
