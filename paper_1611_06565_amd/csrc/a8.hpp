@@ -130,19 +130,38 @@ __global__ void __launch_bounds__(512) k_input_a8(const float* __restrict__ x, f
     const int q0 = ti[0] * MM - a.pad[0] + i0;
     const bool v0 = live && (unsigned)q0 < (unsigned)a.X[0];
     const int64_t off0 = int64_t(min(max(q0, 0), a.X[0] - 1)) * a.X[1];
+    // each window row is one 32-byte load from a start clamped into the input
+    // row, shifted and zero-masked in registers (rows shorter than the
+    // window: one load per value)
+    const int XL = a.X[2];
     const int s2 = ti[2] * MM - a.pad[2];
+    const bool wide = XL >= A;
+    const int sL = wide ? min(max(s2, 0), XL - A) : 0;
+    const int delta = s2 - sL;
     float d[PL];
 #pragma unroll
     for (int i1 = 0; i1 < A; ++i1) {
       const int q1 = ti[1] * MM - a.pad[1] + i1;
       const bool v1 = v0 && (unsigned)q1 < (unsigned)a.X[1];
-      const float* xr = xc + (off0 + min(max(q1, 0), a.X[1] - 1)) * a.X[2];
+      const float* xr = xc + (off0 + min(max(q1, 0), a.X[1] - 1)) * XL;
       float row[A];
+      if (wide) {
+        float ld[A];
+        __builtin_memcpy(ld, xr + sL, sizeof(ld));
 #pragma unroll
-      for (int i2 = 0; i2 < A; ++i2) {
-        const int q2 = s2 + i2;
-        const float v = xr[min(max(q2, 0), a.X[2] - 1)];
-        row[i2] = (v1 && (unsigned)q2 < (unsigned)a.X[2]) ? v : 0.0f;
+        for (int i2 = 0; i2 < A; ++i2) {
+          float v = 0.0f;
+#pragma unroll
+          for (int j = 0; j < A; ++j) v = (j == i2 + delta) ? ld[j] : v;
+          row[i2] = v1 ? v : 0.0f;
+        }
+      } else {
+#pragma unroll
+        for (int i2 = 0; i2 < A; ++i2) {
+          const int q2 = s2 + i2;
+          const float v = xr[min(max(q2, 0), XL - 1)];
+          row[i2] = (v1 && (unsigned)q2 < (unsigned)XL) ? v : 0.0f;
+        }
       }
       apply_vec<A, A>(BT, row, 1, d + i1 * A, 1);   // B^T along the row (last axis)
     }
