@@ -80,6 +80,12 @@ int main() {
     CHECK(plan_status(2, 4, 3, 1 << 20, 4, dims, 1) == WINO_OK, "C = 2^20");
     CHECK(plan_status(3, 2, 3, 1 << 20, 1 << 20, dims, 1) == WINO_EINVAL, "C = K = 2^20: filter grid too big");
     CHECK(plan_status(3, 2, 3, 16384, 16384, dims, 1) == WINO_OK, "C = K = 2^14");
+    // the 3-D alpha = 8 sizes: eight filter threads per (channel, kernel)
+    CHECK(plan_status(3, 5, 4, 8192, 8192, dims, 1) == WINO_OK, "F(5^3,4^3) C = K = 2^13");
+    CHECK(plan_status(3, 5, 4, 1 << 20, 1 << 20, dims, 1) == WINO_EINVAL, "F(5^3,4^3) C = K = 2^20");
+    CHECK(plan_status(3, 4, 5, big, 4, dims, 2) == WINO_EINVAL, "F(4^3,5^3) C = 2^31 - 1");
+    CHECK(plan_status(3, 3, 6, 4, 4, dims, 2) == WINO_OK, "F(3^3,6^3)");
+    CHECK(plan_status(3, 3, 2, 4, 4, dims, 1) == WINO_OK, "F(3^3,2^3)");
   }
   // extents: tile counts, byte counts and grids past their ranges
   {
