@@ -165,7 +165,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
                                                      float* __restrict__ y, AccArgs g, FMats fm) {
   using G = AccGeom<N, MM, R>;
   using S = MfmaShape<32>;
-  constexpr int A = G::A, E = G::E, NOUT = G::NOUT, G4 = G::G4, NG = G::NG;
+  constexpr int E = G::E, NOUT = G::NOUT, G4 = G::G4, NG = G::NG;
   constexpr int TB = G::TB, KB = G::KB, NW = G::NW, NBUF = G::NBUF, DEPTH = G::DEPTH;
 
   // The stage buffers are distinct LDS objects, always named with a

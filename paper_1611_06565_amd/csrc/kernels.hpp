@@ -723,9 +723,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
                                                       float* __restrict__ y, GemmArgs g, FMats fm) {
   using S = MfmaShape<BLK>;
   using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
-  constexpr int A = Geo::A, NXI = Geo::NXI, NT = Geo::NT, XPW = Geo::XPW;
-  constexpr int UPW = Geo::UPW, UNIT = Geo::UNIT, OLOC = Geo::OLOC, PL = Geo::PL;
-  constexpr int NUNIT = Geo::NUNIT;
+  constexpr int NXI = Geo::NXI, XPW = Geo::XPW;
   static_assert(VEC == 1 || VEC == 2 || VEC == 4, "operand load width");
 
   __shared__ float sm[Geo::LDS_FLOATS];
