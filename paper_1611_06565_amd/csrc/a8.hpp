@@ -49,7 +49,10 @@ struct A8Shape {
   static constexpr int SC = 16;                     // channels per operand stage (4 groups)
   static constexpr int EPL = BLK * BLK + 8;         // LDS plane stride (bank spread)
   static constexpr int NPLANE = A * 2 * MM;         // (xi1, half, o2) planes
-  static constexpr int LDS_FLOATS = NPLANE * EPL;
+  static constexpr int NOUT3 = MM * MM * MM;        // outputs of a (tile, kernel)
+  static constexpr int TROW = BLK * MM + 1;         // store stage row: 16 tiles x m values (+1 bank spread)
+  static constexpr int STORE_FLOATS = BLK * MM * MM * TROW;   // [kernel][o0][o1] rows
+  static constexpr int LDS_FLOATS = NPLANE * EPL > STORE_FLOATS ? NPLANE * EPL : STORE_FLOATS;
   static constexpr int ITEMS = MM * BLK * BLK;      // (o2, kernel, tile) output columns
   static constexpr int IPT = (ITEMS + NT - 1) / NT; // columns per thread
   static constexpr int NOUT = MM * MM;              // outputs (o0, o1) of a column
@@ -204,6 +207,7 @@ __global__ void __launch_bounds__(1024) k_gemm_a8(const float* __restrict__ V, c
   constexpr int IPT = S::IPT, NOUT = S::NOUT;
   __shared__ float sm[S::LDS_FLOATS];
   __shared__ float bsm[BLK];
+  __shared__ int tsm[BLK][4];   // per tile of the block: sample (-1 past T), output origin on each axis
 
   const int lane = int(threadIdx.x) & 63;
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
@@ -218,6 +222,13 @@ __global__ void __launch_bounds__(1024) k_gemm_a8(const float* __restrict__ V, c
   if (g.bias != nullptr && int(threadIdx.x) < BLK) {
     const int kg = kb * BLK + int(threadIdx.x);
     bsm[threadIdx.x] = kg < g.K ? g.bias[kg] : 0.0f;
+  }
+  if (int(threadIdx.x) < BLK) {
+    const int t = tb * BLK + int(threadIdx.x);
+    int ti[3] = {0, 0, 0};
+    const int n = split_tile<3>(t < g.T ? t : 0, g.tiles, ti);
+    tsm[threadIdx.x][0] = t < g.T ? n : -1;
+    for (int ax = 0; ax < 3; ++ax) tsm[threadIdx.x][1 + ax] = ti[ax] * MM;
   }
 
   // the thread's output columns: item i = tid + NT q -> (o2, kernel, tile)
@@ -290,32 +301,34 @@ __global__ void __launch_bounds__(1024) k_gemm_a8(const float* __restrict__ V, c
     __syncthreads();   // the planes are rewritten by the next pass
   }
 
-  // bias, activation, crop, store
+  // bias and activation, then through LDS into rows [kernel][o0][o1][tile][o2]
+  // (the planes are free: the last pass ended with a barrier), so that the
+  // stores below write each output row's runs contiguously
 #pragma unroll
   for (int q = 0; q < IPT; ++q) {
     const int i = int(threadIdx.x) + S::NT * q;
     if (i >= S::ITEMS) continue;
     const int tl = i % BLK, kl = (i / BLK) % BLK, o2 = i / (BLK * BLK);
-    const int t = tb * BLK + tl, kg = kb * BLK + kl;
-    if (t >= g.T || kg >= g.K) continue;
-    int ti[3] = {0, 0, 0};
-    const int n = split_tile<3>(t, g.tiles, ti);
-    const int y2 = ti[2] * MM + o2;
-    if (y2 >= g.Y[2]) continue;
     const float bk = g.bias != nullptr ? bsm[kl] : 0.0f;
-    float* yk = y + (int64_t(n) * g.K + kg) * g.ystride_k;
 #pragma unroll
-    for (int o0 = 0; o0 < MM; ++o0) {
-      const int y0 = ti[0] * MM + o0;
-      if (y0 >= g.Y[0]) continue;
-#pragma unroll
-      for (int o1 = 0; o1 < MM; ++o1) {
-        const int y1 = ti[1] * MM + o1;
-        if (y1 >= g.Y[1]) continue;
-        const float val = activate(out[q][o0 * MM + o1] + bk, g.act, g.slope);
-        yk[(int64_t(y0) * g.Y[1] + y1) * g.Y[2] + y2] = val;
-      }
-    }
+    for (int o = 0; o < NOUT; ++o)
+      sm[(kl * NOUT + o) * S::TROW + tl * MM + o2] = activate(out[q][o] + bk, g.act, g.slope);
+  }
+  __syncthreads();
+  // crop and store: item (kernel, o0, o1, value of the 16-tile row), the
+  // row's values fastest, so a wave writes runs of consecutive outputs
+  constexpr int RV = BLK * MM;                      // values of a stage row
+  for (int i = int(threadIdx.x); i < BLK * NOUT * RV; i += S::NT) {
+    const int v = i % RV, row = i / RV;             // row = kl * NOUT + o0 * MM + o1
+    const int kl = row / NOUT, o01 = row % NOUT;
+    const int o0 = o01 / MM, o1 = o01 % MM;
+    const int tl = v / MM, o2 = v % MM;
+    const int n = tsm[tl][0], kg = kb * BLK + kl;
+    if (n < 0 || kg >= g.K) continue;
+    const int y0 = tsm[tl][1] + o0, y1 = tsm[tl][2] + o1, y2 = tsm[tl][3] + o2;
+    if (y0 >= g.Y[0] || y1 >= g.Y[1] || y2 >= g.Y[2]) continue;
+    y[(int64_t(n) * g.K + kg) * g.ystride_k + (int64_t(y0) * g.Y[1] + y1) * g.Y[2] + y2] =
+        sm[row * S::TROW + v];
   }
 }
 
