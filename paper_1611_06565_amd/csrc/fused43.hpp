@@ -78,7 +78,7 @@ __device__ __forceinline__ int p_index(int i0, int j, int ch, int tl) {
   return ((i0 * Fused43Geom::PL + j) * (Fused43Geom::CH / 2) + (ch >> 1)) * 32 + tl * 2 + (ch & 1);
 }
 
-template <bool CONST>
+template <bool CONST, bool KLOOP>
 __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x, const float* __restrict__ U,
                                                     float* __restrict__ y, FusedArgs a, FMats fm) {
   using G = Fused43Geom;
@@ -91,7 +91,7 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   // consecutive logical blocks (the kernel blocks of one tile block, then the
   // next tile block) run on one XCD and share the input windows in its L2
   const int L = xcd_remap(int(blockIdx.x), a.nblocks);
-  const int tb = L / a.nkb, kb = L % a.nkb;
+  const int tb = KLOOP ? L : L / a.nkb, kb = KLOOP ? 0 : L % a.nkb;
   const MatRef<Which::BT, CONST, MM, R> BT{&fm};
 
   // ---- producer role: lane = tile of the block, 16-lane row = (channel, plane)
@@ -235,10 +235,11 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   // chunk's 18 operands are loaded together after its producing.
   const int uplane = int(a.uplane);
   // per-lane base at element (0, jw); the element offsets are wave-uniform
-  const float* ubase = U + jw * uplane + ((kr >> 1) * a.K_pad + kb * BLK + col) * 4 + 2 * (kr & 1);
+  // (the kernel block is part of the base, except in the kernel-block loop)
+  const float* ubase = U + jw * uplane + ((kr >> 1) * a.K_pad + (KLOOP ? 0 : kb * BLK) + col) * 4 + 2 * (kr & 1);
   float2 ur[XPW];
-  auto load_u = [&](int chunk) {
-    const float* uc = ubase + chunk * 8 * a.K_pad;
+  auto load_u = [&](int chunk, int kbx) {
+    const float* uc = ubase + chunk * 8 * a.K_pad + (KLOOP ? kbx * (BLK * 4) : 0);
 #pragma unroll
     for (int p = 0; p < G::NPOS; ++p)
 #pragma unroll
@@ -278,22 +279,62 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   // chunks past the last real channel hold only zero padding (x and U are
   // zero there): they are skipped
   const int nchunks = (a.C + CH - 1) / CH;
-  for (int chunk = 0; chunk < nchunks; ++chunk) {
-    if (chunk > 0) __syncthreads();             // the previous chunk's planes are read
-    produce(chunk);
-    load_u(chunk);
-    __syncthreads();
-    consume();
+  if constexpr (!KLOOP) {
+    for (int chunk = 0; chunk < nchunks; ++chunk) {
+      if (chunk > 0) __syncthreads();           // the previous chunk's planes are read
+      produce(chunk);
+      load_u(chunk, kb);
+      __syncthreads();
+      consume();
+    }
   }
 
-  // ---- epilogue (eq. 4 inverted): A^T along the first axis in registers,
-  // then along the last two axes, bias, activation, crop and store.
-  // Part 1: wave w writes, for each of its positions j and output o0, the
-  // 16 x 16 (tile, kernel) block to LDS plane (j, o0) at [k][t ^ k].
+  // One chunk (C <= 8, the kernel-block loop): the planes are formed once,
+  // each wave turns them into its 18 elements of V in registers, and the
+  // work-group multiplies them with every kernel block's U in turn; the LDS
+  // is then free for each block's epilogue.
+  [[maybe_unused]] float2 vv[XPW];
+  if constexpr (KLOOP) {
+  produce(0);
+  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < G::NPOS; ++p) {
+    float2 pv[A];
+    fetch(pv, p);
+    float vx[A], vy[A], ox[A], oy[A];
+#pragma unroll
+    for (int i = 0; i < A; ++i) {
+      vx[i] = pv[i].x;
+      vy[i] = pv[i].y;
+    }
+    apply_vec<A, A>(BT, vx, 1, ox, 1);
+    apply_vec<A, A>(BT, vy, 1, oy, 1);
+#pragma unroll
+    for (int x0 = 0; x0 < A; ++x0) vv[p * A + x0] = make_float2(ox[x0], oy[x0]);
+  }
+  }
+  // ---- epilogue of kernel block kbx (eq. 4 inverted): A^T along the first
+  // axis in registers, then along the last two axes, bias, activation, crop
+  // and store.  Part 1: wave w writes, for each of its positions j and
+  // output o0, the 16 x 16 (tile, kernel) block to LDS plane (j, o0) at
+  // [k][t ^ k].
   const MatRef<Which::AT, CONST, MM, R> AT{&fm};
   __shared__ float bsm[BLK];
+  // the kernel blocks of this work-group: its own, or every one in the loop
+  const int kb0 = KLOOP ? 0 : kb, kb1 = KLOOP ? a.nkb : kb + 1;
+  for (int kbx = kb0; kbx < kb1; ++kbx) {
+  if constexpr (KLOOP) {
+    if (kbx > 0) __syncthreads();               // the previous block's stores have read the LDS
+    load_u(0, kbx);
+#pragma unroll
+    for (int e = 0; e < XPW; ++e) {
+      acc[e] = typename S::acc_t{};
+      acc[e] = S::mma(vv[e].x, ur[e].x, acc[e]);
+      acc[e] = S::mma(vv[e].y, ur[e].y, acc[e]);
+    }
+  }
   if (a.bias != nullptr && int(threadIdx.x) < BLK) {
-    const int kg = kb * BLK + int(threadIdx.x);
+    const int kg = kbx * BLK + int(threadIdx.x);
     bsm[threadIdx.x] = kg < a.K ? a.bias[kg] : 0.0f;
   }
   __syncthreads();                              // the planes' LDS is reused below
@@ -321,7 +362,7 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   for (int i = int(threadIdx.x); i < ITEMS; i += G::NT) {
     const int tl2 = i % BLK, kl = (i / BLK) % BLK, o0 = i / (BLK * BLK);
     const int t2 = tb * BLK + tl2;
-    const int kg = kb * BLK + kl;
+    const int kg = kbx * BLK + kl;
     if (t2 >= a.T || kg >= a.K) continue;
     int ti[3] = {0, 0, 0};
     const int n = split_tile<N>(t2, a.tiles, ti);
@@ -350,6 +391,7 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
           if (y2 + o2 < a.Y[2]) row[o2] = out[o1 * MM + o2];
       }
     }
+  }
   }
 }
 

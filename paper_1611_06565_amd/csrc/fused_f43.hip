@@ -16,7 +16,6 @@ wino_status launch_fused43(const wino_plan_s& p, bool const_mats, const float* x
   a.C = p.C; a.C_pad = p.C_pad; a.K = p.K; a.K_pad = p.K_pad;
   a.T = int32_t(p.T);
   a.nkb = p.K_pad / Fused43Geom::BLK;
-  a.nblocks = int32_t(p.grid_fused);
   for (int i = 0; i < 3; ++i) {
     a.X[i] = int32_t(p.X[i]); a.tiles[i] = int32_t(p.tiles[i]); a.pad[i] = p.pad[i]; a.Y[i] = int32_t(p.Y[i]);
   }
@@ -26,13 +25,22 @@ wino_status launch_fused43(const wino_plan_s& p, bool const_mats, const float* x
   // every output row a whole number of 4-wide tiles, y 16-byte aligned:
   // the epilogue stores rows of four as one 16-byte store
   a.vec_store = (p.Y[2] % 4 == 0 && (reinterpret_cast<uintptr_t>(y) & 15) == 0) ? 1 : 0;
+  // one chunk of channels (C <= 8) and several kernel blocks, default points:
+  // every kernel block of a tile block in one work-group (the planes formed
+  // once), one work-group per tile block
+  const bool kloop = const_mats && p.C <= Fused43Geom::CH && a.nkb > 1;
+  const uint32_t grid = kloop ? p.grid_fused / uint32_t(a.nkb) : p.grid_fused;
+  a.nblocks = int32_t(grid);
   a.act = act_kind(p);
   a.slope = p.slope;
   a.bias = bias;
-  if (const_mats)
-    hipLaunchKernelGGL((k_fused43<true>), dim3(p.grid_fused), dim3(Fused43Geom::NT), 0, s, x, U, y, a, p.fm);
+  const dim3 nt(Fused43Geom::NT);
+  if (kloop)
+    hipLaunchKernelGGL((k_fused43<true, true>), dim3(grid), nt, 0, s, x, U, y, a, p.fm);
+  else if (const_mats)
+    hipLaunchKernelGGL((k_fused43<true, false>), dim3(grid), nt, 0, s, x, U, y, a, p.fm);
   else
-    hipLaunchKernelGGL((k_fused43<false>), dim3(p.grid_fused), dim3(Fused43Geom::NT), 0, s, x, U, y, a, p.fm);
+    hipLaunchKernelGGL((k_fused43<false, false>), dim3(grid), nt, 0, s, x, U, y, a, p.fm);
   return launch_status();
 }
 

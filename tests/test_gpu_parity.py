@@ -101,6 +101,14 @@ F43_BOTH = [s for s in SMALL + EDGE + ROWFAST if s.N == 3 and s.m == 4] + [
               x_dist="relu_normal", w_dist="he"),
     LayerSpec("f4x3_row_c33_k48", N=3, m=4, r=3, batch=1, C=33, K=48, X=(6, 5, 64), pad=1,
               x_dist="uniform", w_dist="he"),
+    # one chunk of channels (C <= 8) with several kernel blocks: a work-group
+    # forms the planes once and runs every kernel block of its tiles
+    LayerSpec("f4x3_kloop_row_c3_k64", N=3, m=4, r=3, batch=2, C=3, K=64, X=(6, 7, 64), pad=1,
+              x_dist="uniform", w_dist="he"),
+    LayerSpec("f4x3_kloop_c8_k40", N=3, m=4, r=3, batch=1, C=8, K=40, X=(9, 10, 11), pad=1,
+              x_dist="normal", w_dist="he"),
+    LayerSpec("f4x3_kloop_c1_k33", N=3, m=4, r=3, batch=1, C=1, K=33, X=(7, 6, 9), pad=0,
+              x_dist="normal", w_dist="normal"),
 ]
 
 
