@@ -7,10 +7,11 @@
 //
 //   k_filter_a8  one thread per (channel, kernel, xi0) forms one xi0-plane
 //                of U = g x_0 G x_1 G x_2 G (64 values);
-//   k_input_a8   a work-group forms one V block (16 tiles x 4 channels):
-//                wave i0 transforms plane i0 of each window along the last
-//                two axes into LDS, then wave xi0 combines the eight planes
-//                along the first axis and stores V[.][xi0 * 64 + j];
+//   k_input_a8   a work-group forms half a V block (8 tiles x 4 channels):
+//                each half wave transforms plane i0 of each window along the
+//                last two axes into LDS, then each half wave combines the
+//                eight planes along the first axis for one xi0 and stores
+//                V[.][xi0 * 64 + j];
 //   k_gemm_a8    a work-group owns 16 tiles x 16 kernels and walks the first
 //                axis: pass xi0 accumulates M_xi = sum_c V_xi U_xi for the 64
 //                elements of plane xi0 (16 waves, half an alpha-row each),
@@ -104,27 +105,42 @@ __global__ void __launch_bounds__(64) k_filter_a8(const float* __restrict__ w, f
 }
 
 // ------------------------------------------------------------- input
-// One work-group per V block (16 tiles x one group of 4 channels), 8 waves.
-// Phase 1: wave i0, lane (channel cl = lane / 16, tile tl = lane % 16) loads
+// One work-group per half V block (8 of its 16 tiles x one group of 4
+// channels), 4 waves.  The 64 plane values j go through LDS in two halves
+// (32 KB), the second half held in registers meanwhile, so that four
+// work-groups share a CU.
+// Phase 1: lane (plane i0 = 2 * wave + lane / 32, channel cl, tile tl) loads
 // plane i0 of its tile's 8 x 8 x 8 window (zero outside the padded input and
-// for channels past C) and transforms it along the last two axes into
-// P[i0][j][tl][cl] in LDS.  Phase 2: wave xi0, lane (tl = lane / 4,
-// cl = lane % 4) forms V[xi0 * 64 + j] = sum_i0 B^T[xi0][i0] P[i0][j] and
-// stores it (one 256-byte run per j and wave).
+// for channels past C) and transforms it along the last two axes.  A window
+// whose rows lie inside the input row is read as one 32-byte load per row;
+// one that crosses an end of the row (the first and last tiles of a row)
+// value by value, clamped and masked.
+// Phase 2, once per half of the plane values: the lanes write their half to
+// P[i0][j][tl][cl]; item (j, tl, cl) reads P[0..7][j], applies B^T along the
+// first axis (one matrix application for all eight xi0) and stores
+// V[xi0 * 64 + j] for every xi0; a half wave covers the half block's 128
+// contiguous bytes of one j.
 template <int MM, int R, bool CONST>
-__global__ void __launch_bounds__(512) k_input_a8(const float* __restrict__ x, float* __restrict__ V,
-                                                   InputArgs a, FMats fm) {
+__global__ void __launch_bounds__(256) k_input_a8(const float* __restrict__ x, float* __restrict__ V,
+                                                  InputArgs a, FMats fm) {
   using S = A8Shape<MM, R>;
   constexpr int A = S::A, PL = S::PL, BLK = S::BLK, CG = S::CG;
-  __shared__ float P[A * PL * BLK * CG];   // 128 KB
-  const int lane = int(threadIdx.x) & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+  constexpr int HB = BLK / 2;              // tiles of a half block
+  constexpr int HQ = HB * CG;              // (tile, channel) pairs of a half block (32)
+  constexpr int NT = 256;
+  constexpr int PH = PL / 2;               // plane values per half
+  __shared__ float P[A * PH * HQ];         // 32 KB: one half of the planes
+  const int tid = int(threadIdx.x);
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ncg = a.C_pad / CG;
-  const int tb = int(blockIdx.x) / ncg, cg = int(blockIdx.x) % ncg;
+  const int hb = int(blockIdx.x) & 1;
+  const int tb = (int(blockIdx.x) >> 1) / ncg, cg = (int(blockIdx.x) >> 1) % ncg;
   const MatRef<Which::BT, CONST, MM, R> BT{&fm};
+  float d[PL];   // plane i0 of the window, then of its transform
   {
-    const int i0 = wave, tl = lane & 15, cl = lane >> 4;
-    const int t = tb * BLK + tl;
+    const int i0 = 2 * wave + (lane >> 5), tl = lane & (HB - 1), cl = (lane & 31) / HB;
+    const int t = tb * BLK + hb * HB + tl;
     const int c = cg * CG + cl;
     const bool live = t < a.T && c < a.C;
     int ti[3] = {0, 0, 0};
@@ -133,62 +149,66 @@ __global__ void __launch_bounds__(512) k_input_a8(const float* __restrict__ x, f
     const int q0 = ti[0] * MM - a.pad[0] + i0;
     const bool v0 = live && (unsigned)q0 < (unsigned)a.X[0];
     const int64_t off0 = int64_t(min(max(q0, 0), a.X[0] - 1)) * a.X[1];
-    // each window row is one 32-byte load from a start clamped into the input
-    // row, shifted and zero-masked in registers (rows shorter than the
-    // window: one load per value)
     const int XL = a.X[2];
     const int s2 = ti[2] * MM - a.pad[2];
-    const bool wide = XL >= A;
-    const int sL = wide ? min(max(s2, 0), XL - A) : 0;
-    const int delta = s2 - sL;
-    float d[PL];
+    if (s2 >= 0 && s2 + A <= XL) {
 #pragma unroll
-    for (int i1 = 0; i1 < A; ++i1) {
-      const int q1 = ti[1] * MM - a.pad[1] + i1;
-      const bool v1 = v0 && (unsigned)q1 < (unsigned)a.X[1];
-      const float* xr = xc + (off0 + min(max(q1, 0), a.X[1] - 1)) * XL;
-      float row[A];
-      if (wide) {
+      for (int i1 = 0; i1 < A; ++i1) {
+        const int q1 = ti[1] * MM - a.pad[1] + i1;
+        const bool v1 = v0 && (unsigned)q1 < (unsigned)a.X[1];
+        const float* xr = xc + (off0 + min(max(q1, 0), a.X[1] - 1)) * XL;
         float ld[A];
-        __builtin_memcpy(ld, xr + sL, sizeof(ld));
+        __builtin_memcpy(ld, xr + s2, sizeof(ld));
 #pragma unroll
-        for (int i2 = 0; i2 < A; ++i2) {
-          float v = 0.0f;
+        for (int i2 = 0; i2 < A; ++i2) d[i1 * A + i2] = v1 ? ld[i2] : 0.0f;
+      }
+    } else {
 #pragma unroll
-          for (int j = 0; j < A; ++j) v = (j == i2 + delta) ? ld[j] : v;
-          row[i2] = v1 ? v : 0.0f;
-        }
-      } else {
+      for (int i1 = 0; i1 < A; ++i1) {
+        const int q1 = ti[1] * MM - a.pad[1] + i1;
+        const bool v1 = v0 && (unsigned)q1 < (unsigned)a.X[1];
+        const float* xr = xc + (off0 + min(max(q1, 0), a.X[1] - 1)) * XL;
 #pragma unroll
         for (int i2 = 0; i2 < A; ++i2) {
           const int q2 = s2 + i2;
           const float v = xr[min(max(q2, 0), XL - 1)];
-          row[i2] = (v1 && (unsigned)q2 < (unsigned)XL) ? v : 0.0f;
+          d[i1 * A + i2] = (v1 && (unsigned)q2 < (unsigned)XL) ? v : 0.0f;
         }
       }
-      apply_vec<A, A>(BT, row, 1, d + i1 * A, 1);   // B^T along the row (last axis)
+    }
+#pragma unroll
+    for (int i1 = 0; i1 < A; ++i1) {
+      float row[A];
+      apply_vec<A, A>(BT, d + i1 * A, 1, row, 1);   // B^T along the row (last axis)
+#pragma unroll
+      for (int i2 = 0; i2 < A; ++i2) d[i1 * A + i2] = row[i2];
     }
 #pragma unroll
     for (int i2 = 0; i2 < A; ++i2) {
       float cv[A];
       apply_vec<A, A>(BT, d + i2, A, cv, 1);          // B^T along the columns (middle axis)
 #pragma unroll
-      for (int j1 = 0; j1 < A; ++j1) P[((i0 * PL + j1 * A + i2) * BLK + tl) * CG + cl] = cv[j1];
+      for (int j1 = 0; j1 < A; ++j1) d[j1 * A + i2] = cv[j1];   // d[j] = plane value j
     }
   }
-  __syncthreads();
-  {
-    const int xi0 = wave;
-    float bt[A];
+  float* const dst = V + (int64_t(tb) * ncg + cg) * S::NXI * (BLK * CG) + hb * HQ;
+  const int pidx = ((2 * wave + (lane >> 5)) * PH) * HQ + (lane & (HB - 1)) * CG + (lane & 31) / HB;
 #pragma unroll
-    for (int i0 = 0; i0 < A; ++i0) bt[i0] = BT(xi0, i0);
-    float* dst = V + ((int64_t(tb) * ncg + cg) * S::NXI + xi0 * PL) * (BLK * CG) + lane;
-#pragma unroll 4
-    for (int j = 0; j < PL; ++j) {
-      float v = 0.0f;
+  for (int h = 0; h < 2; ++h) {
+    if (h == 1) __syncthreads();                  // the first half has been read
 #pragma unroll
-      for (int i0 = 0; i0 < A; ++i0) v = __builtin_fmaf(bt[i0], P[(i0 * PL + j) * (BLK * CG) + lane], v);
-      __builtin_nontemporal_store(v, dst + j * (BLK * CG));
+    for (int jj = 0; jj < PH; ++jj) P[pidx + jj * HQ] = d[h * PH + jj];
+    __syncthreads();
+#pragma unroll 2
+    for (int i = tid; i < PH * HQ; i += NT) {
+      const int q = i % HQ, jj = i / HQ, j = h * PH + jj;
+      float pv[A], vo[A];
+#pragma unroll
+      for (int i0 = 0; i0 < A; ++i0) pv[i0] = P[(i0 * PH + jj) * HQ + q];
+      apply_vec<A, A>(BT, pv, 1, vo, 1);
+#pragma unroll
+      for (int xi0 = 0; xi0 < A; ++xi0)
+        __builtin_nontemporal_store(vo[xi0], dst + (xi0 * PL + j) * (BLK * CG) + q);
     }
   }
 }

@@ -56,6 +56,12 @@ struct FusedArgs {
   int32_t act;         // activation f of eq. (2): 0 none, 1 ReLU, 2 leaky ReLU
   float slope;
   const float* bias;   // [K] or null
+  // Kernel-block loop only.  Work-group b runs on XCD b % 8 as its unit
+  // b / 8; XCD x owns tile blocks xb0[x] .. xb0[x] + xn[x] - 1.  Its last
+  // xs[x] blocks (those past its last full round of work-groups) are tail
+  // blocks, each split into nkb units of one kernel block, so that the last
+  // round is short.  Surplus units exit at once.
+  int32_t xb0[8], xn[8], xs[8];
 };
 
 struct Fused43Geom {
@@ -90,8 +96,21 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   const int wave = int(threadIdx.x) >> 6;
   // consecutive logical blocks (the kernel blocks of one tile block, then the
   // next tile block) run on one XCD and share the input windows in its L2
-  const int L = xcd_remap(int(blockIdx.x), a.nblocks);
-  const int tb = KLOOP ? L : L / a.nkb, kb = KLOOP ? 0 : L % a.nkb;
+  int tb, kb = 0;          // tile block, and kernel block outside the loop
+  int kbs = 0, kbe = 0;    // the loop's kernel blocks kbs .. kbe - 1
+  if constexpr (KLOOP) {
+    const int xcd = int(blockIdx.x) & 7, j = int(blockIdx.x) >> 3;
+    const int xs = a.xs[xcd], nwhole = a.xn[xcd] - xs;
+    if (j >= nwhole + xs * a.nkb) return;        // surplus unit: the whole work-group leaves
+    const int u = j - nwhole;
+    tb = a.xb0[xcd] + (u < 0 ? j : nwhole + u / a.nkb);
+    kbs = u < 0 ? 0 : u % a.nkb;
+    kbe = u < 0 ? a.nkb : kbs + 1;
+  } else {
+    const int L = xcd_remap(int(blockIdx.x), a.nblocks);
+    tb = L / a.nkb;
+    kb = L % a.nkb;
+  }
   const MatRef<Which::BT, CONST, MM, R> BT{&fm};
 
   // ---- producer role: lane = tile of the block, 16-lane row = (channel, plane)
@@ -320,11 +339,11 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   // [k][t ^ k].
   const MatRef<Which::AT, CONST, MM, R> AT{&fm};
   __shared__ float bsm[BLK];
-  // the kernel blocks of this work-group: its own, or every one in the loop
-  const int kb0 = KLOOP ? 0 : kb, kb1 = KLOOP ? a.nkb : kb + 1;
+  // the kernel blocks of this work-group: its own, or those of the loop
+  const int kb0 = KLOOP ? kbs : kb, kb1 = KLOOP ? kbe : kb + 1;
   for (int kbx = kb0; kbx < kb1; ++kbx) {
   if constexpr (KLOOP) {
-    if (kbx > 0) __syncthreads();               // the previous block's stores have read the LDS
+    if (kbx > kb0) __syncthreads();             // the previous block's stores have read the LDS
     load_u(0, kbx);
 #pragma unroll
     for (int e = 0; e < XPW; ++e) {

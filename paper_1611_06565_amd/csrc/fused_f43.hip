@@ -1,5 +1,6 @@
 // Kernel instances and launch of k_fused43: F(4^3, 3^3) with the input
 // transform inside the product.
+#include <algorithm>
 #include <cstdint>
 
 #include "fused43.hpp"
@@ -29,7 +30,23 @@ wino_status launch_fused43(const wino_plan_s& p, bool const_mats, const float* x
   // every kernel block of a tile block in one work-group (the planes formed
   // once), one work-group per tile block
   const bool kloop = const_mats && p.C <= Fused43Geom::CH && a.nkb > 1;
-  const uint32_t grid = kloop ? p.grid_fused / uint32_t(a.nkb) : p.grid_fused;
+  uint32_t grid = p.grid_fused;
+  if (kloop) {
+    // tile blocks in contiguous ranges per XCD (one work-group per CU, 1/8 of
+    // the CUs per XCD); the blocks past an XCD's last full round are split into
+    // one unit per kernel block when those units fit in one round
+    const int nb = int(p.grid_fused / uint32_t(a.nkb));
+    const int slots = device_cu_count() / 8;
+    int units = 0;
+    for (int xc = 0; xc < 8; ++xc) {
+      a.xn[xc] = nb / 8 + (xc < nb % 8 ? 1 : 0);
+      a.xb0[xc] = xc * (nb / 8) + (xc < nb % 8 ? xc : nb % 8);
+      const int xs = slots > 0 ? a.xn[xc] % slots : 0;
+      a.xs[xc] = (xs * a.nkb <= slots) ? xs : 0;
+      units = std::max(units, a.xn[xc] - a.xs[xc] + a.xs[xc] * a.nkb);
+    }
+    grid = uint32_t(units) * 8u;
+  }
   a.nblocks = int32_t(grid);
   a.act = act_kind(p);
   a.slope = p.slope;

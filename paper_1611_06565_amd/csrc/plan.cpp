@@ -333,6 +333,9 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   if (aniso) {
     // k_input_ax: one V block per work-group, alpha0 waves
     if (!mul_ok(tpad / p.blk, groups, &ig) || !grid_ok(ig, p.av[0] * 64, &p.grid_input)) return WINO_EINVAL;
+  } else if (t.KIND == 4) {
+    // k_input_a8: half a V block (8 tiles x one channel group) per work-group
+    if (!mul_ok(tpad / p.blk, 2 * groups, &ig) || !grid_ok(ig, 256, &p.grid_input)) return WINO_EINVAL;
   } else if (p.nxi > 64) {
     // k_input_split: one V block (BLK tiles x one channel group) per work-group
     if (!mul_ok(tpad / p.blk, groups, &ig) || !grid_ok(ig, alpha * 64, &p.grid_input)) return WINO_EINVAL;

@@ -32,7 +32,7 @@ struct LaunchA8 {
     }
     a.ntb = int32_t(p.T_pad / S::BLK);
     a.nblocks = int32_t(p.grid_input);
-    hipLaunchKernelGGL((k_input_a8<MM, R, CONST>), dim3(p.grid_input), dim3(512), 0, s, x, V, a, p.fm);
+    hipLaunchKernelGGL((k_input_a8<MM, R, CONST>), dim3(p.grid_input), dim3(256), 0, s, x, V, a, p.fm);
     return launch_status();
   }
 

@@ -109,6 +109,11 @@ F43_BOTH = [s for s in SMALL + EDGE + ROWFAST if s.N == 3 and s.m == 4] + [
               x_dist="normal", w_dist="he"),
     LayerSpec("f4x3_kloop_c1_k33", N=3, m=4, r=3, batch=1, C=1, K=33, X=(7, 6, 9), pad=0,
               x_dist="normal", w_dist="normal"),
+    # 300 tile blocks: whole work-groups for every kernel block plus, on each
+    # XCD, the blocks past its last full round split into one unit per kernel
+    # block
+    LayerSpec("f4x3_kloop_tail_c3_k64", N=3, m=4, r=3, batch=1, C=3, K=64, X=(48, 100, 64), pad=1,
+              x_dist="relu_normal", w_dist="he"),
 ]
 
 
