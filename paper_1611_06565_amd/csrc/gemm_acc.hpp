@@ -332,11 +332,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
               buf(std::integral_constant<int, b + DEPTH>{}), real);
   };
 
-  // Pass epilogue for pass p = (row, half h): the two elements xi_last = 2h,
-  // 2h + 1 of the row are reduced by the matching columns of A^T along the last
-  // axis, then added to every output with the product of A^T over the leading
-  // axes; the accumulators are cleared for the next pass.
-  auto epilogue = [&](int pass) {
+  auto epilogue_direct = [&](int pass) {
     const int row = pass / G::HALVES, h = pass % G::HALVES;
     float c[G::NLEAD], at[MM][E];
 #pragma unroll
@@ -362,6 +358,64 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
       }
 #pragma unroll
       for (int o = 0; o < NOUT; ++o) yacc[o][r] = __builtin_fmaf(c[o / MM], rv[o % MM], yacc[o][r]);
+    }
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = typename S::acc_t{};
+  };
+  // Pass epilogue for pass p = (row, half h): the two elements xi_last = 2h,
+  // 2h + 1 of the row are reduced by the matching columns of A^T along the last
+  // axis, then added to every output with the product of A^T over the leading
+  // axes.  With the compiled-in matrices the reduced values are first summed
+  // over the halves of the row (rsum), and added to the outputs once, after
+  // the row's last half or the last pass of this work unit; with matrices
+  // from the argument (their registers leave no room for rsum) every pass
+  // adds its own.  The accumulators are cleared for the next pass.
+  [[maybe_unused]] float rsum[MM][S::NACC];
+  auto epilogue = [&](int pass) {
+    if constexpr (!CONST) {
+      epilogue_direct(pass);
+      return;
+    }
+    const int row = pass / G::HALVES, h = pass % G::HALVES;
+    float at[MM][E];
+#pragma unroll
+    for (int ol = 0; ol < MM; ++ol)
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        float v = AT(ol, e);
+#pragma unroll
+        for (int hh = 1; hh < G::HALVES; ++hh) v = (h == hh) ? AT(ol, hh * E + e) : v;
+        at[ol][e] = v;
+      }
+    if (h == 0 || pass == p0) {                   // first half of a row seen by this unit
+#pragma unroll
+      for (int r = 0; r < S::NACC; ++r)
+#pragma unroll
+        for (int ol = 0; ol < MM; ++ol) {
+          float v = at[ol][0] * acc[0][r];
+#pragma unroll
+          for (int e = 1; e < E; ++e) v = __builtin_fmaf(at[ol][e], acc[e][r], v);
+          rsum[ol][r] = v;
+        }
+    } else {
+#pragma unroll
+      for (int r = 0; r < S::NACC; ++r)
+#pragma unroll
+        for (int ol = 0; ol < MM; ++ol) {
+          float v = rsum[ol][r];
+#pragma unroll
+          for (int e = 0; e < E; ++e) v = __builtin_fmaf(at[ol][e], acc[e][r], v);
+          rsum[ol][r] = v;
+        }
+    }
+    if (h == G::HALVES - 1 || pass == p0 + npass - 1) {   // the row (or the unit) ends
+      float c[G::NLEAD];
+#pragma unroll
+      for (int oo = 0; oo < G::NLEAD; ++oo) c[oo] = lead_coef<N, MM, R, CONST>(AT, row, oo);
+#pragma unroll
+      for (int r = 0; r < S::NACC; ++r)
+#pragma unroll
+        for (int o = 0; o < NOUT; ++o) yacc[o][r] = __builtin_fmaf(c[o / MM], rsum[o % MM][r], yacc[o][r]);
     }
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = typename S::acc_t{};
