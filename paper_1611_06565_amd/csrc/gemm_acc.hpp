@@ -159,6 +159,38 @@ __device__ __forceinline__ float lead_coef(const MatRef<Which::AT, CONST, MM, R>
   return c;
 }
 
+// The same coefficients of the compiled-in matrices as a table in constant
+// memory: the pass epilogue indexes it with wave-uniform row and half, so
+// the coefficients arrive by scalar loads instead of select chains.
+// lead[row][oo] = lead_coef(row, oo); at[h][ol][e] = A^T[ol][h * E + e].
+template <int N, int MM, int R>
+struct AccCoef {
+  float lead[AccGeom<N, MM, R>::NROW][AccGeom<N, MM, R>::NLEAD];
+  float at[AccGeom<N, MM, R>::HALVES][MM][AccGeom<N, MM, R>::E];
+};
+template <int N, int MM, int R>
+constexpr AccCoef<N, MM, R> make_acc_coef() {
+  using G = AccGeom<N, MM, R>;
+  AccCoef<N, MM, R> t{};
+  for (int q = 0; q < G::NROW; ++q)
+    for (int oo = 0; oo < G::NLEAD; ++oo) {
+      float v = 1.0f;
+      int rr = q, o2 = oo;
+      for (int ax = 0; ax < N - 1; ++ax) {
+        v *= kDefaultF<MM, R>.AT[o2 % MM][rr % G::A];
+        rr /= G::A;
+        o2 /= MM;
+      }
+      t.lead[q][oo] = v;
+    }
+  for (int h = 0; h < G::HALVES; ++h)
+    for (int ol = 0; ol < MM; ++ol)
+      for (int e = 0; e < G::E; ++e) t.at[h][ol][e] = kDefaultF<MM, R>.AT[ol][h * G::E + e];
+  return t;
+}
+template <int N, int MM, int R>
+__constant__ AccCoef<N, MM, R> kAccCoef = make_acc_coef<N, MM, R>();
+
 template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V,
                                                      const float* __restrict__ U,
@@ -377,16 +409,12 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
       return;
     }
     const int row = pass / G::HALVES, h = pass % G::HALVES;
+    const AccCoef<N, MM, R>& tab = kAccCoef<N, MM, R>;
     float at[MM][E];
 #pragma unroll
     for (int ol = 0; ol < MM; ++ol)
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        float v = AT(ol, e);
-#pragma unroll
-        for (int hh = 1; hh < G::HALVES; ++hh) v = (h == hh) ? AT(ol, hh * E + e) : v;
-        at[ol][e] = v;
-      }
+      for (int e = 0; e < E; ++e) at[ol][e] = tab.at[h][ol][e];
     if (h == 0 || pass == p0) {                   // first half of a row seen by this unit
 #pragma unroll
       for (int r = 0; r < S::NACC; ++r)
@@ -411,7 +439,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
     if (h == G::HALVES - 1 || pass == p0 + npass - 1) {   // the row (or the unit) ends
       float c[G::NLEAD];
 #pragma unroll
-      for (int oo = 0; oo < G::NLEAD; ++oo) c[oo] = lead_coef<N, MM, R, CONST>(AT, row, oo);
+      for (int oo = 0; oo < G::NLEAD; ++oo) c[oo] = tab.lead[row][oo];
 #pragma unroll
       for (int r = 0; r < S::NACC; ++r)
 #pragma unroll
