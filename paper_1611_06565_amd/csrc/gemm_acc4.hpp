@@ -70,6 +70,29 @@ struct Acc4Geom {
   static_assert(KB * 4 * 2 == 256, "a U copy moves two 512 B chunks");
 };
 
+// The epilogue's coefficients of the compiled-in matrices as a table in
+// constant memory, indexed by the wave-uniform row and third (scalar loads
+// instead of select chains): lead[xr][o0] = A^T[o0][xr], at[h][ol][e] =
+// A^T[ol][h * E + e].
+template <int N, int MM, int R>
+struct Acc4Coef {
+  float lead[Acc4Geom<N, MM, R>::A][Acc4Geom<N, MM, R>::NLEAD];
+  float at[Acc4Geom<N, MM, R>::HALVES][MM][Acc4Geom<N, MM, R>::E];
+};
+template <int N, int MM, int R>
+constexpr Acc4Coef<N, MM, R> make_acc4_coef() {
+  using G = Acc4Geom<N, MM, R>;
+  Acc4Coef<N, MM, R> t{};
+  for (int q = 0; q < G::A; ++q)
+    for (int o0 = 0; o0 < G::NLEAD; ++o0) t.lead[q][o0] = kDefaultF<MM, R>.AT[o0][q];
+  for (int h = 0; h < G::HALVES; ++h)
+    for (int ol = 0; ol < MM; ++ol)
+      for (int e = 0; e < G::E; ++e) t.at[h][ol][e] = kDefaultF<MM, R>.AT[ol][h * G::E + e];
+  return t;
+}
+template <int N, int MM, int R>
+__constant__ Acc4Coef<N, MM, R> kAcc4Coef = make_acc4_coef<N, MM, R>();
+
 template <int N, int MM, int R, bool CONST>
 __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ V,
                                                       const float* __restrict__ U,
@@ -247,22 +270,32 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
   auto epilogue = [&](int pass) {
     const int xr = pass / G::HALVES, h3 = pass % G::HALVES;
     float c[G::NLEAD], at[MM][E];
+    if constexpr (CONST) {
+      const Acc4Coef<N, MM, R>& tab = kAcc4Coef<N, MM, R>;
 #pragma unroll
-    for (int o0 = 0; o0 < G::NLEAD; ++o0) {
-      float v = AT(o0, 0);
+      for (int o0 = 0; o0 < G::NLEAD; ++o0) c[o0] = tab.lead[xr][o0];
 #pragma unroll
-      for (int q = 1; q < A; ++q) v = (xr == q) ? AT(o0, q) : v;
-      c[o0] = v;
-    }
+      for (int ol = 0; ol < MM; ++ol)
 #pragma unroll
-    for (int ol = 0; ol < MM; ++ol)
+        for (int e = 0; e < E; ++e) at[ol][e] = tab.at[h3][ol][e];
+    } else {
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        float v = AT(ol, e);
+      for (int o0 = 0; o0 < G::NLEAD; ++o0) {
+        float v = AT(o0, 0);
 #pragma unroll
-        for (int hh = 1; hh < G::HALVES; ++hh) v = (h3 == hh) ? AT(ol, hh * E + e) : v;
-        at[ol][e] = v;
+        for (int q = 1; q < A; ++q) v = (xr == q) ? AT(o0, q) : v;
+        c[o0] = v;
       }
+#pragma unroll
+      for (int ol = 0; ol < MM; ++ol)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          float v = AT(ol, e);
+#pragma unroll
+          for (int hh = 1; hh < G::HALVES; ++hh) v = (h3 == hh) ? AT(ol, hh * E + e) : v;
+          at[ol][e] = v;
+        }
+    }
 #pragma unroll
     for (int h = 0; h < NH; ++h)
 #pragma unroll
