@@ -296,14 +296,23 @@ def bench_stack(args):
             Y = spec.out_spatial
             py = torch.empty((spec.batch, spec.K) + tuple(yy // p for yy, p in zip(Y, pool.window)),
                              dtype=torch.float32, device="cuda")
-        layers.append((spec, pool, plan, U, wsp, y, py))
+        # the pool rides on the fused F(4^3) forward's epilogue (wino_forward_pool)
+        fpool = (pool is not None and not args.no_fuse_pool and plan.desc["fused"] == 1
+                 and tuple(pool.window) in ((1, 2, 2), (2, 2, 2)))
+        layers.append((spec, pool, plan, U, wsp, y, py, fpool))
     torch.cuda.synchronize()
+    fused_pools = [L[0].name for L in layers if L[7]]
+    pool_note = ("; max-pool in the fused forward's epilogue on " + ",".join(fused_pools)) if fused_pools else ""
 
     def step(ev=None):
         cur = x0
-        for i, (spec, pool, plan, U, wsp, y, py) in enumerate(layers):
+        for i, (spec, pool, plan, U, wsp, y, py, fpool) in enumerate(layers):
             if ev is not None:
                 ev[i].record()
+            if fpool:
+                plan.forward_pool(cur, U, pool.window, y=py)
+                cur = py
+                continue
             plan.forward(cur, U, y=y, workspace=wsp)
             cur = y
             if pool is not None:
@@ -342,7 +351,7 @@ def bench_stack(args):
             "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
             "config": {"workload": "C3D-style stack: batch 4, 3x16x112x112, eight 3x3x3 pad-1 layers "
                                    "(64, 128, 256, 256, 512 x4), ReLU, max-pools; tiles per layer " + ",".join(codes)
-                                   + "; one HIP graph per step"}}), flush=True)
+                                   + pool_note + "; one HIP graph per step"}}), flush=True)
         return
     nev = len(layers) + 1
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
@@ -359,11 +368,13 @@ def bench_stack(args):
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": "C3D-style stack: batch 4, 3x16x112x112, eight 3x3x3 pad-1 layers "
-                               "(64, 128, 256, 256, 512 x4), ReLU, max-pools; tiles per layer " + ",".join(codes)},
+                               "(64, 128, 256, 256, 512 x4), ReLU, max-pools; tiles per layer " + ",".join(codes)
+                               + pool_note},
         "layers": [{"name": spec.name, "C": spec.C, "K": spec.K, "X": list(spec.X), "pool": bool(pool),
                     "tile": plan.desc["tile"],
-                    "ms": float(st[i]), "tflops": flops[i] / (float(st[i]) * 1e-3) / 1e12}
-                   for i, (spec, pool, plan, *_) in enumerate(layers)],
+                    "ms": float(st[i]), "tflops": flops[i] / (float(st[i]) * 1e-3) / 1e12,
+                    "pool_fused": bool(fpool)}
+                   for i, (spec, pool, plan, U, wsp, y, py, fpool) in enumerate(layers)],
     }
     print(json.dumps(out), flush=True)
 
@@ -454,6 +465,8 @@ def main():
                          "(pad (r - 1) // 2)")
     ap.add_argument("--no-fuse", action="store_true",
                     help="keep an F(4^3) forward in two stages (input transform to V, then the product)")
+    ap.add_argument("--no-fuse-pool", action="store_true",
+                    help="with --config 5: run every max-pool as its own kernel (not in the fused forward)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="only run a 1 GiB device copy (for HBM counter scaling)")
     ap.add_argument("--fig4", type=int, default=0, metavar="BATCH",

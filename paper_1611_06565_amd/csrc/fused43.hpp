@@ -62,6 +62,11 @@ struct FusedArgs {
   // blocks, each split into nkb units of one kernel block, so that the last
   // round is short.  Surplus units exit at once.
   int32_t xb0[8], xn[8], xs[8];
+  // Max-pool of the activated outputs (POOL > 0): window = stride (1, 2, 2)
+  // (POOL 1) or (2, 2, 2) (POOL 2), floor rounding: y is [n][K][Yp] with
+  // Yp_i = Y_i / window_i, and ystride_p = prod Yp_i.
+  int32_t Yp[3];
+  int64_t ystride_p;
 };
 
 struct Fused43Geom {
@@ -84,7 +89,7 @@ __device__ __forceinline__ int p_index(int i0, int j, int ch, int tl) {
   return ((i0 * Fused43Geom::PL + j) * (Fused43Geom::CH / 2) + (ch >> 1)) * 32 + tl * 2 + (ch & 1);
 }
 
-template <bool CONST, bool KLOOP>
+template <bool CONST, bool KLOOP, int POOL = 0>
 __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x, const float* __restrict__ U,
                                                     float* __restrict__ y, FusedArgs a, FMats fm) {
   using G = Fused43Geom;
@@ -373,41 +378,98 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   }
   __syncthreads();
 
-  // Part 2: item (o0, kernel, tile), tiles fastest, reads the 36 values of
-  // its plane, applies A^T along the last two axes and stores 4 x 4 outputs,
-  // each row of 4 as one 16-byte store when every row of the output is a
-  // whole number of aligned tiles (a.vec_store)
-  constexpr int ITEMS = MM * BLK * BLK;
-  for (int i = int(threadIdx.x); i < ITEMS; i += G::NT) {
-    const int tl2 = i % BLK, kl = (i / BLK) % BLK, o0 = i / (BLK * BLK);
-    const int t2 = tb * BLK + tl2;
-    const int kg = kbx * BLK + kl;
-    if (t2 >= a.T || kg >= a.K) continue;
-    int ti[3] = {0, 0, 0};
-    const int n = split_tile<N>(t2, a.tiles, ti);
-    const int y0 = ti[0] * MM + o0;
-    if (y0 >= a.Y[0]) continue;
-    float v[PL], out[MM * MM];
+  if constexpr (POOL == 0) {
+    // Part 2: item (o0, kernel, tile), tiles fastest, reads the 36 values of
+    // its plane, applies A^T along the last two axes and stores 4 x 4 outputs,
+    // each row of 4 as one 16-byte store when every row of the output is a
+    // whole number of aligned tiles (a.vec_store)
+    constexpr int ITEMS = MM * BLK * BLK;
+    for (int i = int(threadIdx.x); i < ITEMS; i += G::NT) {
+      const int tl2 = i % BLK, kl = (i / BLK) % BLK, o0 = i / (BLK * BLK);
+      const int t2 = tb * BLK + tl2;
+      const int kg = kbx * BLK + kl;
+      if (t2 >= a.T || kg >= a.K) continue;
+      int ti[3] = {0, 0, 0};
+      const int n = split_tile<N>(t2, a.tiles, ti);
+      const int y0 = ti[0] * MM + o0;
+      if (y0 >= a.Y[0]) continue;
+      float v[PL], out[MM * MM];
+  #pragma unroll
+      for (int j = 0; j < PL; ++j) v[j] = sm[(j * MM + o0) * G::EPL + kl * BLK + (tl2 ^ kl)];
+      transform_nd<2, A, MM>(v, out, AT);
+      const float bk = a.bias != nullptr ? bsm[kl] : 0.0f;
+  #pragma unroll
+      for (int q2 = 0; q2 < MM * MM; ++q2) out[q2] = activate(out[q2] + bk, a.act, a.slope);
+      float* yk = y + (int64_t(n) * a.K + kg) * a.ystride_k + int64_t(y0) * a.Y[1] * a.Y[2];
+      const int y2 = ti[2] * MM;
+  #pragma unroll
+      for (int o1 = 0; o1 < MM; ++o1) {
+        const int y1 = ti[1] * MM + o1;
+        if (y1 >= a.Y[1]) continue;
+        float* row = yk + int64_t(y1) * a.Y[2] + y2;
+        if (a.vec_store) {
+          const f32x4 v4 = {out[o1 * MM], out[o1 * MM + 1], out[o1 * MM + 2], out[o1 * MM + 3]};
+          __builtin_nontemporal_store(v4, reinterpret_cast<f32x4*>(row));
+        } else {
+  #pragma unroll
+          for (int o2 = 0; o2 < MM; ++o2)
+            if (y2 + o2 < a.Y[2]) row[o2] = out[o1 * MM + o2];
+        }
+      }
+    }
+  } else {
+    // Part 2 with the max-pool: item (o0 group, kernel, tile) reads the 36
+    // values of each plane of its group (one o0 for window (1, 2, 2), the
+    // pair 2h, 2h + 1 for (2, 2, 2)), applies A^T along the last two axes,
+    // bias and activation, and stores the maximum over each window of the
+    // tile (a tile of 4 holds whole windows of 2 along every axis).  The
+    // window is scanned first axis slowest with a strict comparison from
+    // -inf, as the stand-alone max-pool does, so both give the same bits.
+    constexpr int P0 = POOL == 2 ? 2 : 1;       // window along the first axis
+    constexpr int NG0 = MM / P0;                // o0 groups per tile
+    constexpr int ITEMS = NG0 * BLK * BLK;
+    for (int i = int(threadIdx.x); i < ITEMS; i += G::NT) {
+      const int tl2 = i % BLK, kl = (i / BLK) % BLK, h0 = i / (BLK * BLK);
+      const int t2 = tb * BLK + tl2;
+      const int kg = kbx * BLK + kl;
+      if (t2 >= a.T || kg >= a.K) continue;
+      int ti[3] = {0, 0, 0};
+      const int n = split_tile<N>(t2, a.tiles, ti);
+      const int p0 = ti[0] * NG0 + h0;          // pooled index along the first axis
+      if (p0 >= a.Yp[0]) continue;
+      const float bk = a.bias != nullptr ? bsm[kl] : 0.0f;
+      float out[P0][MM * MM];
 #pragma unroll
-    for (int j = 0; j < PL; ++j) v[j] = sm[(j * MM + o0) * G::EPL + kl * BLK + (tl2 ^ kl)];
-    transform_nd<2, A, MM>(v, out, AT);
-    const float bk = a.bias != nullptr ? bsm[kl] : 0.0f;
+      for (int g0 = 0; g0 < P0; ++g0) {
+        const int o0 = h0 * P0 + g0;
+        float v[PL];
 #pragma unroll
-    for (int q2 = 0; q2 < MM * MM; ++q2) out[q2] = activate(out[q2] + bk, a.act, a.slope);
-    float* yk = y + (int64_t(n) * a.K + kg) * a.ystride_k + int64_t(y0) * a.Y[1] * a.Y[2];
-    const int y2 = ti[2] * MM;
+        for (int j = 0; j < PL; ++j) v[j] = sm[(j * MM + o0) * G::EPL + kl * BLK + (tl2 ^ kl)];
+        transform_nd<2, A, MM>(v, out[g0], AT);
 #pragma unroll
-    for (int o1 = 0; o1 < MM; ++o1) {
-      const int y1 = ti[1] * MM + o1;
-      if (y1 >= a.Y[1]) continue;
-      float* row = yk + int64_t(y1) * a.Y[2] + y2;
-      if (a.vec_store) {
-        const f32x4 v4 = {out[o1 * MM], out[o1 * MM + 1], out[o1 * MM + 2], out[o1 * MM + 3]};
-        __builtin_nontemporal_store(v4, reinterpret_cast<f32x4*>(row));
-      } else {
+        for (int q2 = 0; q2 < MM * MM; ++q2) out[g0][q2] = activate(out[g0][q2] + bk, a.act, a.slope);
+      }
+      float* yk = y + (int64_t(n) * a.K + kg) * a.ystride_p + int64_t(p0) * a.Yp[1] * a.Yp[2];
 #pragma unroll
-        for (int o2 = 0; o2 < MM; ++o2)
-          if (y2 + o2 < a.Y[2]) row[o2] = out[o1 * MM + o2];
+      for (int w1 = 0; w1 < MM / 2; ++w1) {
+        const int p1 = ti[1] * (MM / 2) + w1;
+        if (p1 >= a.Yp[1]) continue;
+#pragma unroll
+        for (int w2 = 0; w2 < MM / 2; ++w2) {
+          const int p2 = ti[2] * (MM / 2) + w2;
+          if (p2 >= a.Yp[2]) continue;
+          float best = -__builtin_inff();
+#pragma unroll
+          for (int g0 = 0; g0 < P0; ++g0)
+#pragma unroll
+            for (int i1 = 0; i1 < 2; ++i1)
+#pragma unroll
+              for (int i2 = 0; i2 < 2; ++i2) {
+                const float vv = out[g0][(2 * w1 + i1) * MM + 2 * w2 + i2];
+                best = vv > best ? vv : best;
+              }
+          yk[int64_t(p1) * a.Yp[2] + p2] = best;
+        }
       }
     }
   }

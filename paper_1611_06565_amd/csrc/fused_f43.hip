@@ -8,8 +8,24 @@
 
 namespace wino {
 
+namespace {
+
+template <int POOL>
+void launch_pool(bool kloop, bool const_mats, dim3 grid, const float* x, const float* U, float* y,
+                 const FusedArgs& a, const FMats& fm, hipStream_t s) {
+  const dim3 nt(Fused43Geom::NT);
+  if (kloop)
+    hipLaunchKernelGGL((k_fused43<true, true, POOL>), grid, nt, 0, s, x, U, y, a, fm);
+  else if (const_mats)
+    hipLaunchKernelGGL((k_fused43<true, false, POOL>), grid, nt, 0, s, x, U, y, a, fm);
+  else
+    hipLaunchKernelGGL((k_fused43<false, false, POOL>), grid, nt, 0, s, x, U, y, a, fm);
+}
+
+}  // namespace
+
 wino_status launch_fused43(const wino_plan_s& p, bool const_mats, const float* x, const float* U,
-                           const float* bias, float* y, hipStream_t s) {
+                           const float* bias, float* y, hipStream_t s, int pool) {
   FusedArgs a{};
   a.xstride_c = p.X[0] * p.X[1] * p.X[2];
   a.uplane = int64_t(p.C_pad) * p.K_pad;
@@ -51,13 +67,15 @@ wino_status launch_fused43(const wino_plan_s& p, bool const_mats, const float* x
   a.act = act_kind(p);
   a.slope = p.slope;
   a.bias = bias;
-  const dim3 nt(Fused43Geom::NT);
-  if (kloop)
-    hipLaunchKernelGGL((k_fused43<true, true>), dim3(grid), nt, 0, s, x, U, y, a, p.fm);
-  else if (const_mats)
-    hipLaunchKernelGGL((k_fused43<true, false>), dim3(grid), nt, 0, s, x, U, y, a, p.fm);
-  else
-    hipLaunchKernelGGL((k_fused43<false, false>), dim3(grid), nt, 0, s, x, U, y, a, p.fm);
+  // the max-pool's output extents (floor rounding) and per-kernel stride
+  const int w0 = pool == 2 ? 2 : 1, w12 = pool > 0 ? 2 : 1;
+  a.Yp[0] = int32_t(p.Y[0] / w0);
+  a.Yp[1] = int32_t(p.Y[1] / w12);
+  a.Yp[2] = int32_t(p.Y[2] / w12);
+  a.ystride_p = int64_t(a.Yp[0]) * a.Yp[1] * a.Yp[2];
+  if (pool == 1) launch_pool<1>(kloop, const_mats, dim3(grid), x, U, y, a, p.fm, s);
+  else if (pool == 2) launch_pool<2>(kloop, const_mats, dim3(grid), x, U, y, a, p.fm, s);
+  else launch_pool<0>(kloop, const_mats, dim3(grid), x, U, y, a, p.fm, s);
   return launch_status();
 }
 

@@ -28,8 +28,9 @@ inline int32_t act_kind(const wino_plan_s& p) {
 
 // k_fused43 (F(4^3) with the input transform inside the product), defined in
 // fused_f43.hip.
+// pool: 0 none, 1 max-pool window (1, 2, 2), 2 window (2, 2, 2) (y pooled).
 wino_status launch_fused43(const wino_plan_s& p, bool const_mats, const float* x, const float* U,
-                           const float* bias, float* y, hipStream_t s);
+                           const float* bias, float* y, hipStream_t s, int pool = 0);
 
 // The launches of one size, as plain function pointers.
 struct SizeOps {

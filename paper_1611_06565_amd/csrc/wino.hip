@@ -172,6 +172,24 @@ wino_status wino_forward_noalloc(const wino_plan_t* p, const float* x, const flo
   return wino_forward_ex(p, x, U, bias, y, ws, WINO_NOALLOC_SCRATCH_BYTES, stream);
 }
 
+wino_status wino_forward_pool(const wino_plan_t* p, const float* x, const float* U, const float* bias,
+                              const int32_t* window, float* y, void* stream) {
+  if (p == nullptr || x == nullptr || U == nullptr || y == nullptr || window == nullptr) return WINO_EINVAL;
+  if (!aligned16(x) || !aligned16(U) || !aligned16(y)) return WINO_EINVAL;
+  if (bias != nullptr && (reinterpret_cast<uintptr_t>(bias) & 3u) != 0) return WINO_EINVAL;
+  for (int i = 0; i < 3; ++i)
+    if (window[i] < 1) return WINO_EINVAL;
+  int pool = 0;
+  if (window[0] == 1 && window[1] == 2 && window[2] == 2) pool = 1;
+  else if (window[0] == 2 && window[1] == 2 && window[2] == 2) pool = 2;
+  else return WINO_EUNSUPPORTED;
+  // the max-pool rides on the fused F(4^3) forward's epilogue only
+  if (p->N != 3 || !p->fused) return WINO_EUNSUPPORTED;
+  for (int i = 0; i < 3; ++i)
+    if (p->Y[i] / window[i] < 1) return WINO_EINVAL;
+  return launch_fused43(*p, p->const_mats, x, U, bias, y, static_cast<hipStream_t>(stream), pool);
+}
+
 wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const float* x, float* y,
                            void* stream) {
   if (dims == nullptr || window == nullptr || x == nullptr || y == nullptr) return WINO_EINVAL;
