@@ -296,13 +296,13 @@ def bench_stack(args):
             Y = spec.out_spatial
             py = torch.empty((spec.batch, spec.K) + tuple(yy // p for yy, p in zip(Y, pool.window)),
                              dtype=torch.float32, device="cuda")
-        # the pool rides on the fused F(4^3) forward's epilogue (wino_forward_pool)
-        fpool = (pool is not None and not args.no_fuse_pool and plan.desc["fused"] == 1
+        # the pool rides on the F(4^3) product's epilogue (wino_forward_pool)
+        fpool = (pool is not None and not args.no_fuse_pool and tuple(plan.desc["tile"]) == (4, 4, 4)
                  and tuple(pool.window) in ((1, 2, 2), (2, 2, 2)))
         layers.append((spec, pool, plan, U, wsp, y, py, fpool))
     torch.cuda.synchronize()
     fused_pools = [L[0].name for L in layers if L[7]]
-    pool_note = ("; max-pool in the fused forward's epilogue on " + ",".join(fused_pools)) if fused_pools else ""
+    pool_note = ("; max-pool in the product's epilogue on " + ",".join(fused_pools)) if fused_pools else ""
 
     def step(ev=None):
         cur = x0
@@ -310,7 +310,7 @@ def bench_stack(args):
             if ev is not None:
                 ev[i].record()
             if fpool:
-                plan.forward_pool(cur, U, pool.window, y=py)
+                plan.forward_pool(cur, U, pool.window, y=py, workspace=wsp)
                 cur = py
                 continue
             plan.forward(cur, U, y=y, workspace=wsp)
@@ -466,7 +466,7 @@ def main():
     ap.add_argument("--no-fuse", action="store_true",
                     help="keep an F(4^3) forward in two stages (input transform to V, then the product)")
     ap.add_argument("--no-fuse-pool", action="store_true",
-                    help="with --config 5: run every max-pool as its own kernel (not in the fused forward)")
+                    help="with --config 5: run every max-pool as its own kernel (not in the F(4^3) product's epilogue)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="only run a 1 GiB device copy (for HBM counter scaling)")
     ap.add_argument("--fig4", type=int, default=0, metavar="BATCH",

@@ -313,22 +313,27 @@ wino_status wino_forward_noalloc(const wino_plan_t* plan, const float* x, const 
 wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const float* x, float* y,
                            void* stream);
 
-/* wino_forward_ex followed by wino_maxpool3d in one pass: the fused F(4^3)
- * forward (wino_plan_info.fused = 1) takes the maximum over each pooling
- * window of the activated outputs in its epilogue, so only the pooled
- * outputs reach memory.  eq. (2)'s f (the plan's activation) is applied
- * before the maximum, as a pooling layer after the convolution does; the
- * result has the same bits as wino_forward_ex then wino_maxpool3d.
- *   window  host, [3] int32: (1, 2, 2) or (2, 2, 2), window = stride, floor
- *           rounding
- *   y       device, [batch][K][Y_1/w_1][Y_2/w_2][Y_3/w_3] float32, 16-byte
- *           aligned (Y of wino_output_dims)
- *   bias    as for wino_forward_ex; no workspace (the fused forward has none)
+/* wino_forward_ex followed by wino_maxpool3d, with the pooling inside the
+ * product's epilogue, so only the pooled outputs reach memory: F(4^3)
+ * plans, fused (wino_plan_info.fused = 1, no workspace) or in two stages
+ * (the input transform to the workspace, then the product).  eq. (2)'s f
+ * (the plan's activation) is applied before the maximum, as a pooling layer
+ * after the convolution does; the result has the same bits as
+ * wino_forward_ex then wino_maxpool3d.
+ *   window     host, [3] int32: (1, 2, 2) or (2, 2, 2), window = stride,
+ *              floor rounding
+ *   y          device, [batch][K][Y_1/w_1][Y_2/w_2][Y_3/w_3] float32,
+ *              16-byte aligned (Y of wino_output_dims)
+ *   bias       as for wino_forward_ex
+ *   workspace  as for wino_forward_ex: wino_forward_workspace_bytes(plan)
+ *              bytes (0 and NULL for a fused plan)
  * Errors: WINO_EINVAL for null or misaligned pointers, a window entry below
- * 1 or a pooled extent of 0; WINO_EUNSUPPORTED for other windows and for
- * plans whose forward is not fused (pool those with wino_maxpool3d). */
+ * 1 or a pooled extent of 0; WINO_EWORKSPACE for a short workspace;
+ * WINO_EUNSUPPORTED for other windows and for other sizes (pool those with
+ * wino_maxpool3d). */
 wino_status wino_forward_pool(const wino_plan_t* plan, const float* x, const float* U, const float* bias,
-                              const int32_t* window, float* y, void* stream);
+                              const int32_t* window, float* y, void* workspace, size_t workspace_bytes,
+                              void* stream);
 
 /* Accuracy of a point set (§2.2, §3.3: the points trade fp32 accuracy).
  * wino_points_error_growth: kappa = kappa_1^N, where kappa_1 is the largest

@@ -64,6 +64,10 @@ struct GemmArgs {
   int32_t act;        // activation f of eq. (2): 0 none, 1 ReLU, 2 leaky ReLU
   float slope;        // leaky ReLU: f(v) = slope * v for v <= 0
   const float* bias;  // [K] or null: b_k of eq. (2), added before the activation
+  // max-pool in the epilogue (k_gemm_inv with POOL > 0): pooled extents
+  // Y_i / window_i and their product
+  int32_t Yp[3];
+  int64_t ystride_p;
 };
 
 // Tile t (linear over batch and the tile grid, last axis fastest) -> sample
@@ -585,6 +589,11 @@ struct GemmGeom {
   static_assert(LOC >= 1 && LOC < N, "at least one axis is reduced in registers, one across waves");
 };
 
+// Value of the neighbouring lane of the pair (lanes 2i and 2i + 1 swap).
+__device__ __forceinline__ float dpp_swap_pair(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0xb1, 0xf, 0xf, false));
+}
+
 struct EpiArgs {
   float* y;
   int32_t K;
@@ -593,6 +602,8 @@ struct EpiArgs {
   int32_t act;
   float slope;
   const float* bias;  // [K] or null
+  int32_t Yp[3];      // POOL > 0: pooled extents, y is [n][K][Yp]
+  int64_t ystride_p;  // prod Yp_i
 };
 
 // Inverse transform of a work-group's accumulators (eq. 4), stitched into y.
@@ -605,7 +616,8 @@ struct EpiArgs {
 // Part 2: A^T along the N-LOC leading axes, ReLU, crop, store.  Item
 // (o_loc, k, t) runs with the last-axis output fastest, then the tile, so
 // neighbouring lanes write neighbouring outputs of a row.
-template <int N, int MM, int R, bool CONST, int BLK, int NW, int LOC, bool BIAS, class AccT, class TileFn>
+template <int N, int MM, int R, bool CONST, int BLK, int NW, int LOC, bool BIAS, int POOL = 0, class AccT,
+          class TileFn>
 __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb, const EpiArgs& g,
                                               const FMats& fm, TileFn tile_of) {
   using S = MfmaShape<BLK>;
@@ -686,30 +698,77 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
     for (int uu = 0; uu < NUNIT; ++uu) v[uu] = sm[(uu * OLOC + jj) * PL + k_l * BLK + (tl ^ k_l)];
     float out[OLEAD];
     transform_nd<LEAD, A, MM>(v, out, AT);
-    float* yk = g.y + (int64_t(n) * g.K + kg) * g.ystride_k;
-    if constexpr (BIAS) {
-      const float bk = bsm[k_l];
+    if constexpr (POOL == 0) {
+      float* yk = g.y + (int64_t(n) * g.K + kg) * g.ystride_k;
+      if constexpr (BIAS) {
+        const float bk = bsm[k_l];
 #pragma unroll
-      for (int q = 0; q < OLEAD; ++q) out[q] += bk;
-    }
-#pragma unroll
-    for (int q = 0; q < OLEAD; ++q) {
-      int rem = q;
-      bool in = true;
-#pragma unroll
-      for (int ax = LEAD - 1; ax >= 0; --ax) {
-        const int oa = rem % MM;
-        rem /= MM;
-        yc[ax] = ti[ax] * MM + oa;
-        in = in && yc[ax] < g.Y[ax];
+        for (int q = 0; q < OLEAD; ++q) out[q] += bk;
       }
-      if (!in) continue;
-      int64_t off = yc[0];
 #pragma unroll
-      for (int ax = 1; ax < N; ++ax) off = off * g.Y[ax] + yc[ax];
-      float val = out[q];
-      val = activate(val, g.act, g.slope);
-      yk[off] = val;
+      for (int q = 0; q < OLEAD; ++q) {
+        int rem = q;
+        bool in = true;
+#pragma unroll
+        for (int ax = LEAD - 1; ax >= 0; --ax) {
+          const int oa = rem % MM;
+          rem /= MM;
+          yc[ax] = ti[ax] * MM + oa;
+          in = in && yc[ax] < g.Y[ax];
+        }
+        if (!in) continue;
+        int64_t off = yc[0];
+#pragma unroll
+        for (int ax = 1; ax < N; ++ax) off = off * g.Y[ax] + yc[ax];
+        float val = out[q];
+        val = activate(val, g.act, g.slope);
+        yk[off] = val;
+      }
+    } else {
+      // Max-pool with window (1, 2, 2) (POOL 1) or (2, 2, 2) (POOL 2), floor
+      // rounding, after the activation.  Neighbouring lanes hold the last-axis
+      // outputs 2w and 2w + 1 of the same (tile, kernel): the even lane takes
+      // its partner's values by a DPP swap and scans each window first axis
+      // slowest, last axis fastest, with a strict comparison from -inf, as
+      // the stand-alone max-pool does (same bits).  A pooled output whose
+      // window reaches past Y is dropped, so the even lane only reads a
+      // partner that is live.
+      static_assert(N == 3 && LOC == 1 && MM == 4, "pooling: F(4^3), last axis reduced in registers");
+      constexpr int W0 = POOL == 2 ? 2 : 1;
+      if constexpr (BIAS) {
+        const float bk = bsm[k_l];
+#pragma unroll
+        for (int q = 0; q < OLEAD; ++q) out[q] += bk;
+      }
+#pragma unroll
+      for (int q = 0; q < OLEAD; ++q) out[q] = activate(out[q], g.act, g.slope);
+      float other[OLEAD];
+#pragma unroll
+      for (int q = 0; q < OLEAD; ++q) other[q] = dpp_swap_pair(out[q]);
+      const int p2 = y_last >> 1;
+      if ((o_last & 1) == 0 && p2 < g.Yp[2]) {
+        float* yk = g.y + (int64_t(n) * g.K + kg) * g.ystride_p + p2;
+#pragma unroll
+        for (int g0 = 0; g0 < MM / W0; ++g0) {
+          const int p0 = ti[0] * (MM / W0) + g0;
+          if (p0 >= g.Yp[0]) continue;
+#pragma unroll
+          for (int w1 = 0; w1 < MM / 2; ++w1) {
+            const int p1 = ti[1] * (MM / 2) + w1;
+            if (p1 >= g.Yp[1]) continue;
+            float best = -__builtin_inff();
+#pragma unroll
+            for (int i0 = 0; i0 < W0; ++i0)
+#pragma unroll
+              for (int i1 = 0; i1 < 2; ++i1) {
+                const int q = (g0 * W0 + i0) * MM + 2 * w1 + i1;
+                best = out[q] > best ? out[q] : best;
+                best = other[q] > best ? other[q] : best;
+              }
+            yk[(int64_t(p0) * g.Yp[1] + p1) * g.Yp[2]] = best;
+          }
+        }
+      }
     }
   }
 }
@@ -717,7 +776,7 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
 // VEC = floats per operand load (one load feeds VEC MFMA k-steps).  DEPTH =
 // stages in the register ring (DEPTH-1 stages in flight while one is
 // consumed).
-template <int N, int MM, int R, bool CONST, int BLK, int NW, int LOC, int VEC, int DEPTH>
+template <int N, int MM, int R, bool CONST, int BLK, int NW, int LOC, int VEC, int DEPTH, int POOL = 0>
 __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ V,
                                                       const float* __restrict__ U,
                                                       float* __restrict__ y, GemmArgs g, FMats fm) {
@@ -802,14 +861,15 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
     }
   }
 
-  EpiArgs e{y, g.K, g.ystride_k, {g.Y[0], g.Y[1], g.Y[2]}, g.act, g.slope, g.bias};
+  EpiArgs e{y, g.K, g.ystride_k, {g.Y[0], g.Y[1], g.Y[2]}, g.act, g.slope, g.bias,
+            {g.Yp[0], g.Yp[1], g.Yp[2]}, g.ystride_p};
   auto tile_of = [&](int tl, int* ti) -> int {
     const int t = tb * BLK + tl;
     if (t >= g.T) return -1;
     return split_tile<N>(t, g.tiles, ti);
   };
-  if (g.bias != nullptr) gemm_epilogue<N, MM, R, CONST, BLK, NW, LOC, true>(acc, sm, kb, e, fm, tile_of);
-  else gemm_epilogue<N, MM, R, CONST, BLK, NW, LOC, false>(acc, sm, kb, e, fm, tile_of);
+  if (g.bias != nullptr) gemm_epilogue<N, MM, R, CONST, BLK, NW, LOC, true, POOL>(acc, sm, kb, e, fm, tile_of);
+  else gemm_epilogue<N, MM, R, CONST, BLK, NW, LOC, false, POOL>(acc, sm, kb, e, fm, tile_of);
 }
 
 // ------------------------------------------------------------ max-pool (a6)

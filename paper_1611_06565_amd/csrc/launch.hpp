@@ -42,6 +42,10 @@ struct SizeOps {
   // the forward with the input transform inside the product (null for sizes without one)
   wino_status (*fused)(const wino_plan_s&, const float* x, const float* U, const float* bias, float* y,
                        hipStream_t);
+  // the product with the max-pool in its epilogue (pool 1: window (1, 2, 2),
+  // 2: (2, 2, 2); y pooled), null for sizes without one
+  wino_status (*gemm_pool)(const wino_plan_s&, const float* V, const float* U, const float* bias, float* y,
+                           int pool, hipStream_t);
 };
 
 template <int N, int MM, int R, bool CONST>
@@ -187,21 +191,52 @@ struct Launch {
     } else {
       using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
       static_assert(Geo::NT <= 768, "the planner sizes k_gemm_inv grids for at most 768 threads");
-      GemmArgs g{};
-      g.uplane = int64_t(p.C_pad) * p.K_pad;
-      g.ystride_k = 1;
-      for (int i = 0; i < N; ++i) g.ystride_k *= p.Y[i];
-      g.T = int32_t(p.T); g.T_pad = int32_t(p.T_pad);
-      g.C_pad = p.C_pad; g.K = p.K; g.K_pad = p.K_pad;
-      g.nkb = p.gemm_nkb;
-      g.nblocks = int32_t(p.grid_gemm);
-      for (int i = 0; i < 3; ++i) { g.tiles[i] = int32_t(p.tiles[i]); g.Y[i] = int32_t(p.Y[i]); }
-      g.act = act_kind(p);
-      g.slope = p.slope;
-      g.bias = bias;
+      const GemmArgs g = gemm_args(p, bias, 0);
       hipLaunchKernelGGL((k_gemm_inv<N, MM, R, CONST, BLK, NW, LOC, VEC, DEPTH>), dim3(p.grid_gemm),
                          dim3(Geo::NT), 0, s, V, U, y, g, p.fm);
       return launch_status();
+    }
+  }
+
+  // Arguments of k_gemm_inv; pool > 0 adds the pooled extents (floor rounding).
+  static GemmArgs gemm_args(const wino_plan_s& p, const float* bias, int pool) {
+    GemmArgs g{};
+    g.uplane = int64_t(p.C_pad) * p.K_pad;
+    g.ystride_k = 1;
+    for (int i = 0; i < N; ++i) g.ystride_k *= p.Y[i];
+    g.T = int32_t(p.T); g.T_pad = int32_t(p.T_pad);
+    g.C_pad = p.C_pad; g.K = p.K; g.K_pad = p.K_pad;
+    g.nkb = p.gemm_nkb;
+    g.nblocks = int32_t(p.grid_gemm);
+    for (int i = 0; i < 3; ++i) { g.tiles[i] = int32_t(p.tiles[i]); g.Y[i] = int32_t(p.Y[i]); }
+    g.act = act_kind(p);
+    g.slope = p.slope;
+    g.bias = bias;
+    if (pool > 0) {
+      g.Yp[0] = int32_t(p.Y[0] / (pool == 2 ? 2 : 1));
+      g.Yp[1] = int32_t(p.Y[1] / 2);
+      g.Yp[2] = int32_t(p.Y[2] / 2);
+      g.ystride_p = int64_t(g.Yp[0]) * g.Yp[1] * g.Yp[2];
+    }
+    return g;
+  }
+
+  // F(4^3) two-stage product with the max-pool in its epilogue.
+  static wino_status gemm_pool(const wino_plan_s& p, const float* V, const float* U, const float* bias, float* y,
+                               int pool, hipStream_t s) {
+    constexpr int KIND = Blocking<N, MM, R>::KIND;
+    if constexpr (N == 3 && MM == 4 && R == 3 && KIND == 2 && LOC == 1) {
+      using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
+      const GemmArgs g = gemm_args(p, bias, pool);
+      if (pool == 1)
+        hipLaunchKernelGGL((k_gemm_inv<N, MM, R, CONST, BLK, NW, LOC, VEC, DEPTH, 1>), dim3(p.grid_gemm),
+                           dim3(Geo::NT), 0, s, V, U, y, g, p.fm);
+      else
+        hipLaunchKernelGGL((k_gemm_inv<N, MM, R, CONST, BLK, NW, LOC, VEC, DEPTH, 2>), dim3(p.grid_gemm),
+                           dim3(Geo::NT), 0, s, V, U, y, g, p.fm);
+      return launch_status();
+    } else {
+      return WINO_EUNSUPPORTED;
     }
   }
 };
@@ -211,7 +246,7 @@ template <int N, int MM, int R, bool CONST>
 constexpr SizeOps make_ops() {
   using L = Launch<N, MM, R, CONST>;
   if constexpr (N == 3 && MM == 4 && R == 3)
-    return SizeOps{&L::filter, &L::input, &L::gemm, &L::wgrad, &L::fused};
+    return SizeOps{&L::filter, &L::input, &L::gemm, &L::wgrad, &L::fused, &L::gemm_pool};
   else
     return SizeOps{&L::filter, &L::input, &L::gemm, &L::wgrad, nullptr};
 }

@@ -173,7 +173,7 @@ wino_status wino_forward_noalloc(const wino_plan_t* p, const float* x, const flo
 }
 
 wino_status wino_forward_pool(const wino_plan_t* p, const float* x, const float* U, const float* bias,
-                              const int32_t* window, float* y, void* stream) {
+                              const int32_t* window, float* y, void* ws, size_t ws_bytes, void* stream) {
   if (p == nullptr || x == nullptr || U == nullptr || y == nullptr || window == nullptr) return WINO_EINVAL;
   if (!aligned16(x) || !aligned16(U) || !aligned16(y)) return WINO_EINVAL;
   if (bias != nullptr && (reinterpret_cast<uintptr_t>(bias) & 3u) != 0) return WINO_EINVAL;
@@ -183,11 +183,23 @@ wino_status wino_forward_pool(const wino_plan_t* p, const float* x, const float*
   if (window[0] == 1 && window[1] == 2 && window[2] == 2) pool = 1;
   else if (window[0] == 2 && window[1] == 2 && window[2] == 2) pool = 2;
   else return WINO_EUNSUPPORTED;
-  // the max-pool rides on the fused F(4^3) forward's epilogue only
-  if (p->N != 3 || !p->fused) return WINO_EUNSUPPORTED;
+  if (p->N != 3) return WINO_EUNSUPPORTED;
+  const SizeOps* ops = ops_of(*p);
+  if (ops == nullptr) return WINO_EUNSUPPORTED;
+  // the max-pool rides on the F(4^3) forward's epilogue (fused, or the
+  // two-stage product)
+  if (p->fused ? ops->fused == nullptr : ops->gemm_pool == nullptr) return WINO_EUNSUPPORTED;
   for (int i = 0; i < 3; ++i)
     if (p->Y[i] / window[i] < 1) return WINO_EINVAL;
-  return launch_fused43(*p, p->const_mats, x, U, bias, y, static_cast<hipStream_t>(stream), pool);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (p->fused) return launch_fused43(*p, p->const_mats, x, U, bias, y, s, pool);
+  if (ws == nullptr) return WINO_EINVAL;
+  if (!aligned16(ws)) return WINO_EINVAL;
+  if (ws_bytes < wino_workspace_bytes(p)) return WINO_EWORKSPACE;
+  float* V = static_cast<float*>(ws);
+  const wino_status st = ops->input(*p, x, V, s);
+  if (st != WINO_OK) return st;
+  return ops->gemm_pool(*p, V, U, bias, y, pool, s);
 }
 
 wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const float* x, float* y,

@@ -88,7 +88,7 @@ def lib():
         "wino_forward_ex": (i32, [vp, vp, vp, vp, vp, vp, sz, vp]),
         "wino_forward_noalloc": (i32, [vp, vp, vp, vp, vp, vp]),
         "wino_maxpool3d": (i32, [P_i64, ctypes.POINTER(i32), vp, vp, vp]),
-        "wino_forward_pool": (i32, [vp, vp, vp, vp, ctypes.POINTER(i32), vp, vp]),
+        "wino_forward_pool": (i32, [vp, vp, vp, vp, ctypes.POINTER(i32), vp, vp, sz, vp]),
         "wino_status_string": (ctypes.c_char_p, [i32]),
         "wino_points_error_growth": (i32, [i32, i32, i32, P_dbl, i32, P_dbl]),
         "wino_search_points": (i32, [i32, i32, i32, P_dbl, P_dbl]),
@@ -377,20 +377,25 @@ class Plan:
         return tuple(self.output_shape[:2]) + tuple(int(yi) // int(w) for yi, w in
                                                     zip(self.output_shape[2:], window))
 
-    def forward_pool(self, x, U, window, y=None, bias=None):
-        """wino_forward_pool: the forward with the max-pool (window = stride,
-        (1, 2, 2) or (2, 2, 2)) in the fused F(4^3) epilogue; y is the pooled
-        output.  Plans whose forward is not fused raise WinoError."""
+    def forward_pool(self, x, U, window, y=None, workspace=None, bias=None):
+        """wino_forward_pool: the F(4^3) forward with the max-pool (window =
+        stride, (1, 2, 2) or (2, 2, 2)) in the product's epilogue; y is the
+        pooled output.  Other sizes raise WinoError."""
         import torch
         self._check_shape(x, self.input_shape, "x")
         shape = self.pooled_shape(window)
         if y is None:
             y = torch.empty(shape, dtype=torch.float32, device="cuda")
         self._check_shape(y, shape, "y")
+        need = self.forward_workspace_bytes
+        if workspace is None and need:
+            workspace = torch.empty(need // 4, dtype=torch.float32, device="cuda")
+        ws_ptr = _dev_ptr(workspace, "workspace") if workspace is not None else ctypes.c_void_p()
+        ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
         win = (ctypes.c_int32 * 3)(*[int(w) for w in window])
         _check(self._L.wino_forward_pool(self._h, _dev_ptr(x, "x", torch.float32),
                                          _dev_ptr(U, "U", torch.float32), self._bias_ptr(bias), win,
-                                         _dev_ptr(y, "y", torch.float32), _stream()),
+                                         _dev_ptr(y, "y", torch.float32), ws_ptr, ws_len, _stream()),
                "wino_forward_pool")
         return y
 

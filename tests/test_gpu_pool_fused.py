@@ -1,6 +1,6 @@
-"""GPU tests of wino_forward_pool: the fused F(4^3) forward with the C3D
-stack's max-pool (windows (1, 2, 2) and (2, 2, 2), window = stride, floor
-rounding) in its epilogue.
+"""GPU tests of wino_forward_pool: the F(4^3) forward, fused or in two
+stages, with the C3D stack's max-pool (windows (1, 2, 2) and (2, 2, 2),
+window = stride, floor rounding) in the product's epilogue.
 
 The pooled output must have the same bits as the forward followed by the
 stand-alone max-pool (both scan each window in the same order), and match
@@ -34,17 +34,28 @@ CASES = [
     (LayerSpec("pool_c12_k16_noact", N=3, m=4, r=3, batch=1, C=12, K=16, X=(6, 8, 64), pad=2,
                x_dist="normal", w_dist="normal"), (2, 2, 2)),
 ]
+# the two-stage product (k_gemm_inv): K > 64, or the fused form switched off
+TWO_STAGE = [
+    (LayerSpec("pool2s_c24_k80", N=3, m=4, r=3, batch=1, C=24, K=80, X=(8, 11, 9), pad=1,
+               x_dist="relu_normal", w_dist="he", relu=True), (1, 2, 2)),
+    (LayerSpec("pool2s_c64_k128", N=3, m=4, r=3, batch=2, C=64, K=128, X=(8, 12, 16), pad=1,
+               x_dist="relu_normal", w_dist="he", relu=True), (2, 2, 2)),
+    (LayerSpec("pool2s_c17_k20_leaky", N=3, m=4, r=3, batch=1, C=17, K=20, X=(9, 10, 11), pad=1,
+               x_dist="normal", w_dist="he", leaky=0.125), (2, 2, 2)),
+    (LayerSpec("pool2s_c5_k16_noact", N=3, m=4, r=3, batch=1, C=5, K=16, X=(7, 9, 13), pad=0,
+               x_dist="normal", w_dist="normal"), (1, 2, 2)),
+]
 
 
-def _run(spec, window, seed, bias=True):
+def _run(spec, window, seed, bias=True, fuse=True):
     torch = require_gpu()
     from paper_1611_06565_amd.wino import Plan, maxpool3d
     log(f"[gpu] {spec.name} window={window} C={spec.C} K={spec.K} X={spec.X} pad={spec.pad}")
     x, w = draw_layer(spec, seed=seed)
     b = (0.25 * np.random.default_rng(seed + 1).standard_normal(spec.K)).astype(np.float32) if bias else None
     plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X), pad=spec.pad,
-                relu=spec.relu, leaky=spec.leaky)
-    assert plan.desc["fused"] == 1
+                relu=spec.relu, leaky=spec.leaky, fuse=fuse)
+    assert plan.desc["fused"] == (1 if fuse and spec.K <= 64 else 0)
     xd = torch.from_numpy(x).cuda()
     U = plan.transform_filter(torch.from_numpy(w).cuda())
     bd = torch.from_numpy(b).cuda() if bias else None
@@ -61,9 +72,10 @@ def _run(spec, window, seed, bias=True):
     return x, w, b, yp.cpu().numpy(), y2.cpu().numpy()
 
 
-@pytest.mark.parametrize("spec,window", CASES, ids=[c[0].name for c in CASES])
-def test_forward_pool_matches_forward_then_pool_and_oracle(spec, window):
-    x, w, b, yp, y2 = _run(spec, window, seed=41)
+@pytest.mark.parametrize("spec,window,fuse", [c + (True,) for c in CASES] + [c + (False,) for c in TWO_STAGE],
+                         ids=[c[0].name for c in CASES] + [c[0].name for c in TWO_STAGE])
+def test_forward_pool_matches_forward_then_pool_and_oracle(spec, window, fuse):
+    x, w, b, yp, y2 = _run(spec, window, seed=41, fuse=fuse)
     assert yp.shape == y2.shape
     assert np.array_equal(yp.view(np.uint32), y2.view(np.uint32)), "fused pool differs from forward + pool"
     y_ref, den = direct_blas(x, w, spec.pad, relu=spec.relu, bias=b, leaky=spec.leaky)
@@ -87,11 +99,6 @@ def test_forward_pool_refusals():
     spec = CASES[0][0]
     x, w = draw_layer(spec, seed=43)
     xd = torch.from_numpy(x).cuda()
-    # a plan whose forward is not fused (two stages through V)
-    p2 = Plan(3, 4, 3, spec.C, spec.K, [spec.batch] + list(spec.X), pad=1, relu=True, fuse=False)
-    U2 = p2.transform_filter(torch.from_numpy(w).cuda())
-    with pytest.raises(WinoError):
-        p2.forward_pool(xd, U2, (1, 2, 2))
     # a window the epilogue does not take, and an invalid one
     p1 = Plan(3, 4, 3, spec.C, spec.K, [spec.batch] + list(spec.X), pad=1, relu=True)
     U1 = p1.transform_filter(torch.from_numpy(w).cuda())
@@ -99,7 +106,7 @@ def test_forward_pool_refusals():
         p1.forward_pool(xd, U1, (2, 1, 1))
     with pytest.raises(WinoError):
         p1.forward_pool(xd, U1, (1, 3, 3))
-    # F(2^3) has no fused forward
+    # F(2^3) takes the stand-alone pool
     p3 = Plan(3, 2, 3, spec.C, spec.K, [spec.batch] + list(spec.X), pad=1, relu=True)
     U3 = p3.transform_filter(torch.from_numpy(w).cuda())
     with pytest.raises(WinoError):
@@ -121,6 +128,28 @@ def test_forward_pool_full_size_conv1_bitwise():
     assert plan.desc["fused"] == 1
     xd = torch.from_numpy(x).cuda()
     U = plan.transform_filter(torch.from_numpy(ws[0]).cuda())
+    yp = plan.forward_pool(xd, U, pool.window)
+    y2 = maxpool3d(plan.forward(xd, U), pool.window)
+    torch.cuda.synchronize()
+    assert torch.equal(yp.view(torch.int32), y2.view(torch.int32))
+
+
+def test_forward_pool_full_size_conv2_two_stage_bitwise():
+    """conv2 of the C3D stack at full size (batch 4, C = 64, K = 128,
+    16 x 56 x 56, window (2, 2, 2), two-stage F(4^3)): the pooled product has
+    the bits of the forward followed by the stand-alone pool."""
+    torch = require_gpu()
+    from paper_1611_06565_amd.wino import Plan, maxpool3d
+    from workloads import C3D_STACK
+    spec, pool = list(C3D_STACK.layers())[1]
+    log(f"[gpu] full-size conv2 C={spec.C} K={spec.K} X={spec.X} window={pool.window}")
+    rng = np.random.default_rng(6)
+    x = np.maximum(rng.standard_normal((spec.batch, spec.C) + tuple(spec.X)), 0).astype(np.float32)
+    w = (rng.standard_normal((spec.K, spec.C, 3, 3, 3)) * np.sqrt(2.0 / (27 * spec.C))).astype(np.float32)
+    plan = Plan(3, 4, 3, spec.C, spec.K, [spec.batch] + list(spec.X), pad=1, relu=True)
+    assert plan.desc["fused"] == 0
+    xd = torch.from_numpy(x).cuda()
+    U = plan.transform_filter(torch.from_numpy(w).cuda())
     yp = plan.forward_pool(xd, U, pool.window)
     y2 = maxpool3d(plan.forward(xd, U), pool.window)
     torch.cuda.synchronize()
