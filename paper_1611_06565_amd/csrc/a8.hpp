@@ -262,63 +262,152 @@ __global__ void __launch_bounds__(1024) k_gemm_a8(const float* __restrict__ V, c
   const float* vbase = V + (int64_t(tb) * ncg + kr) * S::NXI * (BLK * CG) + col * CG;
   const float* ubase = U + (int64_t(kr) * g.K_pad + kb * BLK + col) * CG;
 
-  for (int xi0 = 0; xi0 < A; ++xi0) {
+  if constexpr (MM == 4 && CONST) {
+    // F(4^3, 5^3): the next step's operands load while this step multiplies
+    // and, at the end of a pass, while the pass's inverse transform runs
+    // (two operand buffers).  Measured against the plain loop below on one
+    // box: 961 -> 874 us; slower for m = 5 and m = 3, which keep the loop.
     typename F::acc_t acc[EW];
-#pragma unroll
-    for (int e = 0; e < EW; ++e) acc[e] = typename F::acc_t{};
-    const int xb = xi0 * PL + xi1 * A + half * EW;   // first element of the wave
-    for (int s = 0; s < nstage; ++s) {
-      float4 av[EW], uv[EW];
-#pragma unroll
-      for (int e = 0; e < EW; ++e) {
-        av[e] = *reinterpret_cast<const float4*>(vbase + (int64_t(s) * 4 * S::NXI + xb + e) * (BLK * CG));
-        uv[e] = *reinterpret_cast<const float4*>(ubase + (int64_t(xb + e) * g.uplane) + int64_t(s) * 4 * g.K_pad * CG);
-      }
-#pragma unroll
-      for (int e = 0; e < EW; ++e) {
-        acc[e] = F::mma(av[e].x, uv[e].x, acc[e]);
-        acc[e] = F::mma(av[e].y, uv[e].y, acc[e]);
-        acc[e] = F::mma(av[e].z, uv[e].z, acc[e]);
-        acc[e] = F::mma(av[e].w, uv[e].w, acc[e]);
-      }
-    }
-    // A^T along the last axis over this wave's half row: partial sums of the
-    // m outputs o2 (the other half row's wave adds the rest), to LDS plane
-    // (xi1, half, o2) at [kernel][tile ^ (kernel / 4)]
-#pragma unroll
-    for (int r = 0; r < F::NACC; ++r) {
-      const int t = F::acc_row(lane, r);
-#pragma unroll
-      for (int o2 = 0; o2 < MM; ++o2) {
-        float v = 0.0f;
-#pragma unroll
-        for (int e = 0; e < EW; ++e) v = __builtin_fmaf(AT(o2, half * EW + e), acc[e][r], v);
-        sm[((xi1 * 2 + half) * MM + o2) * EPL + col * BLK + (t ^ (col >> 2))] = v;
-      }
-    }
-    __syncthreads();
-    // A^T along the middle axis, then A^T[o0][xi0] into the outputs
-#pragma unroll
-    for (int q = 0; q < IPT; ++q) {
-      const int i = int(threadIdx.x) + S::NT * q;
-      if (i < S::ITEMS) {
-        const int tl = i % BLK, kl = (i / BLK) % BLK, o2 = i / (BLK * BLK);
-        float v[A], w1[MM];
-#pragma unroll
-        for (int x1 = 0; x1 < A; ++x1) {
-          const int base = kl * BLK + (tl ^ (kl >> 2));
-          v[x1] = sm[((x1 * 2 + 0) * MM + o2) * EPL + base] + sm[((x1 * 2 + 1) * MM + o2) * EPL + base];
-        }
-        apply_vec<A, MM>(AT, v, 1, w1, 1);
-#pragma unroll
-        for (int o0 = 0; o0 < MM; ++o0) {
-          const float c0 = AT(o0, xi0);
-#pragma unroll
-          for (int o1 = 0; o1 < MM; ++o1) out[q][o0 * MM + o1] = __builtin_fmaf(c0, w1[o1], out[q][o0 * MM + o1]);
+    // the end of pass xi0: A^T along the last axis over this wave's half row
+    // (partial sums of the m outputs o2; the other half row's wave adds the
+    // rest) to LDS plane (xi1, half, o2) at [kernel][tile ^ (kernel / 4)], then
+    // A^T along the middle axis and A^T[o0][xi0] into the outputs
+    auto pass_end = [&](int xi0) {
+  #pragma unroll
+      for (int r = 0; r < F::NACC; ++r) {
+        const int t = F::acc_row(lane, r);
+  #pragma unroll
+        for (int o2 = 0; o2 < MM; ++o2) {
+          float v = 0.0f;
+  #pragma unroll
+          for (int e = 0; e < EW; ++e) v = __builtin_fmaf(AT(o2, half * EW + e), acc[e][r], v);
+          sm[((xi1 * 2 + half) * MM + o2) * EPL + col * BLK + (t ^ (col >> 2))] = v;
         }
       }
+      __syncthreads();
+  #pragma unroll
+      for (int q = 0; q < IPT; ++q) {
+        const int i = int(threadIdx.x) + S::NT * q;
+        if (i < S::ITEMS) {
+          const int tl = i % BLK, kl = (i / BLK) % BLK, o2 = i / (BLK * BLK);
+          float v[A], w1[MM];
+  #pragma unroll
+          for (int x1 = 0; x1 < A; ++x1) {
+            const int base = kl * BLK + (tl ^ (kl >> 2));
+            v[x1] = sm[((x1 * 2 + 0) * MM + o2) * EPL + base] + sm[((x1 * 2 + 1) * MM + o2) * EPL + base];
+          }
+          apply_vec<A, MM>(AT, v, 1, w1, 1);
+  #pragma unroll
+          for (int o0 = 0; o0 < MM; ++o0) {
+            const float c0 = AT(o0, xi0);
+  #pragma unroll
+            for (int o1 = 0; o1 < MM; ++o1) out[q][o0 * MM + o1] = __builtin_fmaf(c0, w1[o1], out[q][o0 * MM + o1]);
+          }
+        }
+      }
+      __syncthreads();   // the planes are rewritten by the next pass
+    };
+    // operands of step gs = (pass xi0, channel stage s): 16 bytes of V row
+    // `col` and of U column `col` per element
+    float4 av[2][EW], uv[2][EW];
+    auto load = [&](auto B, int gs) {
+      constexpr int b = decltype(B)::value;
+      const int x0 = gs / nstage, st = gs % nstage;
+      const int xb = x0 * PL + xi1 * A + half * EW;   // first element of the wave
+  #pragma unroll
+      for (int e = 0; e < EW; ++e) {
+        av[b][e] = *reinterpret_cast<const float4*>(vbase + (int64_t(st) * 4 * S::NXI + xb + e) * (BLK * CG));
+        uv[b][e] = *reinterpret_cast<const float4*>(ubase + (int64_t(xb + e) * g.uplane) + int64_t(st) * 4 * g.K_pad * CG);
+      }
+    };
+    auto mma = [&](auto B) {
+      constexpr int b = decltype(B)::value;
+  #pragma unroll
+      for (int e = 0; e < EW; ++e) {
+        acc[e] = F::mma(av[b][e].x, uv[b][e].x, acc[e]);
+        acc[e] = F::mma(av[b][e].y, uv[b][e].y, acc[e]);
+        acc[e] = F::mma(av[b][e].z, uv[b][e].z, acc[e]);
+        acc[e] = F::mma(av[b][e].w, uv[b][e].w, acc[e]);
+      }
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    const int total = A * nstage;
+    auto step = [&](auto B, int gs) {
+      constexpr int b = decltype(B)::value;
+      if (gs % nstage == 0) {
+#pragma unroll
+        for (int e = 0; e < EW; ++e) acc[e] = typename F::acc_t{};
+      }
+      if (gs + 1 < total) load(std::integral_constant<int, b ^ 1>{}, gs + 1);
+      mma(B);
+      if (gs % nstage == nstage - 1) pass_end(gs / nstage);
+    };
+    load(I0{}, 0);
+    for (int gs = 0; gs < total; gs += 2) {
+      step(I0{}, gs);
+      if (gs + 1 < total) step(I1{}, gs + 1);
     }
-    __syncthreads();   // the planes are rewritten by the next pass
+  } else {
+    for (int xi0 = 0; xi0 < A; ++xi0) {
+      typename F::acc_t acc[EW];
+  #pragma unroll
+      for (int e = 0; e < EW; ++e) acc[e] = typename F::acc_t{};
+      const int xb = xi0 * PL + xi1 * A + half * EW;   // first element of the wave
+      for (int s = 0; s < nstage; ++s) {
+        float4 av[EW], uv[EW];
+  #pragma unroll
+        for (int e = 0; e < EW; ++e) {
+          av[e] = *reinterpret_cast<const float4*>(vbase + (int64_t(s) * 4 * S::NXI + xb + e) * (BLK * CG));
+          uv[e] = *reinterpret_cast<const float4*>(ubase + (int64_t(xb + e) * g.uplane) + int64_t(s) * 4 * g.K_pad * CG);
+        }
+  #pragma unroll
+        for (int e = 0; e < EW; ++e) {
+          acc[e] = F::mma(av[e].x, uv[e].x, acc[e]);
+          acc[e] = F::mma(av[e].y, uv[e].y, acc[e]);
+          acc[e] = F::mma(av[e].z, uv[e].z, acc[e]);
+          acc[e] = F::mma(av[e].w, uv[e].w, acc[e]);
+        }
+      }
+      // A^T along the last axis over this wave's half row: partial sums of the
+      // m outputs o2 (the other half row's wave adds the rest), to LDS plane
+      // (xi1, half, o2) at [kernel][tile ^ (kernel / 4)]
+  #pragma unroll
+      for (int r = 0; r < F::NACC; ++r) {
+        const int t = F::acc_row(lane, r);
+  #pragma unroll
+        for (int o2 = 0; o2 < MM; ++o2) {
+          float v = 0.0f;
+  #pragma unroll
+          for (int e = 0; e < EW; ++e) v = __builtin_fmaf(AT(o2, half * EW + e), acc[e][r], v);
+          sm[((xi1 * 2 + half) * MM + o2) * EPL + col * BLK + (t ^ (col >> 2))] = v;
+        }
+      }
+      __syncthreads();
+      // A^T along the middle axis, then A^T[o0][xi0] into the outputs
+  #pragma unroll
+      for (int q = 0; q < IPT; ++q) {
+        const int i = int(threadIdx.x) + S::NT * q;
+        if (i < S::ITEMS) {
+          const int tl = i % BLK, kl = (i / BLK) % BLK, o2 = i / (BLK * BLK);
+          float v[A], w1[MM];
+  #pragma unroll
+          for (int x1 = 0; x1 < A; ++x1) {
+            const int base = kl * BLK + (tl ^ (kl >> 2));
+            v[x1] = sm[((x1 * 2 + 0) * MM + o2) * EPL + base] + sm[((x1 * 2 + 1) * MM + o2) * EPL + base];
+          }
+          apply_vec<A, MM>(AT, v, 1, w1, 1);
+  #pragma unroll
+          for (int o0 = 0; o0 < MM; ++o0) {
+            const float c0 = AT(o0, xi0);
+  #pragma unroll
+            for (int o1 = 0; o1 < MM; ++o1) out[q][o0 * MM + o1] = __builtin_fmaf(c0, w1[o1], out[q][o0 * MM + o1]);
+          }
+        }
+      }
+      __syncthreads();   // the planes are rewritten by the next pass
+    }
+
   }
 
   // bias and activation, then through LDS into rows [kernel][o0][o1][tile][o2]
