@@ -134,8 +134,12 @@ __global__ void __launch_bounds__(256) k_input_a8(const float* __restrict__ x, f
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ncg = a.C_pad / CG;
-  const int hb = int(blockIdx.x) & 1;
-  const int tb = (int(blockIdx.x) >> 1) / ncg, cg = (int(blockIdx.x) >> 1) % ncg;
+  // logical block (channel group, tile block, half), halves and tile blocks
+  // fastest, in contiguous ranges per XCD: an XCD walks consecutive windows of
+  // one channel group, whose overlaps then hit its L2
+  const int L = xcd_remap(int(blockIdx.x), a.nblocks);
+  const int hb = L & 1;
+  const int tb = (L >> 1) % a.ntb, cg = (L >> 1) / a.ntb;
   const MatRef<Which::BT, CONST, MM, R> BT{&fm};
   float d[PL];   // plane i0 of the window, then of its transform
   {
