@@ -105,3 +105,35 @@ def test_gradients_graph_replay():
         plan.weight_gradient(xd, dyd, dw, wsw)
     _replay_check(torch, ga, dx, dx_e, scratch)
     _replay_check(torch, gw, dw, dw_e, scratch)
+
+
+@pytest.mark.parametrize("fuse,window", [(True, (1, 2, 2)), (False, (2, 2, 2))], ids=["fused_122", "two_stage_222"])
+def test_forward_pool_graph_replay(fuse, window):
+    """wino_forward_pool under capture: the fused F(4^3) forward and the
+    two-stage one, each with the max-pool in the product's epilogue."""
+    torch = require_gpu()
+    from paper_1611_06565_amd.wino import Plan
+    spec = CASES[3][0]
+    log(f"[gpu] graph forward_pool fuse={fuse} window={window}")
+    x, w = draw_layer(spec, seed=23)
+    plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X), pad=spec.pad,
+                relu=True, fuse=fuse)
+    assert plan.desc["fused"] == (1 if fuse else 0)
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    U = plan.transform_filter(wd)
+    ws = plan.new_workspace() if not fuse else None
+    y = torch.empty(plan.pooled_shape(window), device="cuda")
+    plan.forward_pool(xd, U, window, y=y, workspace=ws)
+    torch.cuda.synchronize()
+    eager = y.clone()
+    scratch = torch.ones(1 << 20, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        plan.forward_pool(xd, U, window, y=y, workspace=ws)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        plan.forward_pool(xd, U, window, y=y, workspace=ws)
+    _replay_check(torch, g, y, eager, scratch)
