@@ -109,6 +109,11 @@ F43_BOTH = [s for s in SMALL + EDGE + ROWFAST if s.N == 3 and s.m == 4] + [
               x_dist="normal", w_dist="he"),
     LayerSpec("f4x3_kloop_c1_k33", N=3, m=4, r=3, batch=1, C=1, K=33, X=(7, 6, 9), pad=0,
               x_dist="normal", w_dist="normal"),
+    # one chunk of 4 and of 5 channels (the chunk's other channels zero)
+    LayerSpec("f4x3_kloop_c4_k48", N=3, m=4, r=3, batch=2, C=4, K=48, X=(9, 8, 64), pad=1,
+              x_dist="normal", w_dist="he"),
+    LayerSpec("f4x3_kloop_c5_k32", N=3, m=4, r=3, batch=1, C=5, K=32, X=(10, 7, 11), pad=2,
+              x_dist="normal", w_dist="he"),
     # 300 tile blocks: whole work-groups for every kernel block plus, on each
     # XCD, the blocks past its last full round split into one unit per kernel
     # block
