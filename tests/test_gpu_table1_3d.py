@@ -7,7 +7,7 @@ weight gradient; the data gradient runs on the same kernels."""
 import numpy as np
 import pytest
 
-from gpu_util import check_full, log, require_gpu, run_layer
+from gpu_util import check_full, check_sampled, log, require_gpu, run_layer
 from oracle.adjoint import direct_adjoint
 from oracle.metric import normalised_error
 from oracle.winograd import transform_filter as o_filter
@@ -126,3 +126,30 @@ def test_table1_3d_no_weight_gradient():
     dy = torch.zeros(plan.output_shape, device="cuda")
     with pytest.raises(WinoError):
         plan.weight_gradient(x, dy)
+
+
+
+@pytest.mark.parametrize("m,r", [(5, 4), (4, 5), (3, 6)], ids=["f5x4", "f4x5", "f3x6"])
+def test_table1_3d_full_size_config4_shape(m, r):
+    """The alpha = 8 sizes at the size bench.py --config 4 --size M,R times
+    (batch 1, C = K = 32, 128^3, pad (r - 1) // 2): 20,000 sampled outputs and
+    the corners (the full fp64 correlation of this volume takes minutes), and
+    every output finite; the same kernels run on every output of a 48^3 cut
+    of the layer below."""
+    from workloads import CONFIGS
+    spec = CONFIGS[4].with_(m=m, r=r, pad=(r - 1) // 2, name=f"c4_f{m}x{r}")
+    x, w = draw_layer(spec, seed=4)
+    y, plan = run_layer(spec, x, w)
+    assert plan.desc["n_xi"] == 512
+    assert y.shape == (spec.batch, spec.K) + spec.out_spatial
+    assert np.all(np.isfinite(y))
+    check_sampled(spec, y, x, w, n=20000, seed=m)
+
+
+@pytest.mark.parametrize("m,r", [(5, 4), (4, 5), (3, 6)], ids=["f5x4", "f4x5", "f3x6"])
+def test_table1_3d_48cube_full_output(m, r):
+    from workloads import CONFIGS
+    spec = CONFIGS[4].with_(m=m, r=r, pad=(r - 1) // 2, X=(48, 48, 48), name=f"c4cut_f{m}x{r}")
+    x, w = draw_layer(spec, seed=5)
+    y, _ = run_layer(spec, x, w, guard=512)
+    check_full(spec, y, x, w)
