@@ -89,6 +89,13 @@ __device__ __forceinline__ int p_index(int i0, int j, int ch, int tl) {
   return ((i0 * Fused43Geom::PL + j) * (Fused43Geom::CH / 2) + (ch >> 1)) * 32 + tl * 2 + (ch & 1);
 }
 
+// Work-group barrier that waits for this wave's LDS accesses only (lgkmcnt(0)),
+// not for its global loads (__syncthreads() would wait for those too, vmcnt(0)).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);             // lgkmcnt(0); vmcnt and expcnt untouched
+  asm volatile("s_barrier" ::: "memory");
+}
+
 template <bool CONST, bool KLOOP, int POOL = 0>
 __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x, const float* __restrict__ U,
                                                     float* __restrict__ y, FusedArgs a, FMats fm) {
@@ -316,11 +323,15 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   // One chunk (C <= 8, the kernel-block loop): the planes are formed once,
   // each wave turns them into its 18 elements of V in registers, and the
   // work-group multiplies them with every kernel block's U in turn; the LDS
-  // is then free for each block's epilogue.
+  // is then free for each block's epilogue.  Each block's U operands are
+  // loaded ahead: the first block's before the barrier after the producing
+  // (the barrier waits for LDS traffic only, so they arrive during the
+  // elements' formation), the next block's during the epilogue's second part.
   [[maybe_unused]] float2 vv[XPW];
   if constexpr (KLOOP) {
   produce(0);
-  __syncthreads();
+  load_u(0, kbs);
+  lds_barrier();
 #pragma unroll
   for (int p = 0; p < G::NPOS; ++p) {
     float2 pv[A];
@@ -349,7 +360,6 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   for (int kbx = kb0; kbx < kb1; ++kbx) {
   if constexpr (KLOOP) {
     if (kbx > kb0) __syncthreads();             // the previous block's stores have read the LDS
-    load_u(0, kbx);
 #pragma unroll
     for (int e = 0; e < XPW; ++e) {
       acc[e] = typename S::acc_t{};
@@ -377,6 +387,9 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
     }
   }
   __syncthreads();
+  if constexpr (KLOOP) {
+    if (kbx + 1 < kb1) load_u(0, kbx + 1);      // the accumulators are in LDS: U for the next block
+  }
 
   if constexpr (POOL == 0) {
     // Part 2: item (o0, kernel, tile), tiles fastest, reads the 36 values of
