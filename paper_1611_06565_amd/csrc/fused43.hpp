@@ -96,7 +96,7 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_barrier" ::: "memory");
 }
 
-template <bool CONST, bool KLOOP, int POOL = 0>
+template <bool CONST, bool KLOOP, int POOL = 0, bool NARROW = false>
 __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x, const float* __restrict__ U,
                                                     float* __restrict__ y, FusedArgs a, FMats fm) {
   using G = Fused43Geom;
@@ -327,25 +327,50 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   // loaded ahead: the first block's before the barrier after the producing
   // (the barrier waits for LDS traffic only, so they arrive during the
   // elements' formation), the next block's during the epilogue's second part.
+  //
+  // With at most 4 channels (narrow) one MFMA k-step per element suffices:
+  // lane group kr takes channel kr (element value and U operand in .x), and
+  // the planes of channels 4..7 (the odd waves' producing) are not formed.
   [[maybe_unused]] float2 vv[XPW];
+  static_assert(!NARROW || KLOOP, "the narrow form is a kernel-block loop");
+  constexpr bool narrow = NARROW;
+  auto load_u_narrow = [&](int kbx) {
+    const float* uc = U + jw * uplane + (kbx * BLK + col) * 4 + kr;
+#pragma unroll
+    for (int p = 0; p < G::NPOS; ++p)
+#pragma unroll
+      for (int x0 = 0; x0 < A; ++x0) ur[p * A + x0].x = uc[(x0 * PL + p) * uplane];
+  };
+  auto load_u_block = [&](int kbx) {
+    if constexpr (narrow) load_u_narrow(kbx);
+    else load_u(0, kbx);
+  };
   if constexpr (KLOOP) {
-  produce(0);
-  load_u(0, kbs);
+  if (!narrow || pch < 4) produce(0);           // pch < 4: the even waves
+  load_u_block(kbs);
   lds_barrier();
 #pragma unroll
   for (int p = 0; p < G::NPOS; ++p) {
-    float2 pv[A];
-    fetch(pv, p);
     float vx[A], vy[A], ox[A], oy[A];
+    if constexpr (narrow) {
 #pragma unroll
-    for (int i = 0; i < A; ++i) {
-      vx[i] = pv[i].x;
-      vy[i] = pv[i].y;
+      for (int i = 0; i < A; ++i) vx[i] = sm[p_index(i, jw + p, kr, col)];
+      apply_vec<A, A>(BT, vx, 1, ox, 1);
+#pragma unroll
+      for (int x0 = 0; x0 < A; ++x0) vv[p * A + x0].x = ox[x0];
+    } else {
+      float2 pv[A];
+      fetch(pv, p);
+#pragma unroll
+      for (int i = 0; i < A; ++i) {
+        vx[i] = pv[i].x;
+        vy[i] = pv[i].y;
+      }
+      apply_vec<A, A>(BT, vx, 1, ox, 1);
+      apply_vec<A, A>(BT, vy, 1, oy, 1);
+#pragma unroll
+      for (int x0 = 0; x0 < A; ++x0) vv[p * A + x0] = make_float2(ox[x0], oy[x0]);
     }
-    apply_vec<A, A>(BT, vx, 1, ox, 1);
-    apply_vec<A, A>(BT, vy, 1, oy, 1);
-#pragma unroll
-    for (int x0 = 0; x0 < A; ++x0) vv[p * A + x0] = make_float2(ox[x0], oy[x0]);
   }
   }
   // ---- epilogue of kernel block kbx (eq. 4 inverted): A^T along the first
@@ -360,11 +385,16 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   for (int kbx = kb0; kbx < kb1; ++kbx) {
   if constexpr (KLOOP) {
     if (kbx > kb0) __syncthreads();             // the previous block's stores have read the LDS
+    if constexpr (narrow) {
 #pragma unroll
-    for (int e = 0; e < XPW; ++e) {
-      acc[e] = typename S::acc_t{};
-      acc[e] = S::mma(vv[e].x, ur[e].x, acc[e]);
-      acc[e] = S::mma(vv[e].y, ur[e].y, acc[e]);
+      for (int e = 0; e < XPW; ++e) acc[e] = S::mma(vv[e].x, ur[e].x, typename S::acc_t{});
+    } else {
+#pragma unroll
+      for (int e = 0; e < XPW; ++e) {
+        acc[e] = typename S::acc_t{};
+        acc[e] = S::mma(vv[e].x, ur[e].x, acc[e]);
+        acc[e] = S::mma(vv[e].y, ur[e].y, acc[e]);
+      }
     }
   }
   if (a.bias != nullptr && int(threadIdx.x) < BLK) {
@@ -388,7 +418,7 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   }
   __syncthreads();
   if constexpr (KLOOP) {
-    if (kbx + 1 < kb1) load_u(0, kbx + 1);      // the accumulators are in LDS: U for the next block
+    if (kbx + 1 < kb1) load_u_block(kbx + 1);   // the accumulators are in LDS: U for the next block
   }
 
   if constexpr (POOL == 0) {

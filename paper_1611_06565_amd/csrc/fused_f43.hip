@@ -14,7 +14,9 @@ template <int POOL>
 void launch_pool(bool kloop, bool const_mats, dim3 grid, const float* x, const float* U, float* y,
                  const FusedArgs& a, const FMats& fm, hipStream_t s) {
   const dim3 nt(Fused43Geom::NT);
-  if (kloop)
+  if (kloop && a.C <= 4)
+    hipLaunchKernelGGL((k_fused43<true, true, POOL, true>), grid, nt, 0, s, x, U, y, a, fm);
+  else if (kloop)
     hipLaunchKernelGGL((k_fused43<true, true, POOL>), grid, nt, 0, s, x, U, y, a, fm);
   else if (const_mats)
     hipLaunchKernelGGL((k_fused43<true, false, POOL>), grid, nt, 0, s, x, U, y, a, fm);
