@@ -25,6 +25,9 @@ CASES = [
     # kernel-block loop, gathered rows, odd extents (floor rounding drops the last row)
     (LayerSpec("pool_kloop_c8_k40", N=3, m=4, r=3, batch=1, C=8, K=40, X=(10, 9, 13), pad=1,
                x_dist="normal", w_dist="he", relu=True), (2, 2, 2)),
+    # kernel-block loop with at most 4 channels (one MFMA k-step per element), gathered rows
+    (LayerSpec("pool_kloop_narrow_c2_k48", N=3, m=4, r=3, batch=1, C=2, K=48, X=(10, 11, 13), pad=1,
+               x_dist="normal", w_dist="he", leaky=0.125), (2, 2, 2)),
     # chunk loop (C > 8), partial tiles on every axis, leaky activation
     (LayerSpec("pool_c17_k20_leaky", N=3, m=4, r=3, batch=1, C=17, K=20, X=(9, 10, 11), pad=1,
                x_dist="normal", w_dist="he", leaky=0.125), (2, 2, 2)),
