@@ -316,12 +316,13 @@ wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const flo
 /* wino_forward_ex followed by wino_maxpool3d, with the pooling inside the
  * product's epilogue, so only the pooled outputs reach memory: F(4^3)
  * plans, fused (wino_plan_info.fused = 1, no workspace) or in two stages
- * (the input transform to the workspace, then the product).  eq. (2)'s f
+ * (the input transform to the workspace, then the product), and F(2^3)
+ * plans with window (2, 2, 2) (a window is one tile).  eq. (2)'s f
  * (the plan's activation) is applied before the maximum, as a pooling layer
  * after the convolution does; the result has the same bits as
  * wino_forward_ex then wino_maxpool3d.
- *   window     host, [3] int32: (1, 2, 2) or (2, 2, 2), window = stride,
- *              floor rounding
+ *   window     host, [3] int32: (1, 2, 2) or (2, 2, 2) (F(2^3): (2, 2, 2)),
+ *              window = stride, floor rounding
  *   y          device, [batch][K][Y_1/w_1][Y_2/w_2][Y_3/w_3] float32,
  *              16-byte aligned (Y of wino_output_dims)
  *   bias       as for wino_forward_ex

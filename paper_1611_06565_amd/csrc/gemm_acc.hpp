@@ -53,6 +53,10 @@ struct AccArgs {
   const float* bias;  // [K] or null: b_k of eq. (2), added before the activation
   float* part;
   int32_t nparts;
+  // (2, 2, 2) max-pool in the epilogue (k_gemm_acc with POOL, k_part_reduce_pool):
+  // pooled extents Y / 2 (floor) and the pooled stride per kernel
+  int32_t Yp[3];
+  int64_t ystride_p;
 };
 
 template <int N, int MM, int R>
@@ -191,7 +195,7 @@ constexpr AccCoef<N, MM, R> make_acc_coef() {
 template <int N, int MM, int R>
 __constant__ AccCoef<N, MM, R> kAccCoef = make_acc_coef<N, MM, R>();
 
-template <int N, int MM, int R, bool CONST>
+template <int N, int MM, int R, bool CONST, int POOL = 0>
 __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V,
                                                      const float* __restrict__ U,
                                                      float* __restrict__ y, AccArgs g, FMats fm) {
@@ -502,6 +506,39 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc(const float* __restrict__ V
     return;
   }
 
+  if constexpr (POOL != 0) {
+    // Window (2, 2, 2), stride 2: a tile of 2 is one window, whose 8 outputs
+    // are this lane's yacc[0..7][r].  Bias, activation and the maximum in
+    // registers, scanned in the stand-alone pool's order (first axis
+    // slowest, strict comparison from -inf), so the result has the bits of
+    // the forward followed by that pool; one store per complete window
+    // (floor rounding drops the tiles cut by the output's end).
+    static_assert(N == 3 && MM == 2, "the pooled epilogue takes 3-D tiles of 2");
+    __builtin_amdgcn_s_waitcnt(0x0f70);           // vmcnt(0): no copy still writes LDS
+    const int kg = kb * KB + kq * 32 + col;
+    if (kg >= g.K) return;
+    const float bk = g.bias != nullptr ? g.bias[kg] : 0.0f;
+    float* const yk = y + int64_t(kg) * g.ystride_p;
+#pragma unroll
+    for (int r = 0; r < S::NACC; ++r) {
+      const int t = tb * TB + tq * 32 + S::acc_row(lane, r);
+      if (t >= g.T) continue;
+      int ti[3] = {0, 0, 0};
+      const int n = split_tile<N>(t, g.tiles, ti);
+      if (ti[0] >= g.Yp[0] || ti[1] >= g.Yp[1] || ti[2] >= g.Yp[2]) continue;
+      float best = -__builtin_inff();
+#pragma unroll
+      for (int o = 0; o < NOUT; ++o) {
+        float v = yacc[o][r];
+        if (g.bias != nullptr) v += bk;
+        v = activate(v, g.act, g.slope);
+        best = v > best ? v : best;
+      }
+      yk[int64_t(n) * g.K * g.ystride_p + (int64_t(ti[0]) * g.Yp[1] + ti[1]) * g.Yp[2] + ti[2]] = best;
+    }
+    return;
+  }
+
   // ---- stitch: outputs through LDS so that neighbouring lanes store
   // neighbouring outputs of a row, PPR output planes per round.  Plane o
   // ([k][t], t XOR-swizzled by k) of a round lives in buffer o % PPR.
@@ -599,6 +636,64 @@ __global__ void __launch_bounds__(256) k_part_reduce(float* __restrict__ y, AccA
   if (g.bias != nullptr) v += g.bias[kg];
   v = activate(v, g.act, g.slope);
   y[(int64_t(n) * g.K + kg) * g.ystride_k + off] = v;
+}
+
+// k_part_reduce with the (2, 2, 2) max-pool of k_gemm_acc's pooled epilogue
+// (3-D tiles of 2): one thread per (tail block, tile, kernel) forms the 8
+// outputs of its tile as k_part_reduce does (parts summed in order, bias,
+// activation) and stores their maximum, scanned in the stand-alone pool's
+// order, for every complete window.
+template <int N, int MM, int TB, int KB>
+__global__ void __launch_bounds__(256) k_part_reduce_pool(float* __restrict__ y, AccArgs g, int32_t ntail) {
+  static_assert(N == 3 && MM == 2, "windows of one tile of 2");
+  constexpr int NOUT = ipow(MM, N);
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;   // (tail block, tile, kernel)
+  const int k_l = int(i % KB), tl = int((i / KB) % TB);
+  const int tix = int(i / (KB * TB));
+  if (tix >= ntail) return;
+  int blk = -1;                                   // tail block tix -> its block
+#pragma unroll
+  for (int x = 0; x < 8; ++x)
+    if (tix >= g.xt0[x] && tix < g.xt0[x] + g.xs[x]) blk = g.xb0[x] + g.xn[x] - g.xs[x] + (tix - g.xt0[x]);
+  if (blk < 0) return;
+  const int tb = blk / g.nkb, kb = blk % g.nkb;
+  const int t = tb * TB + tl, kg = kb * KB + k_l;
+  if (t >= g.T || kg >= g.K) return;
+  int ti[3] = {0, 0, 0};
+  const int n = split_tile<N>(t, g.tiles, ti);
+  if (ti[0] >= g.Yp[0] || ti[1] >= g.Yp[1] || ti[2] >= g.Yp[2]) return;
+  const float* pp = g.part + int64_t(tix) * g.nparts * NOUT * (TB * KB) + tl * KB + k_l;
+  // each output's parts are added in part order, as k_part_reduce does; the
+  // loads of four parts of all 8 outputs are issued together (a thread here
+  // does 8 times the loads of a k_part_reduce thread)
+  float v[NOUT];
+#pragma unroll
+  for (int o = 0; o < NOUT; ++o) v[o] = 0.0f;
+  int q = 0;
+  for (; q + 4 <= g.nparts; q += 4) {
+    float ld[4][NOUT];
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq)
+#pragma unroll
+      for (int o = 0; o < NOUT; ++o)
+        ld[qq][o] = __builtin_nontemporal_load(pp + (int64_t(q + qq) * NOUT + o) * (TB * KB));
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq)
+#pragma unroll
+      for (int o = 0; o < NOUT; ++o) v[o] += ld[qq][o];
+  }
+  for (; q < g.nparts; ++q)
+#pragma unroll
+    for (int o = 0; o < NOUT; ++o) v[o] += __builtin_nontemporal_load(pp + (int64_t(q) * NOUT + o) * (TB * KB));
+  float best = -__builtin_inff();
+#pragma unroll
+  for (int o = 0; o < NOUT; ++o) {
+    float u = v[o];
+    if (g.bias != nullptr) u += g.bias[kg];
+    u = activate(u, g.act, g.slope);
+    best = u > best ? u : best;
+  }
+  y[(int64_t(n) * g.K + kg) * g.ystride_p + (int64_t(ti[0]) * g.Yp[1] + ti[1]) * g.Yp[2] + ti[2]] = best;
 }
 
 }  // namespace wino

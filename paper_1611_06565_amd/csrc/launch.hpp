@@ -43,9 +43,9 @@ struct SizeOps {
   wino_status (*fused)(const wino_plan_s&, const float* x, const float* U, const float* bias, float* y,
                        hipStream_t);
   // the product with the max-pool in its epilogue (pool 1: window (1, 2, 2),
-  // 2: (2, 2, 2); y pooled), null for sizes without one
-  wino_status (*gemm_pool)(const wino_plan_s&, const float* V, const float* U, const float* bias, float* y,
-                           int pool, hipStream_t);
+  // 2: (2, 2, 2); y pooled), null for sizes without one; part as for gemm
+  wino_status (*gemm_pool)(const wino_plan_s&, const float* V, float* part, const float* U, const float* bias,
+                           float* y, int pool, hipStream_t);
 };
 
 template <int N, int MM, int R, bool CONST>
@@ -221,11 +221,25 @@ struct Launch {
     return g;
   }
 
-  // F(4^3) two-stage product with the max-pool in its epilogue.
-  static wino_status gemm_pool(const wino_plan_s& p, const float* V, const float* U, const float* bias, float* y,
-                               int pool, hipStream_t s) {
+  // The product with the max-pool in its epilogue: F(4^3) two-stage
+  // (windows (1, 2, 2) and (2, 2, 2)) and F(2^3) (window (2, 2, 2), one tile).
+  static wino_status gemm_pool(const wino_plan_s& p, const float* V, float* part, const float* U,
+                               const float* bias, float* y, int pool, hipStream_t s) {
     constexpr int KIND = Blocking<N, MM, R>::KIND;
-    if constexpr (N == 3 && MM == 4 && R == 3 && KIND == 2 && LOC == 1) {
+    if constexpr (N == 3 && MM == 2 && KIND == 0) {
+      if (pool != 2) return WINO_EUNSUPPORTED;
+      using G = AccGeom<N, MM, R>;
+      AccArgs a{};
+      acc_args(p, a, G::TB, bias, part);
+      for (int i = 0; i < 3; ++i) a.Yp[i] = int32_t(p.Y[i] / 2);
+      a.ystride_p = int64_t(a.Yp[0]) * a.Yp[1] * a.Yp[2];
+      hipLaunchKernelGGL((k_gemm_acc<N, MM, R, CONST, 1>), dim3(p.grid_gemm), dim3(G::NT), 0, s, V, U, y, a,
+                         p.fm);
+      if (p.nparts > 1)
+        hipLaunchKernelGGL((k_part_reduce_pool<N, MM, G::TB, G::KB>), dim3(p.grid_reduce / G::NOUT), dim3(256),
+                           0, s, y, a, int32_t(p.ntail));
+      return launch_status();
+    } else if constexpr (N == 3 && MM == 4 && R == 3 && KIND == 2 && LOC == 1) {
       using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
       const GemmArgs g = gemm_args(p, bias, pool);
       if (pool == 1)
@@ -247,6 +261,8 @@ constexpr SizeOps make_ops() {
   using L = Launch<N, MM, R, CONST>;
   if constexpr (N == 3 && MM == 4 && R == 3)
     return SizeOps{&L::filter, &L::input, &L::gemm, &L::wgrad, &L::fused, &L::gemm_pool};
+  else if constexpr (N == 3 && MM == 2)
+    return SizeOps{&L::filter, &L::input, &L::gemm, &L::wgrad, nullptr, &L::gemm_pool};
   else
     return SizeOps{&L::filter, &L::input, &L::gemm, &L::wgrad, nullptr};
 }

@@ -187,8 +187,9 @@ wino_status wino_forward_pool(const wino_plan_t* p, const float* x, const float*
   const SizeOps* ops = ops_of(*p);
   if (ops == nullptr) return WINO_EUNSUPPORTED;
   // the max-pool rides on the F(4^3) forward's epilogue (fused, or the
-  // two-stage product)
+  // two-stage product) or on the F(2^3) product's (window (2, 2, 2): one tile)
   if (p->fused ? ops->fused == nullptr : ops->gemm_pool == nullptr) return WINO_EUNSUPPORTED;
+  if (p->m == 2 && pool != 2) return WINO_EUNSUPPORTED;
   for (int i = 0; i < 3; ++i)
     if (p->Y[i] / window[i] < 1) return WINO_EINVAL;
   const hipStream_t s = static_cast<hipStream_t>(stream);
@@ -197,9 +198,10 @@ wino_status wino_forward_pool(const wino_plan_t* p, const float* x, const float*
   if (!aligned16(ws)) return WINO_EINVAL;
   if (ws_bytes < wino_workspace_bytes(p)) return WINO_EWORKSPACE;
   float* V = static_cast<float*>(ws);
+  float* part = p->nparts > 1 ? V + p->v_floats : nullptr;
   const wino_status st = ops->input(*p, x, V, s);
   if (st != WINO_OK) return st;
-  return ops->gemm_pool(*p, V, U, bias, y, pool, s);
+  return ops->gemm_pool(*p, V, part, U, bias, y, pool, s);
 }
 
 wino_status wino_maxpool3d(const int64_t* dims, const int32_t* window, const float* x, float* y,

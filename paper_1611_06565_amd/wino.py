@@ -379,8 +379,9 @@ class Plan:
 
     def forward_pool(self, x, U, window, y=None, workspace=None, bias=None):
         """wino_forward_pool: the F(4^3) forward with the max-pool (window =
-        stride, (1, 2, 2) or (2, 2, 2)) in the product's epilogue; y is the
-        pooled output.  Other sizes raise WinoError."""
+        stride, (1, 2, 2) or (2, 2, 2)), or the F(2^3) forward with window
+        (2, 2, 2), in the product's epilogue; y is the pooled output.  Other
+        sizes and windows raise WinoError."""
         import torch
         self._check_shape(x, self.input_shape, "x")
         shape = self.pooled_shape(window)

@@ -178,13 +178,15 @@ def test_device_calls_reject_bad_arguments(L):
 
 def test_forward_pool_rejects_before_launch(L):
     """wino_forward_pool's refusals, all decided on the host: windows other
-    than (1, 2, 2) and (2, 2, 2), sizes whose product has no pooled epilogue,
-    pooled extents of 0, bad pointers and a missing workspace."""
+    than (1, 2, 2) and (2, 2, 2) (F(2^3): (2, 2, 2) only), sizes whose
+    product has no pooled epilogue, pooled extents of 0, bad pointers and a
+    missing workspace."""
     vp = ctypes.c_void_p
     W = lambda *w: (ctypes.c_int32 * 3)(*w)
     fused = wino.Plan(3, 4, 3, 4, 16, [1, 8, 8, 8], pad=1)          # F(4^3), K <= 64: fused
     two = wino.Plan(3, 4, 3, 4, 80, [1, 8, 8, 8], pad=1)            # K > 64: two stages
-    m2 = wino.Plan(3, 2, 3, 4, 16, [1, 8, 8, 8], pad=1)             # F(2^3): stand-alone pool only
+    m2 = wino.Plan(3, 2, 3, 4, 16, [1, 8, 8, 8], pad=1)             # F(2^3): window (2, 2, 2) only
+    m32 = wino.Plan(3, 3, 2, 4, 16, [1, 8, 8, 8], pad=0)            # F(3^3, 2^3): stand-alone pool only
     d2 = wino.Plan(2, 4, 3, 4, 16, [1, 8, 8], pad=1)                # 2-D
     tiny = wino.Plan(3, 4, 3, 4, 16, [1, 1, 8, 8], pad=1)           # Y_0 = 1
     assert fused.desc["fused"] == 1 and two.desc["fused"] == 0
@@ -199,7 +201,8 @@ def test_forward_pool_rejects_before_launch(L):
     assert L.wino_forward_pool(fused.handle, *args, W(1, 2, 2), vp(16384 + 8), None, 0, None) == -1
     assert L.wino_forward_pool(fused.handle, vp(4096), vp(8192), vp(512 + 2), W(1, 2, 2), vp(16384), None, 0,
                                None) == -1
-    assert L.wino_forward_pool(m2.handle, *args, W(2, 2, 2), vp(16384), vp(32768), ws, None) == -2
+    assert L.wino_forward_pool(m2.handle, *args, W(1, 2, 2), vp(16384), vp(32768), ws, None) == -2
+    assert L.wino_forward_pool(m32.handle, *args, W(2, 2, 2), vp(16384), vp(32768), ws, None) == -2
     assert L.wino_forward_pool(d2.handle, *args, W(1, 2, 2), vp(16384), vp(32768), ws, None) == -2
     assert L.wino_forward_pool(tiny.handle, *args, W(2, 2, 2), vp(16384), None, 0, None) == -1
     # the two-stage product needs its workspace (V)

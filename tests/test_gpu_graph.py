@@ -107,18 +107,24 @@ def test_gradients_graph_replay():
     _replay_check(torch, gw, dw, dw_e, scratch)
 
 
-@pytest.mark.parametrize("fuse,window", [(True, (1, 2, 2)), (False, (2, 2, 2))], ids=["fused_122", "two_stage_222"])
-def test_forward_pool_graph_replay(fuse, window):
-    """wino_forward_pool under capture: the fused F(4^3) forward and the
-    two-stage one, each with the max-pool in the product's epilogue."""
+@pytest.mark.parametrize("case,fuse,window,split",
+                         [(3, True, (1, 2, 2), True), (3, False, (2, 2, 2), True),
+                          (0, False, (2, 2, 2), True), (1, False, (2, 2, 2), False)],
+                         ids=["fused_122", "two_stage_222", "f2x3_parts_222", "f2x3_nosplit_222"])
+def test_forward_pool_graph_replay(case, fuse, window, split):
+    """wino_forward_pool under capture: the fused F(4^3) forward, the
+    two-stage one and the F(2^3) one (split into parts reduced and pooled
+    together, and unsplit), each with the max-pool in the product."""
     torch = require_gpu()
     from paper_1611_06565_amd.wino import Plan
-    spec = CASES[3][0]
-    log(f"[gpu] graph forward_pool fuse={fuse} window={window}")
+    spec = CASES[case][0]
+    log(f"[gpu] graph forward_pool {spec.name} fuse={fuse} window={window} split={split}")
     x, w = draw_layer(spec, seed=23)
     plan = Plan(spec.N, spec.m, spec.r, spec.C, spec.K, [spec.batch] + list(spec.X), pad=spec.pad,
-                relu=True, fuse=fuse)
+                relu=True, fuse=fuse, split=split)
     assert plan.desc["fused"] == (1 if fuse else 0)
+    if case == 0:
+        assert plan.desc["gemm_parts"] > 1, "the split case must split"
     xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
     U = plan.transform_filter(wd)
     ws = plan.new_workspace() if not fuse else None
