@@ -328,7 +328,7 @@ def bench_stack(args):
         step()
     torch.cuda.synchronize()
     if args.graph:
-        # the whole step (26 launches) captured once as a HIP graph and replayed
+        # the whole step (19 launches) captured once as a HIP graph and replayed
         s = torch.cuda.Stream()
         s.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(s):
