@@ -154,8 +154,12 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
   // Wave w does copies w, w + 4 (V) and w + 8 (U), so whether a wave's copy
   // i is V or U is known at compile time.
   constexpr int64_t VX = TB * 4, VG = int64_t(G::NXI) * TB * 4;    // V element / group strides
-  const float* vsrc = V + int64_t(tb) * g.vblock + lane * 4;
-  const float* usrc = U + int64_t(kb) * (KB * 4) + (lane & 31) * 4 + int64_t(lane >> 5) * g.K_pad * 4;
+  // wave-uniform sources plus the lane's byte offset (V: 16 l; U: lanes
+  // 32..63 read the next channel group, K_pad * 16 bytes further)
+  const float* vsrc = V + int64_t(tb) * g.vblock;
+  const float* usrc = U + int64_t(kb) * (KB * 4);
+  const uint32_t vloff = uint32_t(lane) * 16u;
+  const uint32_t uloff = uint32_t(lane & 31) * 16u + uint32_t(lane >> 5) * uint32_t(g.K_pad) * 16u;
   int64_t off[G::CPS];
   int dsto[G::CPS];
   constexpr int NVC = G::SAV / 256 / NW;           // V copies per wave
@@ -175,12 +179,12 @@ __global__ void __launch_bounds__(256, 2) k_gemm_acc4(const float* __restrict__ 
   }
   const int64_t vstage = G4 * VG, ustage = int64_t(G4) * g.K_pad * 4;
   // copy i of a step; a step past the last one (real == false) copies the
-  // block's first V chunk again into the dump area instead
+  // block's first V (or U) chunk again into the dump area instead
   auto copy_one = [&](auto I, const float* vs, const float* us, float* base, bool real) {
     constexpr int i = decltype(I)::value;
     // non-temporal V rows: see lds_copy16
-    if constexpr (i < NVC) lds_copy16<true>(real ? vs + off[i] : vsrc, real ? base + dsto[i] : dump);
-    else lds_copy16<false>(real ? us + off[i] : vsrc, real ? base + dsto[i] : dump);
+    if constexpr (i < NVC) lds_copy16<true>(real ? vs + off[i] : vsrc, vloff, real ? base + dsto[i] : dump);
+    else lds_copy16<false>(real ? us + off[i] : usrc, uloff, real ? base + dsto[i] : dump);
   };
   int cpass = p0, cst = 0;
   auto cursor_src = [&](const float*& vs, const float*& us) {
