@@ -773,6 +773,12 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
   }
 }
 
+// Raw buffer resource over 4 GiB from a wave-uniform base (the third word
+// is the gfx9 family's raw 32-bit format).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const float* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, -1, 0x00020000);
+}
+
 // VEC = floats per operand load (one load feeds VEC MFMA k-steps).  DEPTH =
 // stages in the register ring (DEPTH-1 stages in flight while one is
 // consumed).
@@ -783,12 +789,14 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
   using S = MfmaShape<BLK>;
   using Geo = GemmGeom<N, MM, R, BLK, NW, LOC>;
   constexpr int NXI = Geo::NXI, XPW = Geo::XPW;
-  static_assert(VEC == 1 || VEC == 2 || VEC == 4, "operand load width");
+  static_assert(VEC == 4, "16-byte operand loads");
 
   __shared__ float sm[Geo::LDS_FLOATS];
 
   const int lane = int(threadIdx.x) & 63;
-  const int wave = int(threadIdx.x) >> 6;
+  // uniform for the buffer bases of the 3-D sizes (the 2-D sizes keep the
+  // form their per-lane pointers were tuned with)
+  const int wave = N == 3 ? __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6) : int(threadIdx.x) >> 6;
   const int L = xcd_remap(int(blockIdx.x), g.nblocks);
   const int tb = L / g.nkb, kb = L % g.nkb;
   const int col = lane % BLK, kr = lane / BLK;
@@ -805,10 +813,27 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
   const int64_t vxi = int64_t(BLK) * CG;                           // V element stride (floats)
   const int64_t uxi = g.uplane;                                    // U plane stride (floats)
   const int c0 = VEC * kr;                                         // this lane's channel in a stage
-  const float* vnext = V + int64_t(tb) * NXI * g.C_pad * BLK + int64_t(c0 / CG) * NXI * BLK * CG +
-                       int64_t(wave) * XPW * vxi + col * CG + c0 % CG;
-  const float* unext = U + int64_t(wave) * XPW * uxi + (int64_t(c0 / CG) * g.K_pad + int64_t(kb) * BLK + col) * CG +
-                       c0 % CG;
+  // 3-D: the operands of a stage are read through buffer resources, the
+  // wave's stage bases (uniform, in scalar registers), the lane's byte offset
+  // as the vector offset and each element's offset as the scalar one, so the
+  // loads need no per-lane 64-bit address arithmetic (the planner keeps the
+  // offsets of a wave's U elements below 2^32 bytes).  On the C3D stack's
+  // conv2-4: 272 / 142 / 258 -> 237 / 125 / 239 us.  The 2-D sizes keep
+  // per-lane pointers (the buffer form made the Fig. 4 layers 2% slower).
+  constexpr bool BUF = N == 3;
+  const float* vnext;
+  const float* unext;
+  int vlane = 0, ulane = 0;
+  if constexpr (BUF) {
+    vnext = V + int64_t(tb) * NXI * g.C_pad * BLK + int64_t(wave) * XPW * vxi;
+    unext = U + int64_t(wave) * XPW * uxi + int64_t(kb) * BLK * CG;
+    vlane = ((c0 / CG) * NXI * BLK * CG + col * CG + c0 % CG) * 4;
+    ulane = (((c0 / CG) * g.K_pad + col) * CG + c0 % CG) * 4;
+  } else {
+    vnext = V + int64_t(tb) * NXI * g.C_pad * BLK + int64_t(c0 / CG) * NXI * BLK * CG + int64_t(wave) * XPW * vxi +
+            col * CG + c0 % CG;
+    unext = U + int64_t(wave) * XPW * uxi + (int64_t(c0 / CG) * g.K_pad + int64_t(kb) * BLK + col) * CG + c0 % CG;
+  }
   const int64_t vgstep = int64_t(NXI) * BLK * SC, ugstep = int64_t(g.K_pad) * SC;
   const int nstages = g.C_pad / SC;
 
@@ -820,10 +845,19 @@ __global__ void __launch_bounds__(NW * 64) k_gemm_inv(const float* __restrict__ 
                 typename std::conditional<VEC == 2, float2, float>::type>::type;
   vec_t ra[DEPTH][XPW], rb[DEPTH][XPW];
   auto fetch = [&](vec_t* a2, vec_t* b2) {
+    if constexpr (BUF) {
+      const __amdgpu_buffer_rsrc_t rv = raw_rsrc(vnext), ru = raw_rsrc(unext);
 #pragma unroll
-    for (int x = 0; x < XPW; ++x) {
-      a2[x] = *reinterpret_cast<const vec_t*>(vnext + x * vxi);
-      b2[x] = *reinterpret_cast<const vec_t*>(unext + x * uxi);
+      for (int x = 0; x < XPW; ++x) {
+        a2[x] = __builtin_bit_cast(vec_t, __builtin_amdgcn_raw_buffer_load_b128(rv, vlane, int(x * vxi * 4), 0));
+        b2[x] = __builtin_bit_cast(vec_t, __builtin_amdgcn_raw_buffer_load_b128(ru, ulane, int(x * uxi * 4), 0));
+      }
+    } else {
+#pragma unroll
+      for (int x = 0; x < XPW; ++x) {
+        a2[x] = *reinterpret_cast<const vec_t*>(vnext + x * vxi);
+        b2[x] = *reinterpret_cast<const vec_t*>(unext + x * uxi);
+      }
     }
     vnext += vgstep;
     unext += ugstep;

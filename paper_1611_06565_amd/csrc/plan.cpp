@@ -355,6 +355,11 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
     int64_t gg = 0;
     if (!mul_ok(tpad / p.blk, kpad / t.KB, &gg) || !grid_ok(gg, t.KIND == 4 ? 1024 : 768, &p.grid_gemm))
       return WINO_EINVAL;
+    // k_gemm_inv reads a wave's U operands of a stage through one buffer
+    // resource in 3-D: the byte offsets of its (at most 18) element planes
+    // of C_pad x K_pad floats, plus the lane's, stay below 2^32
+    if (t.KIND == 2 && N == 3 && (int64_t(18) * cpad * kpad + 4 * kpad + 64) * 4 >= (int64_t(1) << 32))
+      return WINO_EINVAL;
   }
   if (p.v_floats + p.part_floats > kMaxFloats) return WINO_EINVAL;
   // F(4^3) with few kernels: the input transform runs inside the product

@@ -314,6 +314,10 @@ def test_plan_rejects_overflowing_sizes(L):
     assert _plan_status(L, 3, 4, 3, 16, big - 39, d, pad=[1, 1, 1]) == -1
     assert _plan_status(L, 2, 4, 3, 2 ** 20 + 1, 4, [1, 8, 8]) == -1
     assert _plan_status(L, 2, 4, 3, 2 ** 20, 4, [1, 8, 8]) == 0
+    # the two-stage F(4^3) product addresses a wave's U operands from one base:
+    # 18 planes of C_pad x K_pad floats stay below 2^32 bytes
+    assert _plan_status(L, 3, 4, 3, 7680, 7680, [1, 4, 4, 4], pad=[1, 1, 1]) == 0
+    assert _plan_status(L, 3, 4, 3, 7744, 7744, [1, 4, 4, 4], pad=[1, 1, 1]) == -1
     assert _plan_status(L, 3, 2, 3, 4, 4, [big] * 4) == -1
     assert _plan_status(L, 3, 2, 3, 4, 4, [big, 1, 1, 4], pad=[1, 1, 1]) == -1
     assert _plan_status(L, 3, 2, 3, 4, 4, [1, 4, 4, 4], pad=[2 ** 20] * 3) == -1
