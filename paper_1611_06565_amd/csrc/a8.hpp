@@ -262,9 +262,25 @@ __global__ void __launch_bounds__(1024) k_gemm_a8(const float* __restrict__ V, c
 #pragma unroll
     for (int o = 0; o < NOUT; ++o) out[q][o] = 0.0f;
 
-  // operand rows of lane (kr, col): V[tb][cg][xi][col][.], U[xi][cg][kb*16+col][.]
-  const float* vbase = V + (int64_t(tb) * ncg + kr) * S::NXI * (BLK * CG) + col * CG;
-  const float* ubase = U + (int64_t(kr) * g.K_pad + kb * BLK + col) * CG;
+  // operand rows of lane (kr, col): V[tb][cg][xi][col][.], U[xi][cg][kb*16+col][.],
+  // read through buffer resources: wave-uniform bases per step (scalar
+  // registers), the lane's byte offset as the vector offset and each
+  // element's offset as the scalar one, so the loads need no per-lane 64-bit
+  // address arithmetic (the planner keeps 4 U planes below 2^32 bytes)
+  const float* vbase = V + int64_t(tb) * ncg * S::NXI * (BLK * CG);
+  const float* ubase = U + int64_t(kb) * BLK * CG;
+  const int vlane = (kr * S::NXI * (BLK * CG) + col * CG) * 4;
+  const int ulane = (kr * g.K_pad * CG + col * CG) * 4;
+  // the EW operands of V and of U of element run xb (the wave's) at channel stage st
+  auto load_ops = [&](float4* av, float4* uv, int xb, int st) {
+    const __amdgpu_buffer_rsrc_t rv = raw_rsrc(vbase + (int64_t(st) * 4 * S::NXI + xb) * (BLK * CG));
+    const __amdgpu_buffer_rsrc_t ru = raw_rsrc(ubase + int64_t(xb) * g.uplane + int64_t(st) * 4 * g.K_pad * CG);
+#pragma unroll
+    for (int e = 0; e < EW; ++e) {
+      av[e] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rv, vlane, e * (BLK * CG) * 4, 0));
+      uv[e] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(ru, ulane, int(e * g.uplane * 4), 0));
+    }
+  };
 
   if constexpr (MM == 4 && CONST) {
     // F(4^3, 5^3): the next step's operands load while this step multiplies
@@ -318,11 +334,7 @@ __global__ void __launch_bounds__(1024) k_gemm_a8(const float* __restrict__ V, c
       constexpr int b = decltype(B)::value;
       const int x0 = gs / nstage, st = gs % nstage;
       const int xb = x0 * PL + xi1 * A + half * EW;   // first element of the wave
-  #pragma unroll
-      for (int e = 0; e < EW; ++e) {
-        av[b][e] = *reinterpret_cast<const float4*>(vbase + (int64_t(st) * 4 * S::NXI + xb + e) * (BLK * CG));
-        uv[b][e] = *reinterpret_cast<const float4*>(ubase + (int64_t(xb + e) * g.uplane) + int64_t(st) * 4 * g.K_pad * CG);
-      }
+      load_ops(av[b], uv[b], xb, st);
     };
     auto mma = [&](auto B) {
       constexpr int b = decltype(B)::value;
@@ -360,11 +372,7 @@ __global__ void __launch_bounds__(1024) k_gemm_a8(const float* __restrict__ V, c
       const int xb = xi0 * PL + xi1 * A + half * EW;   // first element of the wave
       for (int s = 0; s < nstage; ++s) {
         float4 av[EW], uv[EW];
-  #pragma unroll
-        for (int e = 0; e < EW; ++e) {
-          av[e] = *reinterpret_cast<const float4*>(vbase + (int64_t(s) * 4 * S::NXI + xb + e) * (BLK * CG));
-          uv[e] = *reinterpret_cast<const float4*>(ubase + (int64_t(xb + e) * g.uplane) + int64_t(s) * 4 * g.K_pad * CG);
-        }
+        load_ops(av, uv, xb, s);
   #pragma unroll
         for (int e = 0; e < EW; ++e) {
           acc[e] = F::mma(av[e].x, uv[e].x, acc[e]);

@@ -210,17 +210,20 @@ __global__ void __launch_bounds__(768) k_gemm_ax(const float* __restrict__ V, co
   __shared__ float bsm[BLK];
 
   const int lane = int(threadIdx.x) & 63;
-  const int wave = int(threadIdx.x) >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
   const int L = xcd_remap(int(blockIdx.x), g.nblocks);
   const int tb = L / g.nkb, kb = L % g.nkb;
   const int col = lane % BLK, kr = lane / BLK;
 
+  // operands through buffer resources, as in k_gemm_inv: wave-uniform stage
+  // bases, the lane's byte offset, each element's offset as the scalar one
+  // (the planner keeps a wave's U offsets below 2^32 bytes)
   const int64_t vxi = int64_t(BLK) * CG, uxi = g.uplane;
   const int c0 = VEC * kr;
-  const float* vnext = V + int64_t(tb) * NXI * g.C_pad * BLK + int64_t(c0 / CG) * NXI * BLK * CG +
-                       int64_t(wave) * XPW * vxi + col * CG + c0 % CG;
-  const float* unext = U + int64_t(wave) * XPW * uxi + (int64_t(c0 / CG) * g.K_pad + int64_t(kb) * BLK + col) * CG +
-                       c0 % CG;
+  const float* vnext = V + int64_t(tb) * NXI * g.C_pad * BLK + int64_t(wave) * XPW * vxi;
+  const float* unext = U + int64_t(wave) * XPW * uxi + int64_t(kb) * BLK * CG;
+  const int vlane = ((c0 / CG) * NXI * BLK * CG + col * CG + c0 % CG) * 4;
+  const int ulane = (((c0 / CG) * g.K_pad + col) * CG + c0 % CG) * 4;
   const int64_t vgstep = int64_t(NXI) * BLK * SC, ugstep = int64_t(g.K_pad) * SC;
   const int nstages = g.C_pad / SC;
 
@@ -229,10 +232,11 @@ __global__ void __launch_bounds__(768) k_gemm_ax(const float* __restrict__ V, co
   for (int e = 0; e < XPW; ++e) acc[e] = typename MS::acc_t{};
   for (int s = 0; s < nstages; ++s) {
     float4 ra[XPW], rb[XPW];
+    const __amdgpu_buffer_rsrc_t rv = raw_rsrc(vnext), ru = raw_rsrc(unext);
 #pragma unroll
     for (int e = 0; e < XPW; ++e) {
-      ra[e] = *reinterpret_cast<const float4*>(vnext + e * vxi);
-      rb[e] = *reinterpret_cast<const float4*>(unext + e * uxi);
+      ra[e] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rv, vlane, int(e * vxi * 4), 0));
+      rb[e] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(ru, ulane, int(e * uxi * 4), 0));
     }
     vnext += vgstep;
     unext += ugstep;

@@ -355,11 +355,13 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
     int64_t gg = 0;
     if (!mul_ok(tpad / p.blk, kpad / t.KB, &gg) || !grid_ok(gg, t.KIND == 4 ? 1024 : 768, &p.grid_gemm))
       return WINO_EINVAL;
-    // k_gemm_inv reads a wave's U operands of a stage through one buffer
-    // resource in 3-D: the byte offsets of its (at most 18) element planes
-    // of C_pad x K_pad floats, plus the lane's, stay below 2^32
-    if (t.KIND == 2 && N == 3 && (int64_t(18) * cpad * kpad + 4 * kpad + 64) * 4 >= (int64_t(1) << 32))
-      return WINO_EINVAL;
+    // k_gemm_inv (3-D), k_gemm_ax and k_gemm_a8 read a wave's U operands of a
+    // stage through one buffer resource: the byte offsets of its element
+    // planes of C_pad x K_pad floats (at most 18; 4 for k_gemm_a8), plus the
+    // lane's, stay below 2^32
+    const bool buffered = (t.KIND == 2 && N == 3) || t.KIND == 3;
+    if (buffered && (int64_t(18) * cpad * kpad + 4 * kpad + 64) * 4 >= (int64_t(1) << 32)) return WINO_EINVAL;
+    if (t.KIND == 4 && (int64_t(4) * cpad * kpad + 4 * kpad + 64) * 4 >= (int64_t(1) << 32)) return WINO_EINVAL;
   }
   if (p.v_floats + p.part_floats > kMaxFloats) return WINO_EINVAL;
   // F(4^3) with few kernels: the input transform runs inside the product
