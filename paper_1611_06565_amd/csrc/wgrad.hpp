@@ -161,7 +161,9 @@ __global__ void __launch_bounds__(256) k_wgrad_gemm(const float* __restrict__ V,
   constexpr int CP = 260;                          // padded chunk stride (floats)
   __shared__ __attribute__((aligned(16))) float Ds[16 * CP];
   __shared__ __attribute__((aligned(16))) float Vs[16 * CP];
-  const int lane = int(threadIdx.x) & 63, wave = int(threadIdx.x) >> 6;
+  // wave index uniform (scalar): the chunk choice, its bounds test and the
+  // source address of every load are then scalar work, the lane adds 16 bytes
+  const int lane = int(threadIdx.x) & 63, wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
   const int L = xcd_remap(int(blockIdx.x), a.nblocks);
   const int cb = L % a.ncb, kb = (L / a.ncb) % a.nkb;
   const int xi = (L / (a.ncb * a.nkb)) % nxi, sp = L / (a.ncb * a.nkb * nxi);
