@@ -265,17 +265,22 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   // chunk; 32-bit offsets (the planner bounds U below 2^31 floats).  The
   // chunk's 18 operands are loaded together after its producing.
   const int uplane = int(a.uplane);
-  // per-lane base at element (0, jw); the element offsets are wave-uniform
-  // (the kernel block is part of the base, except in the kernel-block loop)
-  const float* ubase = U + jw * uplane + ((kr >> 1) * a.K_pad + (KLOOP ? 0 : kb * BLK) + col) * 4 + 2 * (kr & 1);
+  // Loaded through a buffer resource: the wave-uniform base at element
+  // (0, jw) of the chunk (and of the kernel block) in scalar registers, the
+  // lane's byte offset as the vector offset and each element's offset as the
+  // scalar one (the planner keeps them below 2^32 bytes), so the loads need
+  // no per-lane 64-bit address arithmetic.
+  const float* ubase = U + jw * uplane + (KLOOP ? 0 : kb * BLK * 4);
+  const int ulane = (((kr >> 1) * a.K_pad + col) * 4 + 2 * (kr & 1)) * 4;
   float2 ur[XPW];
   auto load_u = [&](int chunk, int kbx) {
-    const float* uc = ubase + chunk * 8 * a.K_pad + (KLOOP ? kbx * (BLK * 4) : 0);
+    const __amdgpu_buffer_rsrc_t ru = raw_rsrc(ubase + chunk * 8 * a.K_pad + (KLOOP ? kbx * (BLK * 4) : 0));
 #pragma unroll
     for (int p = 0; p < G::NPOS; ++p)
 #pragma unroll
       for (int x0 = 0; x0 < A; ++x0)
-        ur[p * A + x0] = *reinterpret_cast<const float2*>(uc + (x0 * PL + p) * uplane);
+        ur[p * A + x0] =
+            __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(ru, ulane, (x0 * PL + p) * uplane * 4, 0));
   };
   const float2* P2 = reinterpret_cast<const float2*>(sm);
   auto fetch = [&](float2* pv, int p) {
@@ -335,11 +340,13 @@ __global__ void __launch_bounds__(768, 1) k_fused43(const float* __restrict__ x,
   static_assert(!NARROW || KLOOP, "the narrow form is a kernel-block loop");
   constexpr bool narrow = NARROW;
   auto load_u_narrow = [&](int kbx) {
-    const float* uc = U + jw * uplane + (kbx * BLK + col) * 4 + kr;
+    const __amdgpu_buffer_rsrc_t ru = raw_rsrc(U + jw * uplane + kbx * BLK * 4);
 #pragma unroll
     for (int p = 0; p < G::NPOS; ++p)
 #pragma unroll
-      for (int x0 = 0; x0 < A; ++x0) ur[p * A + x0].x = uc[(x0 * PL + p) * uplane];
+      for (int x0 = 0; x0 < A; ++x0)
+        ur[p * A + x0].x = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(ru, (col * 4 + kr) * 4, (x0 * PL + p) * uplane * 4, 0));
   };
   auto load_u_block = [&](int kbx) {
     if constexpr (narrow) load_u_narrow(kbx);

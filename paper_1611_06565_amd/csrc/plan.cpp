@@ -368,8 +368,11 @@ wino_status wino_plan(int N, int m, int r, int C, int K, const int64_t* dims, co
   // (recomputed for each block of 16 kernels, so only while there are at
   // most 4 such blocks); same grid as k_gemm_inv
   // (its offsets inside one channel's input volume and into U are 32-bit)
+  // (k_fused43 reads U from one buffer base per chunk: element offsets of up
+  // to 182 planes of C_pad x K_pad floats stay below 2^32 bytes)
   p.fused = !aniso && N == 3 && m == 4 && r == 3 && p.K_pad <= 64 && !(o.flags & WINO_NO_FUSE) &&
-            p.X[0] * p.X[1] * p.X[2] <= kMaxI32 && uf <= kMaxI32;
+            p.X[0] * p.X[1] * p.X[2] <= kMaxI32 && uf <= kMaxI32 &&
+            (int64_t(182) * cpad * kpad + 4 * kpad + 64) * 4 < (int64_t(1) << 32);
   if (p.fused && !grid_ok(int64_t(p.T_pad / p.blk) * (p.K_pad / 16), 768, &p.grid_fused)) return WINO_EINVAL;
 
   if (aniso) {
