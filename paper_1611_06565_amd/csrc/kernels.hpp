@@ -773,8 +773,10 @@ __device__ __forceinline__ void gemm_epilogue(const AccT* acc, float* sm, int kb
   }
 }
 
-// Raw buffer resource over 4 GiB from a wave-uniform base (the third word
-// is the gfx9 family's raw 32-bit format).
+// Raw buffer resource covering the 4 GiB that follow a wave-uniform base
+// (num_records 2^32 - 1 bytes, stride 0; the fourth word is the gfx9
+// family's raw 32-bit format).  Loads through it add a 32-bit vector offset
+// and a 32-bit scalar offset to the base.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const float* base) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, -1, 0x00020000);
 }
